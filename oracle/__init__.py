@@ -1,0 +1,19 @@
+"""Plain fp64 CPU oracle of the MoE layer forward and backward.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this package: only the tests, the package's smoke check and the
+benchmark's CPU-baseline leg use it.  It shares no code with the HIP path.
+"""
+from .moe_oracle import (  # noqa: F401
+    RouterSpec,
+    spec_from_config,
+    router_logits,
+    route,
+    sort_maps,
+    permute_rows,
+    expert_forward,
+    expert_backward,
+    layer_forward,
+    layer_backward,
+    router_backward,
+)

@@ -1,0 +1,378 @@
+"""fp64 oracle of one MoE layer: router, permutation, SwiGLU experts, combine,
+and the full backward (expert dgrad/wgrad, router gradient).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+benchmark's CPU-baseline leg, never by the product path.  It shares no code
+with the HIP implementation; it receives the same seeded inputs, upcast
+exactly to float64.
+
+What it follows.  The paper (PithTrain, arxiv 2605.31463) trains MoE models
+built from a top-k router and SwiGLU experts (section 3.2, "Other
+optimizations": fused SwiGLU forward and backward, EP token scatter; appendix
+B.3, DynMoE task: the framework's top-k routing kernel) and checks a routing
+trace by three rules: expert ids lie in [0, num_experts), gating weights are
+non-negative and sum to one over the selected top-k (appendix B.2.2, "Collect
+Routing Trace").  It prints no layer equations, so this oracle writes out the
+standard definitions of the three router families of the workloads it is
+tested on (Qwen3-30B-A3B and GPT-OSS-20B style softmax routers, DeepSeek-V3
+style group-limited sigmoid router) and of a SwiGLU expert, in float64, with
+no blocking, fusion or reordering beyond plain matrix products.  Every reading
+the paper leaves open is listed with the design notes (ties go to the lower
+index; slots are ordered by descending key; rows within an expert by
+ascending token; the DeepSeek group score is the sum of the top two keys of
+the group).
+
+Conventions.  x [T][d]; W_r [d][E]; expert e: W_gate, W_up [d][f],
+W_down [f][d], optional biases b_gate, b_up [f], b_down [d].
+Routing outputs topk_idx [T][k] (slot order = descending selection key,
+ties to the lower expert), topk_w [T][k].  Maps: row r of the permuted
+matrix holds (token t, slot s) with token_of[r] = t*k + s and
+row_of[t][s] = r; rows are grouped by expert (ascending expert), and within
+an expert ordered by ascending token.
+"""
+from dataclasses import dataclass
+
+import numpy as np
+
+
+@dataclass
+class RouterSpec:
+    """Which router family and its constants.
+
+    router:       'softmax_topk'  softmax over all experts, keep the top k,
+                                  renormalise over the k (equal, in exact
+                                  arithmetic, to a softmax over the k logits)
+                  'topk_softmax'  top k logits, softmax over those k
+                  'sigmoid_grouped'  s = sigmoid(logit), selection key s+beta,
+                                  group-limited top-k, w = scale*s/sum(s)
+    k, n_groups, topk_groups, route_scale as in the workload configs;
+    bias_mode:    'none', 'select' (bias in the selection key only) or
+                  'logit' (bias added to the logits, for selection and weights).
+    """
+    router: str
+    E: int
+    k: int
+    n_groups: int = 1
+    topk_groups: int = 1
+    route_scale: float = 1.0
+    bias_mode: str = "none"
+
+
+def spec_from_config(cfg):
+    return RouterSpec(router=cfg["router"], E=cfg["E"], k=cfg["k"],
+                      n_groups=cfg["n_groups"], topk_groups=cfg["topk_groups"],
+                      route_scale=cfg["route_scale"], bias_mode=cfg["bias_mode"])
+
+
+def sigmoid(z):
+    return 1.0 / (1.0 + np.exp(-z))
+
+
+def silu(z):
+    return z * sigmoid(z)
+
+
+# ----------------------------------------------------------------------------
+# Router forward
+# ----------------------------------------------------------------------------
+
+def router_logits(x, w_r):
+    """l[t][e] = sum_i x[t][i] * W_r[i][e], in float64."""
+    return np.asarray(x, np.float64) @ np.asarray(w_r, np.float64)
+
+
+def _desc_order(keys):
+    """Per row, indices sorted by descending key; equal keys keep ascending index."""
+    return np.argsort(-keys, axis=-1, kind="stable")
+
+
+def _adjacent_gap_min(sorted_keys, upto):
+    """Smallest gap between consecutive sorted keys among the first upto+1."""
+    n = min(upto + 1, sorted_keys.shape[1])
+    if n < 2:
+        return np.full(sorted_keys.shape[0], np.inf)
+    gaps = sorted_keys[:, :n - 1] - sorted_keys[:, 1:n]
+    return gaps.min(axis=1)
+
+
+def route(spec, logits, beta=None):
+    """Expert selection and gating weights for every token.
+
+    Returns a dict with
+      topk_idx [T][k] int64   selected experts, slot order = descending key
+      topk_w   [T][k]         gating weights
+      s_sel    [T][k] or None sigmoid scores of the selected experts
+                              (sigmoid_grouped router only)
+      keys     [T][E]         selection keys
+      margin   [T]            smallest gap between consecutive keys among the
+                              top k+1 candidates (and, for the grouped router,
+                              between the kept and the first dropped group
+                              score); a token is ambiguous when it is < 1e-6
+    """
+    l = np.asarray(logits, np.float64)
+    T, E = l.shape
+    k = spec.k
+    b = None if beta is None else np.asarray(beta, np.float64)
+    if spec.bias_mode != "none" and b is None:
+        raise ValueError("router bias required")
+
+    if spec.router in ("softmax_topk", "topk_softmax"):
+        wl = l + b if spec.bias_mode == "logit" else l          # logits seen by the weights
+        keys = l + b if spec.bias_mode in ("logit", "select") else l
+        order = _desc_order(keys)
+        idx = order[:, :k]
+        sk = np.take_along_axis(keys, order, axis=1)
+        margin = _adjacent_gap_min(sk, k)
+        sel = np.take_along_axis(wl, idx, axis=1)
+        m = sel.max(axis=1, keepdims=True)
+        p = np.exp(sel - m)
+        w = spec.route_scale * p / p.sum(axis=1, keepdims=True)
+        return dict(topk_idx=idx, topk_w=w, s_sel=None, keys=keys, margin=margin)
+
+    if spec.router == "sigmoid_grouped":
+        s = sigmoid(l)
+        keys = s + b if b is not None else s.copy()
+        G = spec.n_groups
+        if E % G:
+            raise ValueError("E must be a multiple of n_groups")
+        per = E // G
+        grouped = keys.reshape(T, G, per)
+        top2 = -np.sort(-grouped, axis=2)[:, :, :2]
+        gscore = top2.sum(axis=2) if per >= 2 else top2[:, :, 0]
+        gorder = _desc_order(gscore)
+        kept = gorder[:, :spec.topk_groups]
+        if spec.topk_groups < G:
+            sg = np.take_along_axis(gscore, gorder, axis=1)
+            gmargin = sg[:, spec.topk_groups - 1] - sg[:, spec.topk_groups]
+        else:
+            gmargin = np.full(T, np.inf)
+        allowed = np.zeros((T, G), dtype=bool)
+        np.put_along_axis(allowed, kept, True, axis=1)
+        allowed_e = np.repeat(allowed, per, axis=1)
+        masked = np.where(allowed_e, keys, -np.inf)
+        order = _desc_order(masked)
+        idx = order[:, :k]
+        n_cand = spec.topk_groups * per
+        sk = np.take_along_axis(masked, order, axis=1)[:, :n_cand]
+        margin = np.minimum(_adjacent_gap_min(sk, k), gmargin)
+        ssel = np.take_along_axis(s, idx, axis=1)
+        w = spec.route_scale * ssel / ssel.sum(axis=1, keepdims=True)
+        return dict(topk_idx=idx, topk_w=w, s_sel=ssel, keys=keys, margin=margin)
+
+    raise ValueError("unknown router " + spec.router)
+
+
+# ----------------------------------------------------------------------------
+# Permutation maps (stable counting sort by expert, then token)
+# ----------------------------------------------------------------------------
+
+def sort_maps(topk_idx, E):
+    """Counts, offsets and the row maps of the expert-contiguous layout.
+
+    counts[e] = number of (t, s) with topk_idx[t][s] == e;
+    offsets[e] = sum of counts of experts below e (offsets[E] = T*k);
+    the rows of expert e are offsets[e] .. offsets[e+1]-1, filled by
+    ascending token t (a token holds an expert in at most one slot).
+    """
+    idx = np.asarray(topk_idx)
+    T, k = idx.shape
+    counts = np.zeros(E, dtype=np.int64)
+    for e in idx.reshape(-1):
+        counts[e] += 1
+    offsets = np.zeros(E + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    cursor = offsets[:-1].copy()
+    row_of = np.empty((T, k), dtype=np.int64)
+    token_of = np.empty(T * k, dtype=np.int64)
+    for t in range(T):                       # ascending token: stable within expert
+        for s in range(k):
+            e = idx[t, s]
+            r = cursor[e]
+            cursor[e] += 1
+            row_of[t, s] = r
+            token_of[r] = t * k + s
+    return dict(counts=counts, offsets=offsets, row_of=row_of, token_of=token_of)
+
+
+def permute_rows(x, token_of, k):
+    """x_perm[r] = x[token_of[r] // k]."""
+    return np.asarray(x)[np.asarray(token_of) // k]
+
+
+# ----------------------------------------------------------------------------
+# SwiGLU expert
+# ----------------------------------------------------------------------------
+
+def expert_forward(xe, wg, wu, wd, bg=None, bu=None, bd=None):
+    """g = x W_gate (+b_gate), u = x W_up (+b_up), h = silu(g) * u,
+    o = h W_down (+b_down), for the rows xe [M][d]."""
+    g = xe @ wg
+    u = xe @ wu
+    if bg is not None:
+        g = g + bg
+    if bu is not None:
+        u = u + bu
+    h = silu(g) * u
+    o = h @ wd
+    if bd is not None:
+        o = o + bd
+    return g, u, h, o
+
+
+def expert_backward(xe, g, u, h, do, wg, wu, wd, with_bias=False):
+    """Gradients of sum(<do, o>) for one expert's rows.
+
+    dh = do W_down^T; dW_down = h^T do; db_down = sum_rows do
+    dg = dh * u * sig(g) * (1 + g (1 - sig(g)));  du = dh * silu(g)
+    dW_gate = x^T dg; dW_up = x^T du; db_gate, db_up = row sums
+    dx = dg W_gate^T + du W_up^T
+    """
+    sg = sigmoid(g)
+    dh = do @ wd.T
+    dg = dh * u * sg * (1.0 + g * (1.0 - sg))
+    du = dh * g * sg
+    out = dict(
+        dw_down=h.T @ do,
+        dw_gate=xe.T @ dg,
+        dw_up=xe.T @ du,
+        dx=dg @ wg.T + du @ wu.T,
+        dg=dg, du=du,
+    )
+    if with_bias:
+        out["db_down"] = do.sum(axis=0)
+        out["db_gate"] = dg.sum(axis=0)
+        out["db_up"] = du.sum(axis=0)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Router backward
+# ----------------------------------------------------------------------------
+
+def router_backward(spec, rt, omega):
+    """dL/dlogit on the selected experts, dl [T][k].
+
+    omega[t][j] = dL/dw[t][j] = <dy_t, o_j(x_t)>.
+    Softmax families, w_j = c * p_j with p the softmax over the selected
+    (weight) logits:  dl_j = w_j * (omega_j - sum_i w_i omega_i / c).
+    Sigmoid family, w_j = c * s_j / Z, Z = sum_S s:
+        ds_j = (c * omega_j - sum_i w_i omega_i) / Z,  dl_j = ds_j s_j (1 - s_j).
+    The bias has no gradient.
+    """
+    w = rt["topk_w"]
+    c = spec.route_scale
+    wo = (w * omega).sum(axis=1, keepdims=True)
+    if spec.router in ("softmax_topk", "topk_softmax"):
+        return w * (omega - wo / c)
+    s = rt["s_sel"]
+    Z = s.sum(axis=1, keepdims=True)
+    ds = (c * omega - wo) / Z
+    return ds * s * (1.0 - s)
+
+
+# ----------------------------------------------------------------------------
+# Whole layer
+# ----------------------------------------------------------------------------
+
+def layer_forward(spec, x, w_r, beta, expert_fn, shared=None):
+    """Forward of one MoE layer.
+
+    x [T][d] float64; w_r [d][E]; beta [E] or None;
+    expert_fn(e) -> (wg, wu, wd, bg, bu, bd) float64 (biases may be None);
+    shared = (wsg, wsu, wsd) or None for an always-on expert of weight 1.
+    Returns routing, maps and the per-row activations (permuted order) and y.
+    """
+    x = np.asarray(x, np.float64)
+    T, d = x.shape
+    E, k = spec.E, spec.k
+    l = router_logits(x, w_r)
+    rt = route(spec, l, beta)
+    mp = sort_maps(rt["topk_idx"], E)
+    R = T * k
+    x_perm = permute_rows(x, mp["token_of"], k)
+    fwidth = None
+    o = np.zeros((R, d))
+    gs, us, hs = {}, {}, {}
+    for e in range(E):
+        r0, r1 = mp["offsets"][e], mp["offsets"][e + 1]
+        if r1 == r0:
+            continue
+        wg, wu, wd, bg, bu, bd = expert_fn(e)
+        g, u, h, oe = expert_forward(x_perm[r0:r1], wg, wu, wd, bg, bu, bd)
+        gs[e], us[e], hs[e] = g, u, h
+        o[r0:r1] = oe
+        fwidth = wg.shape[1]
+    # combine: y_t = sum_s w[t][s] * o[row_of[t][s]]
+    y = np.zeros((T, d))
+    for s in range(k):
+        y += rt["topk_w"][:, s:s + 1] * o[mp["row_of"][:, s]]
+    sh = None
+    if shared is not None:
+        g, u, h, osh = expert_forward(x, *shared)
+        y = y + osh
+        sh = dict(g=g, u=u, h=h, o=osh)
+    return dict(logits=l, route=rt, maps=mp, x_perm=x_perm, o=o, g=gs, u=us,
+                h=hs, y=y, shared=sh, f=fwidth)
+
+
+def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bias=False):
+    """Backward of L = sum_t <dy_t, y_t> through the whole layer.
+
+    Returns dx [T][d], dw_r [d][E], per-expert dict of dW/db, shared-expert
+    grads, omega [T][k] and dl [T][k].
+    """
+    x = np.asarray(x, np.float64)
+    dy = np.asarray(dy, np.float64)
+    T, d = x.shape
+    E, k = spec.E, spec.k
+    rt, mp = fwd["route"], fwd["maps"]
+    w = rt["topk_w"]
+    o = fwd["o"]
+    # combine backward
+    omega = np.zeros((T, k))
+    do = np.zeros_like(o)
+    for s in range(k):
+        rows = mp["row_of"][:, s]
+        omega[:, s] = (dy * o[rows]).sum(axis=1)
+        do[rows] = w[:, s:s + 1] * dy
+    # experts
+    dx = np.zeros((T, d))
+    dx_perm = np.zeros((T * k, d))
+    grads = {}
+    for e in range(E):
+        r0, r1 = mp["offsets"][e], mp["offsets"][e + 1]
+        wg, wu, wd, bg, bu, bd = expert_fn(e)
+        if r1 == r0:
+            grads[e] = dict(dw_gate=np.zeros_like(wg), dw_up=np.zeros_like(wu),
+                            dw_down=np.zeros_like(wd))
+            if with_bias:
+                grads[e].update(db_gate=np.zeros(wg.shape[1]), db_up=np.zeros(wu.shape[1]),
+                                db_down=np.zeros(wd.shape[1]))
+            continue
+        ge = expert_backward(fwd["x_perm"][r0:r1], fwd["g"][e], fwd["u"][e], fwd["h"][e],
+                             do[r0:r1], wg, wu, wd, with_bias=with_bias)
+        dx_perm[r0:r1] = ge.pop("dx")
+        ge.pop("dg")
+        ge.pop("du")
+        grads[e] = ge
+    # unpermute: dx_t += sum_s dx_perm[row_of[t][s]]
+    for s in range(k):
+        dx += dx_perm[mp["row_of"][:, s]]
+    # router
+    dl = router_backward(spec, rt, omega)
+    dl_dense = np.zeros((T, E))
+    np.put_along_axis(dl_dense, rt["topk_idx"], dl, axis=1)
+    dw_r = x.T @ dl_dense
+    dx_router = dl_dense @ np.asarray(w_r, np.float64).T
+    dx += dx_router
+    sh = None
+    if shared is not None:
+        wsg, wsu, wsd = shared
+        s_ = fwd["shared"]
+        gsh = expert_backward(x, s_["g"], s_["u"], s_["h"], dy, wsg, wsu, wsd)
+        dx += gsh.pop("dx")
+        gsh.pop("dg")
+        gsh.pop("du")
+        sh = gsh
+    return dict(dx=dx, dw_r=dw_r, experts=grads, shared=sh, omega=omega, dl=dl,
+                dx_perm=dx_perm, do=do, dx_router=dx_router)

@@ -1,0 +1,425 @@
+"""Pins of the fp64 oracle against facts that do not come from the oracle itself:
+hand-worked examples, a dense every-expert brute force, torch autograd on an
+independently written dense masked formulation, central finite differences,
+closed-form special cases, brute-force enumeration of the group-limited
+router, a library sort for the permutation maps, and the routing-trace
+invariants (ids in range, weights non-negative and summing to one over the
+top-k; appendix B.2.2, "Collect Routing Trace")."""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import (RouterSpec, expert_backward, expert_forward, layer_backward,
+                    layer_forward, route, router_logits, sort_maps)
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+SPECS = {
+    "softmax_topk": RouterSpec("softmax_topk", E=8, k=2),
+    "topk_softmax": RouterSpec("topk_softmax", E=8, k=3),
+    "softmax_logit_bias": RouterSpec("softmax_topk", E=8, k=2, bias_mode="logit"),
+    "sigmoid_grouped": RouterSpec("sigmoid_grouped", E=16, k=4, n_groups=4, topk_groups=2,
+                                  route_scale=2.5, bias_mode="select"),
+}
+
+
+def make_case(spec, T=24, d=16, f=12, seed=0, expert_bias=False, shared=False, wr_std=0.3):
+    rng = np.random.default_rng(seed)
+    E = spec.E
+    c = dict(
+        x=rng.standard_normal((T, d)),
+        w_r=rng.standard_normal((d, E)) * wr_std,
+        beta=(rng.standard_normal(E) * 0.1 if spec.bias_mode != "none" else None),
+        wg=rng.standard_normal((E, d, f)) * 0.3,
+        wu=rng.standard_normal((E, d, f)) * 0.3,
+        wd=rng.standard_normal((E, f, d)) * 0.3,
+        bg=rng.standard_normal((E, f)) * 0.1 if expert_bias else None,
+        bu=rng.standard_normal((E, f)) * 0.1 if expert_bias else None,
+        bd=rng.standard_normal((E, d)) * 0.1 if expert_bias else None,
+        dy=rng.standard_normal((T, d)),
+        shared=((rng.standard_normal((d, f)) * 0.3, rng.standard_normal((d, f)) * 0.3,
+                 rng.standard_normal((f, d)) * 0.3) if shared else None),
+    )
+    return c
+
+
+def efn(c):
+    def fn(e):
+        return (c["wg"][e], c["wu"][e], c["wd"][e],
+                None if c["bg"] is None else c["bg"][e],
+                None if c["bu"] is None else c["bu"][e],
+                None if c["bd"] is None else c["bd"][e])
+    return fn
+
+
+def run(spec, c):
+    fwd = layer_forward(spec, c["x"], c["w_r"], c["beta"], efn(c), c["shared"])
+    bwd = layer_backward(spec, c["x"], c["w_r"], c["beta"], efn(c), fwd, c["dy"], c["shared"],
+                         with_bias=c["bg"] is not None)
+    return fwd, bwd
+
+
+def rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300)
+
+
+# ---------------------------------------------------------------------------
+# Hand-worked examples
+# ---------------------------------------------------------------------------
+
+def test_worked_example_softmax():
+    g = json.load(open(os.path.join(GOLDEN, "route_worked_examples.json")))["softmax"]
+    spec = RouterSpec("topk_softmax", E=g["E"], k=g["k"])
+    l = np.log(np.asarray(g["logits_ln"], np.float64))
+    rt = route(spec, l)
+    assert rt["topk_idx"].tolist() == g["topk_idx"]
+    want = np.array([[n / m for n, m in row] for row in g["topk_w_frac"]])
+    np.testing.assert_allclose(rt["topk_w"], want, rtol=0, atol=1e-15)
+    mp = sort_maps(rt["topk_idx"], g["E"])
+    assert mp["counts"].tolist() == g["counts"]
+    assert mp["offsets"].tolist() == g["offsets"]
+    assert mp["row_of"].tolist() == g["row_of"]
+    assert mp["token_of"].tolist() == g["token_of"]
+    # the softmax-then-renormalise family is the same function
+    rt2 = route(RouterSpec("softmax_topk", E=g["E"], k=g["k"]), l)
+    assert rt2["topk_idx"].tolist() == g["topk_idx"]
+    np.testing.assert_allclose(rt2["topk_w"], want, rtol=0, atol=1e-15)
+
+
+def test_worked_example_sigmoid_grouped():
+    g = json.load(open(os.path.join(GOLDEN, "route_worked_examples.json")))["sigmoid_grouped"]
+    spec = RouterSpec("sigmoid_grouped", E=g["E"], k=g["k"], n_groups=g["n_groups"],
+                      topk_groups=g["topk_groups"], route_scale=g["route_scale"], bias_mode="select")
+    l = np.zeros((1, g["E"]))
+    rt = route(spec, l, np.asarray(g["beta"]))
+    assert rt["topk_idx"].tolist() == g["topk_idx"]
+    want = np.array([[n / m for n, m in row] for row in g["topk_w_frac"]])
+    np.testing.assert_allclose(rt["topk_w"], want, rtol=0, atol=1e-15)
+
+
+# ---------------------------------------------------------------------------
+# Dense every-expert brute force of the forward
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", list(SPECS))
+def test_forward_matches_dense_bruteforce(name):
+    spec = SPECS[name]
+    c = make_case(spec, expert_bias=True, shared=(name == "sigmoid_grouped"))
+    fwd = layer_forward(spec, c["x"], c["w_r"], c["beta"], efn(c), c["shared"])
+    T = c["x"].shape[0]
+    gate = np.zeros((T, spec.E))
+    for t in range(T):
+        for s in range(spec.k):
+            gate[t, fwd["route"]["topk_idx"][t, s]] = fwd["route"]["topk_w"][t, s]
+    y = np.zeros_like(c["x"])
+    for e in range(spec.E):
+        g = c["x"] @ c["wg"][e] + c["bg"][e]
+        u = c["x"] @ c["wu"][e] + c["bu"][e]
+        o = (g / (1 + np.exp(-g)) * u) @ c["wd"][e] + c["bd"][e]
+        y += gate[:, e:e + 1] * o
+    if c["shared"] is not None:
+        a, b, w = c["shared"]
+        g, u = c["x"] @ a, c["x"] @ b
+        y += (g / (1 + np.exp(-g)) * u) @ w
+    assert rel(fwd["y"], y) < 1e-12
+
+
+# ---------------------------------------------------------------------------
+# torch autograd on a dense masked formulation (independent of the oracle)
+# ---------------------------------------------------------------------------
+
+def torch_dense_loss(spec, c, params):
+    x, w_r, wg, wu, wd = (params[n] for n in ("x", "w_r", "wg", "wu", "wd"))
+    l = x @ w_r
+    T, E = l.shape
+    beta = None if c["beta"] is None else torch.tensor(c["beta"], dtype=torch.float64)
+    if spec.router in ("softmax_topk", "topk_softmax"):
+        key = l + beta if spec.bias_mode in ("logit", "select") else l
+        wl = l + beta if spec.bias_mode == "logit" else l
+        sel = torch.topk(key.detach(), spec.k, dim=1).indices
+        mask = torch.zeros(T, E, dtype=torch.bool).scatter(1, sel, True)
+        gate = spec.route_scale * torch.softmax(wl.masked_fill(~mask, float("-inf")), dim=1)
+    else:
+        s = torch.sigmoid(l)
+        key = (s + beta).detach()
+        per = E // spec.n_groups
+        gs = key.view(T, spec.n_groups, per).topk(2, dim=2).values.sum(-1)
+        gsel = gs.topk(spec.topk_groups, dim=1).indices
+        gmask = torch.zeros(T, spec.n_groups, dtype=torch.bool).scatter(1, gsel, True)
+        emask = gmask.repeat_interleave(per, dim=1)
+        sel = key.masked_fill(~emask, float("-inf")).topk(spec.k, dim=1).indices
+        mask = torch.zeros(T, E, dtype=torch.bool).scatter(1, sel, True)
+        sm = s * mask
+        gate = spec.route_scale * sm / sm.sum(1, keepdim=True)
+    y = torch.zeros_like(x)
+    for e in range(E):
+        g = x @ wg[e]
+        u = x @ wu[e]
+        if "bg" in params:
+            g = g + params["bg"][e]
+            u = u + params["bu"][e]
+        o = (torch.nn.functional.silu(g) * u) @ wd[e]
+        if "bd" in params:
+            o = o + params["bd"][e]
+        y = y + gate[:, e:e + 1] * o
+    if "sg" in params:
+        g = x @ params["sg"]
+        u = x @ params["su"]
+        y = y + (torch.nn.functional.silu(g) * u) @ params["sd"]
+    dy = torch.tensor(c["dy"], dtype=torch.float64)
+    return (dy * y).sum(), sel
+
+
+@pytest.mark.parametrize("name", list(SPECS))
+def test_backward_matches_torch_autograd(name):
+    spec = SPECS[name]
+    shared = name == "sigmoid_grouped"
+    c = make_case(spec, expert_bias=True, shared=shared, seed=1)
+    fwd, bwd = run(spec, c)
+    params = {n: torch.tensor(c[n], dtype=torch.float64, requires_grad=True)
+              for n in ("x", "w_r", "wg", "wu", "wd", "bg", "bu", "bd")}
+    if shared:
+        for n, a in zip(("sg", "su", "sd"), c["shared"]):
+            params[n] = torch.tensor(a, dtype=torch.float64, requires_grad=True)
+    loss, sel = torch_dense_loss(spec, c, params)
+    loss.backward()
+    # same selected sets
+    assert [sorted(r) for r in sel.tolist()] == [sorted(r) for r in fwd["route"]["topk_idx"].tolist()]
+    assert abs(loss.item() - (c["dy"] * fwd["y"]).sum()) < 1e-10 * abs(loss.item())
+    assert rel(bwd["dx"], params["x"].grad.numpy()) < 1e-11
+    assert rel(bwd["dw_r"], params["w_r"].grad.numpy()) < 1e-11
+    for e in range(spec.E):
+        ge = bwd["experts"][e]
+        for ours, theirs in (("dw_gate", "wg"), ("dw_up", "wu"), ("dw_down", "wd"),
+                             ("db_gate", "bg"), ("db_up", "bu"), ("db_down", "bd")):
+            want = params[theirs].grad[e].numpy()
+            if np.linalg.norm(want) == 0:
+                assert np.linalg.norm(ge[ours]) == 0
+            else:
+                assert rel(ge[ours], want) < 1e-11, (e, ours)
+    if shared:
+        for ours, theirs in (("dw_gate", "sg"), ("dw_up", "su"), ("dw_down", "sd")):
+            assert rel(bwd["shared"][ours], params[theirs].grad.numpy()) < 1e-11
+
+
+# ---------------------------------------------------------------------------
+# Central finite differences along random directions
+# ---------------------------------------------------------------------------
+
+def _loss(spec, c):
+    fwd = layer_forward(spec, c["x"], c["w_r"], c["beta"], efn(c), c["shared"])
+    return float((c["dy"] * fwd["y"]).sum()), fwd["route"]["topk_idx"]
+
+
+@pytest.mark.parametrize("name", list(SPECS))
+def test_gradients_match_finite_differences(name):
+    spec = SPECS[name]
+    shared = name == "sigmoid_grouped"
+    c = make_case(spec, T=12, d=8, f=6, expert_bias=True, shared=shared, seed=2)
+    fwd, bwd = run(spec, c)
+    rng = np.random.default_rng(5)
+    grads = {"x": bwd["dx"], "w_r": bwd["dw_r"]}
+    for ours, key in (("dw_gate", "wg"), ("dw_up", "wu"), ("dw_down", "wd"),
+                      ("db_gate", "bg"), ("db_up", "bu"), ("db_down", "bd")):
+        grads[key] = np.stack([bwd["experts"][e][ours] for e in range(spec.E)])
+    h = 1e-6
+    for key, gr in grads.items():
+        for _ in range(3):
+            v = rng.standard_normal(c[key].shape)
+            v /= np.linalg.norm(v)
+            cp, cm = dict(c), dict(c)
+            cp[key] = c[key] + h * v
+            cm[key] = c[key] - h * v
+            lp, ip = _loss(spec, cp)
+            lm, im = _loss(spec, cm)
+            if not (np.array_equal(ip, fwd["route"]["topk_idx"])
+                    and np.array_equal(im, fwd["route"]["topk_idx"])):
+                continue  # the step crossed a selection boundary; draw again
+            fd = (lp - lm) / (2 * h)
+            an = float((gr * v).sum())
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (key, fd, an)
+    if shared:
+        for i, ours in enumerate(("dw_gate", "dw_up", "dw_down")):
+            v = rng.standard_normal(c["shared"][i].shape)
+            v /= np.linalg.norm(v)
+            sp = list(c["shared"])
+            sm = list(c["shared"])
+            sp[i] = sp[i] + h * v
+            sm[i] = sm[i] - h * v
+            lp, _ = _loss(spec, dict(c, shared=tuple(sp)))
+            lm, _ = _loss(spec, dict(c, shared=tuple(sm)))
+            fd = (lp - lm) / (2 * h)
+            an = float((bwd["shared"][ours] * v).sum())
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an))
+
+
+# ---------------------------------------------------------------------------
+# Closed-form special cases
+# ---------------------------------------------------------------------------
+
+def test_single_expert_is_plain_swiglu_mlp():
+    spec = RouterSpec("softmax_topk", E=1, k=1)
+    c = make_case(spec, seed=3)
+    fwd, bwd = run(spec, c)
+    x, wg, wu, wd = c["x"], c["wg"][0], c["wu"][0], c["wd"][0]
+    g, u = x @ wg, x @ wu
+    h = g / (1 + np.exp(-g)) * u
+    assert rel(fwd["y"], h @ wd) < 1e-13
+    assert np.all(fwd["route"]["topk_w"] == 1.0)
+    assert np.all(bwd["dl"] == 0.0)
+    assert np.all(bwd["dw_r"] == 0.0)
+    # dx of a plain MLP, written with the chain rule for silu'(g) = sig(g)(1+g(1-sig(g)))
+    sg = 1 / (1 + np.exp(-g))
+    dh = c["dy"] @ wd.T
+    dx = (dh * u * sg * (1 + g * (1 - sg))) @ wg.T + (dh * g * sg) @ wu.T
+    assert rel(bwd["dx"], dx) < 1e-13
+
+
+def test_k_equals_E_gives_full_softmax():
+    from scipy.special import softmax
+    spec = RouterSpec("softmax_topk", E=8, k=8)
+    c = make_case(spec, seed=4)
+    l = router_logits(c["x"], c["w_r"])
+    rt = route(spec, l)
+    full = softmax(l, axis=1)
+    got = np.zeros_like(full)
+    np.put_along_axis(got, rt["topk_idx"], rt["topk_w"], axis=1)
+    assert rel(got, full) < 1e-14
+    assert np.all(np.diff(np.take_along_axis(l, rt["topk_idx"], 1), axis=1) <= 0)
+
+
+def test_zero_router_ties_go_to_lower_index():
+    spec = RouterSpec("softmax_topk", E=8, k=3)
+    c = make_case(spec, seed=5)
+    c["w_r"][:] = 0.0
+    fwd, bwd = run(spec, c)
+    T = c["x"].shape[0]
+    assert fwd["route"]["topk_idx"].tolist() == [[0, 1, 2]] * T
+    assert np.all(fwd["route"]["topk_w"] == 1.0 / 3.0)
+    assert fwd["maps"]["counts"].tolist() == [T, T, T, 0, 0, 0, 0, 0]
+    assert fwd["maps"]["token_of"].tolist() == [t * 3 + s for s in range(3) for t in range(T)]
+
+
+def test_zero_router_sigmoid_selects_by_bias_alone():
+    spec = SPECS["sigmoid_grouped"]
+    c = make_case(spec, seed=6)
+    c["w_r"][:] = 0.0
+    fwd, _ = run(spec, c)
+    beta = c["beta"]
+    per = spec.E // spec.n_groups
+    gscore = [sum(sorted(beta[g * per:(g + 1) * per], reverse=True)[:2]) for g in range(spec.n_groups)]
+    keep = sorted(range(spec.n_groups), key=lambda g: (-gscore[g], g))[:spec.topk_groups]
+    cand = [e for g in keep for e in range(g * per, (g + 1) * per)]
+    want = sorted(cand, key=lambda e: (-beta[e], e))[:spec.k]
+    T = c["x"].shape[0]
+    assert fwd["route"]["topk_idx"].tolist() == [want] * T
+    np.testing.assert_allclose(fwd["route"]["topk_w"], 2.5 / spec.k, rtol=0, atol=1e-15)
+
+
+# ---------------------------------------------------------------------------
+# Brute-force enumeration of the group-limited router
+# ---------------------------------------------------------------------------
+
+def test_grouped_router_matches_subset_enumeration():
+    spec = SPECS["sigmoid_grouped"]
+    c = make_case(spec, T=40, seed=7)
+    l = router_logits(c["x"], c["w_r"])
+    rt = route(spec, l, c["beta"])
+    per = spec.E // spec.n_groups
+    for t in range(l.shape[0]):
+        s = [1.0 / (1.0 + np.exp(-v)) for v in l[t]]
+        key = [s[e] + c["beta"][e] for e in range(spec.E)]
+        score = [sum(sorted(key[g * per:(g + 1) * per], reverse=True)[:2]) for g in range(spec.n_groups)]
+        best = max(itertools.combinations(range(spec.n_groups), spec.topk_groups),
+                   key=lambda sub: sum(score[g] for g in sub))
+        cand = [e for g in best for e in range(g * per, (g + 1) * per)]
+        want = sorted(cand, key=lambda e: (-key[e], e))[:spec.k]
+        assert rt["topk_idx"][t].tolist() == want
+        tot = sum(s[e] for e in want)
+        np.testing.assert_allclose(rt["topk_w"][t], [2.5 * s[e] / tot for e in want], rtol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# Permutation maps against a library sort, and the invariants
+# ---------------------------------------------------------------------------
+
+def test_maps_match_library_stable_sort():
+    rng = np.random.default_rng(8)
+    T, E, k = 200, 13, 4
+    idx = np.stack([rng.permutation(E)[:k] for _ in range(T)])
+    mp = sort_maps(idx, E)
+    t_of = np.repeat(np.arange(T), k)
+    s_of = np.tile(np.arange(k), T)
+    order = np.lexsort((t_of, idx.reshape(-1)))     # by expert, then token
+    assert mp["token_of"].tolist() == (t_of[order] * k + s_of[order]).tolist()
+    assert mp["counts"].tolist() == np.bincount(idx.reshape(-1), minlength=E).tolist()
+
+
+@pytest.mark.parametrize("name", list(SPECS))
+def test_invariants(name):
+    spec = SPECS[name]
+    c = make_case(spec, T=64, seed=9)
+    fwd, bwd = run(spec, c)
+    rt, mp = fwd["route"], fwd["maps"]
+    T, k, E = c["x"].shape[0], spec.k, spec.E
+    idx, w = rt["topk_idx"], rt["topk_w"]
+    assert idx.min() >= 0 and idx.max() < E
+    assert all(len(set(r)) == k for r in idx.tolist())
+    assert np.all(w >= 0)
+    np.testing.assert_allclose(w.sum(1), spec.route_scale, rtol=1e-14)
+    assert mp["counts"].sum() == T * k == mp["offsets"][E]
+    assert np.all(np.diff(mp["offsets"]) == mp["counts"])
+    assert sorted(mp["token_of"].tolist()) == list(range(T * k))
+    for e in range(E):
+        toks = mp["token_of"][mp["offsets"][e]:mp["offsets"][e + 1]] // k
+        assert np.all(np.diff(toks) > 0)
+    for t in range(T):
+        for s in range(k):
+            assert mp["token_of"][mp["row_of"][t, s]] == t * k + s
+            assert np.array_equal(fwd["x_perm"][mp["row_of"][t, s]], c["x"][t])
+    if spec.router != "sigmoid_grouped":
+        # softmax routers: every row of dl sums to zero, so do the rows of dW_r
+        np.testing.assert_allclose(bwd["dl"].sum(1), 0.0, atol=1e-12)
+        assert np.abs(bwd["dw_r"].sum(1)).max() < 1e-11 * np.abs(bwd["dw_r"]).max()
+
+
+def test_unpermute_of_permute_is_identity():
+    spec = RouterSpec("softmax_topk", E=8, k=4)
+    c = make_case(spec, T=50, seed=10)
+    fwd = layer_forward(spec, c["x"], c["w_r"], c["beta"], efn(c))
+    back = np.zeros_like(c["x"])
+    for s in range(spec.k):
+        back += 0.25 * fwd["x_perm"][fwd["maps"]["row_of"][:, s]]
+    assert np.array_equal(back, c["x"])
+
+
+def test_margin_flags_near_ties():
+    spec = RouterSpec("softmax_topk", E=4, k=2)
+    l = np.array([[0.3, 0.1, 0.1 + 5e-7, -1.0], [0.3, 0.2, 0.1, -1.0]])
+    rt = route(spec, l)
+    assert rt["margin"][0] < 1e-6 <= rt["margin"][1]
+
+
+def test_expert_backward_matches_finite_differences_on_its_own():
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((5, 4))
+    wg, wu, wd = (rng.standard_normal(s) for s in ((4, 3), (4, 3), (3, 4)))
+    do = rng.standard_normal((5, 4))
+    g, u, h, o = expert_forward(x, wg, wu, wd)
+    gr = expert_backward(x, g, u, h, do, wg, wu, wd)
+    eps = 1e-6
+    for name, arr in (("dw_gate", wg), ("dw_up", wu), ("dw_down", wd)):
+        for idx in [(0, 0), (1, 2), (2, 1)]:
+            ap = arr.copy(); ap[idx] += eps
+            am = arr.copy(); am[idx] -= eps
+            args_p = {"dw_gate": (ap, wu, wd), "dw_up": (wg, ap, wd), "dw_down": (wg, wu, ap)}[name]
+            args_m = {"dw_gate": (am, wu, wd), "dw_up": (wg, am, wd), "dw_down": (wg, wu, am)}[name]
+            fp = (do * expert_forward(x, *args_p)[3]).sum()
+            fm = (do * expert_forward(x, *args_m)[3]).sum()
+            assert abs((fp - fm) / (2 * eps) - gr[name][idx]) < 1e-7
