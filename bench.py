@@ -1,0 +1,241 @@
+"""Throughput of one MoE layer forward + backward on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload qwen3] [--no-cpu-baseline]
+
+A step is moe_layer_fwd + moe_layer_bwd over one batch of synthetic input
+already resident in HBM (routing, permutation, grouped SwiGLU expert GEMMs,
+combine, expert dgrad/wgrad, router gradient, unpermute).  Prints one JSON
+line: algorithmic TFLOP/s (value), tokens/s, the dominant kernel against its
+roofline (average launch time from HIP events recorded on the launch stream
+during the timed steps), and the fp64 CPU oracle timed on a bounded sample of
+the same workload on this host.
+
+Only one GPU: the layer's one-GPU share is the workload; --gpus above 1 is
+refused.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE layer fwd+bwd TFLOP/s and tokens/s on 1 MI355X; % of MFMA/HBM roofline"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+GEMM_SOURCE = os.path.join(ROOT, "paper_2605_31463_amd", "csrc", "gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def layer_flops(cfg):
+    """Algorithmic FLOPs (2 per multiply-add): fwd = 2TdE + 6Tkdf (+ 6Td f_shared), bwd = 2 fwd."""
+    T, d, E, k, f = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["f"]
+    fwd = 2 * T * d * E + 6 * T * k * d * f
+    if cfg["n_shared"]:
+        fwd += 6 * T * d * cfg["f_shared"]
+    return fwd, 2 * fwd
+
+
+def kernel_work(cfg):
+    """Per-launch algorithmic work of the layer's main kernels: (bound, amount, unit)."""
+    T, d, E, k, f = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["f"]
+    R = T * k
+    eb = 2 if cfg["dtype"] == "bf16" else 4
+    gu = 2.0 * R * d * 2 * f
+    dn = 2.0 * R * f * d
+    return {
+        "gemm_gateup_fwd": ("mfma", gu), "gemm_down_fwd": ("mfma", dn),
+        "gemm_down_dgrad": ("mfma", dn), "gemm_gateup_dgrad": ("mfma", gu),
+        "gemm_down_wgrad": ("mfma", dn), "gemm_gateup_wgrad": ("mfma", gu),
+        # bytes: reads + writes of the HBM operands, once each
+        "route": ("hbm", T * d * eb + d * E * 4 + R * 8),
+        "scatter": ("hbm", T * d * eb + R * d * eb + R * 4 * 3),
+        "combine_fwd": ("hbm", R * d * eb + T * d * eb + R * 8),
+        "combine_bwd": ("hbm", T * d * eb + 2 * R * d * eb + R * 12),
+        "unpermute": ("hbm", R * d * eb + T * d * eb + R * 12),
+    }
+
+
+def file_hash(path):
+    with open(path, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def traffic_for(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current GEMM source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("gemm_source_sha256_16") != file_hash(GEMM_SOURCE) or t.get("workload") != workload:
+        return None
+    ent = t.get("kernels", {}).get(kernel)
+    return None if ent is None else ent.get("bytes_per_launch")
+
+
+def cpu_baseline(cfg, seed, tokens):
+    """The fp64 oracle, as it stands, on the first `tokens` tokens of the workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from moe_inputs import layer_inputs, variant
+    from oracle import layer_backward, layer_forward, spec_from_config
+    from moe_inputs import to_f64
+
+    scfg = variant(cfg["name"].split("[")[0], T=tokens)
+    inp = layer_inputs(scfg, seed=seed)
+    dt = scfg["dtype"]
+    spec = spec_from_config(scfg)
+    x = to_f64(inp["x"], dt)
+    dy = to_f64(inp["dy"], dt)
+    w_r = inp["w_r"].astype(np.float64)
+    beta = None if inp["router_bias"] is None else inp["router_bias"].astype(np.float64)
+
+    def efn(e):
+        b = scfg["expert_bias"]
+        return (to_f64(inp["w_gate"][e], dt), to_f64(inp["w_up"][e], dt), to_f64(inp["w_down"][e], dt),
+                to_f64(inp["b_gate"][e], dt) if b else None, to_f64(inp["b_up"][e], dt) if b else None,
+                to_f64(inp["b_down"][e], dt) if b else None)
+
+    shared = None
+    if scfg["n_shared"]:
+        shared = tuple(to_f64(inp[n], dt) for n in ("ws_gate", "ws_up", "ws_down"))
+    t0 = time.perf_counter()
+    fwd = layer_forward(spec, x, w_r, beta, efn, shared)
+    layer_backward(spec, x, w_r, beta, efn, fwd, dy, shared, with_bias=scfg["expert_bias"])
+    wall = time.perf_counter() - t0
+    _, fb = layer_flops(scfg)
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    return {"value": round(fb / wall / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "fp64 oracle fwd+bwd of the first %d of %d tokens (same shapes, seed %d), %.1f s wall"
+                      % (tokens, cfg["T"], seed, wall),
+            "tokens_per_s": round(tokens / wall, 1)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen3")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-tokens", type=int, default=2048)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the MoE layer's one-GPU share is the workload "
+              "(no collectives are built); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from moe_inputs import config, layer_inputs
+    from paper_2605_31463_amd import _lib as L
+    from paper_2605_31463_amd.layer import MoELayer
+
+    cfg = config(args.workload)
+    dt = cfg["dtype"]
+    torch.cuda.set_device(0)
+    inp = layer_inputs(cfg, seed=args.seed)
+
+    def dev(a):
+        import numpy as np
+        if a is None:
+            return None
+        if dt == "bf16" and a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(a).cuda()
+
+    params = {n: dev(inp.get(n)) for n in ("w_r", "router_bias", "w_gate", "w_up", "w_down", "b_gate",
+                                           "b_up", "b_down", "ws_gate", "ws_up", "ws_down")}
+    x = dev(inp["x"])
+    dy = dev(inp["dy"])
+    del inp
+    layer = MoELayer(L.shape_from_config(cfg))
+    grads = layer.alloc_grads()
+    stream = torch.cuda.current_stream()
+
+    def step():
+        layer.forward(params, x)
+        layer.backward(params, x, dy, grads)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # per-kernel times over a few untimed steps, to pick the dominant kernel
+    work = kernel_work(cfg)
+    per_kernel = {}
+    for name in work:
+        L.moe_timing_select(L.kernel_id(name))
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
+        ms, n = L.moe_timing_read()
+        per_kernel[name] = ms / max(n, 1)
+    L.moe_timing_select(-1)
+    dominant = max(per_kernel, key=lambda n: per_kernel[n])
+
+    # timed region: exactly K steps, the dominant kernel's launches timed with events
+    L.moe_timing_select(L.kernel_id(dominant))
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dom_ms, dom_n = L.moe_timing_read()
+    L.moe_timing_select(-1)
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+
+    _, fb = layer_flops(cfg)
+    tflops = fb / (ms_per_step / 1e3) / 1e12
+    bound, amount = work[dominant]
+    dom_avg_s = dom_ms / max(dom_n, 1) / 1e3
+    if bound == "mfma":
+        achieved = amount / dom_avg_s / 1e12
+        peak, unit = PEAK_BF16_TFLOPS, "TFLOP/s"
+    else:
+        achieved = amount / dom_avg_s / 1e9
+        peak, unit = PEAK_HBM_GBS, "GB/s"
+    workload = "%s moe layer T=%d d=%d E=%d k=%d f=%d" % (cfg["name"], cfg["T"], cfg["d"], cfg["E"],
+                                                         cfg["k"], cfg["f"])
+    kernels = {}
+    for name, ms in per_kernel.items():
+        b, amt = work[name]
+        rate = amt / (ms / 1e3) / (1e12 if b == "mfma" else 1e9)
+        kernels[name] = {"avg_us": round(ms * 1e3, 2), "bound": b,
+                         "achieved": round(rate, 1), "unit": "TFLOP/s" if b == "mfma" else "GB/s",
+                         "frac": round(rate / (PEAK_BF16_TFLOPS if b == "mfma" else PEAK_HBM_GBS), 4)}
+    out = {
+        "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dt,
+        "data": "synthetic (seeded; shapes and distributions of the workload)",
+        "config": {"workload": workload, "T": cfg["T"], "d": cfg["d"], "E": cfg["E"], "k": cfg["k"],
+                   "f": cfg["f"], "router": cfg["router"]},
+        "tokens_per_s": round(cfg["T"] / (ms_per_step / 1e3), 1),
+        "wall_s_timed": round(wall, 4),
+        "roofline": {"bound": bound, "kernel": dominant, "achieved": round(achieved, 2), "peak": peak,
+                     "unit": unit, "frac": round(achieved / peak, 4),
+                     "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": dom_n,
+                     "traffic": traffic_for(dominant, workload)},
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, args.seed, args.cpu_tokens)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

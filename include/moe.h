@@ -1,0 +1,292 @@
+/*
+ * moe.h -- C ABI of libmoe: one Mixture-of-Experts layer, forward and
+ * backward, on one AMD Instinct MI355X (gfx950).
+ *
+ * The layer is the one the PithTrain paper (arxiv 2605.31463) trains:
+ * a router that picks the top-k experts of every token (section 3.2 and
+ * appendix B.3 name the framework's top-k routing kernel), a scatter of the
+ * tokens into expert-contiguous rows (section 3.2, "fused ... EP token
+ * scatter"), SwiGLU experts with fused forward and backward activation
+ * (section 3.2, "fused SwiGLU forward and backward kernels"), a
+ * gating-weighted combine, and the backward split into data-gradient and
+ * weight-gradient passes so that the weight gradients can be delayed
+ * (section 3.2, "wgrad delay").  Routing outputs obey the paper's
+ * routing-trace rules (appendix B.2.2): expert ids in [0, E), gating
+ * weights non-negative and summing to one over the top-k (route_scale for
+ * the DeepSeek-style router).
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller; the
+ *     library never allocates, frees or synchronises.  Every call only
+ *     enqueues work on `stream` and returns; results are ready when the
+ *     stream reaches that point.  Pointers must be 16-byte aligned.
+ *   - Layouts are dense row-major.  T tokens, d hidden, E routed experts,
+ *     k experts per token, f expert width, R = T*k routed rows.
+ *       x, y, dy, dx            [T][d]        activation dtype
+ *       w_r, dw_r               [d][E]        float32
+ *       router_bias             [E]           float32
+ *       w_gate, w_up            [E][d][f]     activation dtype
+ *       w_down                  [E][f][d]     activation dtype
+ *       b_gate, b_up            [E][f];  b_down [E][d]
+ *       topk_idx, row_of        [T][k]        int32
+ *       topk_w, s_sel, d_topk_w [T][k]        float32
+ *       expert_offsets          [E+1]         int32 (exclusive scan of counts)
+ *       token_of                [R]           int32 (= t*k + slot)
+ *       x_perm, o, d_o, dx_perm [R][d]        activation dtype
+ *       gu, dgu                 [R][2f]       columns [0,f) gate, [f,2f) up
+ *       h                       [R][f]
+ *     The activation dtype is moe_shape.dtype: MOE_F32 or MOE_BF16.  With
+ *     MOE_BF16, products accumulate in float32 and every stored value is
+ *     rounded to nearest-even.
+ *   - Slot order: topk_idx[t][0..k-1] lists the chosen experts by
+ *     descending selection key, equal keys to the lower expert index.
+ *     Rows of expert e are expert_offsets[e] .. expert_offsets[e+1]-1, in
+ *     ascending token order; row_of[t][s] is the row of (t, s).
+ *   - Results are bitwise reproducible run to run: no floating-point atomics.
+ *   - Gradients overwrite their outputs (no accumulation).
+ *   - Return value: MOE_OK or a negative MOE_ERR_* code.  Argument checks run
+ *     on the host before anything is enqueued; on error nothing is enqueued
+ *     and moe_last_error() gives a message (thread-local).
+ *   - T = 0 is valid: token outputs are empty, counts/offsets and gradients
+ *     are written as zeros.
+ *
+ * Limits (MOE_ERR_UNSUPPORTED beyond them): 1 <= E <= 256, 1 <= k <= 16,
+ * d and f multiples of 64, d <= 16384, renorm = 1.
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = -1, /* null pointer, non-positive size, k > E, bad groups */
+  MOE_ERR_UNSUPPORTED = -2, /* valid but outside the limits above */
+  MOE_ERR_HIP = -3,         /* a kernel launch failed (hipGetLastError) */
+  MOE_ERR_WORKSPACE = -4    /* workspace pointer null or ws_bytes too small */
+};
+
+/* Router families.
+ * SOFTMAX_TOPK: softmax over all E logits, keep the k largest, renormalise
+ *   over the k (the Qwen3-30B-A3B router); equal to a softmax over the k
+ *   selected logits.
+ * TOPK_SOFTMAX: keep the k largest logits, softmax over those (GPT-OSS).
+ * SIGMOID_GROUPED: s = sigmoid(logit); selection key s + router_bias; the E
+ *   experts form n_groups contiguous groups, a group scores the sum of its two
+ *   largest keys, the topk_groups best groups are kept and the top-k keys
+ *   among their experts selected; weight = route_scale * s / sum of the
+ *   selected s (DeepSeek-V3). */
+enum { MOE_ROUTER_SOFTMAX_TOPK = 0, MOE_ROUTER_TOPK_SOFTMAX = 1, MOE_ROUTER_SIGMOID_GROUPED = 2 };
+
+/* Router bias: none; added to the selection key only; added to the logits
+ * (selection and weights).  The bias never receives a gradient. */
+enum { MOE_BIAS_NONE = 0, MOE_BIAS_SELECT_ONLY = 1, MOE_BIAS_LOGIT = 2 };
+
+enum { MOE_F32 = 0, MOE_BF16 = 1 };
+
+/* passes of moe_grouped_gemm_bwd (bit mask) */
+enum { MOE_DGRAD = 1, MOE_WGRAD = 2 };
+
+typedef struct moe_shape {
+  int64_t T, d, E, k, f;       /* tokens, hidden, routed experts, top-k, expert width */
+  int32_t n_groups;            /* expert groups for SIGMOID_GROUPED (1 = none) */
+  int32_t topk_groups;         /* groups kept (= n_groups when not grouped) */
+  int32_t n_shared;            /* 0 or 1 always-on shared expert of weight 1 */
+  int64_t f_shared;            /* its width */
+  int32_t router;              /* MOE_ROUTER_* */
+  int32_t renorm;              /* must be 1: weights renormalised over the top-k */
+  float route_scale;           /* factor on the renormalised weights (1, or 2.5) */
+  int32_t bias_mode;           /* MOE_BIAS_* */
+  int32_t expert_bias;         /* 1: experts carry b_gate, b_up, b_down */
+  int32_t dtype;               /* MOE_F32 or MOE_BF16 activation / expert dtype */
+} moe_shape;
+
+/* Parameters of the layer (device pointers; unused ones may be NULL). */
+typedef struct moe_params {
+  const float* w_r;            /* [d][E] */
+  const float* router_bias;    /* [E], bias_mode != NONE */
+  const void* w_gate;          /* [E][d][f] */
+  const void* w_up;            /* [E][d][f] */
+  const void* w_down;          /* [E][f][d] */
+  const void* b_gate;          /* [E][f], expert_bias */
+  const void* b_up;            /* [E][f], expert_bias */
+  const void* b_down;          /* [E][d], expert_bias */
+  const void* ws_gate;         /* [d][f_shared], n_shared */
+  const void* ws_up;           /* [d][f_shared], n_shared */
+  const void* ws_down;         /* [f_shared][d], n_shared */
+} moe_params;
+
+/* Tensors the forward writes and the backward reads (caller-allocated). */
+typedef struct moe_saved {
+  int32_t* topk_idx;           /* [T][k] */
+  float* topk_w;               /* [T][k] */
+  float* s_sel;                /* [T][k], SIGMOID_GROUPED only (else may be NULL) */
+  int32_t* expert_offsets;     /* [E+1] */
+  int32_t* row_of;             /* [T][k] */
+  int32_t* token_of;           /* [R] */
+  void* x_perm;                /* [R][d] */
+  void* gu;                    /* [R][2f] */
+  void* h;                     /* [R][f] */
+  void* o;                     /* [R][d] */
+  void* gu_sh;                 /* [T][2 f_shared], n_shared */
+  void* h_sh;                  /* [T][f_shared], n_shared */
+  void* o_sh;                  /* [T][d], n_shared */
+} moe_saved;
+
+/* Gradients of the parameters (overwritten). */
+typedef struct moe_grads {
+  float* dw_r;                 /* [d][E] float32 */
+  void* dw_gate;               /* [E][d][f] */
+  void* dw_up;                 /* [E][d][f] */
+  void* dw_down;               /* [E][f][d] */
+  void* db_gate;               /* [E][f], expert_bias */
+  void* db_up;                 /* [E][f], expert_bias */
+  void* db_down;               /* [E][d], expert_bias */
+  void* dws_gate;              /* [d][f_shared], n_shared */
+  void* dws_up;                /* [d][f_shared], n_shared */
+  void* dws_down;              /* [f_shared][d], n_shared */
+} moe_grads;
+
+/* Workspace bytes.  fwd_ws: enough for moe_route, moe_permute and
+ * moe_layer_fwd; bwd_ws: enough for moe_route_bwd, moe_grouped_gemm_bwd,
+ * moe_shared_expert_bwd and moe_layer_bwd (which keeps d_o, dgu, dx_perm
+ * and the router gradient scratch there); saved_bytes: total size of the
+ * moe_saved tensors, for information.  Pure host arithmetic. */
+int moe_workspace_size(const moe_shape* shape, size_t* fwd_ws, size_t* saved_bytes, size_t* bwd_ws);
+
+/* Router forward (one fused kernel: logits x W_r (+ bias), selection,
+ * weights, per-block expert histogram; then the counts).
+ * Logits are accumulated with float32 partial sums of 16 products folded
+ * into a float64 total, and selection compares float64 keys.
+ * out: topk_idx, topk_w [T][k]; s_sel [T][k] (SIGMOID_GROUPED, else may be
+ * NULL); expert_counts [E] int32 (may be NULL).  ws: fwd_ws bytes. */
+int moe_route(const moe_shape* shape, const void* x, const float* w_r, const float* router_bias,
+              int32_t* topk_idx, float* topk_w, float* s_sel, int32_t* expert_counts,
+              void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Token-to-expert permutation (section 3.2, EP token scatter, on one GPU):
+ * per-block expert histogram, exclusive scan, then an atomic-free stable
+ * scatter of x rows into expert-contiguous rows.
+ * out: expert_offsets [E+1], row_of [T][k], token_of [R], x_perm [R][d].
+ * Every topk_idx entry must lie in [0, E) and a token must not repeat an
+ * expert (as moe_route produces); other values are undefined behaviour. */
+int moe_permute(const moe_shape* shape, const void* x, const int32_t* topk_idx,
+                int32_t* expert_offsets, int32_t* row_of, int32_t* token_of, void* x_perm,
+                void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Grouped SwiGLU expert forward (section 3.2, fused SwiGLU forward):
+ *   [g|u] = x_perm_e [W_gate,e | W_up,e] (+ b_gate,e | b_up,e),
+ *   h = silu(g) * u  (from the float32 accumulators),
+ *   o = h W_down,e (+ b_down,e),
+ * for every expert e over its rows expert_offsets[e] .. expert_offsets[e+1]-1,
+ * scheduled on the device from expert_offsets (no host synchronisation).
+ * b_* may be NULL when shape->expert_bias is 0.  out: gu, h, o. */
+int moe_grouped_gemm_fwd(const moe_shape* shape, const void* x_perm, const int32_t* expert_offsets,
+                         const void* w_gate, const void* w_up, const void* w_down,
+                         const void* b_gate, const void* b_up, const void* b_down,
+                         void* gu, void* h, void* o, hipStream_t stream);
+
+/* Grouped expert backward, as one or both passes (section 3.2, wgrad delay):
+ *  MOE_DGRAD: dh = d_o W_down^T with the fused SwiGLU backward
+ *             dg = dh * u * sig(g) * (1 + g (1 - sig(g))), du = dh * silu(g)
+ *             (g, u read from gu) -> dgu; then dx_perm = [dg|du] [W_gate|W_up]^T.
+ *  MOE_WGRAD: dW_down = h^T d_o, dW_gate = x_perm^T dg, dW_up = x_perm^T du
+ *             per expert, and with expert_bias the column sums db_down, db_gate,
+ *             db_up.  Reads dgu, so it runs after a DGRAD pass.
+ * Pointers of a pass that is not requested may be NULL. */
+int moe_grouped_gemm_bwd(const moe_shape* shape, int32_t passes,
+                         const void* x_perm, const int32_t* expert_offsets,
+                         const void* gu, const void* h, const void* d_o,
+                         const void* w_gate, const void* w_up, const void* w_down,
+                         void* dgu, void* dx_perm,
+                         void* dw_gate, void* dw_up, void* dw_down,
+                         void* db_gate, void* db_up, void* db_down, hipStream_t stream);
+
+/* Weighted combine (gather, fixed slot order, float32 sum):
+ *   y_t = sum_s topk_w[t][s] * o[row_of[t][s]]  (+ shared_o[t] if non-NULL). */
+int moe_combine_fwd(const moe_shape* shape, const void* o, const float* topk_w,
+                    const int32_t* row_of, const void* shared_o, void* y, hipStream_t stream);
+
+/* Combine backward:
+ *   d_o[row_of[t][s]] = topk_w[t][s] * dy_t,
+ *   d_topk_w[t][s]    = <dy_t, o[row_of[t][s]]>  (float32). */
+int moe_combine_bwd(const moe_shape* shape, const void* dy, const void* o, const float* topk_w,
+                    const int32_t* row_of, void* d_o, float* d_topk_w, hipStream_t stream);
+
+/* Router backward.  dl on the selected experts only:
+ *   softmax families: dl_j = w_j (omega_j - sum_i w_i omega_i / route_scale)
+ *   SIGMOID_GROUPED:  dl_j = (route_scale omega_j - sum_i w_i omega_i) / sum_i s_i
+ *                            * s_j (1 - s_j)
+ * with omega = d_topk_w; then dw_r[:, e] = sum over the rows of expert e of
+ * x[token] * dl (using expert_offsets and token_of from moe_permute, in row
+ * order), and dx_router[t] = sum_s dl[t][s] * W_r[:, topk_idx[t][s]] (float32,
+ * may be NULL to skip).  ws: bwd_ws bytes. */
+int moe_route_bwd(const moe_shape* shape, const void* x, const float* w_r,
+                  const int32_t* topk_idx, const float* topk_w, const float* s_sel,
+                  const float* d_topk_w, const int32_t* expert_offsets, const int32_t* token_of,
+                  float* dw_r, float* dx_router, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Unpermute-reduce: dx_t = sum_s dx_perm[row_of[t][s]] (slot order)
+ *   + dx_router[t] (float32, may be NULL) + dx_shared[t] (may be NULL). */
+int moe_unpermute_bwd(const moe_shape* shape, const void* dx_perm, const int32_t* row_of,
+                      const float* dx_router, const void* dx_shared, void* dx, hipStream_t stream);
+
+/* Always-on shared expert (DeepSeek-V3 style, weight 1), forward:
+ *   [g|u] = x [Ws_gate | Ws_up], h = silu(g) * u, o_sh = h Ws_down.
+ * out: gu_sh [T][2 f_shared], h_sh [T][f_shared], o_sh [T][d]. */
+int moe_shared_expert_fwd(const moe_shape* shape, const void* x,
+                          const void* ws_gate, const void* ws_up, const void* ws_down,
+                          void* gu_sh, void* h_sh, void* o_sh, hipStream_t stream);
+
+/* Shared expert backward with upstream gradient dy (its weight is 1):
+ * dWs_down = h_sh^T dy, SwiGLU backward into dgu_sh (kept in ws),
+ * dWs_gate, dWs_up, and dx_shared = dgu_sh [Ws_gate|Ws_up]^T.
+ * ws: bwd_ws bytes. */
+int moe_shared_expert_bwd(const moe_shape* shape, const void* x, const void* dy,
+                          const void* gu_sh, const void* h_sh,
+                          const void* ws_gate, const void* ws_up, const void* ws_down,
+                          void* dx_shared, void* dws_gate, void* dws_up, void* dws_down,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Whole layer forward: route, permute, grouped SwiGLU experts, shared expert,
+ * combine.  Fills every pointer of *saved (s_sel only for SIGMOID_GROUPED,
+ * the *_sh tensors only with a shared expert) and y.  ws: fwd_ws bytes. */
+int moe_layer_fwd(const moe_shape* shape, const moe_params* params, const void* x,
+                  const moe_saved* saved, void* y, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Whole layer backward of L = sum_t <dy_t, y_t>: combine backward, expert
+ * dgrad and wgrad, router backward, shared expert backward, unpermute.
+ * dx includes the expert, router and shared-expert paths.  ws: bwd_ws bytes. */
+int moe_layer_bwd(const moe_shape* shape, const moe_params* params, const void* x,
+                  const moe_saved* saved, const void* dy, void* dx, const moe_grads* grads,
+                  void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Status code -> static string. */
+const char* moe_status_string(int status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* moe_last_error(void);
+
+/* Kernel timing for benchmarks.  Kernels are numbered 0 .. moe_kernel_count()-1
+ * and named by moe_kernel_name().  moe_timing_select(id) makes every later
+ * launch of kernel id (in any entry point, on the calling thread) record a
+ * pair of HIP events on its stream; id < 0 switches it off and drops the
+ * records.  moe_timing_read() waits for the recorded events and returns the
+ * summed milliseconds and the number of timed launches.  Up to 4096 launches
+ * are kept.  Not for concurrent use from several threads. */
+int moe_kernel_count(void);
+const char* moe_kernel_name(int id);
+int moe_timing_select(int id);
+int moe_timing_read(double* total_ms, int* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H */

@@ -16,4 +16,7 @@ from .moe_oracle import (  # noqa: F401
     layer_forward,
     layer_backward,
     router_backward,
+    combine,
+    combine_backward,
+    unpermute,
 )

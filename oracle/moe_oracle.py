@@ -130,8 +130,9 @@ def route(spec, logits, beta=None):
         return dict(topk_idx=idx, topk_w=w, s_sel=None, keys=keys, margin=margin)
 
     if spec.router == "sigmoid_grouped":
-        s = sigmoid(l)
-        keys = s + b if b is not None else s.copy()
+        lb = l + b if spec.bias_mode == "logit" else l          # biased logits
+        s = sigmoid(lb)
+        keys = s + b if spec.bias_mode == "select" else s.copy()
         G = spec.n_groups
         if E % G:
             raise ValueError("E must be a multiple of n_groups")
@@ -271,6 +272,42 @@ def router_backward(spec, rt, omega):
 
 
 # ----------------------------------------------------------------------------
+# Combine and unpermute
+# ----------------------------------------------------------------------------
+
+def combine(o, topk_w, row_of, shared_o=None):
+    """y_t = sum_s w[t][s] * o[row_of[t][s]] (+ shared_o[t])."""
+    T, k = topk_w.shape
+    y = np.zeros((T, o.shape[1]))
+    for s in range(k):
+        y += topk_w[:, s:s + 1] * o[row_of[:, s]]
+    if shared_o is not None:
+        y = y + shared_o
+    return y
+
+
+def combine_backward(dy, o, topk_w, row_of):
+    """d_o[row_of[t][s]] = w[t][s] dy_t and omega[t][s] = <dy_t, o[row_of[t][s]]>."""
+    T, k = topk_w.shape
+    omega = np.zeros((T, k))
+    do = np.zeros_like(o, dtype=np.float64)
+    for s in range(k):
+        rows = row_of[:, s]
+        omega[:, s] = (dy * o[rows]).sum(axis=1)
+        do[rows] = topk_w[:, s:s + 1] * dy
+    return do, omega
+
+
+def unpermute(dx_perm, row_of):
+    """dx_t = sum_s dx_perm[row_of[t][s]]."""
+    T, k = row_of.shape
+    dx = np.zeros((T, dx_perm.shape[1]))
+    for s in range(k):
+        dx += dx_perm[row_of[:, s]]
+    return dx
+
+
+# ----------------------------------------------------------------------------
 # Whole layer
 # ----------------------------------------------------------------------------
 
@@ -302,15 +339,11 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None):
         gs[e], us[e], hs[e] = g, u, h
         o[r0:r1] = oe
         fwidth = wg.shape[1]
-    # combine: y_t = sum_s w[t][s] * o[row_of[t][s]]
-    y = np.zeros((T, d))
-    for s in range(k):
-        y += rt["topk_w"][:, s:s + 1] * o[mp["row_of"][:, s]]
     sh = None
     if shared is not None:
         g, u, h, osh = expert_forward(x, *shared)
-        y = y + osh
         sh = dict(g=g, u=u, h=h, o=osh)
+    y = combine(o, rt["topk_w"], mp["row_of"], None if sh is None else sh["o"])
     return dict(logits=l, route=rt, maps=mp, x_perm=x_perm, o=o, g=gs, u=us,
                 h=hs, y=y, shared=sh, f=fwidth)
 
@@ -328,13 +361,7 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
     rt, mp = fwd["route"], fwd["maps"]
     w = rt["topk_w"]
     o = fwd["o"]
-    # combine backward
-    omega = np.zeros((T, k))
-    do = np.zeros_like(o)
-    for s in range(k):
-        rows = mp["row_of"][:, s]
-        omega[:, s] = (dy * o[rows]).sum(axis=1)
-        do[rows] = w[:, s:s + 1] * dy
+    do, omega = combine_backward(dy, o, w, mp["row_of"])
     # experts
     dx = np.zeros((T, d))
     dx_perm = np.zeros((T * k, d))
@@ -355,9 +382,7 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
         ge.pop("dg")
         ge.pop("du")
         grads[e] = ge
-    # unpermute: dx_t += sum_s dx_perm[row_of[t][s]]
-    for s in range(k):
-        dx += dx_perm[mp["row_of"][:, s]]
+    dx += unpermute(dx_perm, mp["row_of"])
     # router
     dl = router_backward(spec, rt, omega)
     dl_dense = np.zeros((T, E))

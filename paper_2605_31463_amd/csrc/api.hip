@@ -1,0 +1,840 @@
+// libmoe C ABI: argument checks, workspace planning, the component entry
+// points and the fused layer forward / backward.  Everything here runs on the
+// host and only enqueues kernels on the caller's stream.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <vector>
+
+#include "common.h"
+#include "kernels.h"
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+static thread_local char g_err[512];
+
+int moe_set_error(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+namespace moe {
+
+int check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return moe_set_error(MOE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return MOE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// kernel timing (benchmarks)
+// ---------------------------------------------------------------------------
+namespace {
+struct Timing {
+  int sel = -1;
+  std::vector<hipEvent_t> ev;  // start, stop pairs
+  int used = 0;
+  bool open = false;
+};
+thread_local Timing g_timing;
+constexpr int kMaxTimed = 4096;
+}  // namespace
+
+void timing_before(int id, hipStream_t s) {
+  Timing& t = g_timing;
+  t.open = false;
+  if (t.sel != id || t.used >= kMaxTimed) return;
+  if ((int)t.ev.size() < 2 * (t.used + 1)) {
+    hipEvent_t a, b;
+    if (hipEventCreate(&a) != hipSuccess) return;
+    if (hipEventCreate(&b) != hipSuccess) {
+      (void)hipEventDestroy(a);
+      return;
+    }
+    t.ev.push_back(a);
+    t.ev.push_back(b);
+  }
+  if (hipEventRecord(t.ev[2 * t.used], s) == hipSuccess) t.open = true;
+}
+
+void timing_after(int id, hipStream_t s) {
+  Timing& t = g_timing;
+  if (!t.open || t.sel != id) return;
+  t.open = false;
+  if (hipEventRecord(t.ev[2 * t.used + 1], s) == hipSuccess) ++t.used;
+}
+
+const char* kernel_name(int id) {
+  static const char* names[K_NUM_KERNELS] = {
+      "route", "count_zero", "hist", "scan", "scatter", "gemm_gateup_fwd", "gemm_down_fwd",
+      "combine_fwd", "combine_bwd", "route_dl", "route_dwr_partial", "route_dwr_reduce",
+      "wr_transpose", "route_dx", "gemm_down_dgrad", "gemm_gateup_dgrad", "gemm_down_wgrad",
+      "gemm_gateup_wgrad", "unpermute"};
+  if (id < 0 || id >= K_NUM_KERNELS) return nullptr;
+  return names[id];
+}
+
+// ---------------------------------------------------------------------------
+// shape checks and workspace plan
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int check_shape(const moe_shape* sh) {
+  if (!sh) return moe_set_error(MOE_ERR_INVALID_ARG, "shape is NULL");
+  const moe_shape& s = *sh;
+  if (s.T < 0 || s.d <= 0 || s.E <= 0 || s.k <= 0 || s.f <= 0)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "sizes must be positive (T >= 0): T=%lld d=%lld E=%lld k=%lld f=%lld",
+                         (long long)s.T, (long long)s.d, (long long)s.E, (long long)s.k, (long long)s.f);
+  if (s.k > s.E) return moe_set_error(MOE_ERR_INVALID_ARG, "k=%lld exceeds E=%lld", (long long)s.k, (long long)s.E);
+  if (s.router < MOE_ROUTER_SOFTMAX_TOPK || s.router > MOE_ROUTER_SIGMOID_GROUPED)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "unknown router %d", s.router);
+  if (s.bias_mode < MOE_BIAS_NONE || s.bias_mode > MOE_BIAS_LOGIT)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "unknown bias_mode %d", s.bias_mode);
+  if (s.dtype != MOE_F32 && s.dtype != MOE_BF16)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "unknown dtype %d", s.dtype);
+  if (s.n_groups < 1 || s.topk_groups < 1 || s.topk_groups > s.n_groups)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "bad groups: n_groups=%d topk_groups=%d", s.n_groups, s.topk_groups);
+  if (s.E % s.n_groups)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "E=%lld not a multiple of n_groups=%d", (long long)s.E, s.n_groups);
+  if (s.k > (s.E / s.n_groups) * s.topk_groups)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "k=%lld exceeds the experts of the kept groups", (long long)s.k);
+  if (s.n_groups > 1 && s.router != MOE_ROUTER_SIGMOID_GROUPED)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "group-limited routing needs the sigmoid grouped router");
+  if (!(s.route_scale > 0.f) || !isfinite(s.route_scale))
+    return moe_set_error(MOE_ERR_INVALID_ARG, "route_scale must be positive and finite");
+  if (s.n_shared < 0 || s.n_shared > 1)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "n_shared must be 0 or 1");
+  if (s.n_shared && s.f_shared <= 0)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "f_shared must be positive with a shared expert");
+  if (s.renorm != 1) return moe_set_error(MOE_ERR_UNSUPPORTED, "only renormalised top-k weights (renorm=1)");
+  if (s.E > 256) return moe_set_error(MOE_ERR_UNSUPPORTED, "E=%lld above 256", (long long)s.E);
+  if (s.k > 16) return moe_set_error(MOE_ERR_UNSUPPORTED, "k=%lld above 16", (long long)s.k);
+  if (s.d % 64 || s.f % 64 || (s.n_shared && s.f_shared % 64))
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "d, f and f_shared must be multiples of 64");
+  if (s.d > 16384) return moe_set_error(MOE_ERR_UNSUPPORTED, "d above 16384");
+  if (s.T * s.k >= (int64_t)1 << 31 || s.T * s.d >= (int64_t)1 << 40)
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "T too large");
+  if (s.router == MOE_ROUTER_SIGMOID_GROUPED && s.n_groups > 1) {
+    const int64_t epl = (s.E + 63) / 64, gs = s.E / s.n_groups;
+    const int64_t lpg = gs / epl;
+    if (gs % epl || lpg < 1 || (lpg & (lpg - 1)))
+      return moe_set_error(MOE_ERR_UNSUPPORTED, "group size %lld does not map onto whole power-of-two lane sets",
+                           (long long)gs);
+  }
+  return MOE_OK;
+}
+
+inline size_t act_bytes(const moe_shape& s) { return s.dtype == MOE_BF16 ? 2 : 4; }
+
+struct Plan {
+  // forward
+  size_t hist;
+  size_t fwd_total;
+  // backward
+  size_t d_o, dgu, dx_perm, dl, partial, w_rt, dgu_sh, dx_sh;
+  size_t bwd_total;
+  size_t saved_total;
+};
+
+Plan plan(const moe_shape& s) {
+  Plan p{};
+  const size_t eb = act_bytes(s);
+  const int64_t R = s.T * s.k;
+  size_t off = 0;
+  p.hist = off;
+  off += align_up((size_t)moe::perm_blocks(s.T) * s.E * 4);
+  p.fwd_total = off;
+  off = 0;
+  p.d_o = off; off += align_up((size_t)R * s.d * eb);
+  p.dgu = off; off += align_up((size_t)R * 2 * s.f * eb);
+  p.dx_perm = off; off += align_up((size_t)R * s.d * eb);
+  p.dl = off; off += align_up((size_t)R * 4);
+  p.partial = off; off += align_up((size_t)moe::route_dwr_tasks(R, s.E) * s.d * 4);
+  p.w_rt = off; off += align_up((size_t)s.E * s.d * 4);
+  p.dgu_sh = off; off += s.n_shared ? align_up((size_t)s.T * 2 * s.f_shared * eb) : 0;
+  p.dx_sh = off; off += s.n_shared ? align_up((size_t)s.T * s.d * eb) : 0;
+  p.bwd_total = off;
+  size_t sv = 0;
+  sv += (size_t)R * (4 + 4 + 4 + 4 + 4);  // topk_idx, topk_w, s_sel, row_of, token_of
+  sv += (size_t)(s.E + 1) * 4;
+  sv += (size_t)R * (s.d + 2 * s.f + s.f + s.d) * eb;
+  if (s.n_shared) sv += (size_t)s.T * (2 * s.f_shared + s.f_shared + s.d) * eb;
+  p.saved_total = sv;
+  return p;
+}
+
+inline char* wsp(void* ws, size_t off) { return static_cast<char*>(ws) + off; }
+
+int check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return MOE_OK;
+  if (!ws) return moe_set_error(MOE_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (have < need) return moe_set_error(MOE_ERR_WORKSPACE, "workspace %zu bytes, %zu needed", have, need);
+  return MOE_OK;
+}
+
+#define MOE_NEED(p, name)                                                        \
+  do {                                                                           \
+    if (!(p)) return moe_set_error(MOE_ERR_INVALID_ARG, "%s is NULL", name);     \
+  } while (0)
+
+#define MOE_TRY(expr)      \
+  do {                     \
+    int st_ = (expr);      \
+    if (st_) return st_;   \
+  } while (0)
+
+GemmArgs gemm_base(const moe_shape& s, int mode, const int32_t* offsets) {
+  GemmArgs g{};
+  g.mode = mode;
+  g.bf16 = s.dtype == MOE_BF16;
+  g.offsets = offsets;
+  g.ngroups = (int)s.E;
+  g.dense_rows = 0;
+  g.max_rows = s.T * s.k;
+  g.d = (int)s.d;
+  g.f = (int)s.f;
+  return g;
+}
+
+GemmArgs gemm_dense(const moe_shape& s, int mode) {
+  GemmArgs g = gemm_base(s, mode, nullptr);
+  g.ngroups = 1;
+  g.dense_rows = s.T;
+  g.max_rows = s.T;
+  g.f = (int)s.f_shared;
+  return g;
+}
+
+int do_route(const moe_shape& s, const void* x, const float* w_r, const float* bias, int32_t* topk_idx,
+             float* topk_w, float* s_sel, int32_t* counts, hipStream_t st) {
+  RouteArgs a{};
+  a.x = x;
+  a.w_r = w_r;
+  a.bias = bias;
+  a.T = s.T;
+  a.d = (int)s.d;
+  a.E = (int)s.E;
+  a.k = (int)s.k;
+  a.router = s.router;
+  a.bias_mode = s.bias_mode;
+  a.n_groups = s.n_groups;
+  a.topk_groups = s.topk_groups;
+  a.route_scale = s.route_scale;
+  a.bf16 = s.dtype == MOE_BF16;
+  a.topk_idx = topk_idx;
+  a.topk_w = topk_w;
+  a.s_sel = s_sel;
+  a.counts = counts;
+  return launch_route(a, st);
+}
+
+int do_permute(const moe_shape& s, const void* x, const int32_t* topk_idx, int32_t* offsets, int32_t* row_of,
+               int32_t* token_of, void* x_perm, void* ws, hipStream_t st) {
+  PermArgs a{};
+  a.x = x;
+  a.topk_idx = topk_idx;
+  a.T = s.T;
+  a.d = (int)s.d;
+  a.E = (int)s.E;
+  a.k = (int)s.k;
+  a.bf16 = s.dtype == MOE_BF16;
+  a.hist = reinterpret_cast<int32_t*>(wsp(ws, plan(s).hist));
+  a.offsets = offsets;
+  a.row_of = row_of;
+  a.token_of = token_of;
+  a.x_perm = x_perm;
+  return launch_permute(a, st);
+}
+
+int do_gemm_fwd(const moe_shape& s, const void* x_perm, const int32_t* offsets, const void* w_gate, const void* w_up,
+                const void* w_down, const void* b_gate, const void* b_up, const void* b_down, void* gu, void* h,
+                void* o, hipStream_t st) {
+  GemmArgs g = gemm_base(s, G_FWD_GATEUP, offsets);
+  g.a = x_perm;
+  g.w0 = w_gate;
+  g.w1 = w_up;
+  g.bias0 = b_gate;
+  g.bias1 = b_up;
+  g.c0 = gu;
+  g.c1 = h;
+  MOE_TRY(launch_gemm(g, st));
+  g = gemm_base(s, G_FWD_DOWN, offsets);
+  g.a = h;
+  g.w0 = w_down;
+  g.bias0 = b_down;
+  g.c0 = o;
+  return launch_gemm(g, st);
+}
+
+int do_gemm_bwd(const moe_shape& s, int passes, const void* x_perm, const int32_t* offsets, const void* gu,
+                const void* h, const void* d_o, const void* w_gate, const void* w_up, const void* w_down, void* dgu,
+                void* dx_perm, void* dw_gate, void* dw_up, void* dw_down, void* db_gate, void* db_up, void* db_down,
+                hipStream_t st) {
+  if (passes & MOE_DGRAD) {
+    GemmArgs g = gemm_base(s, G_DGRAD_DOWN, offsets);
+    g.a = d_o;
+    g.w0 = w_down;
+    g.aux = gu;
+    g.c0 = dgu;
+    MOE_TRY(launch_gemm(g, st));
+    g = gemm_base(s, G_DGRAD_GATEUP, offsets);
+    g.a = dgu;
+    g.w0 = w_gate;
+    g.w1 = w_up;
+    g.c0 = dx_perm;
+    MOE_TRY(launch_gemm(g, st));
+  }
+  if (passes & MOE_WGRAD) {
+    GemmArgs g = gemm_base(s, G_WGRAD_DOWN, offsets);
+    g.a = h;
+    g.b = d_o;
+    g.c0 = dw_down;
+    g.db0 = db_down;
+    MOE_TRY(launch_gemm(g, st));
+    g = gemm_base(s, G_WGRAD_GATEUP, offsets);
+    g.a = x_perm;
+    g.b = dgu;
+    g.c0 = dw_gate;
+    g.c1 = dw_up;
+    g.db0 = db_gate;
+    g.db1 = db_up;
+    MOE_TRY(launch_gemm(g, st));
+  }
+  return MOE_OK;
+}
+
+int do_shared_fwd(const moe_shape& s, const void* x, const void* wsg, const void* wsu, const void* wsd, void* gu_sh,
+                  void* h_sh, void* o_sh, hipStream_t st) {
+  GemmArgs g = gemm_dense(s, G_FWD_GATEUP);
+  g.a = x;
+  g.w0 = wsg;
+  g.w1 = wsu;
+  g.c0 = gu_sh;
+  g.c1 = h_sh;
+  MOE_TRY(launch_gemm(g, st));
+  g = gemm_dense(s, G_FWD_DOWN);
+  g.a = h_sh;
+  g.w0 = wsd;
+  g.c0 = o_sh;
+  return launch_gemm(g, st);
+}
+
+int do_shared_bwd(const moe_shape& s, const void* x, const void* dy, const void* gu_sh, const void* h_sh,
+                  const void* wsg, const void* wsu, const void* wsd, void* dgu_sh, void* dx_sh, void* dwsg, void* dwsu,
+                  void* dwsd, hipStream_t st) {
+  GemmArgs g = gemm_dense(s, G_DGRAD_DOWN);
+  g.a = dy;
+  g.w0 = wsd;
+  g.aux = gu_sh;
+  g.c0 = dgu_sh;
+  MOE_TRY(launch_gemm(g, st));
+  g = gemm_dense(s, G_DGRAD_GATEUP);
+  g.a = dgu_sh;
+  g.w0 = wsg;
+  g.w1 = wsu;
+  g.c0 = dx_sh;
+  MOE_TRY(launch_gemm(g, st));
+  g = gemm_dense(s, G_WGRAD_DOWN);
+  g.a = h_sh;
+  g.b = dy;
+  g.c0 = dwsd;
+  MOE_TRY(launch_gemm(g, st));
+  g = gemm_dense(s, G_WGRAD_GATEUP);
+  g.a = x;
+  g.b = dgu_sh;
+  g.c0 = dwsg;
+  g.c1 = dwsu;
+  return launch_gemm(g, st);
+}
+
+RouteBwdArgs route_bwd_base(const moe_shape& s) {
+  RouteBwdArgs a{};
+  a.T = s.T;
+  a.d = (int)s.d;
+  a.E = (int)s.E;
+  a.k = (int)s.k;
+  a.router = s.router;
+  a.route_scale = s.route_scale;
+  a.bf16 = s.dtype == MOE_BF16;
+  return a;
+}
+
+}  // namespace
+}  // namespace moe
+
+using namespace moe;
+
+// ---------------------------------------------------------------------------
+// exported entry points
+// ---------------------------------------------------------------------------
+extern "C" {
+
+const char* moe_status_string(int status) {
+  switch (status) {
+    case MOE_OK: return "ok";
+    case MOE_ERR_INVALID_ARG: return "invalid argument";
+    case MOE_ERR_UNSUPPORTED: return "unsupported shape or option";
+    case MOE_ERR_HIP: return "HIP launch failure";
+    case MOE_ERR_WORKSPACE: return "workspace missing or too small";
+  }
+  return "unknown status";
+}
+
+const char* moe_last_error(void) { return g_err; }
+
+int moe_kernel_count(void) { return K_NUM_KERNELS; }
+const char* moe_kernel_name(int id) { return kernel_name(id); }
+
+int moe_timing_select(int id) {
+  g_timing.sel = id;
+  g_timing.used = 0;
+  g_timing.open = false;
+  return MOE_OK;
+}
+
+int moe_timing_read(double* total_ms, int* launches) {
+  double tot = 0.0;
+  for (int i = 0; i < g_timing.used; ++i) {
+    if (hipEventSynchronize(g_timing.ev[2 * i + 1]) != hipSuccess)
+      return moe_set_error(MOE_ERR_HIP, "event synchronize failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, g_timing.ev[2 * i], g_timing.ev[2 * i + 1]) != hipSuccess)
+      return moe_set_error(MOE_ERR_HIP, "event elapsed time failed");
+    tot += ms;
+  }
+  if (total_ms) *total_ms = tot;
+  if (launches) *launches = g_timing.used;
+  return MOE_OK;
+}
+
+int moe_workspace_size(const moe_shape* shape, size_t* fwd_ws, size_t* saved_bytes, size_t* bwd_ws) {
+  MOE_TRY(check_shape(shape));
+  const Plan p = plan(*shape);
+  if (fwd_ws) *fwd_ws = p.fwd_total;
+  if (saved_bytes) *saved_bytes = p.saved_total;
+  if (bwd_ws) *bwd_ws = p.bwd_total;
+  return MOE_OK;
+}
+
+int moe_route(const moe_shape* shape, const void* x, const float* w_r, const float* router_bias, int32_t* topk_idx,
+              float* topk_w, float* s_sel, int32_t* expert_counts, void* ws, size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  if (s.T > 0) {
+    MOE_NEED(x, "x");
+    MOE_NEED(topk_idx, "topk_idx");
+    MOE_NEED(topk_w, "topk_w");
+  }
+  MOE_NEED(w_r, "w_r");
+  if (s.bias_mode != MOE_BIAS_NONE) MOE_NEED(router_bias, "router_bias");
+  if (s.router == MOE_ROUTER_SIGMOID_GROUPED && s.T > 0) MOE_NEED(s_sel, "s_sel");
+  return do_route(s, x, w_r, router_bias, topk_idx, topk_w, s_sel, expert_counts, stream);
+}
+
+int moe_permute(const moe_shape* shape, const void* x, const int32_t* topk_idx, int32_t* expert_offsets,
+                int32_t* row_of, int32_t* token_of, void* x_perm, void* ws, size_t ws_bytes, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  MOE_NEED(expert_offsets, "expert_offsets");
+  if (s.T > 0) {
+    MOE_NEED(x, "x");
+    MOE_NEED(topk_idx, "topk_idx");
+    MOE_NEED(row_of, "row_of");
+    MOE_NEED(token_of, "token_of");
+    MOE_NEED(x_perm, "x_perm");
+  }
+  MOE_TRY(check_ws(ws, ws_bytes, plan(s).fwd_total));
+  return do_permute(s, x, topk_idx, expert_offsets, row_of, token_of, x_perm, ws, stream);
+}
+
+int moe_grouped_gemm_fwd(const moe_shape* shape, const void* x_perm, const int32_t* expert_offsets,
+                         const void* w_gate, const void* w_up, const void* w_down, const void* b_gate,
+                         const void* b_up, const void* b_down, void* gu, void* h, void* o, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  MOE_NEED(expert_offsets, "expert_offsets");
+  MOE_NEED(w_gate, "w_gate");
+  MOE_NEED(w_up, "w_up");
+  MOE_NEED(w_down, "w_down");
+  if (s.T > 0) {
+    MOE_NEED(x_perm, "x_perm");
+    MOE_NEED(gu, "gu");
+    MOE_NEED(h, "h");
+    MOE_NEED(o, "o");
+  }
+  if (s.expert_bias) {
+    MOE_NEED(b_gate, "b_gate");
+    MOE_NEED(b_up, "b_up");
+    MOE_NEED(b_down, "b_down");
+  } else {
+    b_gate = b_up = b_down = nullptr;
+  }
+  return do_gemm_fwd(s, x_perm, expert_offsets, w_gate, w_up, w_down, b_gate, b_up, b_down, gu, h, o, stream);
+}
+
+int moe_grouped_gemm_bwd(const moe_shape* shape, int32_t passes, const void* x_perm, const int32_t* expert_offsets,
+                         const void* gu, const void* h, const void* d_o, const void* w_gate, const void* w_up,
+                         const void* w_down, void* dgu, void* dx_perm, void* dw_gate, void* dw_up, void* dw_down,
+                         void* db_gate, void* db_up, void* db_down, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  if (passes <= 0 || passes > (MOE_DGRAD | MOE_WGRAD))
+    return moe_set_error(MOE_ERR_INVALID_ARG, "passes must be MOE_DGRAD, MOE_WGRAD or both");
+  MOE_NEED(expert_offsets, "expert_offsets");
+  if (passes & MOE_DGRAD) {
+    MOE_NEED(w_gate, "w_gate");
+    MOE_NEED(w_up, "w_up");
+    MOE_NEED(w_down, "w_down");
+    if (s.T > 0) {
+      MOE_NEED(gu, "gu");
+      MOE_NEED(d_o, "d_o");
+      MOE_NEED(dgu, "dgu");
+      MOE_NEED(dx_perm, "dx_perm");
+    }
+  }
+  if (passes & MOE_WGRAD) {
+    MOE_NEED(dw_gate, "dw_gate");
+    MOE_NEED(dw_up, "dw_up");
+    MOE_NEED(dw_down, "dw_down");
+    if (s.T > 0) {
+      MOE_NEED(x_perm, "x_perm");
+      MOE_NEED(h, "h");
+      MOE_NEED(d_o, "d_o");
+      MOE_NEED(dgu, "dgu");
+    }
+    if (s.expert_bias) {
+      MOE_NEED(db_gate, "db_gate");
+      MOE_NEED(db_up, "db_up");
+      MOE_NEED(db_down, "db_down");
+    } else {
+      db_gate = db_up = db_down = nullptr;
+    }
+  }
+  return do_gemm_bwd(s, passes, x_perm, expert_offsets, gu, h, d_o, w_gate, w_up, w_down, dgu, dx_perm, dw_gate,
+                     dw_up, dw_down, db_gate, db_up, db_down, stream);
+}
+
+int moe_combine_fwd(const moe_shape* shape, const void* o, const float* topk_w, const int32_t* row_of,
+                    const void* shared_o, void* y, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  if (s.T > 0) {
+    MOE_NEED(o, "o");
+    MOE_NEED(topk_w, "topk_w");
+    MOE_NEED(row_of, "row_of");
+    MOE_NEED(y, "y");
+  }
+  CombineFwdArgs a{o, topk_w, row_of, shared_o, y, s.T, (int)s.d, (int)s.k, s.dtype == MOE_BF16};
+  return launch_combine_fwd(a, stream);
+}
+
+int moe_combine_bwd(const moe_shape* shape, const void* dy, const void* o, const float* topk_w,
+                    const int32_t* row_of, void* d_o, float* d_topk_w, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  if (s.T > 0) {
+    MOE_NEED(dy, "dy");
+    MOE_NEED(o, "o");
+    MOE_NEED(topk_w, "topk_w");
+    MOE_NEED(row_of, "row_of");
+    MOE_NEED(d_o, "d_o");
+    MOE_NEED(d_topk_w, "d_topk_w");
+  }
+  CombineBwdArgs a{};
+  a.dy = dy;
+  a.o = o;
+  a.topk_w = topk_w;
+  a.row_of = row_of;
+  a.d_o = d_o;
+  a.d_topk_w = d_topk_w;
+  a.T = s.T;
+  a.d = (int)s.d;
+  a.k = (int)s.k;
+  a.bf16 = s.dtype == MOE_BF16;
+  a.router = s.router;
+  a.route_scale = s.route_scale;
+  return launch_combine_bwd(a, stream);
+}
+
+int moe_route_bwd(const moe_shape* shape, const void* x, const float* w_r, const int32_t* topk_idx,
+                  const float* topk_w, const float* s_sel, const float* d_topk_w, const int32_t* expert_offsets,
+                  const int32_t* token_of, float* dw_r, float* dx_router, void* ws, size_t ws_bytes,
+                  hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  MOE_NEED(w_r, "w_r");
+  MOE_NEED(dw_r, "dw_r");
+  MOE_NEED(expert_offsets, "expert_offsets");
+  if (s.T > 0) {
+    MOE_NEED(x, "x");
+    MOE_NEED(topk_idx, "topk_idx");
+    MOE_NEED(topk_w, "topk_w");
+    MOE_NEED(d_topk_w, "d_topk_w");
+    MOE_NEED(token_of, "token_of");
+    if (s.router == MOE_ROUTER_SIGMOID_GROUPED) MOE_NEED(s_sel, "s_sel");
+  }
+  const Plan p = plan(s);
+  MOE_TRY(check_ws(ws, ws_bytes, p.bwd_total));
+  RouteBwdArgs a = route_bwd_base(s);
+  a.x = x;
+  a.w_r = w_r;
+  a.topk_idx = topk_idx;
+  a.topk_w = topk_w;
+  a.s_sel = s_sel;
+  a.d_topk_w = d_topk_w;
+  a.offsets = expert_offsets;
+  a.token_of = token_of;
+  a.dw_r = dw_r;
+  a.dx_router = dx_router;
+  a.dl = reinterpret_cast<float*>(wsp(ws, p.dl));
+  a.partial = reinterpret_cast<float*>(wsp(ws, p.partial));
+  a.w_rt = reinterpret_cast<float*>(wsp(ws, p.w_rt));
+  return launch_route_bwd(a, stream);
+}
+
+int moe_unpermute_bwd(const moe_shape* shape, const void* dx_perm, const int32_t* row_of, const float* dx_router,
+                      const void* dx_shared, void* dx, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  if (s.T > 0) {
+    MOE_NEED(dx_perm, "dx_perm");
+    MOE_NEED(row_of, "row_of");
+    MOE_NEED(dx, "dx");
+  }
+  UnpermuteArgs a{};
+  a.dx_perm = dx_perm;
+  a.row_of = row_of;
+  a.dx_router = dx_router;
+  a.dx_shared = dx_shared;
+  a.dx = dx;
+  a.T = s.T;
+  a.d = (int)s.d;
+  a.k = (int)s.k;
+  a.bf16 = s.dtype == MOE_BF16;
+  return launch_unpermute(a, stream);
+}
+
+int moe_shared_expert_fwd(const moe_shape* shape, const void* x, const void* ws_gate, const void* ws_up,
+                          const void* ws_down, void* gu_sh, void* h_sh, void* o_sh, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  if (!s.n_shared) return moe_set_error(MOE_ERR_INVALID_ARG, "shape has no shared expert");
+  MOE_NEED(ws_gate, "ws_gate");
+  MOE_NEED(ws_up, "ws_up");
+  MOE_NEED(ws_down, "ws_down");
+  if (s.T > 0) {
+    MOE_NEED(x, "x");
+    MOE_NEED(gu_sh, "gu_sh");
+    MOE_NEED(h_sh, "h_sh");
+    MOE_NEED(o_sh, "o_sh");
+  }
+  return do_shared_fwd(s, x, ws_gate, ws_up, ws_down, gu_sh, h_sh, o_sh, stream);
+}
+
+int moe_shared_expert_bwd(const moe_shape* shape, const void* x, const void* dy, const void* gu_sh,
+                          const void* h_sh, const void* ws_gate, const void* ws_up, const void* ws_down,
+                          void* dx_shared, void* dws_gate, void* dws_up, void* dws_down, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  if (!s.n_shared) return moe_set_error(MOE_ERR_INVALID_ARG, "shape has no shared expert");
+  MOE_NEED(ws_gate, "ws_gate");
+  MOE_NEED(ws_up, "ws_up");
+  MOE_NEED(ws_down, "ws_down");
+  MOE_NEED(dws_gate, "dws_gate");
+  MOE_NEED(dws_up, "dws_up");
+  MOE_NEED(dws_down, "dws_down");
+  if (s.T > 0) {
+    MOE_NEED(x, "x");
+    MOE_NEED(dy, "dy");
+    MOE_NEED(gu_sh, "gu_sh");
+    MOE_NEED(h_sh, "h_sh");
+    MOE_NEED(dx_shared, "dx_shared");
+  }
+  const Plan p = plan(s);
+  MOE_TRY(check_ws(ws, ws_bytes, p.bwd_total));
+  return do_shared_bwd(s, x, dy, gu_sh, h_sh, ws_gate, ws_up, ws_down, wsp(ws, p.dgu_sh), dx_shared, dws_gate,
+                       dws_up, dws_down, stream);
+}
+
+int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, const moe_saved* sv, void* y,
+                  void* ws, size_t ws_bytes, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  MOE_NEED(prm, "params");
+  MOE_NEED(sv, "saved");
+  MOE_NEED(prm->w_r, "params.w_r");
+  MOE_NEED(prm->w_gate, "params.w_gate");
+  MOE_NEED(prm->w_up, "params.w_up");
+  MOE_NEED(prm->w_down, "params.w_down");
+  MOE_NEED(sv->expert_offsets, "saved.expert_offsets");
+  if (s.bias_mode != MOE_BIAS_NONE) MOE_NEED(prm->router_bias, "params.router_bias");
+  if (s.expert_bias) {
+    MOE_NEED(prm->b_gate, "params.b_gate");
+    MOE_NEED(prm->b_up, "params.b_up");
+    MOE_NEED(prm->b_down, "params.b_down");
+  }
+  if (s.n_shared) {
+    MOE_NEED(prm->ws_gate, "params.ws_gate");
+    MOE_NEED(prm->ws_up, "params.ws_up");
+    MOE_NEED(prm->ws_down, "params.ws_down");
+  }
+  if (s.T > 0) {
+    MOE_NEED(x, "x");
+    MOE_NEED(y, "y");
+    MOE_NEED(sv->topk_idx, "saved.topk_idx");
+    MOE_NEED(sv->topk_w, "saved.topk_w");
+    MOE_NEED(sv->row_of, "saved.row_of");
+    MOE_NEED(sv->token_of, "saved.token_of");
+    MOE_NEED(sv->x_perm, "saved.x_perm");
+    MOE_NEED(sv->gu, "saved.gu");
+    MOE_NEED(sv->h, "saved.h");
+    MOE_NEED(sv->o, "saved.o");
+    if (s.router == MOE_ROUTER_SIGMOID_GROUPED) MOE_NEED(sv->s_sel, "saved.s_sel");
+    if (s.n_shared) {
+      MOE_NEED(sv->gu_sh, "saved.gu_sh");
+      MOE_NEED(sv->h_sh, "saved.h_sh");
+      MOE_NEED(sv->o_sh, "saved.o_sh");
+    }
+  }
+  MOE_TRY(check_ws(ws, ws_bytes, plan(s).fwd_total));
+  const void* bg = s.expert_bias ? prm->b_gate : nullptr;
+  const void* bu = s.expert_bias ? prm->b_up : nullptr;
+  const void* bd = s.expert_bias ? prm->b_down : nullptr;
+  MOE_TRY(do_route(s, x, prm->w_r, prm->router_bias, sv->topk_idx, sv->topk_w, sv->s_sel, nullptr, stream));
+  MOE_TRY(do_permute(s, x, sv->topk_idx, sv->expert_offsets, sv->row_of, sv->token_of, sv->x_perm, ws, stream));
+  MOE_TRY(do_gemm_fwd(s, sv->x_perm, sv->expert_offsets, prm->w_gate, prm->w_up, prm->w_down, bg, bu, bd, sv->gu,
+                      sv->h, sv->o, stream));
+  if (s.n_shared)
+    MOE_TRY(do_shared_fwd(s, x, prm->ws_gate, prm->ws_up, prm->ws_down, sv->gu_sh, sv->h_sh, sv->o_sh, stream));
+  CombineFwdArgs c{sv->o, sv->topk_w, sv->row_of, s.n_shared ? sv->o_sh : nullptr, y, s.T, (int)s.d, (int)s.k,
+                   s.dtype == MOE_BF16};
+  return launch_combine_fwd(c, stream);
+}
+
+int moe_layer_bwd(const moe_shape* shape, const moe_params* prm, const void* x, const moe_saved* sv, const void* dy,
+                  void* dx, const moe_grads* gr, void* ws, size_t ws_bytes, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  MOE_NEED(prm, "params");
+  MOE_NEED(sv, "saved");
+  MOE_NEED(gr, "grads");
+  MOE_NEED(prm->w_r, "params.w_r");
+  MOE_NEED(prm->w_gate, "params.w_gate");
+  MOE_NEED(prm->w_up, "params.w_up");
+  MOE_NEED(prm->w_down, "params.w_down");
+  MOE_NEED(sv->expert_offsets, "saved.expert_offsets");
+  MOE_NEED(gr->dw_r, "grads.dw_r");
+  MOE_NEED(gr->dw_gate, "grads.dw_gate");
+  MOE_NEED(gr->dw_up, "grads.dw_up");
+  MOE_NEED(gr->dw_down, "grads.dw_down");
+  if (s.expert_bias) {
+    MOE_NEED(gr->db_gate, "grads.db_gate");
+    MOE_NEED(gr->db_up, "grads.db_up");
+    MOE_NEED(gr->db_down, "grads.db_down");
+  }
+  if (s.n_shared) {
+    MOE_NEED(prm->ws_gate, "params.ws_gate");
+    MOE_NEED(prm->ws_up, "params.ws_up");
+    MOE_NEED(prm->ws_down, "params.ws_down");
+    MOE_NEED(gr->dws_gate, "grads.dws_gate");
+    MOE_NEED(gr->dws_up, "grads.dws_up");
+    MOE_NEED(gr->dws_down, "grads.dws_down");
+  }
+  if (s.T > 0) {
+    MOE_NEED(x, "x");
+    MOE_NEED(dy, "dy");
+    MOE_NEED(dx, "dx");
+    MOE_NEED(sv->topk_idx, "saved.topk_idx");
+    MOE_NEED(sv->topk_w, "saved.topk_w");
+    MOE_NEED(sv->row_of, "saved.row_of");
+    MOE_NEED(sv->token_of, "saved.token_of");
+    MOE_NEED(sv->x_perm, "saved.x_perm");
+    MOE_NEED(sv->gu, "saved.gu");
+    MOE_NEED(sv->h, "saved.h");
+    MOE_NEED(sv->o, "saved.o");
+    if (s.router == MOE_ROUTER_SIGMOID_GROUPED) MOE_NEED(sv->s_sel, "saved.s_sel");
+    if (s.n_shared) {
+      MOE_NEED(sv->gu_sh, "saved.gu_sh");
+      MOE_NEED(sv->h_sh, "saved.h_sh");
+    }
+  }
+  const Plan p = plan(s);
+  MOE_TRY(check_ws(ws, ws_bytes, p.bwd_total));
+  void* d_o = wsp(ws, p.d_o);
+  void* dgu = wsp(ws, p.dgu);
+  void* dx_perm = wsp(ws, p.dx_perm);
+  float* dl = reinterpret_cast<float*>(wsp(ws, p.dl));
+  float* w_rt = reinterpret_cast<float*>(wsp(ws, p.w_rt));
+
+  // 1. combine backward with the router's dl fused in
+  CombineBwdArgs cb{};
+  cb.dy = dy;
+  cb.o = sv->o;
+  cb.topk_w = sv->topk_w;
+  cb.row_of = sv->row_of;
+  cb.d_o = d_o;
+  cb.d_topk_w = nullptr;
+  cb.T = s.T;
+  cb.d = (int)s.d;
+  cb.k = (int)s.k;
+  cb.bf16 = s.dtype == MOE_BF16;
+  cb.dl = dl;
+  cb.s_sel = sv->s_sel;
+  cb.router = s.router;
+  cb.route_scale = s.route_scale;
+  MOE_TRY(launch_combine_bwd(cb, stream));
+  // 2. expert dgrad then wgrad
+  MOE_TRY(do_gemm_bwd(s, MOE_DGRAD | MOE_WGRAD, sv->x_perm, sv->expert_offsets, sv->gu, sv->h, d_o, prm->w_gate,
+                      prm->w_up, prm->w_down, dgu, dx_perm, gr->dw_gate, gr->dw_up, gr->dw_down,
+                      s.expert_bias ? gr->db_gate : nullptr, s.expert_bias ? gr->db_up : nullptr,
+                      s.expert_bias ? gr->db_down : nullptr, stream));
+  // 3. router weight gradient (dx part fused into the unpermute)
+  RouteBwdArgs rb = route_bwd_base(s);
+  rb.x = x;
+  rb.w_r = prm->w_r;
+  rb.topk_idx = sv->topk_idx;
+  rb.dl_in = dl;
+  rb.offsets = sv->expert_offsets;
+  rb.token_of = sv->token_of;
+  rb.dw_r = gr->dw_r;
+  rb.dx_router = nullptr;
+  rb.partial = reinterpret_cast<float*>(wsp(ws, p.partial));
+  MOE_TRY(launch_route_bwd(rb, stream));
+  MOE_TRY(launch_wr_transpose(prm->w_r, w_rt, (int)s.d, (int)s.E, stream));
+  // 4. shared expert
+  void* dx_sh = nullptr;
+  if (s.n_shared) {
+    dx_sh = wsp(ws, p.dx_sh);
+    MOE_TRY(do_shared_bwd(s, x, dy, sv->gu_sh, sv->h_sh, prm->ws_gate, prm->ws_up, prm->ws_down, wsp(ws, p.dgu_sh),
+                          dx_sh, gr->dws_gate, gr->dws_up, gr->dws_down, stream));
+  }
+  // 5. dx = unpermute(dx_perm) + router dx + shared dx
+  UnpermuteArgs u{};
+  u.dx_perm = dx_perm;
+  u.row_of = sv->row_of;
+  u.dx_router = nullptr;
+  u.dx_shared = dx_sh;
+  u.dl = dl;
+  u.topk_idx = sv->topk_idx;
+  u.w_rt = w_rt;
+  u.dx = dx;
+  u.T = s.T;
+  u.d = (int)s.d;
+  u.k = (int)s.k;
+  u.bf16 = s.dtype == MOE_BF16;
+  return launch_unpermute(u, stream);
+}
+
+}  // extern "C"

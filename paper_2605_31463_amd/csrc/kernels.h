@@ -1,0 +1,152 @@
+// Launchers of the libmoe kernels (host side).  Every launcher only enqueues
+// on the given stream and returns a MOE_* status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+struct RouteArgs {
+  const void* x;
+  const float* w_r;
+  const float* bias;
+  int64_t T;
+  int d, E, k;
+  int router, bias_mode, n_groups, topk_groups;
+  float route_scale;
+  bool bf16;
+  int32_t* topk_idx;
+  float* topk_w;
+  float* s_sel;
+  int32_t* counts;  // may be null
+};
+int launch_route(const RouteArgs& a, hipStream_t s);
+int zero_i32(int32_t* p, int64_t n, hipStream_t s);
+
+// Permutation: histogram per block of PERM_TB tokens, scan, scatter.
+constexpr int PERM_TB = 256;
+inline int64_t perm_blocks(int64_t T) { return (T + PERM_TB - 1) / PERM_TB; }
+struct PermArgs {
+  const void* x;
+  const int32_t* topk_idx;
+  int64_t T;
+  int d, E, k;
+  bool bf16;
+  int32_t* hist;     // [nblk][E] workspace
+  int32_t* offsets;  // [E+1]
+  int32_t* row_of;   // [T][k]
+  int32_t* token_of; // [R]
+  void* x_perm;      // [R][d]
+};
+int launch_permute(const PermArgs& a, hipStream_t s);
+
+struct CombineFwdArgs {
+  const void* o;
+  const float* topk_w;
+  const int32_t* row_of;
+  const void* shared_o;
+  void* y;
+  int64_t T;
+  int d, k;
+  bool bf16;
+};
+int launch_combine_fwd(const CombineFwdArgs& a, hipStream_t s);
+
+// Combine backward; with dl != null it also writes the router logit
+// gradient of the selected experts (fused router backward, first step).
+struct CombineBwdArgs {
+  const void* dy;
+  const void* o;
+  const float* topk_w;
+  const int32_t* row_of;
+  void* d_o;
+  float* d_topk_w;   // may be null
+  int64_t T;
+  int d, k;
+  bool bf16;
+  // fused dl
+  float* dl;         // may be null
+  const float* s_sel;
+  int router;
+  float route_scale;
+};
+int launch_combine_bwd(const CombineBwdArgs& a, hipStream_t s);
+
+struct RouteBwdArgs {
+  const void* x;
+  const float* w_r;
+  const int32_t* topk_idx;
+  const float* topk_w;
+  const float* s_sel;
+  const float* d_topk_w;   // omega; unused when dl_in is given
+  const float* dl_in;      // precomputed dl [T][k] or null
+  const int32_t* offsets;
+  const int32_t* token_of;
+  float* dw_r;
+  float* dx_router;        // may be null
+  int64_t T;
+  int d, E, k;
+  int router;
+  float route_scale;
+  bool bf16;
+  // workspace
+  float* dl;               // [T][k]
+  float* partial;          // [route_dwr_tasks][d]
+  float* w_rt;             // [E][d]
+};
+constexpr int DWR_ROWS = 256;  // rows per partial-sum task of dW_r
+inline int64_t route_dwr_tasks(int64_t R, int64_t E) { return R / DWR_ROWS + E; }
+int launch_route_bwd(const RouteBwdArgs& a, hipStream_t s);
+int launch_wr_transpose(const float* w_r, float* w_rt, int d, int E, hipStream_t s);
+
+struct UnpermuteArgs {
+  const void* dx_perm;
+  const int32_t* row_of;
+  const float* dx_router;   // may be null
+  const void* dx_shared;    // may be null
+  // fused router dx: dx += sum_s dl[t][s] * w_rt[topk_idx[t][s]]
+  const float* dl;          // may be null
+  const int32_t* topk_idx;
+  const float* w_rt;
+  void* dx;
+  int64_t T;
+  int d, k;
+  bool bf16;
+};
+int launch_unpermute(const UnpermuteArgs& a, hipStream_t s);
+
+// Grouped GEMMs.
+enum GemmMode {
+  G_FWD_GATEUP = 0,  // [g|u] = A W_gate|W_up (+b), h = silu(g) u      A=x_perm [rows][d]
+  G_FWD_DOWN,        // o = h W_down (+b)                                A=h [rows][f]
+  G_DGRAD_DOWN,      // dh = d_o W_down^T, dSwiGLU with gu -> dgu        A=d_o [rows][d]
+  G_DGRAD_GATEUP,    // dx_perm = dgu [W_gate|W_up]^T                     A=dgu [rows][2f]
+  G_WGRAD_DOWN,      // dW_down = h^T d_o, db_down                        K = rows
+  G_WGRAD_GATEUP,    // dW_gate|dW_up = x_perm^T dgu, db_gate|db_up       K = rows
+};
+struct GemmArgs {
+  int mode;
+  bool bf16;
+  const int32_t* offsets;  // [ngroups+1] device, or null for one group of dense_rows rows
+  int ngroups;
+  int64_t dense_rows;
+  int64_t max_rows;        // upper bound of the total rows (for the grid)
+  int d, f;
+  // operands
+  const void* a;           // row-major activations (x_perm, h, d_o, dgu)
+  const void* b;           // second activation for wgrad (d_o, dgu)
+  const void* w0;          // w_gate or w_down
+  const void* w1;          // w_up
+  const void* bias0;       // b_gate or b_down  (fwd)
+  const void* bias1;       // b_up
+  const void* aux;         // gu (dgrad down)
+  // outputs
+  void* c0;                // gu | o | dgu | dx_perm | dW_down | dW_gate
+  void* c1;                // h  |   |     |         |         | dW_up
+  void* db0;               // db_down | db_gate
+  void* db1;               // db_up
+};
+int launch_gemm(const GemmArgs& a, hipStream_t s);
+
+}  // namespace moe

@@ -1,0 +1,182 @@
+// Token-to-expert permutation: the single-GPU form of the framework's token
+// scatter (section 3.2, "fused ... EP token scatter").
+//
+//   hist     one block per 256 tokens counts how many of its (token, slot)
+//            pairs chose each expert;
+//   scan     per expert, exclusive prefix of the block counts (each block's
+//            base inside the expert) and the exclusive scan over experts
+//            (expert_offsets);
+//   scatter  one block per 256 tokens ranks its pairs inside each expert in
+//            ascending token order from per-wave 64-bit membership masks
+//            (popcount below the lane), writes row_of / token_of, then copies
+//            each x row once from HBM into its k destination rows with 16-byte
+//            vector loads and stores.
+// No atomics touch the row layout, so the permutation is the stable counting
+// sort by (expert, token) on every run.
+#include "common.h"
+#include "kernels.h"
+
+namespace moe {
+
+namespace {
+
+__global__ __launch_bounds__(256) void hist_kernel(const int32_t* __restrict__ idx, int64_t T, int k,
+                                                   int E, int32_t* __restrict__ hist) {
+  __shared__ int cnt[256];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < E; e += 256) cnt[e] = 0;
+  __syncthreads();
+  const int64_t t = (int64_t)blockIdx.x * PERM_TB + tid;
+  if (t < T) {
+    for (int s = 0; s < k; ++s) {
+      const int e = idx[t * k + s];
+      if ((unsigned)e < (unsigned)E) atomicAdd(&cnt[e], 1);  // out-of-range ids are dropped
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += 256) hist[(int64_t)blockIdx.x * E + e] = cnt[e];
+}
+
+// One block of 1024 threads: thread (e, p) scans a contiguous range of
+// blocks of expert e; the parts are combined through LDS.
+__global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist, int64_t nblk, int E,
+                                                    int EP, int32_t* __restrict__ offsets) {
+  __shared__ int part[1024];
+  __shared__ int tot[257];
+  const int tid = threadIdx.x;
+  const int P = 1024 / EP;
+  const int e = tid % EP;
+  const int p = tid / EP;
+  const int64_t chunk = (nblk + P - 1) / P;
+  const int64_t b0 = p * chunk;
+  const int64_t b1 = b0 + chunk < nblk ? b0 + chunk : nblk;
+  int sum = 0;
+  if (e < E) {
+    for (int64_t b = b0; b < b1; b += 8) {
+      int v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = (b + q < b1) ? hist[(b + q) * E + e] : 0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) sum += v[q];
+    }
+  }
+  part[p * EP + e] = sum;
+  __syncthreads();
+  int pre = 0;
+  for (int q = 0; q < p; ++q) pre += part[q * EP + e];
+  if (e < E) {
+    for (int64_t b = b0; b < b1; b += 8) {
+      int v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = (b + q < b1) ? hist[(b + q) * E + e] : 0;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (b + q < b1) hist[(b + q) * E + e] = pre;
+        pre += v[q];
+      }
+    }
+  }
+  if (p == 0) {
+    int t = 0;
+    for (int q = 0; q < P; ++q) t += part[q * EP + e];
+    if (e < E) tot[e] = t;
+  }
+  __syncthreads();
+  __shared__ int sbuf[256];
+  __shared__ int total;
+  const int ex = block_scan_256(tid < E ? tot[tid] : 0, sbuf, &total);
+  if (tid < E) offsets[tid] = ex;
+  if (tid == 0) offsets[E] = total;
+}
+
+template <class XT>
+__global__ __launch_bounds__(256) void scatter_kernel(PermArgs a) {
+  __shared__ unsigned long long mask[4][256];
+  __shared__ int rows[PERM_TB][16];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int E = a.E, k = a.k;
+  for (int i = tid; i < 4 * 256; i += 256) (&mask[0][0])[i] = 0ull;
+  __syncthreads();
+  const int64_t blk = blockIdx.x;
+  const int64_t t = blk * PERM_TB + tid;
+  const bool live = t < a.T;
+  int ex[16];
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    ex[s] = -1;
+    if (s < k && live) {
+      const int e = a.topk_idx[t * k + s];
+      if ((unsigned)e < (unsigned)E) {
+        ex[s] = e;
+        atomicOr(&mask[wave][e], 1ull << lane);
+      }
+    }
+  }
+  __syncthreads();
+  const unsigned long long below = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int s = 0; s < 16; ++s) {
+    if (s < k && live && ex[s] < 0) {
+      a.row_of[t * k + s] = -1;
+      rows[tid][s] = -1;
+    } else if (s < k && live) {
+      const int e = ex[s];
+      int rank = __popcll(mask[wave][e] & below);
+      for (int w = 0; w < wave; ++w) rank += __popcll(mask[w][e]);
+      const int row = a.offsets[e] + a.hist[blk * E + e] + rank;
+      a.row_of[t * k + s] = row;
+      a.token_of[row] = (int32_t)(t * k + s);
+      rows[tid][s] = row;
+    }
+  }
+  __syncthreads();
+  // copy: one wavefront per token, x row read once, written k times
+  constexpr int V = Vec16<XT>::N;
+  const int nch = a.d / V;
+  const XT* x = reinterpret_cast<const XT*>(a.x);
+  XT* xp = reinterpret_cast<XT*>(a.x_perm);
+  for (int tl = wave; tl < PERM_TB; tl += 4) {
+    const int64_t tt = blk * PERM_TB + tl;
+    if (tt >= a.T) break;
+    for (int c0 = 0; c0 < nch; c0 += 64 * 4) {
+      uint4 v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int c = c0 + j * 64 + lane;
+        if (c < nch) v[j] = *reinterpret_cast<const uint4*>(x + tt * a.d + (int64_t)c * V);
+      }
+      for (int s = 0; s < k; ++s) {
+        const int64_t r = rows[tl][s];
+        if (r < 0) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int c = c0 + j * 64 + lane;
+          if (c < nch) *reinterpret_cast<uint4*>(xp + r * a.d + (int64_t)c * V) = v[j];
+        }
+      }
+    }
+  }
+}
+
+}  // namespace
+
+int launch_permute(const PermArgs& a, hipStream_t s) {
+  const int64_t nblk = perm_blocks(a.T);
+  int st;
+  if (nblk > 0) {
+    st = launch(K_HIST, s, "hist", [&] { hist_kernel<<<nblk, 256, 0, s>>>(a.topk_idx, a.T, a.k, a.E, a.hist); });
+    if (st) return st;
+  }
+  int EP = 1;
+  while (EP < a.E) EP <<= 1;
+  st = launch(K_SCAN, s, "scan", [&] { scan_kernel<<<1, 1024, 0, s>>>(a.hist, nblk, a.E, EP, a.offsets); });
+  if (st) return st;
+  if (nblk == 0) return MOE_OK;
+  if (a.bf16)
+    return launch(K_SCATTER, s, "scatter", [&] { scatter_kernel<bf16_t><<<nblk, 256, 0, s>>>(a); });
+  return launch(K_SCATTER, s, "scatter", [&] { scatter_kernel<float><<<nblk, 256, 0, s>>>(a); });
+}
+
+}  // namespace moe

@@ -1,0 +1,55 @@
+"""Buffers for one MoE layer and thin calls of the fused entry points.
+
+MoELayer allocates (with torch, on the GPU) the saved tensors, the
+workspaces and the gradients for a moe_shape, and calls moe_layer_fwd /
+moe_layer_bwd.  Every computation happens in libmoe's kernels.
+"""
+import torch
+
+from . import _lib as L
+
+
+class MoELayer:
+    def __init__(self, shape, device="cuda"):
+        self.shape = shape
+        self.device = device
+        s = shape
+        T, d, E, k, f = s.T, s.d, s.E, s.k, s.f
+        R = T * k
+        self.act = torch.bfloat16 if s.dtype == L.MOE_BF16 else torch.float32
+        fwd, _, bwd = L.moe_workspace_size(shape)
+        self.ws_fwd = torch.empty(max(fwd, 1), dtype=torch.uint8, device=device)
+        self.ws_bwd = torch.empty(max(bwd, 1), dtype=torch.uint8, device=device)
+        i32, f32, a = torch.int32, torch.float32, self.act
+        e = lambda *shp, dt=a: torch.empty(*shp, dtype=dt, device=device)  # noqa: E731
+        self.saved = dict(
+            topk_idx=e(T, k, dt=i32), topk_w=e(T, k, dt=f32),
+            s_sel=e(T, k, dt=f32) if s.router == L.MOE_ROUTER_SIGMOID_GROUPED else None,
+            expert_offsets=e(E + 1, dt=i32), row_of=e(T, k, dt=i32), token_of=e(R, dt=i32),
+            x_perm=e(R, d), gu=e(R, 2 * f), h=e(R, f), o=e(R, d),
+            gu_sh=e(T, 2 * s.f_shared) if s.n_shared else None,
+            h_sh=e(T, s.f_shared) if s.n_shared else None,
+            o_sh=e(T, d) if s.n_shared else None,
+        )
+        self.y = e(T, d)
+        self.dx = e(T, d)
+
+    def alloc_grads(self):
+        s = self.shape
+        a = self.act
+        e = lambda *shp, dt=a: torch.empty(*shp, dtype=dt, device=self.device)  # noqa: E731
+        g = dict(dw_r=e(s.d, s.E, dt=torch.float32), dw_gate=e(s.E, s.d, s.f), dw_up=e(s.E, s.d, s.f),
+                 dw_down=e(s.E, s.f, s.d))
+        if s.expert_bias:
+            g.update(db_gate=e(s.E, s.f), db_up=e(s.E, s.f), db_down=e(s.E, s.d))
+        if s.n_shared:
+            g.update(dws_gate=e(s.d, s.f_shared), dws_up=e(s.d, s.f_shared), dws_down=e(s.f_shared, s.d))
+        return g
+
+    def forward(self, params, x, stream=None):
+        L.moe_layer_fwd(self.shape, params, x, self.saved, self.y, self.ws_fwd, stream)
+        return self.y
+
+    def backward(self, params, x, dy, grads, stream=None):
+        L.moe_layer_bwd(self.shape, params, x, self.saved, dy, self.dx, grads, self.ws_bwd, stream)
+        return self.dx

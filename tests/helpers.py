@@ -1,0 +1,120 @@
+"""Shared test plumbing: seeded inputs to device tensors, oracle runs, and the
+parity measures (normwise relative error; routing equality outside the 1e-6
+top-k margin)."""
+import numpy as np
+
+from moe_inputs import f32_from_bf16_bits, layer_inputs, to_f64
+from oracle import layer_backward, layer_forward, spec_from_config
+
+MARGIN = 1e-6
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+
+def dev(a, dtype):
+    """Storage array (bf16 bit patterns or float32) -> torch tensor on cuda:0."""
+    import torch
+    if a is None:
+        return None
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
+def host(t):
+    """torch tensor (any device) -> numpy float64 (bf16 read exactly)."""
+    import torch
+    if t is None:
+        return None
+    t = t.detach().cpu()
+    if t.dtype == torch.bfloat16:
+        return f32_from_bf16_bits(t.view(torch.int16).numpy().view(np.uint16)).astype(np.float64)
+    if t.dtype in (torch.int32, torch.int64):
+        return t.numpy()
+    return t.float().numpy().astype(np.float64)
+
+
+def rel(gpu, ref):
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    nr = np.linalg.norm(ref)
+    if nr == 0:
+        return float(np.linalg.norm(gpu))
+    return float(np.linalg.norm(gpu - ref) / nr)
+
+
+def expert_fn(inp, cfg):
+    dt = cfg["dtype"]
+
+    def fn(e):
+        b = cfg["expert_bias"]
+        return (to_f64(inp["w_gate"][e], dt), to_f64(inp["w_up"][e], dt), to_f64(inp["w_down"][e], dt),
+                to_f64(inp["b_gate"][e], dt) if b else None,
+                to_f64(inp["b_up"][e], dt) if b else None,
+                to_f64(inp["b_down"][e], dt) if b else None)
+    return fn
+
+
+def shared_of(inp, cfg):
+    if not cfg["n_shared"]:
+        return None
+    dt = cfg["dtype"]
+    return (to_f64(inp["ws_gate"], dt), to_f64(inp["ws_up"], dt), to_f64(inp["ws_down"], dt))
+
+
+def oracle_run(cfg, inp):
+    spec = spec_from_config(cfg)
+    dt = cfg["dtype"]
+    x = to_f64(inp["x"], dt)
+    w_r = inp["w_r"].astype(np.float64)
+    beta = None if inp["router_bias"] is None else inp["router_bias"].astype(np.float64)
+    efn = expert_fn(inp, cfg)
+    shared = shared_of(inp, cfg)
+    fwd = layer_forward(spec, x, w_r, beta, efn, shared)
+    bwd = layer_backward(spec, x, w_r, beta, efn, fwd, to_f64(inp["dy"], dt), shared,
+                         with_bias=cfg["expert_bias"])
+    return fwd, bwd
+
+
+def device_params(inp, cfg):
+    import torch
+    dt = cfg["dtype"]
+    p = dict(
+        w_r=torch.from_numpy(inp["w_r"]).cuda(),
+        router_bias=None if inp["router_bias"] is None else torch.from_numpy(inp["router_bias"]).cuda(),
+        w_gate=dev(inp["w_gate"], dt), w_up=dev(inp["w_up"], dt), w_down=dev(inp["w_down"], dt),
+        b_gate=dev(inp.get("b_gate"), dt), b_up=dev(inp.get("b_up"), dt), b_down=dev(inp.get("b_down"), dt),
+        ws_gate=dev(inp.get("ws_gate"), dt), ws_up=dev(inp.get("ws_up"), dt), ws_down=dev(inp.get("ws_down"), dt),
+    )
+    return p
+
+
+def check_routing(cfg, fwd, topk_idx_gpu):
+    """Routing parity: equal outside the margin.  Returns (ambiguous mask, all_equal)."""
+    ref = fwd["route"]["topk_idx"]
+    amb = fwd["route"]["margin"] < MARGIN
+    gpu = np.asarray(topk_idx_gpu)
+    same = np.all(gpu == ref, axis=1)
+    bad = np.where(~same & ~amb)[0]
+    assert bad.size == 0, "topk_idx differs on %d non-ambiguous tokens, first %s: gpu %s oracle %s" % (
+        bad.size, bad[:5], gpu[bad[0]], ref[bad[0]])
+    return amb, bool(np.all(same))
+
+
+def check_maps_valid(topk_idx, offsets, row_of, token_of, E):
+    """Maps are the stable (expert, token) counting sort of the given topk_idx."""
+    T, k = topk_idx.shape
+    counts = np.bincount(topk_idx.reshape(-1), minlength=E)
+    assert np.array_equal(np.diff(offsets), counts)
+    assert offsets[0] == 0 and offsets[E] == T * k
+    assert np.array_equal(np.sort(token_of), np.arange(T * k))
+    t_of = token_of // k
+    s_of = token_of % k
+    assert np.array_equal(topk_idx[t_of, s_of], np.repeat(np.arange(E), counts))
+    for e in range(E):
+        seg = t_of[offsets[e]:offsets[e + 1]]
+        assert np.all(np.diff(seg) > 0)
+    assert np.array_equal(row_of[t_of, s_of], np.arange(T * k))
+
+
+def small_inputs(cfg, seed=0):
+    return layer_inputs(cfg, seed=seed)
