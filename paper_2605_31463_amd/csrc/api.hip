@@ -75,7 +75,7 @@ const char* kernel_name(int id) {
       "route", "count_zero", "hist", "scan", "scatter", "gemm_gateup_fwd", "gemm_down_fwd",
       "combine_fwd", "combine_bwd", "route_dl", "route_dwr_partial", "route_dwr_reduce",
       "wr_transpose", "route_dx", "gemm_down_dgrad", "gemm_gateup_dgrad", "gemm_down_wgrad",
-      "gemm_gateup_wgrad", "unpermute"};
+      "gemm_gateup_wgrad", "unpermute", "rank", "wr_split"};
   if (id < 0 || id >= K_NUM_KERNELS) return nullptr;
   return names[id];
 }
@@ -137,7 +137,7 @@ inline size_t act_bytes(const moe_shape& s) { return s.dtype == MOE_BF16 ? 2 : 4
 
 struct Plan {
   // forward
-  size_t hist;
+  size_t hist, wsplit;
   size_t fwd_total;
   // backward
   size_t d_o, dgu, dx_perm, dl, partial, w_rt, dgu_sh, dx_sh;
@@ -152,6 +152,8 @@ Plan plan(const moe_shape& s) {
   size_t off = 0;
   p.hist = off;
   off += align_up((size_t)moe::perm_blocks(s.T) * s.E * 4);
+  p.wsplit = off;
+  off += s.dtype == MOE_BF16 ? align_up((size_t)3 * s.E * s.d * 2) : 0;
   p.fwd_total = off;
   off = 0;
   p.d_o = off; off += align_up((size_t)R * s.d * eb);
@@ -215,8 +217,9 @@ GemmArgs gemm_dense(const moe_shape& s, int mode) {
 }
 
 int do_route(const moe_shape& s, const void* x, const float* w_r, const float* bias, int32_t* topk_idx,
-             float* topk_w, float* s_sel, int32_t* counts, hipStream_t st) {
+             float* topk_w, float* s_sel, int32_t* counts, void* ws, hipStream_t st) {
   RouteArgs a{};
+  a.wsplit = s.dtype == MOE_BF16 ? wsp(ws, plan(s).wsplit) : nullptr;
   a.x = x;
   a.w_r = w_r;
   a.bias = bias;
@@ -427,8 +430,6 @@ int moe_workspace_size(const moe_shape* shape, size_t* fwd_ws, size_t* saved_byt
 
 int moe_route(const moe_shape* shape, const void* x, const float* w_r, const float* router_bias, int32_t* topk_idx,
               float* topk_w, float* s_sel, int32_t* expert_counts, void* ws, size_t ws_bytes, hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   MOE_TRY(check_shape(shape));
   const moe_shape& s = *shape;
   if (s.T > 0) {
@@ -439,7 +440,8 @@ int moe_route(const moe_shape* shape, const void* x, const float* w_r, const flo
   MOE_NEED(w_r, "w_r");
   if (s.bias_mode != MOE_BIAS_NONE) MOE_NEED(router_bias, "router_bias");
   if (s.router == MOE_ROUTER_SIGMOID_GROUPED && s.T > 0) MOE_NEED(s_sel, "s_sel");
-  return do_route(s, x, w_r, router_bias, topk_idx, topk_w, s_sel, expert_counts, stream);
+  MOE_TRY(check_ws(ws, ws_bytes, plan(s).fwd_total));
+  return do_route(s, x, w_r, router_bias, topk_idx, topk_w, s_sel, expert_counts, ws, stream);
 }
 
 int moe_permute(const moe_shape* shape, const void* x, const int32_t* topk_idx, int32_t* expert_offsets,
@@ -712,7 +714,7 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, 
   const void* bg = s.expert_bias ? prm->b_gate : nullptr;
   const void* bu = s.expert_bias ? prm->b_up : nullptr;
   const void* bd = s.expert_bias ? prm->b_down : nullptr;
-  MOE_TRY(do_route(s, x, prm->w_r, prm->router_bias, sv->topk_idx, sv->topk_w, sv->s_sel, nullptr, stream));
+  MOE_TRY(do_route(s, x, prm->w_r, prm->router_bias, sv->topk_idx, sv->topk_w, sv->s_sel, nullptr, ws, stream));
   MOE_TRY(do_permute(s, x, sv->topk_idx, sv->expert_offsets, sv->row_of, sv->token_of, sv->x_perm, ws, stream));
   MOE_TRY(do_gemm_fwd(s, sv->x_perm, sv->expert_offsets, prm->w_gate, prm->w_up, prm->w_down, bg, bu, bd, sv->gu,
                       sv->h, sv->o, stream));

@@ -29,6 +29,8 @@ enum KernelId {
   K_GEMM_DOWN_WGRAD,
   K_GEMM_GATEUP_WGRAD,
   K_UNPERMUTE,
+  K_RANK,
+  K_WR_SPLIT,
   K_NUM_KERNELS
 };
 

@@ -20,6 +20,7 @@ struct RouteArgs {
   float* topk_w;
   float* s_sel;
   int32_t* counts;  // may be null
+  void* wsplit;      // bf16 [3][E][d] workspace for the MFMA path (bf16 x), or null
 };
 int launch_route(const RouteArgs& a, hipStream_t s);
 int zero_i32(int32_t* p, int64_t n, hipStream_t s);

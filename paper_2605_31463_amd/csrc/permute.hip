@@ -6,11 +6,11 @@
 //   scan     per expert, exclusive prefix of the block counts (each block's
 //            base inside the expert) and the exclusive scan over experts
 //            (expert_offsets);
-//   scatter  one block per 256 tokens ranks its pairs inside each expert in
+//   rank     one block per 256 tokens ranks its pairs inside each expert in
 //            ascending token order from per-wave 64-bit membership masks
-//            (popcount below the lane), writes row_of / token_of, then copies
-//            each x row once from HBM into its k destination rows with 16-byte
-//            vector loads and stores.
+//            (popcount below the lane) and writes row_of / token_of;
+//   copy     one wavefront per token reads its x row once from HBM and writes
+//            it to the token's k rows with 16-byte vector loads and stores.
 // No atomics touch the row layout, so the permutation is the stable counting
 // sort by (expert, token) on every run.
 #include "common.h"
@@ -89,10 +89,10 @@ __global__ __launch_bounds__(1024) void scan_kernel(int32_t* __restrict__ hist, 
   if (tid == 0) offsets[E] = total;
 }
 
-template <class XT>
-__global__ __launch_bounds__(256) void scatter_kernel(PermArgs a) {
+// Ranks each (token, slot) pair of a 256-token block inside its expert and
+// writes row_of / token_of.
+__global__ __launch_bounds__(256) void rank_kernel(PermArgs a) {
   __shared__ unsigned long long mask[4][256];
-  __shared__ int rows[PERM_TB][16];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -120,7 +120,6 @@ __global__ __launch_bounds__(256) void scatter_kernel(PermArgs a) {
   for (int s = 0; s < 16; ++s) {
     if (s < k && live && ex[s] < 0) {
       a.row_of[t * k + s] = -1;
-      rows[tid][s] = -1;
     } else if (s < k && live) {
       const int e = ex[s];
       int rank = __popcll(mask[wave][e] & below);
@@ -128,33 +127,41 @@ __global__ __launch_bounds__(256) void scatter_kernel(PermArgs a) {
       const int row = a.offsets[e] + a.hist[blk * E + e] + rank;
       a.row_of[t * k + s] = row;
       a.token_of[row] = (int32_t)(t * k + s);
-      rows[tid][s] = row;
     }
   }
-  __syncthreads();
-  // copy: one wavefront per token, x row read once, written k times
+}
+
+// Row copy: one wavefront per token reads the x row once (16-byte vector
+// loads, 2 per lane in flight) and writes it to the token's k rows.
+template <class XT>
+__global__ __launch_bounds__(256) void permute_copy_kernel(PermArgs a) {
   constexpr int V = Vec16<XT>::N;
+  constexpr int CPL = 4;
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)__builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
+  if (t >= a.T) return;
+  const int k = a.k;
   const int nch = a.d / V;
-  const XT* x = reinterpret_cast<const XT*>(a.x);
+  const XT* x = reinterpret_cast<const XT*>(a.x) + t * a.d;
   XT* xp = reinterpret_cast<XT*>(a.x_perm);
-  for (int tl = wave; tl < PERM_TB; tl += 4) {
-    const int64_t tt = blk * PERM_TB + tl;
-    if (tt >= a.T) break;
-    for (int c0 = 0; c0 < nch; c0 += 64 * 4) {
-      uint4 v[4];
+  int64_t rows[16];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+  for (int s = 0; s < 16; ++s) rows[s] = s < k ? a.row_of[t * k + s] : -1;
+  for (int c0 = 0; c0 < nch; c0 += 64 * CPL) {
+    uint4 v[CPL];
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+      const int c = c0 + j * 64 + lane;
+      if (c < nch) v[j] = *reinterpret_cast<const uint4*>(x + (int64_t)c * V);
+    }
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+      if (s >= k) break;
+      if (rows[s] < 0) continue;
+#pragma unroll
+      for (int j = 0; j < CPL; ++j) {
         const int c = c0 + j * 64 + lane;
-        if (c < nch) v[j] = *reinterpret_cast<const uint4*>(x + tt * a.d + (int64_t)c * V);
-      }
-      for (int s = 0; s < k; ++s) {
-        const int64_t r = rows[tl][s];
-        if (r < 0) continue;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int c = c0 + j * 64 + lane;
-          if (c < nch) *reinterpret_cast<uint4*>(xp + r * a.d + (int64_t)c * V) = v[j];
-        }
+        if (c < nch) *reinterpret_cast<uint4*>(xp + rows[s] * a.d + (int64_t)c * V) = v[j];
       }
     }
   }
@@ -174,9 +181,12 @@ int launch_permute(const PermArgs& a, hipStream_t s) {
   st = launch(K_SCAN, s, "scan", [&] { scan_kernel<<<1, 1024, 0, s>>>(a.hist, nblk, a.E, EP, a.offsets); });
   if (st) return st;
   if (nblk == 0) return MOE_OK;
+  st = launch(K_RANK, s, "rank", [&] { rank_kernel<<<nblk, 256, 0, s>>>(a); });
+  if (st) return st;
+  const int ncopy = (int)((a.T + 3) / 4);
   if (a.bf16)
-    return launch(K_SCATTER, s, "scatter", [&] { scatter_kernel<bf16_t><<<nblk, 256, 0, s>>>(a); });
-  return launch(K_SCATTER, s, "scatter", [&] { scatter_kernel<float><<<nblk, 256, 0, s>>>(a); });
+    return launch(K_SCATTER, s, "scatter", [&] { permute_copy_kernel<bf16_t><<<ncopy, 256, 0, s>>>(a); });
+  return launch(K_SCATTER, s, "scatter", [&] { permute_copy_kernel<float><<<ncopy, 256, 0, s>>>(a); });
 }
 
 }  // namespace moe

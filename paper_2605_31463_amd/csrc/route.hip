@@ -59,92 +59,14 @@ __device__ __forceinline__ double wave_max_d(double v, int width) {
   return v;
 }
 
-template <class XT, int EPT>
-__global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
-  constexpr int EPAD = 16 * EPT;
-  constexpr int STAGE_BYTES = (KS * TB + KS * EPAD) * 4;
-  constexpr int TABLE_BYTES = TB * EPAD * 8;
-  constexpr int SMEM = STAGE_BYTES > TABLE_BYTES ? STAGE_BYTES : TABLE_BYTES;
-  __shared__ __align__(16) unsigned char smem[SMEM];
-  __shared__ int hist[EPAD];
-
+// Top-k selection and gating weights for `ntok` tokens whose float64 logits
+// sit in LDS (lg[token][ld]); one wavefront per token, four wavefronts per
+// block.  Adds each selected expert to the block histogram `hist`.
+__device__ void select_tokens(const RouteArgs& a, const double* lg, int ld, int64_t t0, int ntok, int* hist) {
   const int tid = threadIdx.x;
-  const int tx = tid & 15;
-  const int ty = tid >> 4;
   const int E = a.E;
-  const int d = a.d;
-  const int64_t t0 = (int64_t)blockIdx.x * TB;
-  const XT* x = reinterpret_cast<const XT*>(a.x);
-
-  for (int e = tid; e < EPAD; e += 256) hist[e] = 0;
-
-  float* xs = reinterpret_cast<float*>(smem);   // [KS][TB]
-  float* wsm = xs + KS * TB;                     // [KS][EPAD]
-
-  double acc[2][EPT];
-  float part[2][EPT];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < EPT; ++j) {
-      acc[i][j] = 0.0;
-      part[i][j] = 0.f;
-    }
-
-  for (int k0 = 0; k0 < d; k0 += KS) {
-    // stage x: token tid/8, elements (tid%8)*4 .. +3
-    {
-      const int tl = tid >> 3;
-      const int c = (tid & 7) * 4;
-      const int64_t t = t0 + tl;
-      float v[4] = {0.f, 0.f, 0.f, 0.f};
-      if (t < a.T) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = Elem<XT>::load(x, t * d + k0 + c + q);
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) xs[(c + q) * TB + tl] = v[q];
-    }
-    // stage W_r rows k0..k0+KS-1
-    for (int i = tid; i < KS * EPAD; i += 256) {
-      const int r = i / EPAD;
-      const int e = i - r * EPAD;
-      wsm[i] = e < E ? a.w_r[(int64_t)(k0 + r) * E + e] : 0.f;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) {
-      const float2 xv = *reinterpret_cast<const float2*>(&xs[kk * TB + 2 * ty]);
-      float wv[EPT];
-#pragma unroll
-      for (int j = 0; j < EPT; ++j) wv[j] = wsm[kk * EPAD + tx * EPT + j];
-#pragma unroll
-      for (int j = 0; j < EPT; ++j) {
-        part[0][j] = __builtin_fmaf(xv.x, wv[j], part[0][j]);
-        part[1][j] = __builtin_fmaf(xv.y, wv[j], part[1][j]);
-      }
-      if ((kk % CH) == CH - 1) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < EPT; ++j) {
-            acc[i][j] += (double)part[i][j];
-            part[i][j] = 0.f;
-          }
-      }
-    }
-    __syncthreads();
-  }
-
-  // logits -> LDS table [TB][EPAD] (float64)
-  double* lg = reinterpret_cast<double*>(smem);
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < EPT; ++j) lg[(2 * ty + i) * EPAD + tx * EPT + j] = acc[i][j];
-  __syncthreads();
-
-  // selection: one wavefront per token
+  const int EPAD = ld;
+  const int TB = ntok;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int epl = (E + 63) / 64;              // experts per lane, contiguous
@@ -258,11 +180,282 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
       atomicAdd(&hist[my_idx], 1);
     }
   }
+}
+
+template <class XT, int EPT>
+__global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
+  constexpr int EPAD = 16 * EPT;
+  constexpr int STAGE_BYTES = (KS * TB + KS * EPAD) * 4;
+  constexpr int TABLE_BYTES = TB * EPAD * 8;
+  constexpr int SMEM = STAGE_BYTES > TABLE_BYTES ? STAGE_BYTES : TABLE_BYTES;
+  __shared__ __align__(16) unsigned char smem[SMEM];
+  __shared__ int hist[EPAD];
+
+  const int tid = threadIdx.x;
+  const int tx = tid & 15;
+  const int ty = tid >> 4;
+  const int E = a.E;
+  const int d = a.d;
+  const int64_t t0 = (int64_t)blockIdx.x * TB;
+  const XT* x = reinterpret_cast<const XT*>(a.x);
+
+  for (int e = tid; e < EPAD; e += 256) hist[e] = 0;
+
+  float* xs = reinterpret_cast<float*>(smem);   // [KS][TB]
+  float* wsm = xs + KS * TB;                     // [KS][EPAD]
+
+  double acc[2][EPT];
+  float part[2][EPT];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) {
+      acc[i][j] = 0.0;
+      part[i][j] = 0.f;
+    }
+
+  for (int k0 = 0; k0 < d; k0 += KS) {
+    // stage x: token tid/8, elements (tid%8)*4 .. +3
+    {
+      const int tl = tid >> 3;
+      const int c = (tid & 7) * 4;
+      const int64_t t = t0 + tl;
+      float v[4] = {0.f, 0.f, 0.f, 0.f};
+      if (t < a.T) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = Elem<XT>::load(x, t * d + k0 + c + q);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) xs[(c + q) * TB + tl] = v[q];
+    }
+    // stage W_r rows k0..k0+KS-1
+    for (int i = tid; i < KS * EPAD; i += 256) {
+      const int r = i / EPAD;
+      const int e = i - r * EPAD;
+      wsm[i] = e < E ? a.w_r[(int64_t)(k0 + r) * E + e] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const float2 xv = *reinterpret_cast<const float2*>(&xs[kk * TB + 2 * ty]);
+      float wv[EPT];
+#pragma unroll
+      for (int j = 0; j < EPT; ++j) wv[j] = wsm[kk * EPAD + tx * EPT + j];
+#pragma unroll
+      for (int j = 0; j < EPT; ++j) {
+        part[0][j] = __builtin_fmaf(xv.x, wv[j], part[0][j]);
+        part[1][j] = __builtin_fmaf(xv.y, wv[j], part[1][j]);
+      }
+      if ((kk % CH) == CH - 1) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < EPT; ++j) {
+            acc[i][j] += (double)part[i][j];
+            part[i][j] = 0.f;
+          }
+      }
+    }
+    __syncthreads();
+  }
+
+  // logits -> LDS table [TB][EPAD] (float64)
+  double* lg = reinterpret_cast<double*>(smem);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < EPT; ++j) lg[(2 * ty + i) * EPAD + tx * EPT + j] = acc[i][j];
+  __syncthreads();
+
+  select_tokens(a, lg, EPAD, t0, TB, hist);
   __syncthreads();
   if (a.counts) {
     for (int e = tid; e < E; e += 256)
       if (hist[e]) atomicAdd(&a.counts[e], hist[e]);
   }
+}
+
+
+// ---------------------------------------------------------------------------
+// bf16 path: logits on MFMA.
+//
+// W_r (float32) is split once per call into three bf16 terms,
+// w = w1 + w2 + w3 with w1 = bf16(w), w2 = bf16(w - w1), w3 = bf16(w - w1 - w2),
+// stored expert-major ([3][E][d]).  x is bf16, so every product x * w_i is exact
+// in float32; v_mfma_f32_16x16x32_bf16 sums them, and the float32 partial sums
+// are folded into float64 accumulators every 64 hidden elements.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+__global__ void wr_split_kernel(const float* __restrict__ w, bf16_t* __restrict__ ws, int d, int E) {
+  __shared__ float tile[32][33];
+  const int e0 = blockIdx.x * 32, i0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int r = ty; r < 32; r += 8) {
+    const int i = i0 + r, e = e0 + tx;
+    tile[r][tx] = (i < d && e < E) ? w[(int64_t)i * E + e] : 0.f;
+  }
+  __syncthreads();
+  for (int r = ty; r < 32; r += 8) {
+    const int e = e0 + r, i = i0 + tx;
+    if (e < E && i < d) {
+      const float v = tile[tx][r];
+      const bf16_t p1 = f2bf(v);
+      const float r1 = v - bf2f(p1);
+      const bf16_t p2 = f2bf(r1);
+      const float r2 = r1 - bf2f(p2);
+      const bf16_t p3 = f2bf(r2);
+      const int64_t o = (int64_t)e * d + i;
+      ws[o] = p1;
+      ws[(int64_t)E * d + o] = p2;
+      ws[2 * (int64_t)E * d + o] = p3;
+    }
+  }
+}
+
+// NTW: 16-expert MFMA tiles per wavefront.  Without SPLIT a block is 64 tokens
+// x 16*NTW experts (4 wavefronts stacked over tokens); with SPLIT it is 32
+// tokens x 32*NTW experts (2 x 2 wavefronts).
+template <int NTW, bool SPLIT>
+__global__ __launch_bounds__(256) void route_mfma_kernel(RouteArgs a) {
+  constexpr int TBM = SPLIT ? 32 : 64;
+  constexpr int EW = 16 * NTW;
+  constexpr int EB = SPLIT ? 2 * EW : EW;
+  constexpr int KC = 32;
+  constexpr int STAGE = 3 * EB * KC;  // bf16 elements
+  constexpr int NCH = STAGE / 8;               // 16-byte chunks per stage
+  constexpr int NB = (NCH + 255) / 256;       // per thread
+  constexpr int BYTES_STAGES = 2 * STAGE * 2;
+  constexpr int BYTES_TABLE = TBM * EB * 8;
+  constexpr int LDS = BYTES_STAGES > BYTES_TABLE ? BYTES_STAGES : BYTES_TABLE;
+  __shared__ __align__(16) unsigned char smem[LDS];
+  __shared__ int hist[256];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wt = SPLIT ? (wave >> 1) : wave;
+  const int we = SPLIT ? (wave & 1) : 0;
+  const int E = a.E, d = a.d;
+  const int64_t t0 = (int64_t)blockIdx.x * TBM;
+  const bf16_t* x = reinterpret_cast<const bf16_t*>(a.x);
+  const bf16_t* wsp = reinterpret_cast<const bf16_t*>(a.wsplit);
+  bf16_t* stage = reinterpret_cast<bf16_t*>(smem);
+
+  for (int e = tid; e < 256; e += 256) hist[e] = 0;
+
+  // A fragment source: token row (lane % 16) of this wavefront, 8 k at 8*(lane/16)
+  const int64_t trow = t0 + wt * 16 + (lane & 15);
+  const bool tok_ok = trow < a.T;
+  const bf16_t* xrow = x + (tok_ok ? trow : 0) * d + 8 * (lane >> 4);
+
+  // B staging: chunk q = tid + 256*i -> row (q / 4) of [3][EB], 16-byte chunk q % 4
+  const bf16_t* bsrc[NB];
+  int boff[NB];
+  bool bok[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int q0 = tid + 256 * i;
+    const bool inr = q0 < NCH;
+    const int q = inr ? q0 : 0;
+    const int row = q >> 2, c = q & 3;
+    const int p = row / EB, e = row - p * EB;
+    bok[i] = inr && e < E;
+    bsrc[i] = wsp + ((int64_t)p * E + (e < E ? e : 0)) * d + 8 * c;
+    boff[i] = inr ? row * KC + ((c ^ ((row >> 2) & 3)) << 3) : -1;
+  }
+  uint4 breg[NB];
+  uint4 areg;
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+      breg[i] = bok[i] ? *reinterpret_cast<const uint4*>(bsrc[i] + k0) : make_uint4(0, 0, 0, 0);
+    areg = tok_ok ? *reinterpret_cast<const uint4*>(xrow + k0) : make_uint4(0, 0, 0, 0);
+  };
+  auto store = [&](int buf) {
+    bf16_t* st = stage + buf * STAGE;
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+      if (boff[i] >= 0) *reinterpret_cast<uint4*>(st + boff[i]) = breg[i];
+  };
+
+  floatx4 acc[NTW];
+  double acc64[NTW][4];
+#pragma unroll
+  for (int j = 0; j < NTW; ++j) {
+    acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc64[j][v] = 0.0;
+  }
+  const int nk = d / KC;
+  load(0);
+  store(0);
+  uint4 acur = areg;
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) load((kt + 1) * KC);
+    const bf16_t* st = stage + cur * STAGE;
+    const bf16x8 af = __builtin_bit_cast(bf16x8, acur);
+#pragma unroll
+    for (int p = 0; p < 3; ++p) {
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        const int row = p * EB + we * EW + 16 * j + (lane & 15);
+        const int c = lane >> 4;
+        const bf16x8 bfr = *reinterpret_cast<const bf16x8*>(st + row * KC + ((c ^ ((row >> 2) & 3)) << 3));
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr, acc[j], 0, 0, 0);
+      }
+    }
+    if ((kt & 1) || kt + 1 == nk) {
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc64[j][v] += (double)acc[j][v];
+        acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    if (kt + 1 < nk) {
+      store(cur ^ 1);
+      acur = areg;
+    }
+    __syncthreads();
+  }
+
+  // logits -> LDS table [TBM][EB]
+  double* lg = reinterpret_cast<double*>(smem);
+#pragma unroll
+  for (int j = 0; j < NTW; ++j)
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      lg[(wt * 16 + 4 * (lane >> 4) + v) * EB + we * EW + 16 * j + (lane & 15)] = acc64[j][v];
+  __syncthreads();
+
+  select_tokens(a, lg, EB, t0, TBM, hist);
+  __syncthreads();
+  if (a.counts) {
+    for (int e = tid; e < E; e += 256)
+      if (hist[e]) atomicAdd(&a.counts[e], hist[e]);
+  }
+}
+
+int launch_route_mfma(const RouteArgs& a, hipStream_t s) {
+  {
+    dim3 grid((a.E + 31) / 32, (a.d + 31) / 32);
+    bf16_t* wsp = reinterpret_cast<bf16_t*>(a.wsplit);
+    const int st = launch(K_WR_SPLIT, s, "wr_split", [&] { wr_split_kernel<<<grid, 256, 0, s>>>(a.w_r, wsp, a.d, a.E); });
+    if (st) return st;
+  }
+#define MOE_RM(NTW_, SPLIT_, TBM_)                                                                           \
+  return launch(K_ROUTE, s, "route", [&] {                                                                   \
+    route_mfma_kernel<NTW_, SPLIT_><<<(int)((a.T + TBM_ - 1) / TBM_), 256, 0, s>>>(a);                       \
+  });
+  if (a.E <= 32) { MOE_RM(2, false, 64) }
+  if (a.E <= 64) { MOE_RM(4, false, 64) }
+  if (a.E <= 128) { MOE_RM(8, false, 64) }
+  MOE_RM(8, true, 32)
+#undef MOE_RM
 }
 
 __global__ void zero_i32_kernel(int32_t* p, int64_t n) {
@@ -300,6 +493,7 @@ int launch_route(const RouteArgs& a, hipStream_t s) {
     if (st) return st;
   }
   if (a.T == 0) return MOE_OK;
+  if (a.bf16 && a.wsplit && a.E % 16 == 0) return launch_route_mfma(a, s);
   return a.bf16 ? launch_route_t<bf16_t>(a, s) : launch_route_t<float>(a, s);
 }
 
