@@ -7,23 +7,21 @@
 // bf16 path (MFMA): one 256-thread workgroup computes a 128x128 output tile
 // with 4 wavefronts in a 2x2 arrangement (64x64 each, 4x4 blocks of
 // v_mfma_f32_16x16x32_bf16, float32 accumulators).  K advances 64 at a time
-// through two LDS buffers; the next tile's global loads are in flight while
-// the current one is multiplied.  Both operands sit in LDS as [row][64 k]
-// with the 16-byte chunk index XOR-swizzled by ((row>>1) ^ (row>>3)) & 7, so
-// that the MFMA fragment reads (16 rows, same chunk) and the transposing
-// stores of MN-contiguous operands both spread over the 64 LDS banks.
-// Operands that are contiguous along K are copied with 16-byte loads and
-// stores; operands contiguous along M or N (the weights in the forward, both
-// operands of the weight gradients) are loaded as 4 k-rows x 8 columns per
-// thread and transposed in registers before the LDS store.
+// through two LDS stages filled by buffer_load ... lds (global -> LDS without
+// registers); the next stage's copy runs while the current one is
+// multiplied.  Operands contiguous along K are read with ds_read_b128,
+// operands contiguous along M or N (the weights in the forward, both
+// operands of the weight gradients) with the transposing ds_read_b64_tr_b16,
+// so no operand is ever transposed in registers.
 //
 // Scheduling happens on the device from expert_offsets: a block derives the
 // per-expert m-tile prefix in LDS and finds its (expert, m-tile, n-tile), so
 // variable per-expert row counts need no host synchronisation; blocks beyond
-// the real tile count exit.  Rows past an expert's end, columns past N and
-// (for the weight gradients, whose K is the expert's row count) k past the
-// end are zero-filled on load and not stored.  Block ids are remapped so that
-// each XCD works on a contiguous range of tiles.
+// the real tile count exit.  Buffer descriptors bound each operand to its
+// expert's rows, so rows past an expert's end (and, for the weight gradients,
+// whose K is the expert's row count, k past the end) read as zero; outputs
+// past M or N are not stored.  Block ids are remapped so that each XCD works
+// on a contiguous range of tiles.
 //
 // fp32 path: a plain kernel, one thread per output (or output pair), for the
 // fp32 workload; same modes, same epilogues.
@@ -36,15 +34,34 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) void* lds_void_t;
+typedef __attribute__((address_space(3))) v4i16* lds_v4_t;
 
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int TILE_ELEMS = 128 * BK;
-
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 7; }
-// element offset of 16-byte chunk c (0..7) of row r
-__device__ __forceinline__ int lds_off(int r, int c) { return r * BK + ((c ^ swz(r)) << 3); }
+constexpr int BK = 64;            // k per LDS stage (4 MFMA k-steps of 16)
+constexpr int RSRC_FLAGS = 0x00020000;
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }
+
+template <int MODE>
+__host__ __device__ constexpr bool is_wgrad() { return MODE == G_WGRAD_DOWN || MODE == G_WGRAD_GATEUP; }
+
+// Tile shape: BM x BN outputs per workgroup, WM x WN wavefronts, S LDS stages.
+template <int BM_, int BN_, int WM_, int WN_, int S_>
+struct Cfg {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, S = S_;
+  static constexpr int NW = WM * WN, NT = 64 * NW;
+  static constexpr int TM = BM / WM, TN = BN / WN;  // wavefront tile
+  static constexpr int MI = TM / 32, NI = TN / 32;  // 32x32 MFMA blocks per wavefront
+  static constexpr int A_ELEMS = BM * BK, B_ELEMS = BN * BK;
+  static constexpr int STAGE_ELEMS = A_ELEMS + B_ELEMS;
+  static constexpr int LDS_BYTES = S * STAGE_ELEMS * 2;
+  static_assert(TM % 32 == 0 && TN % 32 == 0, "wavefront tile must be 32-aligned");
+  static_assert(S >= 2 && S <= 4, "2..4 stages");
+  static_assert(LDS_BYTES <= 150 * 1024, "LDS budget");
+};
 
 // ---------------------------------------------------------------------------
 // Tile decode
@@ -53,27 +70,34 @@ struct Tile {
   int g;          // expert
   int row_base;   // first row of the expert in the row-major activations
   int rows;       // rows of the expert (M for fwd/dgrad, K for wgrad)
-  int m0, n0;     // tile origin in the output
-  int ntile;      // n-tile index
+  int m0, n0;     // tile origin in the output (n0 in j units for FWD_GATEUP)
   bool live;
 };
 
+// Output columns covered by one tile, and number of n-tiles.
+template <int MODE, int BN>
+__host__ __device__ inline int tile_cols() { return MODE == G_FWD_GATEUP ? BN / 2 : BN; }
+template <int MODE, int BN>
+__host__ __device__ inline int n_tiles(int d, int f) {
+  const int N = (MODE == G_FWD_GATEUP || MODE == G_DGRAD_DOWN) ? f
+              : (MODE == G_WGRAD_GATEUP ? 2 * f : d);
+  return (N + tile_cols<MODE, BN>() - 1) / tile_cols<MODE, BN>();
+}
 template <int MODE>
+__host__ __device__ inline int wgrad_m(int d, int f) { return MODE == G_WGRAD_DOWN ? f : d; }
+
+template <int MODE, int BM, int BN>
 __device__ __forceinline__ Tile decode_tile(const GemmArgs& a, int* pre, int* sbuf) {
   Tile t;
-  constexpr bool wgrad = MODE == G_WGRAD_DOWN || MODE == G_WGRAD_GATEUP;
-  const int nb = gridDim.x;
-  const int lin = xcd_remap(blockIdx.x, nb);
-  if (wgrad) {
-    const int Mfix = MODE == G_WGRAD_DOWN ? a.f : a.d;
-    const int Nfix = MODE == G_WGRAD_DOWN ? a.d : 2 * a.f;
-    const int mt = (Mfix + BM - 1) / BM, nt = (Nfix + BN - 1) / BN;
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int nt = n_tiles<MODE, BN>(a.d, a.f);
+  if (is_wgrad<MODE>()) {
+    const int mt = (wgrad_m<MODE>(a.d, a.f) + BM - 1) / BM;
     t.g = lin / (mt * nt);
     const int rem = lin - t.g * mt * nt;
     const int im = rem / nt;
-    t.ntile = rem - im * nt;
     t.m0 = im * BM;
-    t.n0 = t.ntile * BN;
+    t.n0 = (rem - im * nt) * BN;
     if (a.offsets) {
       t.row_base = a.offsets[t.g];
       t.rows = a.offsets[t.g + 1] - t.row_base;
@@ -84,13 +108,8 @@ __device__ __forceinline__ Tile decode_tile(const GemmArgs& a, int* pre, int* sb
     t.live = t.g < (a.offsets ? a.ngroups : 1);
     return t;
   }
-  int ntiles;
-  if (MODE == G_FWD_GATEUP) ntiles = a.f / 64;
-  else if (MODE == G_FWD_DOWN || MODE == G_DGRAD_GATEUP) ntiles = (a.d + BN - 1) / BN;
-  else ntiles = (a.f + BN - 1) / BN;
-  const int mt = lin / ntiles;
-  t.ntile = lin - mt * ntiles;
-  t.n0 = t.ntile * (MODE == G_FWD_GATEUP ? 64 : BN);
+  const int mt = lin / nt;
+  t.n0 = (lin - mt * nt) * tile_cols<MODE, BN>();
   if (!a.offsets) {
     t.g = 0;
     t.row_base = 0;
@@ -121,101 +140,148 @@ __device__ __forceinline__ Tile decode_tile(const GemmArgs& a, int* pre, int* sb
 }
 
 // ---------------------------------------------------------------------------
-// Operand loaders (bf16).  Each thread moves 4 x 16 bytes per 128x64 tile.
+// bf16 operand staging.
+//
+// Every operand tile is copied global -> LDS by buffer_load_dwordx4 ... lds
+// (no registers): one instruction moves 64 lanes x 16 bytes into 1 KB of LDS
+// at the wave-uniform address in M0, so each lane picks the global chunk that
+// belongs at its LDS slot.  The copies are issued from inline assembly and
+// counted by hand (s_waitcnt vmcnt), so that up to S-1 stages can be in
+// flight while the compiler keeps scheduling the LDS fragment reads freely;
+// the main loop issues no other vector-memory instruction.  A buffer
+// descriptor spans exactly the valid rows of the operand (one expert's rows,
+// or one expert's weight matrix), so reads past the last row return zeros:
+// ragged expert tails and the weight gradients' K-tail need no masking.
+//
+// K-contiguous tiles (rows x 64 k): row = 128 bytes = 8 chunks of 16 bytes,
+// chunk index XOR-swizzled by kswz(row); fragments read with ds_read_b128
+// (16 consecutive rows, one chunk: 16 distinct bank groups).
+// MN-contiguous tiles (64 k x columns): sub-tiles of 64 columns, row = 8
+// chunks, chunk index XOR-swizzled by mswz(k); fragments read with
+// ds_read_b64_tr_b16, whose lane i of each 16-lane group returns column i of
+// a 4 (k) x 16 (columns) block addressed by its 16 lanes.  The swizzle spreads
+// one read (8 k-rows x 4 chunks) evenly over the banks.
 // ---------------------------------------------------------------------------
+typedef int int32x4_t __attribute__((ext_vector_type(4)));
 
-// K-contiguous source: row r of the tile starts at rowptr[i] (+ k0).
-struct KLoader {
-  const bf16_t* ptr[4];
-  bool ok[4];
-  int lds[4];
-  uint4 reg[4];
-  __device__ __forceinline__ void load(int k0) {
+__device__ __forceinline__ int kswz(int r) { return ((r >> 1) ^ (r >> 3)) & 7; }
+__device__ __forceinline__ int k_off(int r, int c) { return r * BK + ((c ^ kswz(r)) << 3); }
+__device__ __forceinline__ int mswz(int k) { return ((k >> 1) & 1) << 2; }
+__device__ __forceinline__ int mn_off(int k, int col) {
+  return (col >> 6) * (64 * BK) + k * 64 + ((((col & 63) >> 3) ^ mswz(k)) << 3) + (col & 7);
+}
+
+// Buffer descriptor (raw buffer, no stride) over [p, p + bytes), in SGPRs.
+__device__ __forceinline__ int32x4_t make_rsrc(const void* p, int64_t bytes) {
+  const uint64_t b = (uint64_t)p;
+  int32x4_t r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(b >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane((int)(uint32_t)bytes);
+  r[3] = RSRC_FLAGS;
+  return r;
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16_t*)p);
+}
+
+__device__ __forceinline__ void dma16(const int32x4_t& r, uint32_t lds, uint32_t voff, uint32_t soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory");
+}
+
+// s_waitcnt vmcnt(n), expcnt and lgkmcnt left free
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | 0x0F70);
+}
+
+// This wave's share of one K-contiguous ROWS x 64 tile.
+template <int ROWS, int NW>
+struct KOperand {
+  static constexpr int NIW = ROWS / (8 * NW);  // instructions per wave
+  int32x4_t rsrc;
+  uint32_t voff[NIW];
+  __device__ __forceinline__ void init(int wave, int lane, int row0, int ld) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      reg[i] = ok[i] ? *reinterpret_cast<const uint4*>(ptr[i] + k0) : make_uint4(0, 0, 0, 0);
+    for (int j = 0; j < NIW; ++j) {
+      const int q = (NIW * wave + j) * 64 + lane;
+      const int row = q >> 3, phys = q & 7;
+      voff[j] = (uint32_t)(((int64_t)(row0 + row) * ld + 8 * (phys ^ kswz(row))) * 2);
+    }
   }
-  __device__ __forceinline__ void store(bf16_t* tile) {
+  __device__ __forceinline__ void issue(uint32_t tile, int wave, uint32_t soff) const {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) *reinterpret_cast<uint4*>(tile + lds[i]) = reg[i];
+    for (int j = 0; j < NIW; ++j) dma16(rsrc, tile + (NIW * wave + j) * 1024, voff[j], soff);
   }
 };
 
-// MN-contiguous source [K][ld]: thread owns 8 columns (one 16-byte chunk)
-// and 4 consecutive k rows of the tile; stores them transposed.
-struct MNLoader {
-  const bf16_t* col;   // element (k=0, this thread's first column), k rows ld apart
-  int64_t ld;
-  bool colok;
-  int kbase;           // 4*kg: first k row of this thread inside the tile
-  int klimit;          // rows valid (k < klimit), relative to the tile start
-  int lds[8];          // LDS element offsets of columns c = 0..7 (+ k position)
-  uint4 reg[4];
-  __device__ __forceinline__ void load(int k0) {  // k0: tile start (relative)
+// This wave's share of one MN-contiguous 64 x (64*NSUB) tile; sub-tile s
+// comes from descriptor rsrc[s] starting at column col0[s].
+template <int NSUB, int NW>
+struct MNOperand {
+  static constexpr int NIW = 8 / NW;  // instructions per wave per sub-tile
+  int32x4_t rsrc[NSUB];
+  uint32_t voff[NSUB][NIW];
+  __device__ __forceinline__ void init(int wave, int lane, const int* col0, int ld) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int k = k0 + kbase + q;
-      reg[q] = (colok && k < klimit) ? *reinterpret_cast<const uint4*>(col + (int64_t)k * ld)
-                                     : make_uint4(0, 0, 0, 0);
-    }
-  }
-  __device__ __forceinline__ void store(bf16_t* tile) {
-    const uint32_t* r0 = reinterpret_cast<const uint32_t*>(&reg[0]);
-    const uint32_t* r1 = reinterpret_cast<const uint32_t*>(&reg[1]);
-    const uint32_t* r2 = reinterpret_cast<const uint32_t*>(&reg[2]);
-    const uint32_t* r3 = reinterpret_cast<const uint32_t*>(&reg[3]);
+    for (int s = 0; s < NSUB; ++s)
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int w = c >> 1;
-      uint32_t lo, hi;
-      if (c & 1) {
-        lo = (r0[w] >> 16) | (r1[w] & 0xffff0000u);
-        hi = (r2[w] >> 16) | (r3[w] & 0xffff0000u);
-      } else {
-        lo = (r0[w] & 0xffffu) | (r1[w] << 16);
-        hi = (r2[w] & 0xffffu) | (r3[w] << 16);
+      for (int j = 0; j < NIW; ++j) {
+        const int q = (NIW * wave + j) * 64 + lane;
+        const int krow = q >> 3, phys = q & 7;
+        voff[s][j] = (uint32_t)(((int64_t)krow * ld + col0[s] + 8 * (phys ^ mswz(krow))) * 2);
       }
-      *reinterpret_cast<uint2*>(tile + lds[c]) = make_uint2(lo, hi);
-    }
+  }
+  __device__ __forceinline__ void issue(uint32_t tile, int wave, uint32_t soff) const {
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+      for (int j = 0; j < NIW; ++j) dma16(rsrc[s], tile + s * 8192 + (NIW * wave + j) * 1024, voff[s][j], soff);
   }
 };
 
-__device__ __forceinline__ void kloader_init(KLoader& L, int tid) {
-  const int c = tid & 7;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = (tid >> 3) + 32 * i;
-    L.lds[i] = lds_off(r, c);
-  }
+// 32x32x16 fragments.  K-contiguous: rows rb*32 + lane%32, k = ks*16 + 8*(lane/32) .. +7.
+__device__ __forceinline__ bf16x8 frag_k(const bf16_t* tile, int rb, int ks, int lane) {
+  return *reinterpret_cast<const bf16x8*>(tile + k_off(rb * 32 + (lane & 31), 2 * ks + (lane >> 5)));
 }
-
-__device__ __forceinline__ void mnloader_init(MNLoader& L, int tid) {
-  const int nc = tid & 15, kg = tid >> 4;
-  L.kbase = 4 * kg;
-#pragma unroll
-  for (int c = 0; c < 8; ++c) L.lds[c] = lds_off(8 * nc + c, kg >> 1) + 4 * (kg & 1);
+// MN-contiguous: columns cb*32 + lane%32, same k.
+__device__ __forceinline__ bf16x8 frag_mn(const bf16_t* tile, int cb, int ks, int lane) {
+  const int G = lane >> 4, r = lane & 15;
+  const int k = ks * 16 + 8 * (G >> 1) + (r >> 2);
+  const int col = cb * 32 + 16 * (G & 1) + 4 * (r & 3);
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4_t)(tile + mn_off(k, col)));
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4_t)(tile + mn_off(k + 4, col)));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 // ---------------------------------------------------------------------------
-// The bf16 MFMA kernel
+// The bf16 MFMA kernel: BM x BN output tile, WM x WN wavefronts, each
+// BM/WM x BN/WN as blocks of v_mfma_f32_32x32x16_bf16, S-stage LDS pipeline.
 // ---------------------------------------------------------------------------
-template <int MODE>
-__global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs a) {
-  __shared__ __align__(16) bf16_t lds[2][2][TILE_ELEMS];
+template <int MODE, class C>
+__global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
+  constexpr bool wgrad = is_wgrad<MODE>();
+  constexpr bool a_mn = wgrad;                                               // A tile MN-contiguous
+  constexpr bool b_mn = MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN || wgrad;  // B tile MN-contiguous
+  constexpr int BM = C::BM, BN = C::BN, MI = C::MI, NI = C::NI, S = C::S, NW = C::NW;
+  static_assert(MODE != G_FWD_GATEUP || NI % 2 == 0, "gate/up pairs need an even number of column blocks");
+  __shared__ __align__(16) bf16_t lds[S][C::STAGE_ELEMS];
   __shared__ int pre[257];
   __shared__ int sbuf[256];
-  constexpr bool wgrad = MODE == G_WGRAD_DOWN || MODE == G_WGRAD_GATEUP;
 
-  const Tile tl = decode_tile<MODE>(a, pre, sbuf);
+  const Tile tl = decode_tile<MODE, BM, BN>(a, pre, sbuf);
   if (!tl.live) return;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / C::WN, wn = wave % C::WN;
   const int d = a.d, f = a.f;
   const int g = tl.g;
+  const int l32 = lane & 31;
 
-  // problem extents
   int K, M, N;
   if (MODE == G_FWD_GATEUP) { K = d; M = tl.rows; N = f; }
   else if (MODE == G_FWD_DOWN) { K = f; M = tl.rows; N = d; }
@@ -229,135 +295,157 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs a) {
   const bf16_t* W0 = reinterpret_cast<const bf16_t*>(a.w0);
   const bf16_t* W1 = reinterpret_cast<const bf16_t*>(a.w1);
 
-  // ---- operand A
-  KLoader la;
-  MNLoader ma;
-  if (!wgrad) {
-    kloader_init(la, tid);
+  // ---- operand A (BM rows of the output)
+  KOperand<BM, NW> ka;
+  MNOperand<BM / 64, NW> ma;
+  int64_t a_kstride;  // soffset = k0 * a_kstride
+  if (!a_mn) {
     const int lda = MODE == G_FWD_DOWN ? f : (MODE == G_DGRAD_GATEUP ? 2 * f : d);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = tl.m0 + (tid >> 3) + 32 * i;
-      la.ok[i] = r < M;
-      la.ptr[i] = A + (int64_t)(tl.row_base + (r < M ? r : 0)) * lda + 8 * (tid & 7);
-    }
+    ka.rsrc = make_rsrc(A + (int64_t)tl.row_base * lda, (int64_t)M * lda * 2);
+    ka.init(wave, lane, tl.m0, lda);
+    a_kstride = 2;
   } else {
-    mnloader_init(ma, tid);
     const int lda = MODE == G_WGRAD_DOWN ? f : d;  // h rows [f] or x_perm rows [d]
-    const int col = tl.m0 + 8 * (tid & 15);
-    ma.colok = col < M;
-    ma.col = A + (int64_t)tl.row_base * lda + (ma.colok ? col : 0);
-    ma.ld = lda;
-    ma.klimit = K;
-  }
-  // ---- operand B
-  KLoader lb;
-  MNLoader mb;
-  const bf16_t* bk_gate = nullptr;  // DGRAD_GATEUP: per-row pointers into W_gate / W_up
-  const bf16_t* bk_up = nullptr;
-  if (MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN) {
-    mnloader_init(mb, tid);
-    const int nc = tid & 15;
-    if (MODE == G_FWD_GATEUP) {
-      // tile columns: wave-column wn holds 32 gate then 32 up columns of the
-      // same 32 j's; chunk nc -> j = n0 + 32*(nc/8) + 16*((nc%8)/2 % 2) + 8*(nc%2)
-      const int q = nc & 7;
-      const int j = tl.n0 + 32 * (nc >> 3) + 16 * ((q >> 1) & 1) + 8 * (q & 1);
-      const bf16_t* W = (q >> 2) ? W1 : W0;
-      mb.col = W + (int64_t)g * d * f + j;
-      mb.ld = f;
-      mb.colok = true;
-    } else {
-      const int n = tl.n0 + 8 * nc;
-      mb.colok = n < N;
-      mb.col = W0 + (int64_t)g * f * d + (mb.colok ? n : 0);
-      mb.ld = d;
-    }
-    mb.klimit = K;
-  } else if (MODE == G_DGRAD_DOWN || MODE == G_DGRAD_GATEUP) {
-    kloader_init(lb, tid);
+    const int32x4_t r = make_rsrc(A + (int64_t)tl.row_base * lda, (int64_t)K * lda * 2);
+    int col0[BM / 64];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int n = tl.n0 + (tid >> 3) + 32 * i;
-      lb.ok[i] = n < N;
-      const int nn = n < N ? n : 0;
-      if (MODE == G_DGRAD_DOWN)  // B[k=i][n=j] = W_down[g][j][i]
-        lb.ptr[i] = W0 + (int64_t)g * f * d + (int64_t)nn * d + 8 * (tid & 7);
-      else  // B[k=j][n=i] = W_gate[g][i][j] (k < f) or W_up[g][i][j-f]
-        lb.ptr[i] = W0 + (int64_t)g * d * f + (int64_t)nn * f + 8 * (tid & 7);
+    for (int s2 = 0; s2 < BM / 64; ++s2) {
+      ma.rsrc[s2] = r;
+      col0[s2] = tl.m0 + 64 * s2;
     }
-    if (MODE == G_DGRAD_GATEUP) {
-      bk_gate = W0;
-      bk_up = W1;
+    ma.init(wave, lane, col0, lda);
+    a_kstride = (int64_t)lda * 2;
+  }
+  // ---- operand B (BN columns of the output)
+  KOperand<BN, NW> kb;
+  MNOperand<BN / 64, NW> mb;
+  int64_t b_kstride;
+  int32x4_t b_up = make_rsrc(W0, 0);  // DGRAD_GATEUP: W_up rows for k >= f
+  if (MODE == G_FWD_GATEUP) {  // sub-tiles 0 .. BN/128-1: W_gate columns, then W_up columns
+    const int32x4_t rg = make_rsrc(W0 + (int64_t)g * d * f, (int64_t)d * f * 2);
+    const int32x4_t ru = make_rsrc(W1 + (int64_t)g * d * f, (int64_t)d * f * 2);
+    int col0[BN / 64];
+#pragma unroll
+    for (int s2 = 0; s2 < BN / 64; ++s2) {
+      const bool up = s2 >= BN / 128;
+      mb.rsrc[s2] = up ? ru : rg;
+      col0[s2] = tl.n0 + 64 * (up ? s2 - BN / 128 : s2);
     }
+    mb.init(wave, lane, col0, f);
+    b_kstride = (int64_t)f * 2;
+  } else if (MODE == G_FWD_DOWN) {
+    const int32x4_t r = make_rsrc(W0 + (int64_t)g * f * d, (int64_t)f * d * 2);
+    int col0[BN / 64];
+#pragma unroll
+    for (int s2 = 0; s2 < BN / 64; ++s2) {
+      mb.rsrc[s2] = r;
+      col0[s2] = tl.n0 + 64 * s2;
+    }
+    mb.init(wave, lane, col0, d);
+    b_kstride = (int64_t)d * 2;
+  } else if (MODE == G_DGRAD_DOWN) {  // B[k=i][n=j] = W_down[g][j][i]: rows j of length d
+    kb.rsrc = make_rsrc(W0 + (int64_t)g * f * d, (int64_t)f * d * 2);
+    kb.init(wave, lane, tl.n0, d);
+    b_kstride = 2;
+  } else if (MODE == G_DGRAD_GATEUP) {  // B[k=j][n=i] = W_gate[g][i][j] (k < f), W_up[g][i][j-f]
+    kb.rsrc = make_rsrc(W0 + (int64_t)g * d * f, (int64_t)d * f * 2);
+    b_up = make_rsrc(W1 + (int64_t)g * d * f, (int64_t)d * f * 2);
+    kb.init(wave, lane, tl.n0, f);
+    b_kstride = 2;
   } else {
-    mnloader_init(mb, tid);
     const int ldb = MODE == G_WGRAD_DOWN ? d : 2 * f;  // d_o rows or dgu rows
-    const int n = tl.n0 + 8 * (tid & 15);
-    mb.colok = n < N;
-    mb.col = Bact + (int64_t)tl.row_base * ldb + (mb.colok ? n : 0);
-    mb.ld = ldb;
-    mb.klimit = K;
+    const int32x4_t r = make_rsrc(Bact + (int64_t)tl.row_base * ldb, (int64_t)K * ldb * 2);
+    int col0[BN / 64];
+#pragma unroll
+    for (int s2 = 0; s2 < BN / 64; ++s2) {
+      mb.rsrc[s2] = r;
+      col0[s2] = tl.n0 + 64 * s2;
+    }
+    mb.init(wave, lane, col0, ldb);
+    b_kstride = (int64_t)ldb * 2;
   }
+  // DMA instructions per thread per stage
+  constexpr int NL = (a_mn ? (BM / 64) * (8 / NW) : BM / (8 * NW)) + (b_mn ? (BN / 64) * (8 / NW) : BN / (8 * NW));
 
-  floatx4 acc[4][4];
+  floatx16 acc[MI][NI];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NI; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   // bias-gradient column sums (weight-gradient passes, first m-tile, wm == 0)
   const bool colsum = wgrad && a.db0 && tl.m0 == 0 && wm == 0;
-  float bsum[4] = {0.f, 0.f, 0.f, 0.f};
-
-  auto load_tile = [&](int k0) {
-    if (!wgrad) la.load(k0); else ma.load(k0);
-    if (MODE == G_DGRAD_GATEUP) {
-      // whole k-tile lies in W_gate (k0 < f) or in W_up; f % 64 == 0
-      const int64_t shift = (k0 < f) ? (int64_t)k0 : (int64_t)(k0 - f) + (bk_up - bk_gate);
+  float bsum[NI];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        lb.reg[i] = lb.ok[i] ? *reinterpret_cast<const uint4*>(lb.ptr[i] + shift) : make_uint4(0, 0, 0, 0);
+  for (int j = 0; j < NI; ++j) bsum[j] = 0.f;
+
+  const uint32_t lds0 = lds_addr(&lds[0][0]);
+  auto issue_tile = [&](int k0, int buf) {
+    const uint32_t As = lds0 + buf * (C::STAGE_ELEMS * 2);
+    const uint32_t Bs = As + C::A_ELEMS * 2;
+    if (!a_mn) ka.issue(As, wave, (uint32_t)(k0 * a_kstride));
+    else ma.issue(As, wave, (uint32_t)(k0 * a_kstride));
+    if (MODE == G_DGRAD_GATEUP) {
+      KOperand<BN, NW> kk = kb;
+      if (k0 >= f) kk.rsrc = b_up;
+      kk.issue(Bs, wave, (uint32_t)((k0 >= f ? k0 - f : k0) * b_kstride));
     } else if (MODE == G_DGRAD_DOWN) {
-      lb.load(k0);
+      kb.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
     } else {
-      mb.load(k0);
+      mb.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
     }
   };
-  auto store_tile = [&](int buf) {
-    if (!wgrad) la.store(lds[buf][0]); else ma.store(lds[buf][0]);
-    if (MODE == G_DGRAD_DOWN || MODE == G_DGRAD_GATEUP) lb.store(lds[buf][1]); else mb.store(lds[buf][1]);
+  // tile-local 32-column block of this wave's fragment j (FWD_GATEUP: first
+  // half gate columns, second half the matching up columns)
+  auto bcol = [&](int j) {
+    if (MODE == G_FWD_GATEUP)
+      return (j < NI / 2) ? (wn * (NI / 2) + j) : (BN / 64 + wn * (NI / 2) + (j - NI / 2));
+    return wn * NI + j;
   };
 
   const int nk = (K + BK - 1) / BK;
-  if (nk > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
-  __syncthreads();
-  const int r16 = lane & 15, kq = lane >> 4;
+#pragma unroll
+  for (int p = 0; p < S - 1; ++p)
+    if (p < nk) issue_tile(p * BK, p);
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) load_tile((kt + 1) * BK);
-    const bf16_t* As = lds[cur][0];
-    const bf16_t* Bs = lds[cur][1];
+    // tiles issued after kt that may still be in flight
+    const int ahead = min(S - 2, nk - 1 - kt);
+    if (S >= 4 && ahead >= 2) wait_vmcnt<(S >= 4 ? 2 : 0) * NL>();
+    else if (S >= 3 && ahead >= 1) wait_vmcnt<(S >= 3 ? 1 : 0) * NL>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (kt + S - 1 < nk) issue_tile((kt + S - 1) * BK, (kt + S - 1) % S);
+    const bf16_t* As = lds[kt % S];
+    const bf16_t* Bs = As + C::A_ELEMS;
+    // fragments double-buffered in registers: step ks+1 is read while the
+    // MFMAs of step ks run (the scheduling barriers keep that order)
+    bf16x8 af[2][MI], bfr[2][NI];
+    auto load_frags = [&](int ks, int slot) {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 af[4], bfr[4];
+      for (int i = 0; i < MI; ++i)
+        af[slot][i] = a_mn ? frag_mn(As, wm * MI + i, ks, lane) : frag_k(As, wm * MI + i, ks, lane);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        af[i] = *reinterpret_cast<const bf16x8*>(As + lds_off(wm * 64 + i * 16 + r16, ks * 4 + kq));
-        bfr[i] = *reinterpret_cast<const bf16x8*>(Bs + lds_off(wn * 64 + i * 16 + r16, ks * 4 + kq));
-      }
+      for (int j = 0; j < NI; ++j)
+        bfr[slot][j] = b_mn ? frag_mn(Bs, bcol(j), ks, lane) : frag_k(Bs, bcol(j), ks, lane);
+    };
+    load_frags(0, 0);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int ks = 0; ks < 4; ++ks) {
+      const int cur = ks & 1;
+      if (ks < 3) load_frags(ks + 1, cur ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
       if (colsum) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint4 u = __builtin_bit_cast(uint4, bfr[j]);
+        for (int j = 0; j < NI; ++j) {
+          const uint4 u = __builtin_bit_cast(uint4, bfr[cur][j]);
           const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
           for (int q = 0; q < 4; ++q)
@@ -365,107 +453,181 @@ __global__ __launch_bounds__(256, 2) void gemm_bf16_kernel(GemmArgs a) {
         }
       }
     }
-    if (kt + 1 < nk) store_tile(cur ^ 1);
-    __syncthreads();
   }
 
-  // ---- epilogue
-  const int rq = 4 * (lane >> 4);  // row offset of this lane's 4 values in a 16x16 block
+  // ---- epilogue.  With the operands swapped in the MFMA, block (i, j) holds
+  // the transposed product: lane l has output row 32i + l%32 and, in register
+  // v = 4q + t, column 32j + 8q + 4(l/32) + t.  Each lane applies the fused
+  // epilogue math to its values, writes them (bf16, 4 columns = 8 bytes at a
+  // time) into its wavefront's LDS staging area, and the wavefront then
+  // writes whole rows to global memory with 16-byte stores.
+  __syncthreads();  // every wavefront is done with the LDS stages
+  constexpr int TN_OUT = MODE == G_FWD_GATEUP ? C::TN / 2 : C::TN;  // columns per output matrix
+  constexpr int CPR = TN_OUT / 8;                                    // 16-byte chunks per row
+  static_assert(C::NW * C::TM * TN_OUT * 2 * (MODE == G_FWD_GATEUP ? 2 : 1) <= C::LDS_BYTES, "staging fits");
+  const int lrow = lane & 31, hh = lane >> 5;
+  bf16_t* stg = &lds[0][0] + wave * (C::TM * TN_OUT * (MODE == G_FWD_GATEUP ? 2 : 1));
+  // staging layout [TM][TN_OUT], 16-byte chunk index XOR-swizzled by row & 7
+  auto st_off = [&](int r, int c) { return r * TN_OUT + ((((c >> 3) ^ (r & 7)) % CPR) << 3) + (c & 7); };
+  auto put4 = [&](bf16_t* base, int r, int c, float v0, float v1, float v2, float v3) {
+    const uint32_t lo = (uint32_t)f2bf(v0) | ((uint32_t)f2bf(v1) << 16);
+    const uint32_t hi = (uint32_t)f2bf(v2) | ((uint32_t)f2bf(v3) << 16);
+    *reinterpret_cast<uint2*>(base + st_off(r, c)) = make_uint2(lo, hi);
+  };
+  // write the staged [TM][TN_OUT] tile: row r -> dst_row(r) (or skip), column c -> dst_col(c)
+  auto flush = [&](const bf16_t* base, auto&& dst) {
+    __syncthreads();
+#pragma unroll 4
+    for (int idx = lane; idx < C::TM * CPR; idx += 64) {
+      const int r = idx / CPR, c = (idx % CPR) * 8;
+      const uint4 v = *reinterpret_cast<const uint4*>(base + st_off(r, c));
+      bf16_t* p = dst(r, c);
+      if (p) *reinterpret_cast<uint4*>(p) = v;
+    }
+  };
+  const int mrow0 = tl.m0 + wm * C::TM;  // first output row of this wavefront
   if (MODE == G_FWD_GATEUP) {
     bf16_t* gu = reinterpret_cast<bf16_t*>(a.c0);
     bf16_t* h = reinterpret_cast<bf16_t*>(a.c1);
     const bf16_t* bgp = reinterpret_cast<const bf16_t*>(a.bias0);
     const bf16_t* bup = reinterpret_cast<const bf16_t*>(a.bias1);
+    bf16_t* sg = stg;                          // [TM][TN_OUT] gate, then up at + TM*TN_OUT
+    const int jbase = tl.n0 + wn * TN_OUT;     // first j of this wavefront
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = tl.n0 + wn * 32 + j * 16 + r16;
-      const float bg = bgp ? bf2f(bgp[(int64_t)g * f + col]) : 0.f;
-      const float bu = bup ? bf2f(bup[(int64_t)g * f + col]) : 0.f;
+    for (int j = 0; j < NI / 2; ++j)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int q = 0; q < 4; ++q) {
+        const int c = 32 * j + 8 * q + 4 * hh;   // local column of values t = 0..3
+        float bgv[4] = {0.f, 0.f, 0.f, 0.f}, buv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (bgp && jbase + c < N) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int m = tl.m0 + wm * 64 + i * 16 + rq + v;
-          if (m < M) {
-            const int64_t row = tl.row_base + m;
-            const float gv = acc[i][j][v] + bg;
-            const float uv = acc[i][j + 2][v] + bu;
-            gu[row * 2 * f + col] = f2bf(gv);
-            gu[row * 2 * f + f + col] = f2bf(uv);
-            h[row * f + col] = f2bf(silu_f(gv) * uv);
+          for (int t = 0; t < 4; ++t) {
+            bgv[t] = bf2f(bgp[(int64_t)g * f + jbase + c + t]);
+            buv[t] = bf2f(bup[(int64_t)g * f + jbase + c + t]);
           }
         }
-    }
-  } else if (MODE == G_FWD_DOWN || MODE == G_DGRAD_GATEUP) {
-    bf16_t* out = reinterpret_cast<bf16_t*>(a.c0);
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const int r = 32 * i + lrow;
+          float gv[4], uv[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            gv[t] = acc[i][j][4 * q + t] + bgv[t];
+            uv[t] = acc[i][j + NI / 2][4 * q + t] + buv[t];
+          }
+          put4(sg, r, c, gv[0], gv[1], gv[2], gv[3]);
+          put4(sg + C::TM * TN_OUT, r, c, uv[0], uv[1], uv[2], uv[3]);
+          // h overwrites the accumulators of the gate block (already staged)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) acc[i][j][4 * q + t] = silu_f(gv[t]) * uv[t];
+        }
+      }
+    auto dst_gu = [&](int half) {
+      return [&, half](int r, int c) -> bf16_t* {
+        const int m = mrow0 + r, jj = jbase + c;
+        if (m >= M || jj >= N) return nullptr;
+        return gu + (int64_t)(tl.row_base + m) * 2 * f + half * f + jj;
+      };
+    };
+    flush(sg, dst_gu(0));
+    flush(sg + C::TM * TN_OUT, dst_gu(1));
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NI / 2; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+          put4(sg, 32 * i + lrow, 32 * j + 8 * q + 4 * hh, acc[i][j][4 * q], acc[i][j][4 * q + 1],
+               acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+    flush(sg, [&](int r, int c) -> bf16_t* {
+      const int m = mrow0 + r, jj = jbase + c;
+      if (m >= M || jj >= N) return nullptr;
+      return h + (int64_t)(tl.row_base + m) * f + jj;
+    });
+  } else if (MODE == G_FWD_DOWN || MODE == G_DGRAD_GATEUP || MODE == G_DGRAD_DOWN) {
+    const int nbase = tl.n0 + wn * C::TN;
     const bf16_t* bdp = MODE == G_FWD_DOWN ? reinterpret_cast<const bf16_t*>(a.bias0) : nullptr;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = tl.n0 + wn * 64 + j * 16 + r16;
-      if (col >= N) continue;
-      const float bd = bdp ? bf2f(bdp[(int64_t)g * d + col]) : 0.f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int m = tl.m0 + wm * 64 + i * 16 + rq + v;
-          if (m < M) out[(int64_t)(tl.row_base + m) * N + col] = f2bf(acc[i][j][v] + bd);
-        }
-    }
-  } else if (MODE == G_DGRAD_DOWN) {
     const bf16_t* gu = reinterpret_cast<const bf16_t*>(a.aux);
-    bf16_t* dgu = reinterpret_cast<bf16_t*>(a.c0);
+    bf16_t* out = reinterpret_cast<bf16_t*>(a.c0);
+    // DGRAD_DOWN writes dg then du (two staged passes); the others one
+    constexpr int PASSES = MODE == G_DGRAD_DOWN ? 2 : 1;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = tl.n0 + wn * 64 + j * 16 + r16;
-      if (col >= N) continue;
+    for (int pass = 0; pass < PASSES; ++pass) {
+      if (pass) __syncthreads();
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < NI; ++j)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int m = tl.m0 + wm * 64 + i * 16 + rq + v;
-          if (m < M) {
-            const int64_t row = tl.row_base + m;
-            const float gv = bf2f(gu[row * 2 * f + col]);
-            const float uv = bf2f(gu[row * 2 * f + f + col]);
-            const float sg = 1.0f / (1.0f + __expf(-gv));
-            const float dh = acc[i][j][v];
-            dgu[row * 2 * f + col] = f2bf(dh * uv * sg * (1.0f + gv * (1.0f - sg)));
-            dgu[row * 2 * f + f + col] = f2bf(dh * gv * sg);
+        for (int q = 0; q < 4; ++q) {
+          const int c = 32 * j + 8 * q + 4 * hh;
+          const bool cok = nbase + c < N;
+          float bd[4] = {0.f, 0.f, 0.f, 0.f};
+          if (bdp && cok) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) bd[t] = bf2f(bdp[(int64_t)g * d + nbase + c + t]);
+          }
+#pragma unroll
+          for (int i = 0; i < MI; ++i) {
+            const int r = 32 * i + lrow;
+            float o[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) o[t] = acc[i][j][4 * q + t] + bd[t];
+            if (MODE == G_DGRAD_DOWN) {
+              const int m = mrow0 + r;
+              float gv[4] = {0.f, 0.f, 0.f, 0.f}, uv[4] = {0.f, 0.f, 0.f, 0.f};
+              if (m < M && cok) {
+                const int64_t row = tl.row_base + m;
+                const uint2 gr = *reinterpret_cast<const uint2*>(gu + row * 2 * f + nbase + c);
+                const uint2 ur = *reinterpret_cast<const uint2*>(gu + row * 2 * f + f + nbase + c);
+                gv[0] = __uint_as_float(gr.x << 16); gv[1] = __uint_as_float(gr.x & 0xffff0000u);
+                gv[2] = __uint_as_float(gr.y << 16); gv[3] = __uint_as_float(gr.y & 0xffff0000u);
+                uv[0] = __uint_as_float(ur.x << 16); uv[1] = __uint_as_float(ur.x & 0xffff0000u);
+                uv[2] = __uint_as_float(ur.y << 16); uv[3] = __uint_as_float(ur.y & 0xffff0000u);
+              }
+#pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                const float sgm = 1.0f / (1.0f + __expf(-gv[t]));
+                o[t] = pass == 0 ? o[t] * uv[t] * sgm * (1.0f + gv[t] * (1.0f - sgm))   // dg
+                                 : o[t] * gv[t] * sgm;                                    // du
+              }
+            }
+            put4(stg, r, c, o[0], o[1], o[2], o[3]);
           }
         }
+      flush(stg, [&](int r, int c) -> bf16_t* {
+        const int m = mrow0 + r, n = nbase + c;
+        if (m >= M || n >= N) return nullptr;
+        if (MODE == G_DGRAD_DOWN) return out + (int64_t)(tl.row_base + m) * 2 * f + pass * f + n;
+        return out + (int64_t)(tl.row_base + m) * N + n;
+      });
     }
   } else {
     // weight gradients of expert g: [M][N] at c0 (+ c1 for the up half)
+    const int nbase = tl.n0 + wn * C::TN;
     bf16_t* c0 = reinterpret_cast<bf16_t*>(a.c0);
     bf16_t* c1 = reinterpret_cast<bf16_t*>(a.c1);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = tl.n0 + wn * 64 + j * 16 + r16;
-      if (col >= N) continue;
+    for (int j = 0; j < NI; ++j)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int m = tl.m0 + wm * 64 + i * 16 + rq + v;
-          if (m >= M) continue;
-          if (MODE == G_WGRAD_DOWN) {
-            c0[((int64_t)g * f + m) * d + col] = f2bf(acc[i][j][v]);
-          } else if (col < f) {
-            c0[((int64_t)g * d + m) * f + col] = f2bf(acc[i][j][v]);
-          } else {
-            c1[((int64_t)g * d + m) * f + (col - f)] = f2bf(acc[i][j][v]);
-          }
-        }
-    }
+        for (int i = 0; i < MI; ++i)
+          put4(stg, 32 * i + lrow, 32 * j + 8 * q + 4 * hh, acc[i][j][4 * q], acc[i][j][4 * q + 1],
+               acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+    flush(stg, [&](int r, int c) -> bf16_t* {
+      const int m = mrow0 + r, n = nbase + c;
+      if (m >= M || n >= N) return nullptr;
+      if (MODE == G_WGRAD_DOWN) return c0 + ((int64_t)g * f + m) * d + n;
+      if (n < f) return c0 + ((int64_t)g * d + m) * f + n;
+      return c1 + ((int64_t)g * d + m) * f + (n - f);
+    });
     if (colsum) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < NI; ++j) {
         float v = bsum[j];
-        v += __shfl_xor(v, 16, 64);
         v += __shfl_xor(v, 32, 64);
-        const int col = tl.n0 + wn * 64 + j * 16 + r16;
-        if (lane < 16 && col < N) {
+        const int col = tl.n0 + wn * C::TN + j * 32 + l32;
+        if (lane < 32 && col < N) {
           if (MODE == G_WGRAD_DOWN) {
             reinterpret_cast<bf16_t*>(a.db0)[(int64_t)g * d + col] = f2bf(v);
           } else if (col < f) {
@@ -606,28 +768,47 @@ const int kGemmKernelId[6] = {K_GEMM_GATEUP_FWD, K_GEMM_DOWN_FWD, K_GEMM_DOWN_DG
 const char* kGemmName[6] = {"gemm_gateup_fwd", "gemm_down_fwd", "gemm_down_dgrad",
                             "gemm_gateup_dgrad", "gemm_down_wgrad", "gemm_gateup_wgrad"};
 
+// Tile shapes, chosen by measurement on the Qwen3-shaped layer (128 experts of
+// about 512 rows, d = 2048, f = 768): 256 x 256 tiles with 8 wavefronts where
+// the per-expert row count fills them; 128 x 128 tiles for the down dgrad
+// (which is limited by its epilogue's extra gu traffic) and for the row-tiled
+// GEMMs when experts hold fewer than 384 rows on average, where 256-row tiles
+// would leave a large share of their rows empty.
+using CfgBig = Cfg<256, 256, 2, 4, 2>;
+using CfgBigT = Cfg<256, 256, 4, 2, 2>;
+using CfgSmall = Cfg<128, 128, 2, 2, 2>;
+template <int MODE> struct GemmShape { using big = CfgBig; };
+template <> struct GemmShape<G_DGRAD_DOWN> { using big = CfgSmall; };
+template <> struct GemmShape<G_DGRAD_GATEUP> { using big = CfgBigT; };
+
+template <int MODE, class C>
+int launch_bf16(const GemmArgs& a, hipStream_t s) {
+  const int G = a.offsets ? a.ngroups : 1;
+  const int nt = n_tiles<MODE, C::BN>(a.d, a.f);
+  int64_t nb;
+  if (is_wgrad<MODE>()) {
+    nb = (int64_t)G * ((wgrad_m<MODE>(a.d, a.f) + C::BM - 1) / C::BM) * nt;
+  } else {
+    const int64_t mt = a.offsets ? (a.max_rows + (int64_t)G * (C::BM - 1)) / C::BM
+                                 : (a.dense_rows + C::BM - 1) / C::BM;
+    nb = mt * nt;
+  }
+  if (nb <= 0) return MOE_OK;
+  return launch(kGemmKernelId[MODE], s, kGemmName[MODE],
+                [&] { gemm_bf16_kernel<MODE, C><<<(int)nb, C::NT, 0, s>>>(a); });
+}
+
 template <int MODE>
 int launch_mode(const GemmArgs& a, hipStream_t s) {
-  constexpr bool wgrad = MODE == G_WGRAD_DOWN || MODE == G_WGRAD_GATEUP;
+  if (a.bf16) {
+    const int G = a.offsets ? a.ngroups : 1;
+    const int64_t rows_per_group = a.offsets ? a.max_rows / G : a.dense_rows;
+    if (!is_wgrad<MODE>() && rows_per_group < 384) return launch_bf16<MODE, CfgSmall>(a, s);
+    return launch_bf16<MODE, typename GemmShape<MODE>::big>(a, s);
+  }
+  constexpr bool wgrad = is_wgrad<MODE>();
   const int G = a.offsets ? a.ngroups : 1;
   int64_t nb;
-  if (a.bf16) {
-    if (wgrad) {
-      const int Mfix = MODE == G_WGRAD_DOWN ? a.f : a.d;
-      const int Nfix = MODE == G_WGRAD_DOWN ? a.d : 2 * a.f;
-      nb = (int64_t)G * ((Mfix + BM - 1) / BM) * ((Nfix + BN - 1) / BN);
-    } else {
-      int ntiles;
-      if (MODE == G_FWD_GATEUP) ntiles = a.f / 64;
-      else if (MODE == G_FWD_DOWN || MODE == G_DGRAD_GATEUP) ntiles = (a.d + BN - 1) / BN;
-      else ntiles = (a.f + BN - 1) / BN;
-      const int64_t mt = a.offsets ? (a.max_rows + (int64_t)G * (BM - 1)) / BM : (a.dense_rows + BM - 1) / BM;
-      nb = mt * ntiles;
-    }
-    if (nb <= 0) return MOE_OK;
-    return launch(kGemmKernelId[MODE], s, kGemmName[MODE],
-                  [&] { gemm_bf16_kernel<MODE><<<(int)nb, 256, 0, s>>>(a); });
-  }
   constexpr int TS = 16;
   if (wgrad) {
     const int Mfix = MODE == G_WGRAD_DOWN ? a.f : a.d;

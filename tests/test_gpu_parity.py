@@ -23,6 +23,9 @@ CASES = {
     "gptoss": variant("gptoss", T=384),
     "dsv3": variant("dsv3", T=384, d=512, f=256, f_shared=256),
     "stress": variant("stress", T=2048),
+    # >= 384 rows per expert: the 256 x 256 tiles of the row-tiled GEMMs
+    "qwen3_e16": variant("qwen3", T=1024, E=16),
+    "gptoss_big": variant("gptoss", T=3072),
 }
 
 _CACHE = {}
