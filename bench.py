@@ -125,8 +125,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen3")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-tokens", type=int, default=2048)
+    ap.add_argument("--cpu-tokens", type=int, default=0,
+                    help="tokens of the workload the CPU oracle runs (0: all of them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="before the timed steps, run a plain torch copy of this many MiB three times "
+                         "(a kernel of known size for scaling rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the MoE layer's one-GPU share is the workload "
@@ -168,6 +172,14 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.copy_calibration_mb > 0:
+        n = args.copy_calibration_mb << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # per-kernel times over a few untimed steps, to pick the dominant kernel
     work = kernel_work(cfg)
@@ -233,7 +245,7 @@ def main():
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, args.seed, args.cpu_tokens)
+        out["cpu_baseline"] = cpu_baseline(cfg, args.seed, args.cpu_tokens or cfg["T"])
     print(json.dumps(out), flush=True)
 
 
