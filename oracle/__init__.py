@@ -19,4 +19,6 @@ from .moe_oracle import (  # noqa: F401
     combine,
     combine_backward,
     unpermute,
+    token_forward_backward,
+    expert_weight_grads_at,
 )

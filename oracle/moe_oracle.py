@@ -401,3 +401,69 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
         sh = gsh
     return dict(dx=dx, dw_r=dw_r, experts=grads, shared=sh, omega=omega, dl=dl,
                 dx_perm=dx_perm, do=do, dx_router=dx_router)
+
+
+# ----------------------------------------------------------------------------
+# Evaluation of a layer too large to run whole
+# ----------------------------------------------------------------------------
+
+def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None):
+    """Every per-token result of the layer for a batch of tokens: routing, y,
+    omega, dl and dx (no weight gradients).
+
+    Routing, the combine, the expert rows and the input gradient of a token
+    depend only on that token, so running the plain definitions on a subset
+    of the tokens gives exactly their values in the whole layer.  Experts are
+    visited in ascending order, each once, with all of the batch's tokens
+    that selected it.  dl_dense [T][E] holds dl at the selected experts and
+    zero elsewhere: for a batch that contains every token routed to expert e,
+    column e of dW_r is x_batch^T dl_dense[:, e].
+    """
+    x = np.asarray(x, np.float64)
+    dy = np.asarray(dy, np.float64)
+    T, d = x.shape
+    E, k = spec.E, spec.k
+    rt = route(spec, router_logits(x, w_r), beta)
+    idx, w = rt["topk_idx"], rt["topk_w"]
+    y = np.zeros((T, d))
+    dx = np.zeros((T, d))
+    omega = np.zeros((T, k))
+    for e in np.unique(idx):
+        t, s = np.nonzero(idx == e)          # a token holds e in at most one slot
+        wg, wu, wd, bg, bu, bd = expert_fn(int(e))
+        g, u, h, o = expert_forward(x[t], wg, wu, wd, bg, bu, bd)
+        we = w[t, s][:, None]
+        y[t] += we * o
+        omega[t, s] = (dy[t] * o).sum(axis=1)
+        dx[t] += expert_backward(x[t], g, u, h, we * dy[t], wg, wu, wd)["dx"]
+    dl = router_backward(spec, rt, omega)
+    dl_dense = np.zeros((T, E))
+    np.put_along_axis(dl_dense, idx, dl, axis=1)
+    dx += dl_dense @ np.asarray(w_r, np.float64).T
+    if shared is not None:
+        g, u, h, osh = expert_forward(x, *shared)
+        y += osh
+        dx += expert_backward(x, g, u, h, dy, *shared)["dx"]
+    return dict(route=rt, y=y, dx=dx, omega=omega, dl=dl, dl_dense=dl_dense)
+
+
+def expert_weight_grads_at(xe, do, wg, wu, wd, bg=None, bu=None, cols=None, with_bias=False):
+    """Weight gradients of one expert restricted to the intermediate indices
+    `cols`: dW_gate[:, cols], dW_up[:, cols], dW_down[cols, :] (and db_gate,
+    db_up at cols, db_down whole).
+
+    Along the intermediate axis the SwiGLU expert is a set of independent
+    columns (g_j, u_j and h_j use only column j of W_gate and W_up, and
+    dh_j only row j of W_down), so the plain expert forward and backward on
+    the sliced weights give exactly those slices of the full gradients.
+    xe [M][d] are the expert's rows and do [M][d] their output gradients.
+    """
+    cols = np.asarray(cols)
+    wg_c, wu_c, wd_c = wg[:, cols], wu[:, cols], wd[cols, :]
+    g, u, h, _ = expert_forward(xe, wg_c, wu_c, wd_c,
+                                None if bg is None else bg[cols], None if bu is None else bu[cols])
+    out = expert_backward(xe, g, u, h, do, wg_c, wu_c, wd_c, with_bias=with_bias)
+    out.pop("dx")
+    out.pop("dg")
+    out.pop("du")
+    return out

@@ -13,8 +13,9 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import (RouterSpec, expert_backward, expert_forward, layer_backward,
-                    layer_forward, route, router_logits, sort_maps)
+from oracle import (RouterSpec, expert_backward, expert_forward, expert_weight_grads_at,
+                    layer_backward, layer_forward, route, router_logits, sort_maps,
+                    token_forward_backward)
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -423,3 +424,50 @@ def test_expert_backward_matches_finite_differences_on_its_own():
             fp = (do * expert_forward(x, *args_p)[3]).sum()
             fm = (do * expert_forward(x, *args_m)[3]).sum()
             assert abs((fp - fm) / (2 * eps) - gr[name][idx]) < 1e-7
+
+
+# ---------------------------------------------------------------------------
+# Evaluation of a layer too large to run whole: per-token results on a subset
+# of the tokens, weight-gradient slices along the intermediate axis
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", list(SPECS))
+def test_token_subset_equals_whole_layer(name):
+    spec = SPECS[name]
+    c = make_case(spec, T=40, expert_bias=True, shared=(name == "sigmoid_grouped"), seed=7)
+    fwd, bwd = run(spec, c)
+    sub = np.array([39, 3, 17, 0, 22, 5])
+    r = token_forward_backward(spec, c["x"][sub], c["dy"][sub], c["w_r"], c["beta"], efn(c), c["shared"])
+    assert np.array_equal(r["route"]["topk_idx"], fwd["route"]["topk_idx"][sub])
+    for a, b in ((r["y"], fwd["y"][sub]), (r["dx"], bwd["dx"][sub]), (r["omega"], bwd["omega"][sub]),
+                 (r["dl"], bwd["dl"][sub])):
+        assert rel(a, b) < 1e-12
+    # every token routed to expert e: column e of dW_r
+    for e in (0, spec.E - 1, int(fwd["route"]["topk_idx"][11, 0])):
+        toks = np.nonzero((fwd["route"]["topk_idx"] == e).any(axis=1))[0]
+        r = token_forward_backward(spec, c["x"][toks], c["dy"][toks], c["w_r"], c["beta"], efn(c),
+                                   c["shared"])
+        col = c["x"][toks].T @ r["dl_dense"][:, e]
+        assert rel(col, bwd["dw_r"][:, e]) < 1e-12
+
+
+@pytest.mark.parametrize("bias", [False, True])
+def test_weight_grad_slices_equal_full_expert_backward(bias):
+    rng = np.random.default_rng(11)
+    M, d, f = 29, 16, 12
+    xe, do = rng.standard_normal((M, d)), rng.standard_normal((M, d))
+    wg, wu = rng.standard_normal((d, f)) * 0.3, rng.standard_normal((d, f)) * 0.3
+    wd = rng.standard_normal((f, d)) * 0.3
+    bg = rng.standard_normal(f) * 0.1 if bias else None
+    bu = rng.standard_normal(f) * 0.1 if bias else None
+    g, u, h, _ = expert_forward(xe, wg, wu, wd, bg, bu)
+    full = expert_backward(xe, g, u, h, do, wg, wu, wd, with_bias=bias)
+    cols = np.array([11, 0, 5, 6])
+    part = expert_weight_grads_at(xe, do, wg, wu, wd, bg, bu, cols=cols, with_bias=bias)
+    np.testing.assert_allclose(part["dw_gate"], full["dw_gate"][:, cols], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(part["dw_up"], full["dw_up"][:, cols], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(part["dw_down"], full["dw_down"][cols, :], rtol=1e-13, atol=1e-13)
+    if bias:
+        np.testing.assert_allclose(part["db_gate"], full["db_gate"][cols], rtol=1e-13, atol=1e-13)
+        np.testing.assert_allclose(part["db_up"], full["db_up"][cols], rtol=1e-13, atol=1e-13)
+        np.testing.assert_allclose(part["db_down"], full["db_down"], rtol=1e-13, atol=1e-13)
