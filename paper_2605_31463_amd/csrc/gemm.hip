@@ -40,7 +40,6 @@ typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) void* lds_void_t;
 typedef __attribute__((address_space(3))) v4i16* lds_v4_t;
 
-constexpr int BK = 64;            // k per LDS stage (4 MFMA k-steps of 16)
 constexpr int RSRC_FLAGS = 0x00020000;
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }
@@ -48,19 +47,23 @@ __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)
 template <int MODE>
 __host__ __device__ constexpr bool is_wgrad() { return MODE == G_WGRAD_DOWN || MODE == G_WGRAD_GATEUP; }
 
-// Tile shape: BM x BN outputs per workgroup, WM x WN wavefronts, S LDS stages.
-template <int BM_, int BN_, int WM_, int WN_, int S_>
+// Tile shape: BM x BN outputs per workgroup, WM x WN wavefronts, S LDS
+// stages of BK (32 or 64) k each.
+template <int BM_, int BN_, int WM_, int WN_, int S_, int BK_ = 64>
 struct Cfg {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, S = S_;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, S = S_, BK = BK_;
   static constexpr int NW = WM * WN, NT = 64 * NW;
   static constexpr int TM = BM / WM, TN = BN / WN;  // wavefront tile
   static constexpr int MI = TM / 32, NI = TN / 32;  // 32x32 MFMA blocks per wavefront
   static constexpr int A_ELEMS = BM * BK, B_ELEMS = BN * BK;
   static constexpr int STAGE_ELEMS = A_ELEMS + B_ELEMS;
   static constexpr int LDS_BYTES = S * STAGE_ELEMS * 2;
+  static_assert(BK == 32 || BK == 64, "k per stage");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wavefront tile must be 32-aligned");
-  static_assert(S >= 2 && S <= 4, "2..4 stages");
+  static_assert(S >= 2 && S <= 5, "2..5 stages");
   static_assert(LDS_BYTES <= 150 * 1024, "LDS budget");
+  static_assert((BM * BK * 2 / 1024) % NW == 0 && (BN * BK * 2 / 1024) % NW == 0,
+                "every wavefront issues the same number of 1 KB copies");
 };
 
 // ---------------------------------------------------------------------------
@@ -89,9 +92,20 @@ __host__ __device__ inline int wgrad_m(int d, int f) { return MODE == G_WGRAD_DO
 template <int MODE, int BM, int BN>
 __device__ __forceinline__ Tile decode_tile(const GemmArgs& a, int* pre, int* sbuf) {
   Tile t;
-  const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int nt = n_tiles<MODE, BN>(a.d, a.f);
-  if (is_wgrad<MODE>()) {
+  if (is_wgrad<MODE>() || !a.offsets) {
+    // exact grid: every block holds a tile
+    const int lin = xcd_remap(blockIdx.x, gridDim.x);
+    if (!is_wgrad<MODE>()) {
+      const int mt = lin / nt;
+      t.n0 = (lin - mt * nt) * tile_cols<MODE, BN>();
+      t.g = 0;
+      t.row_base = 0;
+      t.rows = (int)a.dense_rows;
+      t.m0 = mt * BM;
+      t.live = t.m0 < t.rows;
+      return t;
+    }
     const int mt = (wgrad_m<MODE>(a.d, a.f) + BM - 1) / BM;
     t.g = lin / (mt * nt);
     const int rem = lin - t.g * mt * nt;
@@ -108,16 +122,9 @@ __device__ __forceinline__ Tile decode_tile(const GemmArgs& a, int* pre, int* sb
     t.live = t.g < (a.offsets ? a.ngroups : 1);
     return t;
   }
-  const int mt = lin / nt;
-  t.n0 = (lin - mt * nt) * tile_cols<MODE, BN>();
-  if (!a.offsets) {
-    t.g = 0;
-    t.row_base = 0;
-    t.rows = (int)a.dense_rows;
-    t.m0 = mt * BM;
-    t.live = t.m0 < t.rows;
-    return t;
-  }
+  // variable rows per expert: the grid is an upper bound, so the live tiles
+  // are counted first and the XCD-contiguous remap runs over them alone
+  // (remapping the whole grid would leave the live tiles on a few XCDs).
   const int G = a.ngroups;
   int c = 0;
   if ((int)threadIdx.x < G) c = (a.offsets[threadIdx.x + 1] - a.offsets[threadIdx.x] + BM - 1) / BM;
@@ -125,8 +132,12 @@ __device__ __forceinline__ Tile decode_tile(const GemmArgs& a, int* pre, int* sb
   const int ex = block_scan_256(c, sbuf, &total);
   if ((int)threadIdx.x < G) pre[threadIdx.x] = ex;
   __syncthreads();
-  t.live = mt < total;
+  const int live_tiles = total * nt;
+  t.live = (int)blockIdx.x < live_tiles;
   if (!t.live) return t;
+  const int lin = xcd_remap(blockIdx.x, live_tiles);
+  const int mt = lin / nt;
+  t.n0 = (lin - mt * nt) * tile_cols<MODE, BN>();
   int lo = 0, hi = G - 1;  // last g with pre[g] <= mt (empty experts share a prefix: take the last)
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -153,20 +164,26 @@ __device__ __forceinline__ Tile decode_tile(const GemmArgs& a, int* pre, int* sb
 // or one expert's weight matrix), so reads past the last row return zeros:
 // ragged expert tails and the weight gradients' K-tail need no masking.
 //
-// K-contiguous tiles (rows x 64 k): row = 128 bytes = 8 chunks of 16 bytes,
-// chunk index XOR-swizzled by kswz(row); fragments read with ds_read_b128
-// (16 consecutive rows, one chunk: 16 distinct bank groups).
-// MN-contiguous tiles (64 k x columns): sub-tiles of 64 columns, row = 8
-// chunks, chunk index XOR-swizzled by mswz(k); fragments read with
+// K-contiguous tiles (rows x BK k): a row is BK/8 chunks of 16 bytes whose
+// index is XOR-swizzled by kswz<BK>(row); fragments are read with
+// ds_read_b128 (32 consecutive rows of one chunk per half-wavefront).  The
+// swizzles were chosen by measuring the fragment read pattern on gfx950:
+// (row >> 1) & 7 for 128-byte rows and ((row >> 2) ^ (row >> 3)) & 3 for
+// 64-byte rows read at ~190 B/clk per CU, unswizzled rows at 30-75.
+// MN-contiguous tiles (BK k x columns): sub-tiles of 64 columns, one k-row =
+// 8 chunks, chunk index XOR-swizzled by mswz(k); fragments read with
 // ds_read_b64_tr_b16, whose lane i of each 16-lane group returns column i of
-// a 4 (k) x 16 (columns) block addressed by its 16 lanes.  The swizzle spreads
-// one read (8 k-rows x 4 chunks) evenly over the banks.
+// a 4 (k) x 16 (columns) block addressed by its 16 lanes (~120 B/clk per CU
+// whatever the swizzle).
 // ---------------------------------------------------------------------------
 typedef int int32x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ int kswz(int r) { return ((r >> 1) ^ (r >> 3)) & 7; }
-__device__ __forceinline__ int k_off(int r, int c) { return r * BK + ((c ^ kswz(r)) << 3); }
+template <int BK>
+__device__ __forceinline__ int kswz(int r) { return BK == 64 ? (r >> 1) & 7 : ((r >> 2) ^ (r >> 3)) & 3; }
+template <int BK>
+__device__ __forceinline__ int k_off(int r, int c) { return r * BK + ((c ^ kswz<BK>(r)) << 3); }
 __device__ __forceinline__ int mswz(int k) { return ((k >> 1) & 1) << 2; }
+template <int BK>
 __device__ __forceinline__ int mn_off(int k, int col) {
   return (col >> 6) * (64 * BK) + k * 64 + ((((col & 63) >> 3) ^ mswz(k)) << 3) + (col & 7);
 }
@@ -198,18 +215,20 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | 0x0F70);
 }
 
-// This wave's share of one K-contiguous ROWS x 64 tile.
-template <int ROWS, int NW>
+// This wave's share of one K-contiguous ROWS x BK tile: 1 KB copies of
+// 1024 / (2 BK) rows each.
+template <int ROWS, int NW, int BK>
 struct KOperand {
-  static constexpr int NIW = ROWS / (8 * NW);  // instructions per wave
+  static constexpr int CPR = BK / 8;                 // chunks per row
+  static constexpr int NIW = ROWS * BK * 2 / 1024 / NW;  // copies per wave
   int32x4_t rsrc;
   uint32_t voff[NIW];
   __device__ __forceinline__ void init(int wave, int lane, int row0, int ld) {
 #pragma unroll
     for (int j = 0; j < NIW; ++j) {
       const int q = (NIW * wave + j) * 64 + lane;
-      const int row = q >> 3, phys = q & 7;
-      voff[j] = (uint32_t)(((int64_t)(row0 + row) * ld + 8 * (phys ^ kswz(row))) * 2);
+      const int row = q / CPR, phys = q % CPR;
+      voff[j] = (uint32_t)(((int64_t)(row0 + row) * ld + 8 * (phys ^ kswz<BK>(row))) * 2);
     }
   }
   __device__ __forceinline__ void issue(uint32_t tile, int wave, uint32_t soff) const {
@@ -218,42 +237,53 @@ struct KOperand {
   }
 };
 
-// This wave's share of one MN-contiguous 64 x (64*NSUB) tile; sub-tile s
-// comes from descriptor rsrc[s] starting at column col0[s].
-template <int NSUB, int NW>
+// This wave's share of one MN-contiguous BK x (64*NSUB) tile.  Copy t covers
+// k-rows 8 (t % (BK/8)) .. +7 of sub-tile t / (BK/8); sub-tile s comes from
+// descriptor src[s] starting at column col0[s].  The descriptors of this
+// wave's copies are picked with constant indices (they stay in SGPRs).
+template <int NSUB, int NW, int BK>
 struct MNOperand {
-  static constexpr int NIW = 8 / NW;  // instructions per wave per sub-tile
-  int32x4_t rsrc[NSUB];
-  uint32_t voff[NSUB][NIW];
-  __device__ __forceinline__ void init(int wave, int lane, const int* col0, int ld) {
+  static constexpr int PER_SUB = BK / 8;               // copies per sub-tile
+  static constexpr int NIW = NSUB * PER_SUB / NW;      // copies per wave
+  int32x4_t rsrc[NIW];
+  uint32_t voff[NIW];
+  __device__ __forceinline__ void init(int wave, int lane, const int32x4_t* src, const int* col0, int ld) {
 #pragma unroll
-    for (int s = 0; s < NSUB; ++s)
+    for (int j = 0; j < NIW; ++j) {
+      const int t = NIW * wave + j;
+      const int sub = t / PER_SUB;
+      const int krow = (t % PER_SUB) * 8 + (lane >> 3), phys = lane & 7;
+      int c0 = 0;
 #pragma unroll
-      for (int j = 0; j < NIW; ++j) {
-        const int q = (NIW * wave + j) * 64 + lane;
-        const int krow = q >> 3, phys = q & 7;
-        voff[s][j] = (uint32_t)(((int64_t)krow * ld + col0[s] + 8 * (phys ^ mswz(krow))) * 2);
-      }
+      for (int q = 0; q < NSUB; ++q)
+        if (q == sub) {
+          rsrc[j] = src[q];
+          c0 = col0[q];
+        }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) rsrc[j][q] = __builtin_amdgcn_readfirstlane(rsrc[j][q]);
+      voff[j] = (uint32_t)(((int64_t)krow * ld + c0 + 8 * (phys ^ mswz(krow))) * 2);
+    }
   }
   __device__ __forceinline__ void issue(uint32_t tile, int wave, uint32_t soff) const {
 #pragma unroll
-    for (int s = 0; s < NSUB; ++s)
-#pragma unroll
-      for (int j = 0; j < NIW; ++j) dma16(rsrc[s], tile + s * 8192 + (NIW * wave + j) * 1024, voff[s][j], soff);
+    for (int j = 0; j < NIW; ++j) dma16(rsrc[j], tile + (NIW * wave + j) * 1024, voff[j], soff);
   }
 };
 
 // 32x32x16 fragments.  K-contiguous: rows rb*32 + lane%32, k = ks*16 + 8*(lane/32) .. +7.
+template <int BK>
 __device__ __forceinline__ bf16x8 frag_k(const bf16_t* tile, int rb, int ks, int lane) {
-  return *reinterpret_cast<const bf16x8*>(tile + k_off(rb * 32 + (lane & 31), 2 * ks + (lane >> 5)));
+  return *reinterpret_cast<const bf16x8*>(tile + k_off<BK>(rb * 32 + (lane & 31), 2 * ks + (lane >> 5)));
 }
 // MN-contiguous: columns cb*32 + lane%32, same k.
+template <int BK>
 __device__ __forceinline__ bf16x8 frag_mn(const bf16_t* tile, int cb, int ks, int lane) {
   const int G = lane >> 4, r = lane & 15;
   const int k = ks * 16 + 8 * (G >> 1) + (r >> 2);
   const int col = cb * 32 + 16 * (G & 1) + 4 * (r & 3);
-  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4_t)(tile + mn_off(k, col)));
-  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4_t)(tile + mn_off(k + 4, col)));
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4_t)(tile + mn_off<BK>(k, col)));
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4_t)(tile + mn_off<BK>(k + 4, col)));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
@@ -266,7 +296,7 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   constexpr bool wgrad = is_wgrad<MODE>();
   constexpr bool a_mn = wgrad;                                               // A tile MN-contiguous
   constexpr bool b_mn = MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN || wgrad;  // B tile MN-contiguous
-  constexpr int BM = C::BM, BN = C::BN, MI = C::MI, NI = C::NI, S = C::S, NW = C::NW;
+  constexpr int BM = C::BM, BN = C::BN, MI = C::MI, NI = C::NI, S = C::S, NW = C::NW, BK = C::BK;
   static_assert(MODE != G_FWD_GATEUP || NI % 2 == 0, "gate/up pairs need an even number of column blocks");
   __shared__ __align__(16) bf16_t lds[S][C::STAGE_ELEMS];
   __shared__ int pre[257];
@@ -296,8 +326,8 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   const bf16_t* W1 = reinterpret_cast<const bf16_t*>(a.w1);
 
   // ---- operand A (BM rows of the output)
-  KOperand<BM, NW> ka;
-  MNOperand<BM / 64, NW> ma;
+  KOperand<BM, NW, BK> ka;
+  MNOperand<BM / 64, NW, BK> ma;
   int64_t a_kstride;  // soffset = k0 * a_kstride
   if (!a_mn) {
     const int lda = MODE == G_FWD_DOWN ? f : (MODE == G_DGRAD_GATEUP ? 2 * f : d);
@@ -307,41 +337,44 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   } else {
     const int lda = MODE == G_WGRAD_DOWN ? f : d;  // h rows [f] or x_perm rows [d]
     const int32x4_t r = make_rsrc(A + (int64_t)tl.row_base * lda, (int64_t)K * lda * 2);
+    int32x4_t src[BM / 64];
     int col0[BM / 64];
 #pragma unroll
     for (int s2 = 0; s2 < BM / 64; ++s2) {
-      ma.rsrc[s2] = r;
+      src[s2] = r;
       col0[s2] = tl.m0 + 64 * s2;
     }
-    ma.init(wave, lane, col0, lda);
+    ma.init(wave, lane, src, col0, lda);
     a_kstride = (int64_t)lda * 2;
   }
   // ---- operand B (BN columns of the output)
-  KOperand<BN, NW> kb;
-  MNOperand<BN / 64, NW> mb;
+  KOperand<BN, NW, BK> kb;
+  MNOperand<BN / 64, NW, BK> mb;
   int64_t b_kstride;
   int32x4_t b_up = make_rsrc(W0, 0);  // DGRAD_GATEUP: W_up rows for k >= f
   if (MODE == G_FWD_GATEUP) {  // sub-tiles 0 .. BN/128-1: W_gate columns, then W_up columns
     const int32x4_t rg = make_rsrc(W0 + (int64_t)g * d * f, (int64_t)d * f * 2);
     const int32x4_t ru = make_rsrc(W1 + (int64_t)g * d * f, (int64_t)d * f * 2);
+    int32x4_t src[BN / 64];
     int col0[BN / 64];
 #pragma unroll
     for (int s2 = 0; s2 < BN / 64; ++s2) {
       const bool up = s2 >= BN / 128;
-      mb.rsrc[s2] = up ? ru : rg;
+      src[s2] = up ? ru : rg;
       col0[s2] = tl.n0 + 64 * (up ? s2 - BN / 128 : s2);
     }
-    mb.init(wave, lane, col0, f);
+    mb.init(wave, lane, src, col0, f);
     b_kstride = (int64_t)f * 2;
   } else if (MODE == G_FWD_DOWN) {
     const int32x4_t r = make_rsrc(W0 + (int64_t)g * f * d, (int64_t)f * d * 2);
+    int32x4_t src[BN / 64];
     int col0[BN / 64];
 #pragma unroll
     for (int s2 = 0; s2 < BN / 64; ++s2) {
-      mb.rsrc[s2] = r;
+      src[s2] = r;
       col0[s2] = tl.n0 + 64 * s2;
     }
-    mb.init(wave, lane, col0, d);
+    mb.init(wave, lane, src, col0, d);
     b_kstride = (int64_t)d * 2;
   } else if (MODE == G_DGRAD_DOWN) {  // B[k=i][n=j] = W_down[g][j][i]: rows j of length d
     kb.rsrc = make_rsrc(W0 + (int64_t)g * f * d, (int64_t)f * d * 2);
@@ -355,17 +388,18 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   } else {
     const int ldb = MODE == G_WGRAD_DOWN ? d : 2 * f;  // d_o rows or dgu rows
     const int32x4_t r = make_rsrc(Bact + (int64_t)tl.row_base * ldb, (int64_t)K * ldb * 2);
+    int32x4_t src[BN / 64];
     int col0[BN / 64];
 #pragma unroll
     for (int s2 = 0; s2 < BN / 64; ++s2) {
-      mb.rsrc[s2] = r;
+      src[s2] = r;
       col0[s2] = tl.n0 + 64 * s2;
     }
-    mb.init(wave, lane, col0, ldb);
+    mb.init(wave, lane, src, col0, ldb);
     b_kstride = (int64_t)ldb * 2;
   }
   // DMA instructions per thread per stage
-  constexpr int NL = (a_mn ? (BM / 64) * (8 / NW) : BM / (8 * NW)) + (b_mn ? (BN / 64) * (8 / NW) : BN / (8 * NW));
+  constexpr int NL = (BM + BN) * BK * 2 / 1024 / NW;
 
   floatx16 acc[MI][NI];
 #pragma unroll
@@ -388,7 +422,7 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
     if (!a_mn) ka.issue(As, wave, (uint32_t)(k0 * a_kstride));
     else ma.issue(As, wave, (uint32_t)(k0 * a_kstride));
     if (MODE == G_DGRAD_GATEUP) {
-      KOperand<BN, NW> kk = kb;
+      KOperand<BN, NW, BK> kk = kb;
       if (k0 >= f) kk.rsrc = b_up;
       kk.issue(Bs, wave, (uint32_t)((k0 >= f ? k0 - f : k0) * b_kstride));
     } else if (MODE == G_DGRAD_DOWN) {
@@ -410,9 +444,10 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   for (int p = 0; p < S - 1; ++p)
     if (p < nk) issue_tile(p * BK, p);
   for (int kt = 0; kt < nk; ++kt) {
-    // tiles issued after kt that may still be in flight
+    // stages issued after kt that may still be in flight
     const int ahead = min(S - 2, nk - 1 - kt);
-    if (S >= 4 && ahead >= 2) wait_vmcnt<(S >= 4 ? 2 : 0) * NL>();
+    if (S >= 5 && ahead >= 3) wait_vmcnt<(S >= 5 ? 3 : 0) * NL>();
+    else if (S >= 4 && ahead >= 2) wait_vmcnt<(S >= 4 ? 2 : 0) * NL>();
     else if (S >= 3 && ahead >= 1) wait_vmcnt<(S >= 3 ? 1 : 0) * NL>();
     else wait_vmcnt<0>();
     __syncthreads();
@@ -425,16 +460,17 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
     auto load_frags = [&](int ks, int slot) {
 #pragma unroll
       for (int i = 0; i < MI; ++i)
-        af[slot][i] = a_mn ? frag_mn(As, wm * MI + i, ks, lane) : frag_k(As, wm * MI + i, ks, lane);
+        af[slot][i] = a_mn ? frag_mn<BK>(As, wm * MI + i, ks, lane) : frag_k<BK>(As, wm * MI + i, ks, lane);
 #pragma unroll
       for (int j = 0; j < NI; ++j)
-        bfr[slot][j] = b_mn ? frag_mn(Bs, bcol(j), ks, lane) : frag_k(Bs, bcol(j), ks, lane);
+        bfr[slot][j] = b_mn ? frag_mn<BK>(Bs, bcol(j), ks, lane) : frag_k<BK>(Bs, bcol(j), ks, lane);
     };
+    constexpr int KS = BK / 16;  // MFMA k-steps per stage
     load_frags(0, 0);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < KS; ++ks) {
       const int cur = ks & 1;
-      if (ks < 3) load_frags(ks + 1, cur ^ 1);
+      if (ks < KS - 1) load_frags(ks + 1, cur ^ 1);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < MI; ++i)
