@@ -440,6 +440,7 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
   };
 
   const int nk = (K + BK - 1) / BK;
+  const bool wave_rows = tl.m0 + wm * C::TM < M;
 #pragma unroll
   for (int p = 0; p < S - 1; ++p)
     if (p < nk) issue_tile(p * BK, p);
@@ -466,6 +467,10 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
         bfr[slot][j] = b_mn ? frag_mn<BK>(Bs, bcol(j), ks, lane) : frag_k<BK>(Bs, bcol(j), ks, lane);
     };
     constexpr int KS = BK / 16;  // MFMA k-steps per stage
+    // a wavefront whose output rows all lie past the expert's last row
+    // (the ragged last tile of an expert) has nothing to multiply; its
+    // SIMD partner then has the matrix pipe to itself
+    if (!wave_rows) continue;
     load_frags(0, 0);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
@@ -810,12 +815,19 @@ const char* kGemmName[6] = {"gemm_gateup_fwd", "gemm_down_fwd", "gemm_down_dgrad
 // (which is limited by its epilogue's extra gu traffic) and for the row-tiled
 // GEMMs when experts hold fewer than 384 rows on average, where 256-row tiles
 // would leave a large share of their rows empty.
-using CfgBig = Cfg<256, 256, 2, 4, 2>;
-using CfgBigT = Cfg<256, 256, 4, 2, 2>;
-using CfgSmall = Cfg<128, 128, 2, 2, 2>;
-template <int MODE> struct GemmShape { using big = CfgBig; };
-template <> struct GemmShape<G_DGRAD_DOWN> { using big = CfgSmall; };
-template <> struct GemmShape<G_DGRAD_GATEUP> { using big = CfgBigT; };
+// Tile shapes per pass, chosen by timing the whole layer at the Qwen3 shape
+// (512 +- 33 rows per expert): 256 x 256 tiles, 8 wavefronts, 2 x 64-k or
+// 4 x 32-k LDS stages.  Experts with fewer than 384 rows on average use
+// 128 x 128.
+using CfgWide = Cfg<256, 256, 2, 4, 2, 64>;    // wavefront tile 128 x 64
+using CfgTall = Cfg<256, 256, 4, 2, 2, 64>;    // wavefront tile 64 x 128
+using CfgTall32 = Cfg<256, 256, 4, 2, 4, 32>;  // 4 stages of 32 k
+using CfgSmall = Cfg<128, 128, 2, 2, 2, 64>;
+template <int MODE> struct GemmShape { using big = CfgTall32; };
+template <> struct GemmShape<G_FWD_GATEUP> { using big = CfgWide; };
+template <> struct GemmShape<G_FWD_DOWN> { using big = CfgWide; };
+template <> struct GemmShape<G_DGRAD_DOWN> { using big = CfgTall; };
+template <> struct GemmShape<G_DGRAD_GATEUP> { using big = CfgTall; };
 
 template <int MODE, class C>
 int launch_bf16(const GemmArgs& a, hipStream_t s) {
