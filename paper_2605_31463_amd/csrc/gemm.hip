@@ -25,6 +25,8 @@
 //
 // fp32 path: a plain kernel, one thread per output (or output pair), for the
 // fp32 workload; same modes, same epilogues.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -204,8 +206,12 @@ __device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) {
 }
 
 __device__ __forceinline__ void dma16(const int32x4_t& r, uint32_t lds, uint32_t voff, uint32_t soff) {
+  int32x4_t rs;  // wave-uniform by construction; keeps the operand in SGPRs
+#pragma unroll
+  for (int q = 0; q < 4; ++q) rs[q] = __builtin_amdgcn_readfirstlane(r[q]);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               :: "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory");
+               :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rs),
+                  "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory");
 }
 
 // s_waitcnt vmcnt(n), expcnt and lgkmcnt left free
@@ -683,6 +689,478 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Persistent variant.  One workgroup per CU walks its share of the tiles
+// (each XCD owns a contiguous range of tile ids, its workgroups take them
+// round-robin), and the LDS pipeline runs across tile boundaries: the copies
+// of the next tile's first stages are in flight while the current tile's
+// epilogue runs.  The epilogue is wavefront-local: each 32 x 32 block of
+// results is staged through a private 2 KB LDS slot and written as 64-byte
+// row pieces, with no workgroup barrier, so wavefronts that finish their
+// multiplies early go on without waiting for the others.
+// ---------------------------------------------------------------------------
+
+// Logical tile count of a launch (block-wide; variable-row passes count the
+// row tiles of every expert from expert_offsets into pre[]).
+template <int MODE, int BM, int BN>
+__device__ __forceinline__ int tile_count(const GemmArgs& a, int* pre, int* sbuf) {
+  const int nt = n_tiles<MODE, BN>(a.d, a.f);
+  if (is_wgrad<MODE>()) {
+    const int G = a.offsets ? a.ngroups : 1;
+    return G * ((wgrad_m<MODE>(a.d, a.f) + BM - 1) / BM) * nt;
+  }
+  if (!a.offsets) return (int)((a.dense_rows + BM - 1) / BM) * nt;
+  const int G = a.ngroups;
+  int c = 0;
+  if ((int)threadIdx.x < G) c = (a.offsets[threadIdx.x + 1] - a.offsets[threadIdx.x] + BM - 1) / BM;
+  __shared__ int total;
+  const int ex = block_scan_256(c, sbuf, &total);
+  if ((int)threadIdx.x < G) pre[threadIdx.x] = ex;
+  __syncthreads();
+  return total * nt;
+}
+
+// Tile with logical id `lin` (pre[] from tile_count for variable-row passes).
+template <int MODE, int BM, int BN>
+__device__ __forceinline__ Tile tile_at(const GemmArgs& a, int lin, const int* pre) {
+  Tile t;
+  const int nt = n_tiles<MODE, BN>(a.d, a.f);
+  t.live = true;
+  if (is_wgrad<MODE>()) {
+    const int mt = (wgrad_m<MODE>(a.d, a.f) + BM - 1) / BM;
+    t.g = lin / (mt * nt);
+    const int rem = lin - t.g * mt * nt;
+    const int im = rem / nt;
+    t.m0 = im * BM;
+    t.n0 = (rem - im * nt) * BN;
+    t.row_base = a.offsets ? a.offsets[t.g] : 0;
+    t.rows = a.offsets ? a.offsets[t.g + 1] - t.row_base : (int)a.dense_rows;
+    return t;
+  }
+  const int mt = lin / nt;
+  t.n0 = (lin - mt * nt) * tile_cols<MODE, BN>();
+  if (!a.offsets) {
+    t.g = 0;
+    t.row_base = 0;
+    t.rows = (int)a.dense_rows;
+    t.m0 = mt * BM;
+    return t;
+  }
+  int lo = 0, hi = a.ngroups - 1;  // last g with pre[g] <= mt
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (pre[mid] <= mt) lo = mid; else hi = mid - 1;
+  }
+  t.g = lo;
+  t.row_base = a.offsets[lo];
+  t.rows = a.offsets[lo + 1] - t.row_base;
+  t.m0 = (mt - pre[lo]) * BM;
+  return t;
+}
+
+template <int MODE>
+__device__ __forceinline__ void tile_dims(const GemmArgs& a, const Tile& tl, int& K, int& M, int& N) {
+  const int d = a.d, f = a.f;
+  if (MODE == G_FWD_GATEUP) { K = d; M = tl.rows; N = f; }
+  else if (MODE == G_FWD_DOWN) { K = f; M = tl.rows; N = d; }
+  else if (MODE == G_DGRAD_DOWN) { K = d; M = tl.rows; N = f; }
+  else if (MODE == G_DGRAD_GATEUP) { K = 2 * f; M = tl.rows; N = d; }
+  else if (MODE == G_WGRAD_DOWN) { K = tl.rows; M = f; N = d; }
+  else { K = tl.rows; M = d; N = 2 * f; }
+}
+
+template <int MODE, class C>
+__global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
+  constexpr bool wgrad = is_wgrad<MODE>();
+  constexpr bool a_mn = wgrad;
+  constexpr bool b_mn = MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN || wgrad;
+  constexpr int BM = C::BM, BN = C::BN, MI = C::MI, NI = C::NI, S = C::S, NW = C::NW, BK = C::BK;
+  static_assert(MODE != G_FWD_GATEUP || NI % 2 == 0, "gate/up pairs need an even number of column blocks");
+  __shared__ __align__(16) bf16_t lds[S][C::STAGE_ELEMS];
+  __shared__ __align__(16) bf16_t epi[NW][32 * 32];
+  __shared__ int pre[257];
+  __shared__ int sbuf[256];
+
+  const int T = tile_count<MODE, BM, BN>(a, pre, sbuf);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / C::WN, wn = wave % C::WN;
+  const int d = a.d, f = a.f;
+  // this workgroup's tiles: lo + jx, lo + jx + per_x, ... < hi (grid is a multiple of 8)
+  const int per_x = gridDim.x >> 3, x = blockIdx.x & 7, jx = blockIdx.x >> 3;
+  const int lo = x * (T >> 3) + min(x, T & 7);
+  const int hi = lo + (T >> 3) + (x < (T & 7) ? 1 : 0);
+
+  const bf16_t* A = reinterpret_cast<const bf16_t*>(a.a);
+  const bf16_t* Bact = reinterpret_cast<const bf16_t*>(a.b);
+  const bf16_t* W0 = reinterpret_cast<const bf16_t*>(a.w0);
+  const bf16_t* W1 = reinterpret_cast<const bf16_t*>(a.w1);
+
+  // ---- producer: copies of (tile, k-step) stages in consumption order
+  KOperand<BM, NW, BK> ka;
+  MNOperand<BM / 64, NW, BK> ma;
+  KOperand<BN, NW, BK> kb;
+  MNOperand<BN / 64, NW, BK> mb;
+  int32x4_t b_up = make_rsrc(W0, 0);
+  int64_t a_kstride = 0, b_kstride = 0;
+  int p_t = lo + jx, p_k = 0, p_nk = 0;
+  auto setup = [&](const Tile& tl) {
+    int K, M, N;
+    tile_dims<MODE>(a, tl, K, M, N);
+    const int g = tl.g;
+    if (!a_mn) {
+      const int lda = MODE == G_FWD_DOWN ? f : (MODE == G_DGRAD_GATEUP ? 2 * f : d);
+      ka.rsrc = make_rsrc(A + (int64_t)tl.row_base * lda, (int64_t)M * lda * 2);
+      ka.init(wave, lane, tl.m0, lda);
+      a_kstride = 2;
+    } else {
+      const int lda = MODE == G_WGRAD_DOWN ? f : d;
+      const int32x4_t r = make_rsrc(A + (int64_t)tl.row_base * lda, (int64_t)K * lda * 2);
+      int32x4_t src[BM / 64];
+      int col0[BM / 64];
+#pragma unroll
+      for (int s2 = 0; s2 < BM / 64; ++s2) {
+        src[s2] = r;
+        col0[s2] = tl.m0 + 64 * s2;
+      }
+      ma.init(wave, lane, src, col0, lda);
+      a_kstride = (int64_t)lda * 2;
+    }
+    if (MODE == G_FWD_GATEUP) {
+      const int32x4_t rg = make_rsrc(W0 + (int64_t)g * d * f, (int64_t)d * f * 2);
+      const int32x4_t ru = make_rsrc(W1 + (int64_t)g * d * f, (int64_t)d * f * 2);
+      int32x4_t src[BN / 64];
+      int col0[BN / 64];
+#pragma unroll
+      for (int s2 = 0; s2 < BN / 64; ++s2) {
+        const bool up = s2 >= BN / 128;
+        src[s2] = up ? ru : rg;
+        col0[s2] = tl.n0 + 64 * (up ? s2 - BN / 128 : s2);
+      }
+      mb.init(wave, lane, src, col0, f);
+      b_kstride = (int64_t)f * 2;
+    } else if (MODE == G_FWD_DOWN) {
+      const int32x4_t r = make_rsrc(W0 + (int64_t)g * f * d, (int64_t)f * d * 2);
+      int32x4_t src[BN / 64];
+      int col0[BN / 64];
+#pragma unroll
+      for (int s2 = 0; s2 < BN / 64; ++s2) {
+        src[s2] = r;
+        col0[s2] = tl.n0 + 64 * s2;
+      }
+      mb.init(wave, lane, src, col0, d);
+      b_kstride = (int64_t)d * 2;
+    } else if (MODE == G_DGRAD_DOWN) {
+      kb.rsrc = make_rsrc(W0 + (int64_t)g * f * d, (int64_t)f * d * 2);
+      kb.init(wave, lane, tl.n0, d);
+      b_kstride = 2;
+    } else if (MODE == G_DGRAD_GATEUP) {
+      kb.rsrc = make_rsrc(W0 + (int64_t)g * d * f, (int64_t)d * f * 2);
+      b_up = make_rsrc(W1 + (int64_t)g * d * f, (int64_t)d * f * 2);
+      kb.init(wave, lane, tl.n0, f);
+      b_kstride = 2;
+    } else {
+      const int ldb = MODE == G_WGRAD_DOWN ? d : 2 * f;
+      const int32x4_t r = make_rsrc(Bact + (int64_t)tl.row_base * ldb, (int64_t)K * ldb * 2);
+      int32x4_t src[BN / 64];
+      int col0[BN / 64];
+#pragma unroll
+      for (int s2 = 0; s2 < BN / 64; ++s2) {
+        src[s2] = r;
+        col0[s2] = tl.n0 + 64 * s2;
+      }
+      mb.init(wave, lane, src, col0, ldb);
+      b_kstride = (int64_t)ldb * 2;
+    }
+  };
+  // advance the producer to the next tile with work (weight-gradient tiles
+  // of experts without rows have none)
+  auto p_seek = [&]() {
+    while (p_t < hi) {
+      const Tile tl = tile_at<MODE, BM, BN>(a, p_t, pre);
+      int K, M, N;
+      tile_dims<MODE>(a, tl, K, M, N);
+      p_nk = (K + BK - 1) / BK;
+      if (p_nk > 0) {
+        setup(tl);
+        return;
+      }
+      p_t += per_x;
+    }
+  };
+  const uint32_t lds0 = lds_addr(&lds[0][0]);
+  auto p_issue = [&](int buf) {
+    const int k0 = p_k * BK;
+    const uint32_t As = lds0 + buf * (C::STAGE_ELEMS * 2);
+    const uint32_t Bs = As + C::A_ELEMS * 2;
+    if (!a_mn) ka.issue(As, wave, (uint32_t)(k0 * a_kstride));
+    else ma.issue(As, wave, (uint32_t)(k0 * a_kstride));
+    if (MODE == G_DGRAD_GATEUP) {
+      KOperand<BN, NW, BK> kk = kb;
+      if (k0 >= f) kk.rsrc = b_up;
+      kk.issue(Bs, wave, (uint32_t)((k0 >= f ? k0 - f : k0) * b_kstride));
+    } else if (MODE == G_DGRAD_DOWN) {
+      kb.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
+    } else {
+      mb.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
+    }
+    if (++p_k == p_nk) {
+      p_k = 0;
+      p_t += per_x;
+      p_seek();
+    }
+  };
+  constexpr int NL = (BM + BN) * BK * 2 / 1024 / NW;  // copies per thread per stage
+  int issued = 0, consumed = 0;
+  p_seek();
+#pragma unroll
+  for (int i = 0; i < S - 1; ++i)
+    if (p_t < hi) {
+      p_issue(issued % S);
+      ++issued;
+    }
+
+  auto bcol = [&](int j) {
+    if (MODE == G_FWD_GATEUP)
+      return (j < NI / 2) ? (wn * (NI / 2) + j) : (BN / 64 + wn * (NI / 2) + (j - NI / 2));
+    return wn * NI + j;
+  };
+  bf16_t* ep = &epi[wave][0];
+  const int hh = lane >> 5, r32 = lane & 31;
+  // stage this lane's 4 x 4 values of a 32 x 32 block (row r32, columns
+  // 8q + 4hh + t) and store the block's rows: dst(r) is row r's pointer at
+  // the block's first column (null: row not stored), ncols valid columns
+  auto put_block = [&](const float* v, auto&& dst, int ncols) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo2 = (uint32_t)f2bf(v[4 * q]) | ((uint32_t)f2bf(v[4 * q + 1]) << 16);
+      const uint32_t hi2 = (uint32_t)f2bf(v[4 * q + 2]) | ((uint32_t)f2bf(v[4 * q + 3]) << 16);
+      *reinterpret_cast<uint2*>(ep + r32 * 32 + ((q ^ ((r32 >> 2) & 3)) << 3) + 4 * hh) = make_uint2(lo2, hi2);
+    }
+#pragma unroll
+    for (int rep = 0; rep < 2; ++rep) {
+      const int idx = lane + 64 * rep, r = idx >> 2, ch = idx & 3;
+      const uint4 val = *reinterpret_cast<const uint4*>(ep + r * 32 + ((ch ^ ((r >> 2) & 3)) << 3));
+      bf16_t* p = dst(r);
+      if (p && 8 * ch < ncols) *reinterpret_cast<uint4*>(p + 8 * ch) = val;
+    }
+  };
+
+  for (int c_t = lo + jx; c_t < hi; c_t += per_x) {
+    const Tile tl = tile_at<MODE, BM, BN>(a, c_t, pre);
+    int K, M, N;
+    tile_dims<MODE>(a, tl, K, M, N);
+    const int g = tl.g;
+    const int nk = (K + BK - 1) / BK;
+    const bool wave_rows = tl.m0 + wm * C::TM < M;
+    const bool colsum = wgrad && a.db0 && tl.m0 == 0 && wm == 0;
+    floatx16 acc[MI][NI];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+    float bsum[NI];
+#pragma unroll
+    for (int j = 0; j < NI; ++j) bsum[j] = 0.f;
+
+    for (int kt = 0; kt < nk; ++kt) {
+      const int ahead = issued - consumed - 1;  // stages issued after this one
+      if (S >= 5 && ahead >= 3) wait_vmcnt<(S >= 5 ? 3 : 0) * NL>();
+      else if (S >= 4 && ahead >= 2) wait_vmcnt<(S >= 4 ? 2 : 0) * NL>();
+      else if (S >= 3 && ahead >= 1) wait_vmcnt<(S >= 3 ? 1 : 0) * NL>();
+      else wait_vmcnt<0>();
+      __syncthreads();
+      if (p_t < hi) {
+        p_issue(issued % S);
+        ++issued;
+      }
+      const bf16_t* As = lds[consumed % S];
+      const bf16_t* Bs = As + C::A_ELEMS;
+      ++consumed;
+      if (!wave_rows) continue;
+      bf16x8 af[2][MI], bfr[2][NI];
+      auto load_frags = [&](int ks, int slot) {
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+          af[slot][i] = a_mn ? frag_mn<BK>(As, wm * MI + i, ks, lane) : frag_k<BK>(As, wm * MI + i, ks, lane);
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+          bfr[slot][j] = b_mn ? frag_mn<BK>(Bs, bcol(j), ks, lane) : frag_k<BK>(Bs, bcol(j), ks, lane);
+      };
+      constexpr int KS = BK / 16;
+      load_frags(0, 0);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int cur = ks & 1;
+        if (ks < KS - 1) load_frags(ks + 1, cur ^ 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+          for (int j = 0; j < NI; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (colsum) {
+#pragma unroll
+          for (int j = 0; j < NI; ++j) {
+            const uint4 u = __builtin_bit_cast(uint4, bfr[cur][j]);
+            const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              bsum[j] += __uint_as_float(w4[q] << 16) + __uint_as_float(w4[q] & 0xffff0000u);
+          }
+        }
+      }
+    }
+
+    // ---- epilogue (this wavefront's rows only).  Block (i, j) holds the
+    // transposed product: lane l has row 32i + l%32, register v = 4q + t
+    // column 32j + 8q + 4(l/32) + t.
+    const int mrow0 = tl.m0 + wm * C::TM;
+    if (MODE == G_FWD_GATEUP) {
+      bf16_t* gu = reinterpret_cast<bf16_t*>(a.c0);
+      bf16_t* h = reinterpret_cast<bf16_t*>(a.c1);
+      const bf16_t* bgp = reinterpret_cast<const bf16_t*>(a.bias0);
+      const bf16_t* bup = reinterpret_cast<const bf16_t*>(a.bias1);
+      const int jbase = tl.n0 + wn * (C::TN / 2);
+#pragma unroll
+      for (int j = 0; j < NI / 2; ++j) {
+        const int jj0 = jbase + 32 * j;
+        const int ncols = min(32, N - jj0);
+        float bgv[16], buv[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int c = jj0 + 8 * (v >> 2) + 4 * hh + (v & 3);
+          bgv[v] = (bgp && c < N) ? bf2f(bgp[(int64_t)g * f + c]) : 0.f;
+          buv[v] = (bup && c < N) ? bf2f(bup[(int64_t)g * f + c]) : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const int m0 = mrow0 + 32 * i;
+          if (m0 >= M || ncols <= 0) continue;
+          float gv[16], uv[16], hv[16];
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            gv[v] = acc[i][j][v] + bgv[v];
+            uv[v] = acc[i][j + NI / 2][v] + buv[v];
+            hv[v] = silu_f(gv[v]) * uv[v];
+          }
+          auto row_gu = [&](int half) {
+            return [&, half](int r) -> bf16_t* {
+              return m0 + r < M ? gu + (int64_t)(tl.row_base + m0 + r) * 2 * f + half * f + jj0 : nullptr;
+            };
+          };
+          put_block(gv, row_gu(0), ncols);
+          put_block(uv, row_gu(1), ncols);
+          put_block(hv, [&](int r) -> bf16_t* {
+            return m0 + r < M ? h + (int64_t)(tl.row_base + m0 + r) * f + jj0 : nullptr;
+          }, ncols);
+        }
+      }
+    } else if (MODE == G_FWD_DOWN || MODE == G_DGRAD_GATEUP || MODE == G_DGRAD_DOWN) {
+      const int nbase = tl.n0 + wn * C::TN;
+      const bf16_t* bdp = MODE == G_FWD_DOWN ? reinterpret_cast<const bf16_t*>(a.bias0) : nullptr;
+      const bf16_t* gup = reinterpret_cast<const bf16_t*>(a.aux);
+      bf16_t* out = reinterpret_cast<bf16_t*>(a.c0);
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int n0 = nbase + 32 * j;
+        const int ncols = min(32, N - n0);
+        float bd[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int c = n0 + 8 * (v >> 2) + 4 * hh + (v & 3);
+          bd[v] = (bdp && c < N) ? bf2f(bdp[(int64_t)g * d + c]) : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const int m0 = mrow0 + 32 * i;
+          if (m0 >= M || ncols <= 0) continue;
+          float o[16];
+#pragma unroll
+          for (int v = 0; v < 16; ++v) o[v] = acc[i][j][v] + bd[v];
+          if (MODE == G_DGRAD_DOWN) {
+            // dSwiGLU with the saved gate/up values of this lane's row
+            const int m = m0 + r32;
+            float dg[16], du[16];
+            const int64_t row = tl.row_base + (m < M ? m : M - 1);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int c = n0 + 8 * q + 4 * hh;
+              uint2 gr = make_uint2(0, 0), ur = make_uint2(0, 0);
+              if (m < M && c < N) {
+                gr = *reinterpret_cast<const uint2*>(gup + row * 2 * f + c);
+                ur = *reinterpret_cast<const uint2*>(gup + row * 2 * f + f + c);
+              }
+              const float gv[4] = {__uint_as_float(gr.x << 16), __uint_as_float(gr.x & 0xffff0000u),
+                                   __uint_as_float(gr.y << 16), __uint_as_float(gr.y & 0xffff0000u)};
+              const float uv[4] = {__uint_as_float(ur.x << 16), __uint_as_float(ur.x & 0xffff0000u),
+                                   __uint_as_float(ur.y << 16), __uint_as_float(ur.y & 0xffff0000u)};
+#pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                const float sgm = 1.0f / (1.0f + __expf(-gv[t]));
+                dg[4 * q + t] = o[4 * q + t] * uv[t] * sgm * (1.0f + gv[t] * (1.0f - sgm));
+                du[4 * q + t] = o[4 * q + t] * gv[t] * sgm;
+              }
+            }
+            put_block(dg, [&](int r) -> bf16_t* {
+              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + n0 : nullptr;
+            }, ncols);
+            put_block(du, [&](int r) -> bf16_t* {
+              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + f + n0 : nullptr;
+            }, ncols);
+          } else {
+            put_block(o, [&](int r) -> bf16_t* {
+              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * N + n0 : nullptr;
+            }, ncols);
+          }
+        }
+      }
+    } else {
+      const int nbase = tl.n0 + wn * C::TN;
+      bf16_t* c0 = reinterpret_cast<bf16_t*>(a.c0);
+      bf16_t* c1 = reinterpret_cast<bf16_t*>(a.c1);
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int n0 = nbase + 32 * j;
+        const int ncols = min(32, N - n0);
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const int m0 = mrow0 + 32 * i;
+          if (m0 >= M || ncols <= 0) continue;
+          float o[16];
+#pragma unroll
+          for (int v = 0; v < 16; ++v) o[v] = acc[i][j][v];
+          put_block(o, [&](int r) -> bf16_t* {
+            const int m = m0 + r;
+            if (m >= M) return nullptr;
+            if (MODE == G_WGRAD_DOWN) return c0 + ((int64_t)g * f + m) * d + n0;
+            if (n0 < f) return c0 + ((int64_t)g * d + m) * f + n0;
+            return c1 + ((int64_t)g * d + m) * f + (n0 - f);
+          }, ncols);
+        }
+      }
+      if (colsum) {
+#pragma unroll
+        for (int j = 0; j < NI; ++j) {
+          float v = bsum[j];
+          v += __shfl_xor(v, 32, 64);
+          const int col = tl.n0 + wn * C::TN + j * 32 + r32;
+          if (lane < 32 && col < N) {
+            if (MODE == G_WGRAD_DOWN) reinterpret_cast<bf16_t*>(a.db0)[(int64_t)g * d + col] = f2bf(v);
+            else if (col < f) reinterpret_cast<bf16_t*>(a.db0)[(int64_t)g * f + col] = f2bf(v);
+            else reinterpret_cast<bf16_t*>(a.db1)[(int64_t)g * f + col - f] = f2bf(v);
+          }
+        }
+      }
+    }
+  }
+  wait_vmcnt<0>();  // no copy may still target this workgroup's LDS at exit
+}
+
+// ---------------------------------------------------------------------------
 // fp32 path: plain kernel, 16x16 outputs per 256-thread block
 // ---------------------------------------------------------------------------
 template <int MODE>
@@ -846,11 +1324,54 @@ int launch_bf16(const GemmArgs& a, hipStream_t s) {
                 [&] { gemm_bf16_kernel<MODE, C><<<(int)nb, C::NT, 0, s>>>(a); });
 }
 
+// Persistent launch: one workgroup per CU (a multiple of 8, so that every
+// XCD gets the same number), never more than the tiles' upper bound.
+inline int cu_count() {
+  static int n = 0;
+  if (n == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+      n = v;
+    else
+      n = 256;
+  }
+  return n;
+}
+
+template <int MODE, class C>
+int launch_bf16_persistent(const GemmArgs& a, hipStream_t s) {
+  const int G = a.offsets ? a.ngroups : 1;
+  const int nt = n_tiles<MODE, C::BN>(a.d, a.f);
+  int64_t nb;
+  if (is_wgrad<MODE>()) {
+    nb = (int64_t)G * ((wgrad_m<MODE>(a.d, a.f) + C::BM - 1) / C::BM) * nt;
+  } else {
+    const int64_t mt = a.offsets ? (a.max_rows + (int64_t)G * (C::BM - 1)) / C::BM
+                                 : (a.dense_rows + C::BM - 1) / C::BM;
+    nb = mt * nt;
+  }
+  if (nb <= 0) return MOE_OK;
+  // workgroups per CU that fit in LDS (stages, epilogue slots, tables)
+  constexpr int kLdsPerBlock = C::LDS_BYTES + C::NW * 2048 + 2 * 1024 + 64;
+  constexpr int kOcc = (160 * 1024) / kLdsPerBlock > 0 ? (160 * 1024) / kLdsPerBlock : 1;
+  const int64_t grid = std::min<int64_t>((cu_count() * kOcc / 8) * 8, (nb + 7) / 8 * 8);
+  return launch(kGemmKernelId[MODE], s, kGemmName[MODE],
+                [&] { gemm_bf16_persistent<MODE, C><<<(int)grid, C::NT, 0, s>>>(a); });
+}
+
+#ifndef MOE_GEMM_PERSISTENT
+#define MOE_GEMM_PERSISTENT 1
+#endif
+
 template <int MODE>
 int launch_mode(const GemmArgs& a, hipStream_t s) {
   if (a.bf16) {
     const int G = a.offsets ? a.ngroups : 1;
     const int64_t rows_per_group = a.offsets ? a.max_rows / G : a.dense_rows;
+    if (MOE_GEMM_PERSISTENT) {
+      if (!is_wgrad<MODE>() && rows_per_group < 384) return launch_bf16_persistent<MODE, CfgSmall>(a, s);
+      return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big>(a, s);
+    }
     if (!is_wgrad<MODE>() && rows_per_group < 384) return launch_bf16<MODE, CfgSmall>(a, s);
     return launch_bf16<MODE, typename GemmShape<MODE>::big>(a, s);
   }
