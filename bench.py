@@ -50,8 +50,10 @@ def kernel_work(cfg):
         "gemm_gateup_fwd": ("mfma", gu), "gemm_down_fwd": ("mfma", dn),
         "gemm_down_dgrad": ("mfma", dn), "gemm_gateup_dgrad": ("mfma", gu),
         "gemm_down_wgrad": ("mfma", dn), "gemm_gateup_wgrad": ("mfma", gu),
+        # router logits: bf16 x times the three bf16 parts of W_r
+        "route": ("mfma", 2.0 * T * d * E * 3),
         # bytes: reads + writes of the HBM operands, once each
-        "route": ("hbm", T * d * eb + d * E * 4 + R * 8),
+        "route_select": ("hbm", T * E * 8 + R * 8),
         "scatter": ("hbm", T * d * eb + R * d * eb + R * 4 * 3),
         "combine_fwd": ("hbm", R * d * eb + T * d * eb + R * 8),
         "combine_bwd": ("hbm", T * d * eb + 2 * R * d * eb + R * 12),

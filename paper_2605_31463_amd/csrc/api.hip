@@ -75,7 +75,7 @@ const char* kernel_name(int id) {
       "route", "count_zero", "hist", "scan", "scatter", "gemm_gateup_fwd", "gemm_down_fwd",
       "combine_fwd", "combine_bwd", "route_dl", "route_dwr_partial", "route_dwr_reduce",
       "wr_transpose", "route_dx", "gemm_down_dgrad", "gemm_gateup_dgrad", "gemm_down_wgrad",
-      "gemm_gateup_wgrad", "unpermute", "rank", "wr_split"};
+      "gemm_gateup_wgrad", "unpermute", "rank", "wr_split", "route_select"};
   if (id < 0 || id >= K_NUM_KERNELS) return nullptr;
   return names[id];
 }
@@ -137,7 +137,7 @@ inline size_t act_bytes(const moe_shape& s) { return s.dtype == MOE_BF16 ? 2 : 4
 
 struct Plan {
   // forward
-  size_t hist, wsplit;
+  size_t hist, wsplit, lg;
   size_t fwd_total;
   // backward
   size_t d_o, dgu, dx_perm, dl, partial, w_rt, dgu_sh, dx_sh;
@@ -154,6 +154,8 @@ Plan plan(const moe_shape& s) {
   off += align_up((size_t)moe::perm_blocks(s.T) * s.E * 4);
   p.wsplit = off;
   off += s.dtype == MOE_BF16 ? align_up((size_t)3 * s.E * s.d * 2) : 0;
+  p.lg = off;
+  off += s.dtype == MOE_BF16 ? align_up((size_t)s.T * s.E * 8) : 0;
   p.fwd_total = off;
   off = 0;
   p.d_o = off; off += align_up((size_t)R * s.d * eb);
@@ -220,6 +222,7 @@ int do_route(const moe_shape& s, const void* x, const float* w_r, const float* b
              float* topk_w, float* s_sel, int32_t* counts, void* ws, hipStream_t st) {
   RouteArgs a{};
   a.wsplit = s.dtype == MOE_BF16 ? wsp(ws, plan(s).wsplit) : nullptr;
+  a.lg = s.dtype == MOE_BF16 ? reinterpret_cast<double*>(wsp(ws, plan(s).lg)) : nullptr;
   a.x = x;
   a.w_r = w_r;
   a.bias = bias;

@@ -31,6 +31,7 @@ enum KernelId {
   K_UNPERMUTE,
   K_RANK,
   K_WR_SPLIT,
+  K_ROUTE_SELECT,
   K_NUM_KERNELS
 };
 
@@ -144,6 +145,49 @@ __device__ __forceinline__ int xcd_remap(int b, int nblocks) {
   const int xcd = b & 7, idx = b >> 3;
   const int per = nblocks >> 3, rem = nblocks & 7;
   return xcd * per + (xcd < rem ? xcd : rem) + idx;
+}
+
+// ---------------------------------------------------------------------------
+// Global -> LDS copies without registers (buffer_load_dwordx4 ... lds): one
+// instruction moves 64 lanes x 16 bytes into 1 KB of LDS at the wave-uniform
+// address in M0.  The copies are issued from inline assembly and counted by
+// hand with s_waitcnt vmcnt, so that several stages can be in flight while
+// the compiler schedules LDS reads freely.  A buffer descriptor bounds every
+// copy: reads past its range return zeros and touch no memory.
+// ---------------------------------------------------------------------------
+typedef int int32x4_t __attribute__((ext_vector_type(4)));
+constexpr int RSRC_FLAGS = 0x00020000;
+
+// Buffer descriptor (raw buffer, no stride) over [p, p + bytes), in SGPRs.
+__device__ __forceinline__ int32x4_t make_rsrc(const void* p, int64_t bytes) {
+  const uint64_t b = (uint64_t)p;
+  int32x4_t r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)b);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(b >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane((int)(uint32_t)bytes);
+  r[3] = RSRC_FLAGS;
+  return r;
+}
+
+template <class T>
+__device__ __forceinline__ uint32_t lds_addr(const T* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) T*)p);
+}
+
+__device__ __forceinline__ void dma16(const int32x4_t& r, uint32_t lds, uint32_t voff, uint32_t soff) {
+  int32x4_t rs;  // wave-uniform by construction; keeps the operand in SGPRs
+#pragma unroll
+  for (int q = 0; q < 4; ++q) rs[q] = __builtin_amdgcn_readfirstlane(r[q]);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rs),
+                  "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory");
+}
+
+// s_waitcnt vmcnt(n), expcnt and lgkmcnt left free
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | 0x0F70);
 }
 
 }  // namespace moe

@@ -42,7 +42,6 @@ typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) void* lds_void_t;
 typedef __attribute__((address_space(3))) v4i16* lds_v4_t;
 
-constexpr int RSRC_FLAGS = 0x00020000;
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }
 
@@ -178,8 +177,6 @@ __device__ __forceinline__ Tile decode_tile(const GemmArgs& a, int* pre, int* sb
 // a 4 (k) x 16 (columns) block addressed by its 16 lanes (~120 B/clk per CU
 // whatever the swizzle).
 // ---------------------------------------------------------------------------
-typedef int int32x4_t __attribute__((ext_vector_type(4)));
-
 template <int BK>
 __device__ __forceinline__ int kswz(int r) { return BK == 64 ? (r >> 1) & 7 : ((r >> 2) ^ (r >> 3)) & 3; }
 template <int BK>
@@ -188,37 +185,6 @@ __device__ __forceinline__ int mswz(int k) { return ((k >> 1) & 1) << 2; }
 template <int BK>
 __device__ __forceinline__ int mn_off(int k, int col) {
   return (col >> 6) * (64 * BK) + k * 64 + ((((col & 63) >> 3) ^ mswz(k)) << 3) + (col & 7);
-}
-
-// Buffer descriptor (raw buffer, no stride) over [p, p + bytes), in SGPRs.
-__device__ __forceinline__ int32x4_t make_rsrc(const void* p, int64_t bytes) {
-  const uint64_t b = (uint64_t)p;
-  int32x4_t r;
-  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)b);
-  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(b >> 32) & 0xffffu));
-  r[2] = __builtin_amdgcn_readfirstlane((int)(uint32_t)bytes);
-  r[3] = RSRC_FLAGS;
-  return r;
-}
-
-__device__ __forceinline__ uint32_t lds_addr(const bf16_t* p) {
-  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) bf16_t*)p);
-}
-
-__device__ __forceinline__ void dma16(const int32x4_t& r, uint32_t lds, uint32_t voff, uint32_t soff) {
-  int32x4_t rs;  // wave-uniform by construction; keeps the operand in SGPRs
-#pragma unroll
-  for (int q = 0; q < 4; ++q) rs[q] = __builtin_amdgcn_readfirstlane(r[q]);
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rs),
-                  "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory");
-}
-
-// s_waitcnt vmcnt(n), expcnt and lgkmcnt left free
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | 0x0F70);
 }
 
 // This wave's share of one K-contiguous ROWS x BK tile: 1 KB copies of

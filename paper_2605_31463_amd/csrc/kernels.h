@@ -21,6 +21,7 @@ struct RouteArgs {
   float* s_sel;
   int32_t* counts;  // may be null
   void* wsplit;      // bf16 [3][E][d] workspace for the MFMA path (bf16 x), or null
+  double* lg;        // float64 [T][E] logits workspace for the MFMA path
 };
 int launch_route(const RouteArgs& a, hipStream_t s);
 int zero_i32(int32_t* p, int64_t n, hipStream_t s);

@@ -1,19 +1,22 @@
 // Router forward: logits, top-k selection, gating weights, expert counts.
 //
-// One fused kernel per block of 32 tokens:
-//   1. logits l = x W_r for the block's tokens and every expert.  Products
-//      run in float32 FMA chains of 16 terms; each chain is folded into a
-//      float64 total, so a logit carries about 1e-7 absolute error at the
-//      workloads' scale and the float64 selection keys order experts the
-//      way an exact evaluation does outside sub-1e-6 near-ties.
-//   2. one wavefront per token selects the top-k over float64 keys with
-//      64-lane butterfly reductions (the framework's top-k routing kernel,
-//      section 3.2 / appendix B.3), optionally restricted to the best
-//      expert groups (group score = sum of the group's two largest keys);
+// Three paths, all computing:
+//   1. logits l = x W_r for every token and expert, accurate enough (float32
+//      partial sums folded into float64) that the float64 selection keys
+//      order experts the way an exact evaluation does outside sub-1e-6
+//      near-ties;
+//   2. top-k over the selection keys with one wavefront per token and 64-lane
+//      butterfly reductions (the framework's top-k routing kernel, section
+//      3.2 / appendix B.3), optionally restricted to the best expert groups
+//      (group score = sum of the group's two largest keys);
 //   3. gating weights over the selected experts: softmax of the selected
 //      (biased) logits, or route_scale * sigmoid / sum of sigmoids; weights
 //      are non-negative and sum to route_scale (appendix B.2.2 rules);
-//   4. per-block expert histogram added into the expert counts.
+//   4. per-block expert histograms added into the expert counts.
+// bf16 activations with E a multiple of 32: a tiled MFMA logits GEMM into a
+// float64 workspace, then a selection kernel.  Other bf16 cases: one fused
+// MFMA kernel per block of tokens.  float32: one fused kernel of float32 FMA
+// chains of 16 terms folded into float64.
 #include <float.h>
 #include <math.h>
 
@@ -314,6 +317,157 @@ __global__ void wr_split_kernel(const float* __restrict__ w, bf16_t* __restrict_
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 path, large expert counts: logits as a tiled GEMM, then a selection
+// kernel.  The logits kernel's workgroup tile is TT tokens x TE experts; K = d
+// advances in stages of 64 copied global -> LDS without registers (x rows and
+// the three bf16 parts of W_r, all K-contiguous 128-byte rows with the 16-byte
+// chunk index XOR-swizzled by (row >> 1) & 7).  One wavefront per 16 tokens
+// runs v_mfma_f32_16x16x32_bf16 over the three parts into one float32
+// accumulator per 16 x 16 block (every product x * w_i is exact in float32)
+// and folds it into float64 after every stage, as the fused kernel does.
+// The expert tiles of one token tile are consecutive in the XCD-contiguous
+// order, so the token rows are fetched from HBM once.
+// ---------------------------------------------------------------------------
+template <int TT, int TE>
+__global__ __launch_bounds__(TT * 4) void route_logits_kernel(RouteArgs a) {
+  constexpr int NW = TT / 16;
+  constexpr int KC = 64, S = 3;
+  constexpr int XROWS = TT, WROWS = 3 * TE;
+  constexpr int STAGE = (XROWS + WROWS) * KC;  // bf16 elements
+  constexpr int NI = (XROWS + WROWS) / 8;      // 1 KB copies per stage
+  static_assert(NI % NW == 0, "every wavefront issues the same number of copies");
+  constexpr int NIW = NI / NW;
+  constexpr int NJ = TE / 16;
+  __shared__ __align__(16) bf16_t st[S][STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int E = a.E, d = a.d;
+  const int net = E / TE;
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int tt = lin / net, et = lin - tt * net;
+  const int64_t t0 = (int64_t)tt * TT;
+  const int e0 = et * TE;
+  const bf16_t* x = reinterpret_cast<const bf16_t*>(a.x);
+  const bf16_t* wsp = reinterpret_cast<const bf16_t*>(a.wsplit);
+  const int32x4_t rx = make_rsrc(x + t0 * d, (a.T - t0) * d * 2);  // rows past T read as zeros
+  const int32x4_t rw = make_rsrc(wsp, (int64_t)3 * E * d * 2);
+  uint32_t voff[NIW];
+  bool isx[NIW];
+#pragma unroll
+  for (int j = 0; j < NIW; ++j) {
+    const int q = (NIW * wave + j) * 64 + lane;
+    const int row = q >> 3, c = (q & 7) ^ ((row >> 1) & 7);
+    isx[j] = 8 * (NIW * wave + j) < XROWS;  // whole copies fall in one part
+    if (row < XROWS) {
+      voff[j] = (uint32_t)(((int64_t)row * d + 8 * c) * 2);
+    } else {
+      const int wr = row - XROWS, p = wr / TE, e = wr - p * TE;
+      voff[j] = (uint32_t)((((int64_t)p * E + e0 + e) * d + 8 * c) * 2);
+    }
+  }
+  const uint32_t lds0 = lds_addr(&st[0][0]);
+  auto issue = [&](int kt) {
+    const uint32_t base = lds0 + (kt % S) * STAGE * 2;
+#pragma unroll
+    for (int j = 0; j < NIW; ++j)
+      dma16(isx[j] ? rx : rw, base + (NIW * wave + j) * 1024, voff[j], (uint32_t)(kt * KC * 2));
+  };
+
+  floatx4 acc[NJ];
+  double acc64[NJ][4];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc64[j][v] = 0.0;
+  }
+  const int nk = d / KC;
+#pragma unroll
+  for (int p = 0; p < S - 1; ++p)
+    if (p < nk) issue(p);
+  const int arow = wave * 16 + (lane & 15);
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) wait_vmcnt<(S - 2) * NIW>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (kt + S - 1 < nk) issue(kt + S - 1);
+    const bf16_t* sx = st[kt % S];
+    const bf16_t* sw = sx + XROWS * KC;
+#pragma unroll
+    for (int ks = 0; ks < KC / 32; ++ks) {
+      const int c = ks * 4 + (lane >> 4);
+      const bf16x8 af = *reinterpret_cast<const bf16x8*>(sx + arow * KC + ((c ^ ((arow >> 1) & 7)) << 3));
+#pragma unroll
+      for (int p = 0; p < 3; ++p)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const int br = p * TE + 16 * j + (lane & 15);
+          const bf16x8 bfr = *reinterpret_cast<const bf16x8*>(sw + br * KC + ((c ^ ((br >> 1) & 7)) << 3));
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr, acc[j], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc64[j][v] += (double)acc[j][v];
+      acc[j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+  // D block (j): lane holds tokens 4 (lane / 16) + v, expert 16 j + lane % 16
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t t = t0 + wave * 16 + 4 * (lane >> 4) + v;
+      if (t < a.T) a.lg[t * E + e0 + 16 * j + (lane & 15)] = acc64[j][v];
+    }
+}
+
+// Selection over the float64 logits in the workspace: one wavefront per token,
+// 16 tokens per workgroup.
+__global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a) {
+  constexpr int TPB = 16;
+  __shared__ int hist[256];
+  for (int e = threadIdx.x; e < 256; e += 256) hist[e] = 0;
+  __syncthreads();
+  const int64_t t0 = (int64_t)blockIdx.x * TPB;
+  const int ntok = (int)min((int64_t)TPB, a.T - t0);
+  select_tokens(a, a.lg + t0 * a.E, a.E, t0, ntok, hist);
+  __syncthreads();
+  if (a.counts) {
+    for (int e = threadIdx.x; e < a.E; e += 256)
+      if (hist[e]) atomicAdd(&a.counts[e], hist[e]);
+  }
+}
+
+int launch_route_gemm(const RouteArgs& a, hipStream_t s) {
+  {
+    dim3 grid((a.E + 31) / 32, (a.d + 31) / 32);
+    bf16_t* wsp = reinterpret_cast<bf16_t*>(a.wsplit);
+    const int st = launch(K_WR_SPLIT, s, "wr_split", [&] { wr_split_kernel<<<grid, 256, 0, s>>>(a.w_r, wsp, a.d, a.E); });
+    if (st) return st;
+  }
+  // a router weight that fits in L2 is re-read per 64-token tile; a larger
+  // one (DeepSeek-like d x 256) per 128 tokens
+  const bool big_w = (int64_t)3 * a.E * a.d * 2 > ((int64_t)2 << 20);
+  int st;
+#define MOE_RL(TT_, TE_)                                                                               \
+  st = launch(K_ROUTE, s, "route", [&] {                                                               \
+    route_logits_kernel<TT_, TE_><<<(int)(((a.T + TT_ - 1) / TT_) * (a.E / TE_)), TT_ * 4, 0, s>>>(a); \
+  });
+  if (a.E % 64 == 0) {
+    if (big_w) { MOE_RL(128, 64) } else { MOE_RL(64, 64) }
+  } else {
+    MOE_RL(64, 32)
+  }
+#undef MOE_RL
+  if (st) return st;
+  return launch(K_ROUTE_SELECT, s, "route_select",
+                [&] { route_select_kernel<<<(int)((a.T + 15) / 16), 256, 0, s>>>(a); });
+}
+
 // NTW: 16-expert MFMA tiles per wavefront.  Without SPLIT a block is 64 tokens
 // x 16*NTW experts (4 wavefronts stacked over tokens); with SPLIT it is 32
 // tokens x 32*NTW experts (2 x 2 wavefronts).
@@ -493,6 +647,7 @@ int launch_route(const RouteArgs& a, hipStream_t s) {
     if (st) return st;
   }
   if (a.T == 0) return MOE_OK;
+  if (a.bf16 && a.wsplit && a.lg && a.E % 32 == 0) return launch_route_gemm(a, s);
   if (a.bf16 && a.wsplit && a.E % 16 == 0) return launch_route_mfma(a, s);
   return a.bf16 ? launch_route_t<bf16_t>(a, s) : launch_route_t<float>(a, s);
 }
