@@ -817,7 +817,7 @@ int moe_layer_bwd(const moe_shape* shape, const moe_params* prm, const void* x, 
   rb.dx_router = nullptr;
   rb.partial = reinterpret_cast<float*>(wsp(ws, p.partial));
   MOE_TRY(launch_route_bwd(rb, stream));
-  MOE_TRY(launch_wr_transpose(prm->w_r, w_rt, (int)s.d, (int)s.E, stream));
+  MOE_TRY(launch_wr_transpose_act(prm->w_r, w_rt, (int)s.d, (int)s.E, s.dtype == MOE_BF16, stream));
   // 4. shared expert
   void* dx_sh = nullptr;
   if (s.n_shared) {

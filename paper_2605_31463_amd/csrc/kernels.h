@@ -101,6 +101,8 @@ constexpr int DWR_ROWS = 256;  // rows per partial-sum task of dW_r
 inline int64_t route_dwr_tasks(int64_t R, int64_t E) { return R / DWR_ROWS + E; }
 int launch_route_bwd(const RouteBwdArgs& a, hipStream_t s);
 int launch_wr_transpose(const float* w_r, float* w_rt, int d, int E, hipStream_t s);
+// W_r^T in the activation type (bf16 rounding for bf16 layers)
+int launch_wr_transpose_act(const float* w_r, void* w_rt, int d, int E, bool bf16, hipStream_t s);
 
 struct UnpermuteArgs {
   const void* dx_perm;
@@ -110,7 +112,7 @@ struct UnpermuteArgs {
   // fused router dx: dx += sum_s dl[t][s] * w_rt[topk_idx[t][s]]
   const float* dl;          // may be null
   const int32_t* topk_idx;
-  const float* w_rt;
+  const void* w_rt;         // W_r^T [E][d] in the activation type
   void* dx;
   int64_t T;
   int d, k;

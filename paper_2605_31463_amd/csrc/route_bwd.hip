@@ -108,7 +108,8 @@ __global__ __launch_bounds__(256) void dwr_reduce_kernel(RouteBwdArgs a) {
   a.dw_r[(int64_t)i * a.E + e] = acc;
 }
 
-__global__ void transpose_kernel(const float* __restrict__ w, float* __restrict__ wt, int d, int E) {
+template <class OT>
+__global__ void transpose_kernel(const float* __restrict__ w, OT* __restrict__ wt, int d, int E) {
   __shared__ float tile[32][33];
   const int e0 = blockIdx.x * 32, i0 = blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 256 threads: 32 x 8
@@ -119,7 +120,7 @@ __global__ void transpose_kernel(const float* __restrict__ w, float* __restrict_
   __syncthreads();
   for (int r = ty; r < 32; r += 8) {
     const int e = e0 + r, i = i0 + tx;
-    if (e < E && i < d) wt[(int64_t)e * d + i] = tile[tx][r];
+    if (e < E && i < d) Elem<OT>::store(wt, (int64_t)e * d + i, tile[tx][r]);
   }
 }
 
@@ -146,7 +147,14 @@ __global__ __launch_bounds__(256) void dx_router_kernel(RouteBwdArgs a, const fl
 
 int launch_wr_transpose(const float* w_r, float* w_rt, int d, int E, hipStream_t s) {
   dim3 grid((E + 31) / 32, (d + 31) / 32);
-  return launch(K_WR_TRANSPOSE, s, "wr_transpose", [&] { transpose_kernel<<<grid, 256, 0, s>>>(w_r, w_rt, d, E); });
+  return launch(K_WR_TRANSPOSE, s, "wr_transpose", [&] { transpose_kernel<float><<<grid, 256, 0, s>>>(w_r, w_rt, d, E); });
+}
+
+int launch_wr_transpose_act(const float* w_r, void* w_rt, int d, int E, bool bf16, hipStream_t s) {
+  if (!bf16) return launch_wr_transpose(w_r, reinterpret_cast<float*>(w_rt), d, E, s);
+  dim3 grid((E + 31) / 32, (d + 31) / 32);
+  bf16_t* o = reinterpret_cast<bf16_t*>(w_rt);
+  return launch(K_WR_TRANSPOSE, s, "wr_transpose", [&] { transpose_kernel<bf16_t><<<grid, 256, 0, s>>>(w_r, o, d, E); });
 }
 
 int launch_route_bwd(const RouteBwdArgs& a, hipStream_t s) {
