@@ -80,8 +80,10 @@ def traffic_for(kernel, workload):
     return None if ent is None else ent.get("bytes_per_launch")
 
 
-def cpu_baseline(cfg, seed, tokens):
-    """The fp64 oracle, as it stands, on the first `tokens` tokens of the workload."""
+def cpu_baseline(cfg, seed, tokens, reps=1):
+    """The fp64 oracle, as it stands, on the first `tokens` tokens of the workload,
+    fwd+bwd repeated `reps` times on the same inputs (so that the timed CPU work is
+    long enough to measure)."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -108,16 +110,17 @@ def cpu_baseline(cfg, seed, tokens):
     if scfg["n_shared"]:
         shared = tuple(to_f64(inp[n], dt) for n in ("ws_gate", "ws_up", "ws_down"))
     t0 = time.perf_counter()
-    fwd = layer_forward(spec, x, w_r, beta, efn, shared)
-    layer_backward(spec, x, w_r, beta, efn, fwd, dy, shared, with_bias=scfg["expert_bias"])
+    for _ in range(reps):
+        fwd = layer_forward(spec, x, w_r, beta, efn, shared)
+        layer_backward(spec, x, w_r, beta, efn, fwd, dy, shared, with_bias=scfg["expert_bias"])
     wall = time.perf_counter() - t0
     _, fb = layer_flops(scfg)
     threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
-    return {"value": round(fb / wall / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
+    return {"value": round(reps * fb / wall / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle",
-            "sample": "fp64 oracle fwd+bwd of the first %d of %d tokens (same shapes, seed %d), %.1f s wall"
-                      % (tokens, cfg["T"], seed, wall),
-            "tokens_per_s": round(tokens / wall, 1)}
+            "sample": "fp64 oracle fwd+bwd of %d of %d tokens (same shapes, seed %d), %d times, %.1f s wall"
+                      % (tokens, cfg["T"], seed, reps, wall),
+            "tokens_per_s": round(reps * tokens / wall, 1)}
 
 
 def main():
@@ -129,6 +132,7 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-tokens", type=int, default=0,
                     help="tokens of the workload the CPU oracle runs (0: all of them)")
+    ap.add_argument("--cpu-reps", type=int, default=3, help="repetitions of the oracle's fwd+bwd")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="before the timed steps, run a plain torch copy of this many MiB three times "
@@ -247,7 +251,7 @@ def main():
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, args.seed, args.cpu_tokens or cfg["T"])
+        out["cpu_baseline"] = cpu_baseline(cfg, args.seed, args.cpu_tokens or cfg["T"], args.cpu_reps)
     print(json.dumps(out), flush=True)
 
 
