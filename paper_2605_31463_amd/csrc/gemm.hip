@@ -1025,7 +1025,65 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
           }, ncols);
         }
       }
-    } else if (MODE == G_FWD_DOWN || MODE == G_DGRAD_GATEUP || MODE == G_DGRAD_DOWN) {
+    } else if (MODE == G_DGRAD_DOWN) {
+      // dSwiGLU with the saved gate/up values: for each 32-row block, every
+      // gate/up load of the wavefront's columns is issued before any math
+      const int nbase = tl.n0 + wn * C::TN;
+      const bf16_t* gup = reinterpret_cast<const bf16_t*>(a.aux);
+      bf16_t* out = reinterpret_cast<bf16_t*>(a.c0);
+      constexpr int JB = NI > 2 ? 2 : NI;  // column blocks per batch of loads
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const int m0 = mrow0 + 32 * i;
+        if (m0 >= M) continue;
+        const int m = m0 + r32;
+        const int64_t row = tl.row_base + (m < M ? m : M - 1);
+#pragma unroll
+        for (int jb = 0; jb < NI; jb += JB) {
+          uint2 gr[JB][4], ur[JB][4];
+#pragma unroll
+          for (int jj = 0; jj < JB; ++jj)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int c = nbase + 32 * (jb + jj) + 8 * q + 4 * hh;
+              gr[jj][q] = make_uint2(0, 0);
+              ur[jj][q] = make_uint2(0, 0);
+              if (m < M && c < N) {
+                gr[jj][q] = *reinterpret_cast<const uint2*>(gup + row * 2 * f + c);
+                ur[jj][q] = *reinterpret_cast<const uint2*>(gup + row * 2 * f + f + c);
+              }
+            }
+#pragma unroll
+          for (int jj = 0; jj < JB; ++jj) {
+            const int j = jb + jj;
+            const int n0 = nbase + 32 * j;
+            const int ncols = min(32, N - n0);
+            if (ncols <= 0) continue;
+            float dg[16], du[16];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float gv[4] = {__uint_as_float(gr[jj][q].x << 16), __uint_as_float(gr[jj][q].x & 0xffff0000u),
+                                   __uint_as_float(gr[jj][q].y << 16), __uint_as_float(gr[jj][q].y & 0xffff0000u)};
+              const float uv[4] = {__uint_as_float(ur[jj][q].x << 16), __uint_as_float(ur[jj][q].x & 0xffff0000u),
+                                   __uint_as_float(ur[jj][q].y << 16), __uint_as_float(ur[jj][q].y & 0xffff0000u)};
+#pragma unroll
+              for (int t = 0; t < 4; ++t) {
+                const float o = acc[i][j][4 * q + t];
+                const float sgm = 1.0f / (1.0f + __expf(-gv[t]));
+                dg[4 * q + t] = o * uv[t] * sgm * (1.0f + gv[t] * (1.0f - sgm));
+                du[4 * q + t] = o * gv[t] * sgm;
+              }
+            }
+            put_block(dg, [&](int r) -> bf16_t* {
+              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + n0 : nullptr;
+            }, ncols);
+            put_block(du, [&](int r) -> bf16_t* {
+              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + f + n0 : nullptr;
+            }, ncols);
+          }
+        }
+      }
+    } else if (MODE == G_FWD_DOWN || MODE == G_DGRAD_GATEUP) {
       const int nbase = tl.n0 + wn * C::TN;
       const bf16_t* bdp = MODE == G_FWD_DOWN ? reinterpret_cast<const bf16_t*>(a.bias0) : nullptr;
       const bf16_t* gup = reinterpret_cast<const bf16_t*>(a.aux);
