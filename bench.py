@@ -115,9 +115,17 @@ def cpu_baseline(cfg, seed, tokens, reps=1):
         layer_backward(spec, x, w_r, beta, efn, fwd, dy, shared, with_bias=scfg["expert_bias"])
     wall = time.perf_counter() - t0
     _, fb = layer_flops(scfg)
-    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+    threads = max([p.get("num_threads", 1) for p in blas] or [1])
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            cpu = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), cpu)
+    except OSError:
+        pass
     return {"value": round(reps * fb / wall / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu": cpu,
+            "blas": ",".join(sorted({"%s %s" % (p.get("internal_api"), p.get("version")) for p in blas})),
             "sample": "fp64 oracle fwd+bwd of %d of %d tokens (same shapes, seed %d), %d times, %.1f s wall"
                       % (tokens, cfg["T"], seed, reps, wall),
             "tokens_per_s": round(reps * tokens / wall, 1)}
@@ -216,6 +224,22 @@ def main():
     L.moe_timing_select(-1)
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
 
+    # after the timed region: forward and backward separately, per step (events
+    # at the step's start, between the two calls and at its end)
+    n_ph = max(10, args.steps)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_ph)]
+    for e in evs:
+        e[0].record(stream)
+        layer.forward(params, x)
+        e[1].record(stream)
+        layer.backward(params, x, dy, grads)
+        e[2].record(stream)
+    torch.cuda.synchronize()
+    f_ms = [e[0].elapsed_time(e[1]) for e in evs][-10:]
+    b_ms = [e[1].elapsed_time(e[2]) for e in evs][-10:]
+    s_ms = [e[0].elapsed_time(e[2]) for e in evs][-10:]
+    med = lambda v: sorted(v)[len(v) // 2]  # noqa: E731
+
     _, fb = layer_flops(cfg)
     tflops = fb / (ms_per_step / 1e3) / 1e12
     bound, amount = work[dominant]
@@ -243,6 +267,10 @@ def main():
         "config": {"workload": workload, "T": cfg["T"], "d": cfg["d"], "E": cfg["E"], "k": cfg["k"],
                    "f": cfg["f"], "router": cfg["router"]},
         "tokens_per_s": round(cfg["T"] / (ms_per_step / 1e3), 1),
+        "phases_median_of_last_10": {"fwd_ms": round(med(f_ms), 4), "bwd_ms": round(med(b_ms), 4),
+                                     "step_ms": round(med(s_ms), 4),
+                                     "fwd_tflops": round(fb / 3 / (med(f_ms) / 1e3) / 1e12, 2),
+                                     "bwd_tflops": round(fb * 2 / 3 / (med(b_ms) / 1e3) / 1e12, 2)},
         "wall_s_timed": round(wall, 4),
         "roofline": {"bound": bound, "kernel": dominant, "achieved": round(achieved, 2), "peak": peak,
                      "unit": unit, "frac": round(achieved / peak, 4),
