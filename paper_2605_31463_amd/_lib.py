@@ -73,6 +73,13 @@ def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError("libmoe.so is not built (%s); run python -m paper_2605_31463_amd.build"
                           % LIB_PATH)
+    # torch carries its own copy of the HIP runtime, whose file name differs
+    # from the one libmoe.so asks for.  Loading torch first makes the dynamic
+    # linker satisfy libmoe's libamdhip64.so.7 with torch's already-loaded copy
+    # (same soname): one runtime in the process, sharing torch's streams and
+    # memory.  Loaded the other way round, the process would hold two runtimes
+    # and the second finds no device.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     S = ctypes.POINTER(moe_shape)
     sz = ctypes.c_size_t

@@ -686,15 +686,18 @@ __device__ __forceinline__ int tile_count(const GemmArgs& a, int* pre, int* sbuf
 }
 
 // Tile with logical id `lin` (pre[] from tile_count for variable-row passes).
+// Weight-gradient passes: ord (or null for the identity) maps the position of
+// a group's tiles in the schedule to the group.
 template <int MODE, int BM, int BN>
-__device__ __forceinline__ Tile tile_at(const GemmArgs& a, int lin, const int* pre) {
+__device__ __forceinline__ Tile tile_at(const GemmArgs& a, int lin, const int* pre, const int* ord = nullptr) {
   Tile t;
   const int nt = n_tiles<MODE, BN>(a.d, a.f);
   t.live = true;
   if (is_wgrad<MODE>()) {
     const int mt = (wgrad_m<MODE>(a.d, a.f) + BM - 1) / BM;
-    t.g = lin / (mt * nt);
-    const int rem = lin - t.g * mt * nt;
+    const int pos = lin / (mt * nt);
+    t.g = ord ? ord[pos] : pos;
+    const int rem = lin - pos * mt * nt;
     const int im = rem / nt;
     t.m0 = im * BM;
     t.n0 = (rem - im * nt) * BN;
@@ -723,6 +726,101 @@ __device__ __forceinline__ Tile tile_at(const GemmArgs& a, int lin, const int* p
   return t;
 }
 
+// Weight-gradient tiles cost in proportion to their expert's row count (the
+// K of the product): a tile of group g costs ceil(rows_g / 32) + kWgradEpi
+// units (the epilogue's share, so that empty experts, whose zero gradients
+// are still written, count too).  The equal-count XCD ranges are kept when
+// they leave no XCD more than 10% above the mean work (near-uniform experts,
+// where re-dealing would only cost).  Otherwise the 8 XCD ranges split the
+// total work evenly: each boundary is the first tile whose work midpoint lies
+// at or past x/8 of the total, rounded to a multiple of the XCD's workgroup
+// count.  When, besides, a single tile holds more than 1/8 of a workgroup's
+// mean share (a few experts with most of the rows), round-robin dealing would
+// still pile the big tiles onto some workgroups, so
+//   * groups are taken in order of decreasing row count (ord[] maps a sorted
+//     position to its group; ties keep the group order), so tiles of similar
+//     cost sit next to each other, and
+//   * inside an XCD the tiles are dealt in rounds of one tile per workgroup,
+//     every other round in reverse workgroup order (snake).
+// Sorting is not the default: it gathers many small experts on the same XCDs,
+// where the fixed per-tile costs the work estimate leaves out add up.
+// Returns whether the sorted order and snake deal are in use.
+constexpr int kWgradEpi = 6;
+template <int MODE, int BM, int BN>
+__device__ __forceinline__ bool wgrad_schedule(const GemmArgs& a, int x, int per_x, int T, int* pre,
+                                               int* ord, int* sbuf, int& lo, int& hi) {
+  const int G = a.ngroups;
+  const int tid = threadIdx.x;
+  const int tpg = ((wgrad_m<MODE>(a.d, a.f) + BM - 1) / BM) * n_tiles<MODE, BN>(a.d, a.f);
+  const int rows = tid < G ? a.offsets[tid + 1] - a.offsets[tid] : 0;
+  __shared__ int wsum;
+  auto scan_work = [&](int r) {
+    const int w = tid < G ? (r + 31) / 32 + kWgradEpi : 0;
+    const int ex = block_scan_256(w, sbuf, &wsum);
+    if (tid < G) pre[tid] = ex;
+    if (tid == 0) pre[G] = wsum;
+    __syncthreads();
+  };
+  scan_work(rows);
+  // per-tile work units: the tiles at position p start at tpg * pre[p]
+  int64_t wall = (int64_t)tpg * wsum;
+  auto work_before = [&](int t) -> int64_t {
+    if (t >= T) return wall;
+    const int p = t / tpg;
+    return (int64_t)tpg * pre[p] + (int64_t)(t - p * tpg) * (pre[p + 1] - pre[p]);
+  };
+  int64_t wmax = 0;
+  for (int xb = 0; xb < 8; ++xb) {
+    const int l = xb * (T >> 3) + min(xb, T & 7);
+    const int h = l + (T >> 3) + (xb < (T & 7) ? 1 : 0);
+    wmax = max(wmax, work_before(h) - work_before(l));
+  }
+  if (wmax * 8 * 10 <= wall * 11) return false;  // lo, hi keep the equal-count ranges
+
+  __shared__ int rmax;
+  if (tid == 0) rmax = 0;
+  __syncthreads();
+  if (tid < G) atomicMax(&rmax, rows);
+  __syncthreads();
+  const bool sorted = ((int64_t)(rmax + 31) / 32 + kWgradEpi) * 64 * per_x > wall;
+  if (sorted) {
+    // rank of each group by decreasing rows, then the work prefix in that order
+    if (tid < G) sbuf[tid] = rows;
+    __syncthreads();
+    int rank = 0;
+    if (tid < G)
+      for (int q = 0; q < G; ++q) {
+        const int rq = sbuf[q];
+        rank += (rq > rows) || (rq == rows && q < tid);
+      }
+    __syncthreads();
+    if (tid < G) ord[rank] = tid;
+    __syncthreads();
+    scan_work(tid < G ? a.offsets[ord[tid] + 1] - a.offsets[ord[tid]] : 0);
+    wall = (int64_t)tpg * wsum;
+  }
+  auto bound = [&](int xb) -> int {
+    if (xb <= 0) return 0;
+    if (xb >= 8) return T;
+    const int64_t B = wall * xb / 8;
+    int l = 0, h = G - 1;  // last position p with tpg * pre[p] <= B
+    while (l < h) {
+      const int mid = (l + h + 1) >> 1;
+      if ((int64_t)tpg * pre[mid] <= B) l = mid; else h = mid - 1;
+    }
+    const int64_t w1 = pre[l + 1] - pre[l];
+    const int64_t num = 2 * (B - (int64_t)tpg * pre[l]) - w1;  // tile j has midpoint >= B iff 2 w1 j >= num
+    int64_t j = num <= 0 ? 0 : (num + 2 * w1 - 1) / (2 * w1);
+    if (j > tpg) j = tpg;
+    int64_t t = (int64_t)l * tpg + j;
+    t = (t + per_x / 2) / per_x * per_x;
+    return (int)(t < T ? t : T);
+  };
+  lo = bound(x);
+  hi = bound(x + 1);
+  return sorted;
+}
+
 template <int MODE>
 __device__ __forceinline__ void tile_dims(const GemmArgs& a, const Tile& tl, int& K, int& M, int& N) {
   const int d = a.d, f = a.f;
@@ -745,6 +843,7 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
   __shared__ __align__(16) bf16_t epi[NW][32 * 32];
   __shared__ int pre[257];
   __shared__ int sbuf[256];
+  __shared__ int ord[wgrad ? 256 : 1];
 
   const int T = tile_count<MODE, BM, BN>(a, pre, sbuf);
   const int tid = threadIdx.x;
@@ -752,10 +851,21 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / C::WN, wn = wave % C::WN;
   const int d = a.d, f = a.f;
-  // this workgroup's tiles: lo + jx, lo + jx + per_x, ... < hi (grid is a multiple of 8)
+  // this workgroup's tiles: in round r, lo + r * per_x + jx (or + per_x - 1 - jx
+  // in the odd rounds of a snake deal), while < hi (grid is a multiple of 8)
   const int per_x = gridDim.x >> 3, x = blockIdx.x & 7, jx = blockIdx.x >> 3;
-  const int lo = x * (T >> 3) + min(x, T & 7);
-  const int hi = lo + (T >> 3) + (x < (T & 7) ? 1 : 0);
+  int lo = x * (T >> 3) + min(x, T & 7);
+  int hi = lo + (T >> 3) + (x < (T & 7) ? 1 : 0);
+  bool snake = false;
+  if (wgrad && a.offsets) {
+    snake = wgrad_schedule<MODE, BM, BN>(a, x, per_x, T, pre, ord, sbuf, lo, hi);
+    // the same in every lane (computed from LDS): keep the tile loops uniform
+    lo = __builtin_amdgcn_readfirstlane(lo);
+    hi = __builtin_amdgcn_readfirstlane(hi);
+    snake = __builtin_amdgcn_readfirstlane((int)snake) != 0;
+  }
+  const int* tord = snake ? ord : nullptr;
+  auto tile_of = [&](int r) { return lo + r * per_x + ((snake && (r & 1)) ? per_x - 1 - jx : jx); };
 
   const bf16_t* A = reinterpret_cast<const bf16_t*>(a.a);
   const bf16_t* Bact = reinterpret_cast<const bf16_t*>(a.b);
@@ -769,7 +879,7 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
   MNOperand<BN / 64, NW, BK> mb;
   int32x4_t b_up = make_rsrc(W0, 0);
   int64_t a_kstride = 0, b_kstride = 0;
-  int p_t = lo + jx, p_k = 0, p_nk = 0;
+  int p_r = 0, p_t = tile_of(0), p_k = 0, p_nk = 0;
   auto setup = [&](const Tile& tl) {
     int K, M, N;
     tile_dims<MODE>(a, tl, K, M, N);
@@ -843,7 +953,7 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
   // of experts without rows have none)
   auto p_seek = [&]() {
     while (p_t < hi) {
-      const Tile tl = tile_at<MODE, BM, BN>(a, p_t, pre);
+      const Tile tl = tile_at<MODE, BM, BN>(a, p_t, pre, tord);
       int K, M, N;
       tile_dims<MODE>(a, tl, K, M, N);
       p_nk = (K + BK - 1) / BK;
@@ -851,7 +961,7 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
         setup(tl);
         return;
       }
-      p_t += per_x;
+      p_t = tile_of(++p_r);
     }
   };
   const uint32_t lds0 = lds_addr(&lds[0][0]);
@@ -872,7 +982,7 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
     }
     if (++p_k == p_nk) {
       p_k = 0;
-      p_t += per_x;
+      p_t = tile_of(++p_r);
       p_seek();
     }
   };
@@ -912,8 +1022,8 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
     }
   };
 
-  for (int c_t = lo + jx; c_t < hi; c_t += per_x) {
-    const Tile tl = tile_at<MODE, BM, BN>(a, c_t, pre);
+  for (int c_r = 0, c_t = tile_of(0); c_t < hi; c_t = tile_of(++c_r)) {
+    const Tile tl = tile_at<MODE, BM, BN>(a, c_t, pre, tord);
     int K, M, N;
     tile_dims<MODE>(a, tl, K, M, N);
     const int g = tl.g;
@@ -1376,7 +1486,7 @@ int launch_bf16_persistent(const GemmArgs& a, hipStream_t s) {
   }
   if (nb <= 0) return MOE_OK;
   // workgroups per CU that fit in LDS (stages, epilogue slots, tables)
-  constexpr int kLdsPerBlock = C::LDS_BYTES + C::NW * 2048 + 2 * 1024 + 64;
+  constexpr int kLdsPerBlock = C::LDS_BYTES + C::NW * 2048 + (is_wgrad<MODE>() ? 3 : 2) * 1024 + 64;
   constexpr int kOcc = (160 * 1024) / kLdsPerBlock > 0 ? (160 * 1024) / kLdsPerBlock : 1;
   const int64_t grid = std::min<int64_t>((cu_count() * kOcc / 8) * 8, (nb + 7) / 8 * 8);
   return launch(kGemmKernelId[MODE], s, kGemmName[MODE],

@@ -122,3 +122,12 @@ def test_binding_arity_matches_header():
     for name, n in ar.items():
         fn = getattr(L.LIB, name)
         assert len(fn.argtypes) == n, (name, len(fn.argtypes), n)
+
+
+def test_one_hip_runtime_in_process():
+    """libmoe.so must bind to the HIP runtime torch already loaded: a second
+    copy of the runtime in the process finds no device at its first launch."""
+    import torch  # noqa: F401
+    maps = open("/proc/self/maps").read().splitlines()
+    hip = {ln.split()[-1] for ln in maps if "libamdhip64" in ln}
+    assert len(hip) == 1, hip

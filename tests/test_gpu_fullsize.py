@@ -18,7 +18,9 @@ a time are compared on samples:
   * the shared expert's weight gradients at sampled intermediate indices;
 and properties checked at every row: permuted rows are exact copies of their
 tokens, weights are non-negative and sum to the route scale, experts without
-rows get exactly zero gradients.
+rows get exactly zero gradients.  The weight gradients of every expert are
+also compared with plain torch float32 products of the routed rows, so that
+each output tile of the weight-gradient GEMMs is covered at full size.
 
 Bar: as for the small shapes (routing bit-exact outside the 1e-6 margin,
 normwise relative error <= 2e-2 for bf16)."""
@@ -134,6 +136,51 @@ def test_fullsize_qwen3_whole_oracle():
     assert not bad, bad
 
 
+def torch_expert_weight_grads(cfg, layer, p, x, dy, grads):
+    """Every expert's weight (and bias) gradients against plain torch float32
+    products, so that every output tile of the weight-gradient GEMMs is checked
+    at full size, whatever order the kernels deal the tiles in.  Built from the
+    rows' tokens and gating weights (checked against the oracle beforehand),
+    x, dy and the weights; none of the layer's saved activations is used.
+    Returns, per tensor, the largest per-expert normwise error and its expert
+    (one wrong 256 x 256 tile moves its expert's error well past the bar)."""
+    import torch
+    k, bias = cfg["k"], cfg["expert_bias"]
+    sv = layer.saved
+    offs = sv["expert_offsets"].long().cpu().tolist()
+    slot = sv["token_of"].long()
+    tok = slot // k
+    wrow = sv["topk_w"].reshape(-1).float()[slot]
+    names = ["dw_gate", "dw_up", "dw_down"] + (["db_gate", "db_up", "db_down"] if bias else [])
+    worst = {n: (0.0, -1) for n in names}
+    for e in range(cfg["E"]):
+        lo, hi = offs[e], offs[e + 1]
+        if hi == lo:
+            continue  # exact zeros, checked by check_properties
+        te = tok[lo:hi]
+        xe = x[te].float()
+        do = wrow[lo:hi, None] * dy[te].float()
+        g = xe @ p["w_gate"][e].float()
+        u = xe @ p["w_up"][e].float()
+        if bias:
+            g = g + p["b_gate"][e].float()
+            u = u + p["b_up"][e].float()
+        sg = torch.sigmoid(g)
+        h = g * sg * u
+        dh = do @ p["w_down"][e].float().t().contiguous()
+        dg = dh * u * sg * (1.0 + g * (1.0 - sg))
+        du = dh * g * sg
+        xt = xe.t().contiguous()
+        ref = {"dw_gate": xt @ dg, "dw_up": xt @ du, "dw_down": h.t().contiguous() @ do}
+        if bias:
+            ref.update(db_gate=dg.sum(0), db_up=du.sum(0), db_down=do.sum(0))
+        for n, r in ref.items():
+            err = (torch.linalg.vector_norm(grads[n][e].float() - r) / torch.linalg.vector_norm(r)).item()
+            if not err <= worst[n][0]:
+                worst[n] = (err, e)
+    return worst
+
+
 def _expert_rows(mp, e, k):
     toks = mp["token_of"][mp["offsets"][e]:mp["offsets"][e + 1]]
     return toks // k, toks % k
@@ -170,6 +217,9 @@ def test_fullsize_sampled(name):
         check_maps_valid(sv["topk_idx"], sv["expert_offsets"], sv["row_of"], sv["token_of"], E)
     counts = np.diff(sv["expert_offsets"])
     check_properties(cfg, layer, xd, grads, counts)
+    _say("torch float32 weight gradients of every expert")
+    for n, (err, e) in torch_expert_weight_grads(cfg, layer, p, xd, dev(inp["dy"], dt), grads).items():
+        errs["%s[every expert, worst e=%d]" % (n, e)] = err
     # experts whose rows are the same on both sides (tokens routed differently excluded)
     differ = np.nonzero(np.any(sv["topk_idx"] != rt["topk_idx"], axis=1))[0]
     touched = set(np.unique(np.concatenate([sv["topk_idx"][differ].ravel(),
