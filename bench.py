@@ -131,6 +131,75 @@ def cpu_baseline(cfg, seed, tokens, reps=1):
             "tokens_per_s": round(reps * tokens / wall, 1)}
 
 
+def memory_kernels(cfg, L, layer, params, x, dy, reps=20, cold_reps=10, scrub_mib=1024):
+    """Warm and cold times of the HBM-bound kernels, each driven through its
+    C-ABI entry point on the layer's own saved buffers and timed with the
+    library's events around that kernel's launch.  Warm: back-to-back calls
+    (operands partly left in the 256 MB MALL by the previous call).  Cold: a
+    read of a 1 GiB scrub buffer before every timed call (a read, so that no
+    dirty lines drain during the timed kernel).  The unpermute entry point sums
+    dx_perm rows only: the layer fuses the router's dx into the same kernel."""
+    import torch
+    T, d, k, E = cfg["T"], cfg["d"], cfg["k"], cfg["E"]
+    R = T * k
+    sv, sh = layer.saved, layer.shape
+    act = layer.act
+    d_o = torch.empty(R, d, dtype=act, device="cuda")
+    d_w = torch.empty(T, k, dtype=torch.float32, device="cuda")
+    counts = torch.empty(E, dtype=torch.int32, device="cuda")
+    y = torch.empty(T, d, dtype=act, device="cuda")
+    dx = torch.empty(T, d, dtype=act, device="cuda")
+    scrub = torch.ones(scrub_mib << 18, dtype=torch.float32, device="cuda")
+    ws = layer.ws_fwd
+    calls = {
+        "route_select": lambda: L.moe_route(sh, x, params["w_r"], params["router_bias"], sv["topk_idx"],
+                                            sv["topk_w"], sv["s_sel"], counts, ws),
+        "scatter": lambda: L.moe_permute(sh, x, sv["topk_idx"], sv["expert_offsets"], sv["row_of"],
+                                         sv["token_of"], sv["x_perm"], ws),
+        "combine_fwd": lambda: L.moe_combine_fwd(sh, sv["o"], sv["topk_w"], sv["row_of"], sv["o_sh"], y),
+        "combine_bwd": lambda: L.moe_combine_bwd(sh, dy, sv["o"], sv["topk_w"], sv["row_of"], d_o, d_w),
+        "unpermute": lambda: L.moe_unpermute_bwd(sh, sv["x_perm"], sv["row_of"], None, None, dx),
+    }
+    work = kernel_work(cfg)
+    out = {}
+    for name, call in calls.items():
+        kid = L.kernel_id(name)
+        res = {}
+        for mode in ("warm", "cold"):
+            for _ in range(2):
+                call()
+            torch.cuda.synchronize()
+            L.moe_timing_select(kid)
+            for _ in range(reps if mode == "warm" else cold_reps):
+                if mode == "cold":
+                    scrub.sum()
+                call()
+            torch.cuda.synchronize()
+            ms, n = L.moe_timing_read()
+            L.moe_timing_select(-1)
+            us = ms / max(n, 1) * 1e3
+            gbs = work[name][1] / (us / 1e6) / 1e9
+            res[mode] = {"avg_us": round(us, 2), "GB/s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+        out[name] = res
+    del scrub
+    return out
+
+
+def gpu_clocks():
+    """Current and available clocks from rocm-smi, as text (None when it is not there)."""
+    import shutil
+    import subprocess
+    exe = shutil.which("rocm-smi")
+    if not exe:
+        return None
+    try:
+        r = subprocess.run([exe, "--showclocks"], capture_output=True, text=True, timeout=30)
+    except (OSError, subprocess.SubprocessError):
+        return None
+    lines = [ln.strip() for ln in r.stdout.splitlines() if "clk" in ln.lower() and ":" in ln]
+    return lines or None
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -142,6 +211,9 @@ def main():
                     help="tokens of the workload the CPU oracle runs (0: all of them)")
     ap.add_argument("--cpu-reps", type=int, default=3, help="repetitions of the oracle's fwd+bwd")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--memory-kernels", action="store_true",
+                    help="instead of the step benchmark: warm and cold (after a 1 GiB read scrub) times "
+                         "of the HBM-bound kernels through their entry points, and the GPU clocks")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="before the timed steps, run a plain torch copy of this many MiB three times "
                          "(a kernel of known size for scaling rocprofv3 byte counters)")
@@ -186,6 +258,13 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.memory_kernels:
+        workload = "%s moe layer T=%d d=%d E=%d k=%d f=%d" % (cfg["name"], cfg["T"], cfg["d"], cfg["E"],
+                                                             cfg["k"], cfg["f"])
+        res = memory_kernels(cfg, L, layer, params, x, dy)
+        print(json.dumps({"memory_kernels": res, "peak_GB/s": PEAK_HBM_GBS, "dtype": dt,
+                          "config": {"workload": workload}, "clocks": gpu_clocks()}), flush=True)
+        return
     if args.copy_calibration_mb > 0:
         n = args.copy_calibration_mb << 20
         src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
