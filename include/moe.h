@@ -5,12 +5,11 @@
  * The layer is the one the PithTrain paper (arxiv 2605.31463) trains:
  * a router that picks the top-k experts of every token (section 3.2 and
  * appendix B.3 name the framework's top-k routing kernel), a scatter of the
- * tokens into expert-contiguous rows (section 3.2, "fused ... EP token
- * scatter"), SwiGLU experts with fused forward and backward activation
- * (section 3.2, "fused SwiGLU forward and backward kernels"), a
- * gating-weighted combine, and the backward split into data-gradient and
+ * tokens into expert-contiguous rows (section 3.2, its fused token scatter),
+ * SwiGLU experts with fused forward and backward activation (section 3.2),
+ * a gating-weighted combine, and the backward split into data-gradient and
  * weight-gradient passes so that the weight gradients can be delayed
- * (section 3.2, "wgrad delay").  Routing outputs obey the paper's
+ * (section 3.2, weight-gradient delay).  Routing outputs obey the paper's
  * routing-trace rules (appendix B.2.2): expert ids in [0, E), gating
  * weights non-negative and summing to one over the top-k (route_scale for
  * the DeepSeek-style router).
@@ -90,8 +89,11 @@ enum { MOE_BIAS_NONE = 0, MOE_BIAS_SELECT_ONLY = 1, MOE_BIAS_LOGIT = 2 };
 
 enum { MOE_F32 = 0, MOE_BF16 = 1 };
 
-/* passes of moe_grouped_gemm_bwd (bit mask) */
-enum { MOE_DGRAD = 1, MOE_WGRAD = 2 };
+/* passes of moe_grouped_gemm_bwd (bit mask).  MOE_ACCUMULATE (with
+ * MOE_WGRAD): add the weight and bias gradients to what the output buffers
+ * hold instead of overwriting them (bf16 gradients: the sum is taken in
+ * float32 and rounded once more to bf16). */
+enum { MOE_DGRAD = 1, MOE_WGRAD = 2, MOE_ACCUMULATE = 4 };
 
 typedef struct moe_shape {
   int64_t T, d, E, k, f;       /* tokens, hidden, routed experts, top-k, expert width */
@@ -198,8 +200,11 @@ int moe_grouped_gemm_fwd(const moe_shape* shape, const void* x_perm, const int32
  *             (g, u read from gu) -> dgu; then dx_perm = [dg|du] [W_gate|W_up]^T.
  *  MOE_WGRAD: dW_down = h^T d_o, dW_gate = x_perm^T dg, dW_up = x_perm^T du
  *             per expert, and with expert_bias the column sums db_down, db_gate,
- *             db_up.  Reads dgu, so it runs after a DGRAD pass.
- * Pointers of a pass that is not requested may be NULL. */
+ *             db_up.  Reads dgu, so it runs after a DGRAD pass.  With
+ *             MOE_ACCUMULATE the gradients are added to dw_* / db_*.
+ * Pointers of a pass that is not requested may be NULL.  Errors:
+ * MOE_ERR_INVALID_ARG for a passes value outside these bits or
+ * MOE_ACCUMULATE without MOE_WGRAD. */
 int moe_grouped_gemm_bwd(const moe_shape* shape, int32_t passes,
                          const void* x_perm, const int32_t* expert_offsets,
                          const void* gu, const void* h, const void* d_o,
@@ -266,6 +271,33 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* params, const void* 
 int moe_layer_bwd(const moe_shape* shape, const moe_params* params, const void* x,
                   const moe_saved* saved, const void* dy, void* dx, const moe_grads* grads,
                   void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The layer backward in two halves, for weight-gradient delay (section 3.2:
+ * the input gradient is produced first, so that the previous layer's
+ * backward can start; the weight gradients are computed later).
+ * moe_layer_bwd equals moe_layer_bwd_dgrad followed by moe_layer_bwd_wgrad
+ * with accumulate = 0, with bitwise equal results.
+ *
+ * moe_layer_bwd_dgrad: combine backward with the router's dl, expert dgrad
+ *   (fused SwiGLU backward), shared-expert dgrad, unpermute -> dx (with the
+ *   router and shared-expert paths).  Leaves d_o, dgu, dl (and the shared
+ *   expert's dgu) in ws, which the caller must keep unchanged until the
+ *   matching moe_layer_bwd_wgrad call.  Pointers of *saved read: topk_idx,
+ *   topk_w, s_sel (SIGMOID_GROUPED), expert_offsets, row_of, gu, o, gu_sh.
+ * moe_layer_bwd_wgrad: expert wgrads (+ biases), dW_r, shared-expert wgrads
+ *   into *grads, from what the dgrad half left in ws.  accumulate = 1 adds
+ *   every gradient to the buffer's current value (gradient accumulation over
+ *   micro-batches), 0 overwrites.  Pointers of *saved read: topk_idx,
+ *   expert_offsets, token_of, x_perm, h, h_sh.
+ * Both: ws of bwd_ws bytes (the same buffer for both halves); x and dy as for
+ * moe_layer_bwd.  Errors as for moe_layer_bwd; accumulate outside {0, 1}
+ * is MOE_ERR_INVALID_ARG. */
+int moe_layer_bwd_dgrad(const moe_shape* shape, const moe_params* params, const void* x,
+                        const moe_saved* saved, const void* dy, void* dx,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
+int moe_layer_bwd_wgrad(const moe_shape* shape, const moe_params* params, const void* x,
+                        const moe_saved* saved, const void* dy, const moe_grads* grads,
+                        int32_t accumulate, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Status code -> static string. */
 const char* moe_status_string(int status);

@@ -31,6 +31,7 @@ MOE_BF16 = 1
 DTYPES = {"f32": MOE_F32, "bf16": MOE_BF16}
 MOE_DGRAD = 1
 MOE_WGRAD = 2
+MOE_ACCUMULATE = 4
 
 
 class MoeError(RuntimeError):
@@ -100,6 +101,10 @@ def _load():
         "moe_layer_fwd": [S, ctypes.POINTER(moe_params), _VP, ctypes.POINTER(moe_saved), _VP, _VP, sz, _VP],
         "moe_layer_bwd": [S, ctypes.POINTER(moe_params), _VP, ctypes.POINTER(moe_saved), _VP, _VP,
                           ctypes.POINTER(moe_grads), _VP, sz, _VP],
+        "moe_layer_bwd_dgrad": [S, ctypes.POINTER(moe_params), _VP, ctypes.POINTER(moe_saved), _VP, _VP,
+                                _VP, sz, _VP],
+        "moe_layer_bwd_wgrad": [S, ctypes.POINTER(moe_params), _VP, ctypes.POINTER(moe_saved), _VP,
+                                ctypes.POINTER(moe_grads), i32, _VP, sz, _VP],
         "moe_kernel_count": [],
         "moe_kernel_name": [ctypes.c_int],
         "moe_timing_select": [ctypes.c_int],
@@ -266,6 +271,24 @@ def moe_layer_bwd(shape, params, x, saved, dy, dx, grads, ws, stream=None):
     return _check("moe_layer_bwd", LIB.moe_layer_bwd(ctypes.byref(shape), ctypes.byref(pr), P(x),
                                                      ctypes.byref(sv), P(dy), P(dx), ctypes.byref(gr),
                                                      wp, wb, _stream(stream)))
+
+
+def moe_layer_bwd_dgrad(shape, params, x, saved, dy, dx, ws, stream=None):
+    wp, wb = _ws(ws)
+    pr = _struct(moe_params, params)
+    sv = _struct(moe_saved, saved)
+    return _check("moe_layer_bwd_dgrad", LIB.moe_layer_bwd_dgrad(
+        ctypes.byref(shape), ctypes.byref(pr), P(x), ctypes.byref(sv), P(dy), P(dx), wp, wb, _stream(stream)))
+
+
+def moe_layer_bwd_wgrad(shape, params, x, saved, dy, grads, accumulate, ws, stream=None):
+    wp, wb = _ws(ws)
+    pr = _struct(moe_params, params)
+    sv = _struct(moe_saved, saved)
+    gr = _struct(moe_grads, grads)
+    return _check("moe_layer_bwd_wgrad", LIB.moe_layer_bwd_wgrad(
+        ctypes.byref(shape), ctypes.byref(pr), P(x), ctypes.byref(sv), P(dy), ctypes.byref(gr),
+        int(accumulate), wp, wb, _stream(stream)))
 
 
 def moe_kernel_count():

@@ -305,6 +305,7 @@ int do_gemm_bwd(const moe_shape& s, int passes, const void* x_perm, const int32_
     g.b = d_o;
     g.c0 = dw_down;
     g.db0 = db_down;
+    g.accumulate = (passes & MOE_ACCUMULATE) != 0;
     MOE_TRY(launch_gemm(g, st));
     g = gemm_base(s, G_WGRAD_GATEUP, offsets);
     g.a = x_perm;
@@ -313,6 +314,7 @@ int do_gemm_bwd(const moe_shape& s, int passes, const void* x_perm, const int32_
     g.c1 = dw_up;
     g.db0 = db_gate;
     g.db1 = db_up;
+    g.accumulate = (passes & MOE_ACCUMULATE) != 0;
     MOE_TRY(launch_gemm(g, st));
   }
   return MOE_OK;
@@ -334,9 +336,9 @@ int do_shared_fwd(const moe_shape& s, const void* x, const void* wsg, const void
   return launch_gemm(g, st);
 }
 
-int do_shared_bwd(const moe_shape& s, const void* x, const void* dy, const void* gu_sh, const void* h_sh,
-                  const void* wsg, const void* wsu, const void* wsd, void* dgu_sh, void* dx_sh, void* dwsg, void* dwsu,
-                  void* dwsd, hipStream_t st) {
+// Shared expert backward: the input-gradient half (dgu_sh, dx_sh) ...
+int do_shared_dgrad(const moe_shape& s, const void* dy, const void* gu_sh, const void* wsg, const void* wsu,
+                    const void* wsd, void* dgu_sh, void* dx_sh, hipStream_t st) {
   GemmArgs g = gemm_dense(s, G_DGRAD_DOWN);
   g.a = dy;
   g.w0 = wsd;
@@ -348,18 +350,32 @@ int do_shared_bwd(const moe_shape& s, const void* x, const void* dy, const void*
   g.w0 = wsg;
   g.w1 = wsu;
   g.c0 = dx_sh;
-  MOE_TRY(launch_gemm(g, st));
-  g = gemm_dense(s, G_WGRAD_DOWN);
+  return launch_gemm(g, st);
+}
+
+// ... and the weight-gradient half, from dgu_sh kept by the first.
+int do_shared_wgrad(const moe_shape& s, const void* x, const void* dy, const void* h_sh, const void* dgu_sh,
+                    void* dwsg, void* dwsu, void* dwsd, bool accumulate, hipStream_t st) {
+  GemmArgs g = gemm_dense(s, G_WGRAD_DOWN);
   g.a = h_sh;
   g.b = dy;
   g.c0 = dwsd;
+  g.accumulate = accumulate;
   MOE_TRY(launch_gemm(g, st));
   g = gemm_dense(s, G_WGRAD_GATEUP);
   g.a = x;
   g.b = dgu_sh;
   g.c0 = dwsg;
   g.c1 = dwsu;
+  g.accumulate = accumulate;
   return launch_gemm(g, st);
+}
+
+int do_shared_bwd(const moe_shape& s, const void* x, const void* dy, const void* gu_sh, const void* h_sh,
+                  const void* wsg, const void* wsu, const void* wsd, void* dgu_sh, void* dx_sh, void* dwsg, void* dwsu,
+                  void* dwsd, hipStream_t st) {
+  MOE_TRY(do_shared_dgrad(s, dy, gu_sh, wsg, wsu, wsd, dgu_sh, dx_sh, st));
+  return do_shared_wgrad(s, x, dy, h_sh, dgu_sh, dwsg, dwsu, dwsd, false, st);
 }
 
 RouteBwdArgs route_bwd_base(const moe_shape& s) {
@@ -382,6 +398,150 @@ using namespace moe;
 // ---------------------------------------------------------------------------
 // exported entry points
 // ---------------------------------------------------------------------------
+// Argument checks of the layer backward; `phase` bit 1: input-gradient half,
+// bit 2: weight-gradient half.
+namespace {
+int check_layer_bwd(const moe_shape& s, const moe_params* prm, const void* x, const moe_saved* sv, const void* dy,
+                    const void* dx, const moe_grads* gr, int phase) {
+  MOE_NEED(prm, "params");
+  MOE_NEED(sv, "saved");
+  MOE_NEED(prm->w_r, "params.w_r");
+  MOE_NEED(sv->expert_offsets, "saved.expert_offsets");
+  if (phase & 1) {
+    MOE_NEED(prm->w_gate, "params.w_gate");
+    MOE_NEED(prm->w_up, "params.w_up");
+    MOE_NEED(prm->w_down, "params.w_down");
+    if (s.n_shared) {
+      MOE_NEED(prm->ws_gate, "params.ws_gate");
+      MOE_NEED(prm->ws_up, "params.ws_up");
+      MOE_NEED(prm->ws_down, "params.ws_down");
+    }
+  }
+  if (phase & 2) {
+    MOE_NEED(gr, "grads");
+    MOE_NEED(gr->dw_r, "grads.dw_r");
+    MOE_NEED(gr->dw_gate, "grads.dw_gate");
+    MOE_NEED(gr->dw_up, "grads.dw_up");
+    MOE_NEED(gr->dw_down, "grads.dw_down");
+    if (s.expert_bias) {
+      MOE_NEED(gr->db_gate, "grads.db_gate");
+      MOE_NEED(gr->db_up, "grads.db_up");
+      MOE_NEED(gr->db_down, "grads.db_down");
+    }
+    if (s.n_shared) {
+      MOE_NEED(gr->dws_gate, "grads.dws_gate");
+      MOE_NEED(gr->dws_up, "grads.dws_up");
+      MOE_NEED(gr->dws_down, "grads.dws_down");
+    }
+  }
+  if (s.T > 0) {
+    MOE_NEED(x, "x");
+    MOE_NEED(dy, "dy");
+    MOE_NEED(sv->topk_idx, "saved.topk_idx");
+    if (phase & 1) {
+      MOE_NEED(dx, "dx");
+      MOE_NEED(sv->topk_w, "saved.topk_w");
+      MOE_NEED(sv->row_of, "saved.row_of");
+      MOE_NEED(sv->gu, "saved.gu");
+      MOE_NEED(sv->o, "saved.o");
+      if (s.router == MOE_ROUTER_SIGMOID_GROUPED) MOE_NEED(sv->s_sel, "saved.s_sel");
+      if (s.n_shared) MOE_NEED(sv->gu_sh, "saved.gu_sh");
+    }
+    if (phase & 2) {
+      MOE_NEED(sv->token_of, "saved.token_of");
+      MOE_NEED(sv->x_perm, "saved.x_perm");
+      MOE_NEED(sv->h, "saved.h");
+      if (s.n_shared) MOE_NEED(sv->h_sh, "saved.h_sh");
+    }
+  }
+  return MOE_OK;
+}
+
+// Input-gradient half: combine backward with the router's dl, expert dgrads,
+// shared-expert dgrad, and dx.  Leaves d_o, dgu, dl (and dgu_sh) in ws.
+int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const moe_saved* sv, const void* dy, void* dx,
+                    const Plan& p, void* ws, hipStream_t stream) {
+  void* d_o = wsp(ws, p.d_o);
+  void* dgu = wsp(ws, p.dgu);
+  void* dx_perm = wsp(ws, p.dx_perm);
+  float* dl = reinterpret_cast<float*>(wsp(ws, p.dl));
+  float* w_rt = reinterpret_cast<float*>(wsp(ws, p.w_rt));
+  // 1. combine backward with the router's dl fused in
+  CombineBwdArgs cb{};
+  cb.dy = dy;
+  cb.o = sv->o;
+  cb.topk_w = sv->topk_w;
+  cb.row_of = sv->row_of;
+  cb.d_o = d_o;
+  cb.d_topk_w = nullptr;
+  cb.T = s.T;
+  cb.d = (int)s.d;
+  cb.k = (int)s.k;
+  cb.bf16 = s.dtype == MOE_BF16;
+  cb.dl = dl;
+  cb.s_sel = sv->s_sel;
+  cb.router = s.router;
+  cb.route_scale = s.route_scale;
+  MOE_TRY(launch_combine_bwd(cb, stream));
+  // 2. expert dgrads
+  MOE_TRY(do_gemm_bwd(s, MOE_DGRAD, nullptr, sv->expert_offsets, sv->gu, nullptr, d_o, prm->w_gate, prm->w_up,
+                      prm->w_down, dgu, dx_perm, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, stream));
+  // 3. W_r^T for the router dx fused into the unpermute
+  MOE_TRY(launch_wr_transpose_act(prm->w_r, w_rt, (int)s.d, (int)s.E, s.dtype == MOE_BF16, stream));
+  // 4. shared expert input gradient
+  void* dx_sh = nullptr;
+  if (s.n_shared) {
+    dx_sh = wsp(ws, p.dx_sh);
+    MOE_TRY(do_shared_dgrad(s, dy, sv->gu_sh, prm->ws_gate, prm->ws_up, prm->ws_down, wsp(ws, p.dgu_sh), dx_sh,
+                            stream));
+  }
+  // 5. dx = unpermute(dx_perm) + router dx + shared dx
+  UnpermuteArgs u{};
+  u.dx_perm = dx_perm;
+  u.row_of = sv->row_of;
+  u.dx_router = nullptr;
+  u.dx_shared = dx_sh;
+  u.dl = dl;
+  u.topk_idx = sv->topk_idx;
+  u.w_rt = w_rt;
+  u.dx = dx;
+  u.T = s.T;
+  u.d = (int)s.d;
+  u.k = (int)s.k;
+  u.bf16 = s.dtype == MOE_BF16;
+  return launch_unpermute(u, stream);
+}
+
+// Weight-gradient half, from d_o, dgu, dl (and dgu_sh) left in ws by the
+// input-gradient half.
+int layer_bwd_wgrad(const moe_shape& s, const moe_params* prm, const void* x, const moe_saved* sv, const void* dy,
+                    const moe_grads* gr, bool accumulate, const Plan& p, void* ws, hipStream_t stream) {
+  void* d_o = wsp(ws, p.d_o);
+  void* dgu = wsp(ws, p.dgu);
+  float* dl = reinterpret_cast<float*>(wsp(ws, p.dl));
+  MOE_TRY(do_gemm_bwd(s, MOE_WGRAD | (accumulate ? MOE_ACCUMULATE : 0), sv->x_perm, sv->expert_offsets, nullptr,
+                      sv->h, d_o, nullptr, nullptr, nullptr, dgu, nullptr, gr->dw_gate, gr->dw_up, gr->dw_down,
+                      s.expert_bias ? gr->db_gate : nullptr, s.expert_bias ? gr->db_up : nullptr,
+                      s.expert_bias ? gr->db_down : nullptr, stream));
+  RouteBwdArgs rb = route_bwd_base(s);
+  rb.x = x;
+  rb.w_r = prm->w_r;
+  rb.topk_idx = sv->topk_idx;
+  rb.dl_in = dl;
+  rb.offsets = sv->expert_offsets;
+  rb.token_of = sv->token_of;
+  rb.dw_r = gr->dw_r;
+  rb.dx_router = nullptr;
+  rb.partial = reinterpret_cast<float*>(wsp(ws, p.partial));
+  rb.accumulate = accumulate;
+  MOE_TRY(launch_route_bwd(rb, stream));
+  if (s.n_shared)
+    MOE_TRY(do_shared_wgrad(s, x, dy, sv->h_sh, wsp(ws, p.dgu_sh), gr->dws_gate, gr->dws_up, gr->dws_down,
+                            accumulate, stream));
+  return MOE_OK;
+}
+}  // namespace
+
 extern "C" {
 
 const char* moe_status_string(int status) {
@@ -494,8 +654,10 @@ int moe_grouped_gemm_bwd(const moe_shape* shape, int32_t passes, const void* x_p
                          void* db_gate, void* db_up, void* db_down, hipStream_t stream) {
   MOE_TRY(check_shape(shape));
   const moe_shape& s = *shape;
-  if (passes <= 0 || passes > (MOE_DGRAD | MOE_WGRAD))
-    return moe_set_error(MOE_ERR_INVALID_ARG, "passes must be MOE_DGRAD, MOE_WGRAD or both");
+  if (passes <= 0 || passes > (MOE_DGRAD | MOE_WGRAD | MOE_ACCUMULATE) || !(passes & (MOE_DGRAD | MOE_WGRAD)))
+    return moe_set_error(MOE_ERR_INVALID_ARG, "passes must be MOE_DGRAD, MOE_WGRAD or both (with MOE_ACCUMULATE)");
+  if ((passes & MOE_ACCUMULATE) && !(passes & MOE_WGRAD))
+    return moe_set_error(MOE_ERR_INVALID_ARG, "MOE_ACCUMULATE needs MOE_WGRAD");
   MOE_NEED(expert_offsets, "expert_offsets");
   if (passes & MOE_DGRAD) {
     MOE_NEED(w_gate, "w_gate");
@@ -732,114 +894,33 @@ int moe_layer_bwd(const moe_shape* shape, const moe_params* prm, const void* x, 
                   void* dx, const moe_grads* gr, void* ws, size_t ws_bytes, hipStream_t stream) {
   MOE_TRY(check_shape(shape));
   const moe_shape& s = *shape;
-  MOE_NEED(prm, "params");
-  MOE_NEED(sv, "saved");
-  MOE_NEED(gr, "grads");
-  MOE_NEED(prm->w_r, "params.w_r");
-  MOE_NEED(prm->w_gate, "params.w_gate");
-  MOE_NEED(prm->w_up, "params.w_up");
-  MOE_NEED(prm->w_down, "params.w_down");
-  MOE_NEED(sv->expert_offsets, "saved.expert_offsets");
-  MOE_NEED(gr->dw_r, "grads.dw_r");
-  MOE_NEED(gr->dw_gate, "grads.dw_gate");
-  MOE_NEED(gr->dw_up, "grads.dw_up");
-  MOE_NEED(gr->dw_down, "grads.dw_down");
-  if (s.expert_bias) {
-    MOE_NEED(gr->db_gate, "grads.db_gate");
-    MOE_NEED(gr->db_up, "grads.db_up");
-    MOE_NEED(gr->db_down, "grads.db_down");
-  }
-  if (s.n_shared) {
-    MOE_NEED(prm->ws_gate, "params.ws_gate");
-    MOE_NEED(prm->ws_up, "params.ws_up");
-    MOE_NEED(prm->ws_down, "params.ws_down");
-    MOE_NEED(gr->dws_gate, "grads.dws_gate");
-    MOE_NEED(gr->dws_up, "grads.dws_up");
-    MOE_NEED(gr->dws_down, "grads.dws_down");
-  }
-  if (s.T > 0) {
-    MOE_NEED(x, "x");
-    MOE_NEED(dy, "dy");
-    MOE_NEED(dx, "dx");
-    MOE_NEED(sv->topk_idx, "saved.topk_idx");
-    MOE_NEED(sv->topk_w, "saved.topk_w");
-    MOE_NEED(sv->row_of, "saved.row_of");
-    MOE_NEED(sv->token_of, "saved.token_of");
-    MOE_NEED(sv->x_perm, "saved.x_perm");
-    MOE_NEED(sv->gu, "saved.gu");
-    MOE_NEED(sv->h, "saved.h");
-    MOE_NEED(sv->o, "saved.o");
-    if (s.router == MOE_ROUTER_SIGMOID_GROUPED) MOE_NEED(sv->s_sel, "saved.s_sel");
-    if (s.n_shared) {
-      MOE_NEED(sv->gu_sh, "saved.gu_sh");
-      MOE_NEED(sv->h_sh, "saved.h_sh");
-    }
-  }
+  MOE_TRY(check_layer_bwd(s, prm, x, sv, dy, dx, gr, 3));
   const Plan p = plan(s);
   MOE_TRY(check_ws(ws, ws_bytes, p.bwd_total));
-  void* d_o = wsp(ws, p.d_o);
-  void* dgu = wsp(ws, p.dgu);
-  void* dx_perm = wsp(ws, p.dx_perm);
-  float* dl = reinterpret_cast<float*>(wsp(ws, p.dl));
-  float* w_rt = reinterpret_cast<float*>(wsp(ws, p.w_rt));
+  MOE_TRY(layer_bwd_dgrad(s, prm, sv, dy, dx, p, ws, stream));
+  return layer_bwd_wgrad(s, prm, x, sv, dy, gr, false, p, ws, stream);
+}
 
-  // 1. combine backward with the router's dl fused in
-  CombineBwdArgs cb{};
-  cb.dy = dy;
-  cb.o = sv->o;
-  cb.topk_w = sv->topk_w;
-  cb.row_of = sv->row_of;
-  cb.d_o = d_o;
-  cb.d_topk_w = nullptr;
-  cb.T = s.T;
-  cb.d = (int)s.d;
-  cb.k = (int)s.k;
-  cb.bf16 = s.dtype == MOE_BF16;
-  cb.dl = dl;
-  cb.s_sel = sv->s_sel;
-  cb.router = s.router;
-  cb.route_scale = s.route_scale;
-  MOE_TRY(launch_combine_bwd(cb, stream));
-  // 2. expert dgrad then wgrad
-  MOE_TRY(do_gemm_bwd(s, MOE_DGRAD | MOE_WGRAD, sv->x_perm, sv->expert_offsets, sv->gu, sv->h, d_o, prm->w_gate,
-                      prm->w_up, prm->w_down, dgu, dx_perm, gr->dw_gate, gr->dw_up, gr->dw_down,
-                      s.expert_bias ? gr->db_gate : nullptr, s.expert_bias ? gr->db_up : nullptr,
-                      s.expert_bias ? gr->db_down : nullptr, stream));
-  // 3. router weight gradient (dx part fused into the unpermute)
-  RouteBwdArgs rb = route_bwd_base(s);
-  rb.x = x;
-  rb.w_r = prm->w_r;
-  rb.topk_idx = sv->topk_idx;
-  rb.dl_in = dl;
-  rb.offsets = sv->expert_offsets;
-  rb.token_of = sv->token_of;
-  rb.dw_r = gr->dw_r;
-  rb.dx_router = nullptr;
-  rb.partial = reinterpret_cast<float*>(wsp(ws, p.partial));
-  MOE_TRY(launch_route_bwd(rb, stream));
-  MOE_TRY(launch_wr_transpose_act(prm->w_r, w_rt, (int)s.d, (int)s.E, s.dtype == MOE_BF16, stream));
-  // 4. shared expert
-  void* dx_sh = nullptr;
-  if (s.n_shared) {
-    dx_sh = wsp(ws, p.dx_sh);
-    MOE_TRY(do_shared_bwd(s, x, dy, sv->gu_sh, sv->h_sh, prm->ws_gate, prm->ws_up, prm->ws_down, wsp(ws, p.dgu_sh),
-                          dx_sh, gr->dws_gate, gr->dws_up, gr->dws_down, stream));
-  }
-  // 5. dx = unpermute(dx_perm) + router dx + shared dx
-  UnpermuteArgs u{};
-  u.dx_perm = dx_perm;
-  u.row_of = sv->row_of;
-  u.dx_router = nullptr;
-  u.dx_shared = dx_sh;
-  u.dl = dl;
-  u.topk_idx = sv->topk_idx;
-  u.w_rt = w_rt;
-  u.dx = dx;
-  u.T = s.T;
-  u.d = (int)s.d;
-  u.k = (int)s.k;
-  u.bf16 = s.dtype == MOE_BF16;
-  return launch_unpermute(u, stream);
+int moe_layer_bwd_dgrad(const moe_shape* shape, const moe_params* prm, const void* x, const moe_saved* sv,
+                        const void* dy, void* dx, void* ws, size_t ws_bytes, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  MOE_TRY(check_layer_bwd(s, prm, x, sv, dy, dx, nullptr, 1));
+  const Plan p = plan(s);
+  MOE_TRY(check_ws(ws, ws_bytes, p.bwd_total));
+  return layer_bwd_dgrad(s, prm, sv, dy, dx, p, ws, stream);
+}
+
+int moe_layer_bwd_wgrad(const moe_shape* shape, const moe_params* prm, const void* x, const moe_saved* sv,
+                        const void* dy, const moe_grads* gr, int32_t accumulate, void* ws, size_t ws_bytes,
+                        hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  if (accumulate != 0 && accumulate != 1) return moe_set_error(MOE_ERR_INVALID_ARG, "accumulate must be 0 or 1");
+  MOE_TRY(check_layer_bwd(s, prm, x, sv, dy, nullptr, gr, 2));
+  const Plan p = plan(s);
+  MOE_TRY(check_ws(ws, ws_bytes, p.bwd_total));
+  return layer_bwd_wgrad(s, prm, x, sv, dy, gr, accumulate != 0, p, ws, stream);
 }
 
 }  // extern "C"

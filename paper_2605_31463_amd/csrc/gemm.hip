@@ -243,6 +243,19 @@ struct MNOperand {
   }
 };
 
+// Eight bf16 pairs (16 bytes each side) added in float32, rounded to nearest even.
+__device__ __forceinline__ uint4 add_bf16x8(uint4 a, uint4 b) {
+  const uint32_t x[4] = {a.x, a.y, a.z, a.w}, y[4] = {b.x, b.y, b.z, b.w};
+  uint32_t r[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float lo = __uint_as_float(x[q] << 16) + __uint_as_float(y[q] << 16);
+    const float hi = __uint_as_float(x[q] & 0xffff0000u) + __uint_as_float(y[q] & 0xffff0000u);
+    r[q] = (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+  }
+  return make_uint4(r[0], r[1], r[2], r[3]);
+}
+
 // 32x32x16 fragments.  K-contiguous: rows rb*32 + lane%32, k = ks*16 + 8*(lane/32) .. +7.
 template <int BK>
 __device__ __forceinline__ bf16x8 frag_k(const bf16_t* tile, int rb, int ks, int lane) {
@@ -1006,7 +1019,7 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
   // stage this lane's 4 x 4 values of a 32 x 32 block (row r32, columns
   // 8q + 4hh + t) and store the block's rows: dst(r) is row r's pointer at
   // the block's first column (null: row not stored), ncols valid columns
-  auto put_block = [&](const float* v, auto&& dst, int ncols) {
+  auto put_block = [&](const float* v, auto&& dst, int ncols, bool accum = false) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const uint32_t lo2 = (uint32_t)f2bf(v[4 * q]) | ((uint32_t)f2bf(v[4 * q + 1]) << 16);
@@ -1018,7 +1031,14 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
       const int idx = lane + 64 * rep, r = idx >> 2, ch = idx & 3;
       const uint4 val = *reinterpret_cast<const uint4*>(ep + r * 32 + ((ch ^ ((r >> 2) & 3)) << 3));
       bf16_t* p = dst(r);
-      if (p && 8 * ch < ncols) *reinterpret_cast<uint4*>(p + 8 * ch) = val;
+      if (p && 8 * ch < ncols) {
+        uint4 w = val;
+        if (accum) {  // (weight gradients) add to the stored values, in float32
+          const uint4 old = *reinterpret_cast<const uint4*>(p + 8 * ch);
+          w = add_bf16x8(old, val);
+        }
+        *reinterpret_cast<uint4*>(p + 8 * ch) = w;
+      }
     }
   };
 
@@ -1273,7 +1293,7 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
             if (MODE == G_WGRAD_DOWN) return c0 + ((int64_t)g * f + m) * d + n0;
             if (n0 < f) return c0 + ((int64_t)g * d + m) * f + n0;
             return c1 + ((int64_t)g * d + m) * f + (n0 - f);
-          }, ncols);
+          }, ncols, a.accumulate);
         }
       }
       if (colsum) {
@@ -1283,9 +1303,10 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
           v += __shfl_xor(v, 32, 64);
           const int col = tl.n0 + wn * C::TN + j * 32 + r32;
           if (lane < 32 && col < N) {
-            if (MODE == G_WGRAD_DOWN) reinterpret_cast<bf16_t*>(a.db0)[(int64_t)g * d + col] = f2bf(v);
-            else if (col < f) reinterpret_cast<bf16_t*>(a.db0)[(int64_t)g * f + col] = f2bf(v);
-            else reinterpret_cast<bf16_t*>(a.db1)[(int64_t)g * f + col - f] = f2bf(v);
+            bf16_t* p = MODE == G_WGRAD_DOWN ? reinterpret_cast<bf16_t*>(a.db0) + (int64_t)g * d + col
+                      : col < f ? reinterpret_cast<bf16_t*>(a.db0) + (int64_t)g * f + col
+                                : reinterpret_cast<bf16_t*>(a.db1) + (int64_t)g * f + col - f;
+            *p = f2bf(a.accumulate ? bf2f(*p) + v : v);
           }
         }
       }
@@ -1333,15 +1354,16 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     }
     float* c0 = reinterpret_cast<float*>(a.c0);
     float* c1 = reinterpret_cast<float*>(a.c1);
+    auto put = [&](float* p, float v) { *p = a.accumulate ? *p + v : v; };
     if (MODE == G_WGRAD_DOWN) {
-      c0[((int64_t)g * f + m) * d + n] = acc;
-      if (colsum) reinterpret_cast<float*>(a.db0)[(int64_t)g * d + n] = bs;
+      put(c0 + ((int64_t)g * f + m) * d + n, acc);
+      if (colsum) put(reinterpret_cast<float*>(a.db0) + (int64_t)g * d + n, bs);
     } else if (n < f) {
-      c0[((int64_t)g * d + m) * f + n] = acc;
-      if (colsum) reinterpret_cast<float*>(a.db0)[(int64_t)g * f + n] = bs;
+      put(c0 + ((int64_t)g * d + m) * f + n, acc);
+      if (colsum) put(reinterpret_cast<float*>(a.db0) + (int64_t)g * f + n, bs);
     } else {
-      c1[((int64_t)g * d + m) * f + n - f] = acc;
-      if (colsum) reinterpret_cast<float*>(a.db1)[(int64_t)g * f + n - f] = bs;
+      put(c1 + ((int64_t)g * d + m) * f + n - f, acc);
+      if (colsum) put(reinterpret_cast<float*>(a.db1) + (int64_t)g * f + n - f, bs);
     }
     return;
   }
@@ -1499,6 +1521,10 @@ int launch_bf16_persistent(const GemmArgs& a, hipStream_t s) {
 
 template <int MODE>
 int launch_mode(const GemmArgs& a, hipStream_t s) {
+  if (a.accumulate && !is_wgrad<MODE>())
+    return moe_set_error(MOE_ERR_INVALID_ARG, "gemm: accumulate applies to the weight-gradient passes only");
+  if (a.bf16 && a.accumulate && !MOE_GEMM_PERSISTENT)
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "gemm: accumulate needs the persistent bf16 kernels");
   if (a.bf16) {
     const int G = a.offsets ? a.ngroups : 1;
     const int64_t rows_per_group = a.offsets ? a.max_rows / G : a.dense_rows;

@@ -96,6 +96,7 @@ struct RouteBwdArgs {
   float* dl;               // [T][k]
   float* partial;          // [route_dwr_tasks][d]
   float* w_rt;             // [E][d]
+  bool accumulate;         // dw_r += the gradient (else dw_r = the gradient)
 };
 constexpr int DWR_ROWS = 256;  // rows per partial-sum task of dW_r
 inline int64_t route_dwr_tasks(int64_t R, int64_t E) { return R / DWR_ROWS + E; }
@@ -150,6 +151,7 @@ struct GemmArgs {
   void* c1;                // h  |   |     |         |         | dW_up
   void* db0;               // db_down | db_gate
   void* db1;               // db_up
+  bool accumulate;         // wgrad passes: add into c0/c1/db0/db1 instead of overwriting
 };
 int launch_gemm(const GemmArgs& a, hipStream_t s);
 

@@ -105,7 +105,8 @@ __global__ __launch_bounds__(256) void dwr_reduce_kernel(RouteBwdArgs a) {
   if (i >= a.d) return;
   float acc = 0.f;
   for (int q = pre[e]; q < pre[e + 1]; ++q) acc += a.partial[(int64_t)q * a.d + i];
-  a.dw_r[(int64_t)i * a.E + e] = acc;
+  float* o = a.dw_r + (int64_t)i * a.E + e;
+  *o = a.accumulate ? *o + acc : acc;
 }
 
 template <class OT>

@@ -53,3 +53,14 @@ class MoELayer:
     def backward(self, params, x, dy, grads, stream=None):
         L.moe_layer_bwd(self.shape, params, x, self.saved, dy, self.dx, grads, self.ws_bwd, stream)
         return self.dx
+
+    def backward_dgrad(self, params, x, dy, stream=None):
+        """Input gradient only; the weight gradients follow with backward_wgrad
+        (the backward workspace carries what it needs in between)."""
+        L.moe_layer_bwd_dgrad(self.shape, params, x, self.saved, dy, self.dx, self.ws_bwd, stream)
+        return self.dx
+
+    def backward_wgrad(self, params, x, dy, grads, accumulate=False, stream=None):
+        """Weight gradients of the last backward_dgrad; accumulate adds them to grads."""
+        L.moe_layer_bwd_wgrad(self.shape, params, x, self.saved, dy, grads, accumulate, self.ws_bwd, stream)
+        return grads

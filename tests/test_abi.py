@@ -131,3 +131,19 @@ def test_one_hip_runtime_in_process():
     maps = open("/proc/self/maps").read().splitlines()
     hip = {ln.split()[-1] for ln in maps if "libamdhip64" in ln}
     assert len(hip) == 1, hip
+
+
+def test_accumulate_arguments_rejected_on_the_host():
+    """accumulate outside {0, 1}, and MOE_ACCUMULATE without the weight-gradient
+    pass, fail validation before any HIP call."""
+    s = L.make_shape(T=16, d=128, E=8, k=2, f=128)
+    pr, sv, gr = L.moe_params(), L.moe_saved(), L.moe_grads()
+    st = L.LIB.moe_layer_bwd_wgrad(ctypes.byref(s), ctypes.byref(pr), None, ctypes.byref(sv), None,
+                                   ctypes.byref(gr), 2, None, 0, None)
+    assert st == L.MOE_ERR_INVALID_ARG and "accumulate" in L.last_error()
+    st = L.LIB.moe_grouped_gemm_bwd(ctypes.byref(s), L.MOE_DGRAD | L.MOE_ACCUMULATE, *([None] * 16), None)
+    assert st == L.MOE_ERR_INVALID_ARG and "MOE_ACCUMULATE" in L.last_error()
+    st = L.LIB.moe_grouped_gemm_bwd(ctypes.byref(s), 8, *([None] * 16), None)
+    assert st == L.MOE_ERR_INVALID_ARG
+    st = L.LIB.moe_layer_bwd_dgrad(ctypes.byref(s), None, None, None, None, None, None, 0, None)
+    assert st == L.MOE_ERR_INVALID_ARG
