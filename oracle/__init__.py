@@ -21,4 +21,7 @@ from .moe_oracle import (  # noqa: F401
     unpermute,
     token_forward_backward,
     expert_weight_grads_at,
+    router_probs,
+    aux_loss,
+    aux_loss_backward,
 )

@@ -311,13 +311,15 @@ def unpermute(dx_perm, row_of):
 # Whole layer
 # ----------------------------------------------------------------------------
 
-def layer_forward(spec, x, w_r, beta, expert_fn, shared=None):
+def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_f=None):
     """Forward of one MoE layer.
 
     x [T][d] float64; w_r [d][E]; beta [E] or None;
     expert_fn(e) -> (wg, wu, wd, bg, bu, bd) float64 (biases may be None);
-    shared = (wsg, wsu, wsd) or None for an always-on expert of weight 1.
-    Returns routing, maps and the per-row activations (permuted order) and y.
+    shared = (wsg, wsu, wsd) or None for an always-on expert of weight 1;
+    aux_coef > 0 adds the load-balancing loss (aux_f: the batch's fractions).
+    Returns routing, maps and the per-row activations (permuted order) and y
+    (and the auxiliary loss, its probabilities and fractions).
     """
     x = np.asarray(x, np.float64)
     T, d = x.shape
@@ -344,8 +346,13 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None):
         g, u, h, osh = expert_forward(x, *shared)
         sh = dict(g=g, u=u, h=h, o=osh)
     y = combine(o, rt["topk_w"], mp["row_of"], None if sh is None else sh["o"])
+    aux = None
+    if aux_coef:
+        probs = router_probs(spec, l, beta)
+        aux = aux_loss(spec, probs, mp["counts"], aux_coef, aux_f)
+        aux.update(probs=probs, coef=aux_coef)
     return dict(logits=l, route=rt, maps=mp, x_perm=x_perm, o=o, g=gs, u=us,
-                h=hs, y=y, shared=sh, f=fwidth)
+                h=hs, y=y, shared=sh, f=fwidth, aux=aux)
 
 
 def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bias=False):
@@ -387,6 +394,9 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
     dl = router_backward(spec, rt, omega)
     dl_dense = np.zeros((T, E))
     np.put_along_axis(dl_dense, rt["topk_idx"], dl, axis=1)
+    aux = fwd.get("aux")
+    if aux is not None:
+        dl_dense = dl_dense + aux_loss_backward(aux["probs"], aux["f"], aux["coef"])
     dw_r = x.T @ dl_dense
     dx_router = dl_dense @ np.asarray(w_r, np.float64).T
     dx += dx_router
@@ -401,6 +411,53 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
         sh = gsh
     return dict(dx=dx, dw_r=dw_r, experts=grads, shared=sh, omega=omega, dl=dl,
                 dx_perm=dx_perm, do=do, dx_router=dx_router)
+
+
+# ----------------------------------------------------------------------------
+# Load-balancing auxiliary loss, global level
+# ----------------------------------------------------------------------------
+# The paper pretrains Qwen3-30B-A3B with a global-level load-balancing loss of
+# coefficient 1e-3 (appendix A.1, training-configuration figure) and defers its
+# definition to the work it cites.  Written out here as that standard loss:
+# over the batch, L = coef * E * sum_e f_e P_e, with P_e the mean over tokens of
+# the router's probability of expert e (softmax over all E logits) and f_e the
+# fraction of the T*k routed slots that chose e; "global level" means f_e is
+# taken over the whole batch, so a caller splitting a batch can pass the
+# batch's f.  f is a count and carries no gradient.  Softmax routers only.
+
+def router_probs(spec, logits, beta=None):
+    """p [T][E]: softmax over all E experts of the logits (plus beta when the
+    bias is added to the logits)."""
+    if spec.router == "sigmoid_grouped":
+        raise ValueError("the auxiliary loss is defined for the softmax routers")
+    v = np.asarray(logits, np.float64)
+    if beta is not None and spec.bias_mode == "logit":
+        v = v + np.asarray(beta, np.float64)[None, :]
+    z = np.exp(v - v.max(axis=1, keepdims=True))
+    return z / z.sum(axis=1, keepdims=True)
+
+
+def aux_loss(spec, p, counts, coef, f=None):
+    """Global-level load-balancing loss.  p [T][E] from router_probs; counts
+    [E] routed slots per expert; f [E] the batch's fractions if given, else
+    counts / (T*k).  Returns dict(loss, P, f)."""
+    p = np.asarray(p, np.float64)
+    T, E = p.shape
+    if f is None:
+        f = np.asarray(counts, np.float64) / float(T * spec.k)
+    f = np.asarray(f, np.float64)
+    P = p.mean(axis=0)
+    return dict(loss=coef * E * float(np.dot(f, P)), P=P, f=f)
+
+
+def aux_loss_backward(p, f, coef):
+    """dL/dlogit [T][E] of aux_loss with f held fixed: through P_e = mean_t
+    p[t][e] and the softmax Jacobian dp_e/dl_j = p_e (delta_ej - p_j),
+    dl[t][j] = coef * E / T * p[t][j] * (f_j - sum_e f_e p[t][e])."""
+    p = np.asarray(p, np.float64)
+    T, E = p.shape
+    F = p @ np.asarray(f, np.float64)
+    return coef * E / T * p * (np.asarray(f, np.float64)[None, :] - F[:, None])
 
 
 # ----------------------------------------------------------------------------

@@ -61,7 +61,7 @@ def shared_of(inp, cfg):
     return (to_f64(inp["ws_gate"], dt), to_f64(inp["ws_up"], dt), to_f64(inp["ws_down"], dt))
 
 
-def oracle_run(cfg, inp):
+def oracle_run(cfg, inp, aux_coef=0.0, aux_f=None):
     spec = spec_from_config(cfg)
     dt = cfg["dtype"]
     x = to_f64(inp["x"], dt)
@@ -69,7 +69,7 @@ def oracle_run(cfg, inp):
     beta = None if inp["router_bias"] is None else inp["router_bias"].astype(np.float64)
     efn = expert_fn(inp, cfg)
     shared = shared_of(inp, cfg)
-    fwd = layer_forward(spec, x, w_r, beta, efn, shared)
+    fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=aux_coef, aux_f=aux_f)
     bwd = layer_backward(spec, x, w_r, beta, efn, fwd, to_f64(inp["dy"], dt), shared,
                          with_bias=cfg["expert_bias"])
     return fwd, bwd

@@ -13,9 +13,9 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import (RouterSpec, expert_backward, expert_forward, expert_weight_grads_at,
-                    layer_backward, layer_forward, route, router_logits, sort_maps,
-                    token_forward_backward)
+from oracle import (RouterSpec, aux_loss, aux_loss_backward, expert_backward, expert_forward,
+                    expert_weight_grads_at, layer_backward, layer_forward, route, router_logits,
+                    router_probs, sort_maps, token_forward_backward)
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -471,3 +471,115 @@ def test_weight_grad_slices_equal_full_expert_backward(bias):
         np.testing.assert_allclose(part["db_gate"], full["db_gate"][cols], rtol=1e-13, atol=1e-13)
         np.testing.assert_allclose(part["db_up"], full["db_up"][cols], rtol=1e-13, atol=1e-13)
         np.testing.assert_allclose(part["db_down"], full["db_down"], rtol=1e-13, atol=1e-13)
+
+
+# ---------------------------------------------------------------------------
+# Global-level load-balancing loss
+# ---------------------------------------------------------------------------
+
+AUX_SPECS = ["softmax_topk", "topk_softmax", "softmax_logit_bias"]
+
+
+def run_aux(spec, c, coef, f=None):
+    fwd = layer_forward(spec, c["x"], c["w_r"], c["beta"], efn(c), c["shared"], aux_coef=coef, aux_f=f)
+    bwd = layer_backward(spec, c["x"], c["w_r"], c["beta"], efn(c), fwd, c["dy"], c["shared"],
+                         with_bias=c["bg"] is not None)
+    return fwd, bwd
+
+
+@pytest.mark.parametrize("name", AUX_SPECS)
+def test_aux_loss_matches_torch_autograd(name):
+    """Loss value and its x / W_r gradients against torch autograd of an
+    independent formulation (softmax over all experts, the load fractions
+    counted from torch.topk of the selection logits and held fixed)."""
+    spec = SPECS[name]
+    c = make_case(spec, seed=11)
+    coef = 0.37
+    fwd, bwd = run_aux(spec, c, coef)
+    _, bwd0 = run(spec, c)
+    x = torch.tensor(c["x"], dtype=torch.float64, requires_grad=True)
+    w = torch.tensor(c["w_r"], dtype=torch.float64, requires_grad=True)
+    v = x @ w
+    if c["beta"] is not None and spec.bias_mode == "logit":
+        v = v + torch.tensor(c["beta"])
+    T, E, k = v.shape[0], spec.E, spec.k
+    sel = torch.topk(v.detach(), k, dim=1).indices
+    cnt = torch.zeros(E, dtype=torch.float64).index_add_(0, sel.reshape(-1), torch.ones(T * k, dtype=torch.float64))
+    loss = coef * E * (cnt / (T * k) * torch.softmax(v, dim=1).mean(0)).sum()
+    loss.backward()
+    assert abs(fwd["aux"]["loss"] - loss.item()) <= 1e-13 * abs(loss.item())
+    assert rel(bwd["dw_r"] - bwd0["dw_r"], w.grad.numpy()) < 1e-11
+    assert rel(bwd["dx"] - bwd0["dx"], x.grad.numpy()) < 1e-11
+
+
+@pytest.mark.parametrize("name", AUX_SPECS)
+def test_aux_loss_gradients_match_finite_differences(name):
+    """d/dx and d/dW_r of sum <dy, y> + L_aux by central differences (routing,
+    and so the load fractions, unchanged by the step)."""
+    spec = SPECS[name]
+    c = make_case(spec, T=12, d=8, f=6, seed=12)
+    coef = 0.5
+    fwd, bwd = run_aux(spec, c, coef)
+
+    def total(cc):
+        fw = layer_forward(spec, cc["x"], cc["w_r"], cc["beta"], efn(cc), None, aux_coef=coef)
+        return float((cc["dy"] * fw["y"]).sum()) + fw["aux"]["loss"], fw["route"]["topk_idx"]
+
+    rng = np.random.default_rng(6)
+    h = 1e-6
+    for key, gr in (("x", bwd["dx"]), ("w_r", bwd["dw_r"])):
+        for _ in range(3):
+            v = rng.standard_normal(c[key].shape)
+            v /= np.linalg.norm(v)
+            lp, ip = total(dict(c, **{key: c[key] + h * v}))
+            lm, im = total(dict(c, **{key: c[key] - h * v}))
+            if not (np.array_equal(ip, fwd["route"]["topk_idx"]) and np.array_equal(im, fwd["route"]["topk_idx"])):
+                continue
+            fd = (lp - lm) / (2 * h)
+            an = float((gr * v).sum())
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (key, fd, an)
+
+
+def test_aux_loss_uniform_router_closed_form():
+    """Equal logits: every probability is 1/E, so L = coef * sum_e f_e = coef for
+    any routing, and dL/dl[t][j] = coef / T * (f_j - 1/E)."""
+    spec = RouterSpec("softmax_topk", E=8, k=2)
+    T = 10
+    p = router_probs(spec, np.zeros((T, 8)))
+    counts = np.array([7, 0, 3, 2, 4, 1, 3, 0])
+    coef = 1e-3
+    out = aux_loss(spec, p, counts, coef)
+    assert out["loss"] == pytest.approx(coef, rel=1e-15)
+    f = counts / 20.0
+    dl = aux_loss_backward(p, f, coef)
+    np.testing.assert_allclose(dl, np.broadcast_to(coef / T * (f - 1 / 8), (T, 8)), rtol=1e-14, atol=1e-20)
+
+
+def test_aux_loss_concentrated_router_is_maximal():
+    """All probability and all load on one expert: L = coef * E, its largest value."""
+    spec = RouterSpec("softmax_topk", E=4, k=1)
+    p = router_probs(spec, np.tile(np.array([[60.0, 0.0, 0.0, 0.0]]), (5, 1)))
+    out = aux_loss(spec, p, np.array([5, 0, 0, 0]), 0.25)
+    assert out["loss"] == pytest.approx(0.25 * 4, rel=1e-12)
+
+
+@pytest.mark.parametrize("name", AUX_SPECS)
+def test_aux_gradient_rows_sum_to_zero(name):
+    """Adding a constant to a token's logits leaves its softmax unchanged, so each
+    row of dL_aux/dl sums to zero."""
+    spec = SPECS[name]
+    c = make_case(spec, seed=13)
+    fwd, _ = run_aux(spec, c, 0.8)
+    dl = aux_loss_backward(fwd["aux"]["probs"], fwd["aux"]["f"], 0.8)
+    assert np.abs(dl.sum(axis=1)).max() <= 1e-15 * np.abs(dl).max() * spec.E
+
+
+def test_aux_loss_batch_fractions_are_used():
+    """Given the batch's fractions, the loss and its gradient use them instead of
+    this call's counts."""
+    spec = SPECS["softmax_topk"]
+    c = make_case(spec, seed=14)
+    f = np.full(spec.E, 1.0 / spec.E)
+    fwd, _ = run_aux(spec, c, 0.3, f=f)
+    assert fwd["aux"]["loss"] == pytest.approx(0.3, rel=1e-12)  # P sums to one
+    assert np.array_equal(fwd["aux"]["f"], f)
