@@ -211,6 +211,9 @@ def main():
                     help="tokens of the workload the CPU oracle runs (0: all of them)")
     ap.add_argument("--cpu-reps", type=int, default=3, help="repetitions of the oracle's fwd+bwd")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--aux-coef", type=float, default=0.0,
+                    help="add the global-level load-balancing loss of this coefficient (the paper "
+                         "pretrains with 1e-3); 0: without it")
     ap.add_argument("--memory-kernels", action="store_true",
                     help="instead of the step benchmark: warm and cold (after a 1 GiB read scrub) times "
                          "of the HBM-bound kernels through their entry points, and the GPU clocks")
@@ -230,6 +233,8 @@ def main():
     from paper_2605_31463_amd.layer import MoELayer
 
     cfg = config(args.workload)
+    if args.aux_coef:
+        cfg = dict(cfg, aux_coef=args.aux_coef)
     dt = cfg["dtype"]
     torch.cuda.set_device(0)
     inp = layer_inputs(cfg, seed=args.seed)
@@ -344,7 +349,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dt,
         "data": "synthetic (seeded; shapes and distributions of the workload)",
         "config": {"workload": workload, "T": cfg["T"], "d": cfg["d"], "E": cfg["E"], "k": cfg["k"],
-                   "f": cfg["f"], "router": cfg["router"]},
+                   "f": cfg["f"], "router": cfg["router"], "aux_coef": cfg.get("aux_coef", 0.0)},
         "tokens_per_s": round(cfg["T"] / (ms_per_step / 1e3), 1),
         "phases_median_of_last_10": {"fwd_ms": round(med(f_ms), 4), "bwd_ms": round(med(b_ms), 4),
                                      "step_ms": round(med(s_ms), 4),

@@ -107,6 +107,9 @@ typedef struct moe_shape {
   int32_t bias_mode;           /* MOE_BIAS_* */
   int32_t expert_bias;         /* 1: experts carry b_gate, b_up, b_down */
   int32_t dtype;               /* MOE_F32 or MOE_BF16 activation / expert dtype */
+  float aux_coef;              /* > 0: the layer entry points add the global-level
+                                  load-balancing loss of this coefficient (softmax
+                                  routers); 0: none */
 } moe_shape;
 
 /* Parameters of the layer (device pointers; unused ones may be NULL). */
@@ -122,6 +125,9 @@ typedef struct moe_params {
   const void* ws_gate;         /* [d][f_shared], n_shared */
   const void* ws_up;           /* [d][f_shared], n_shared */
   const void* ws_down;         /* [f_shared][d], n_shared */
+  const float* aux_f;          /* [E] expert load fractions of the whole batch for the
+                                  auxiliary loss (may be NULL: this call's routed-slot
+                                  fractions counts / (T k)) */
 } moe_params;
 
 /* Tensors the forward writes and the backward reads (caller-allocated). */
@@ -139,6 +145,8 @@ typedef struct moe_saved {
   void* gu_sh;                 /* [T][2 f_shared], n_shared */
   void* h_sh;                  /* [T][f_shared], n_shared */
   void* o_sh;                  /* [T][d], n_shared */
+  float* router_probs;         /* [T][E] softmax over all experts, aux_coef > 0 */
+  float* aux_loss;             /* [1] the auxiliary loss value, aux_coef > 0 */
 } moe_saved;
 
 /* Gradients of the parameters (overwritten). */

@@ -49,6 +49,7 @@ class moe_shape(ctypes.Structure):
         ("router", ctypes.c_int32), ("renorm", ctypes.c_int32),
         ("route_scale", ctypes.c_float), ("bias_mode", ctypes.c_int32),
         ("expert_bias", ctypes.c_int32), ("dtype", ctypes.c_int32),
+        ("aux_coef", ctypes.c_float),
     ]
 
 
@@ -57,12 +58,13 @@ _VP = ctypes.c_void_p
 
 class moe_params(ctypes.Structure):
     _fields_ = [(n, _VP) for n in ("w_r", "router_bias", "w_gate", "w_up", "w_down", "b_gate",
-                                   "b_up", "b_down", "ws_gate", "ws_up", "ws_down")]
+                                   "b_up", "b_down", "ws_gate", "ws_up", "ws_down", "aux_f")]
 
 
 class moe_saved(ctypes.Structure):
     _fields_ = [(n, _VP) for n in ("topk_idx", "topk_w", "s_sel", "expert_offsets", "row_of",
-                                   "token_of", "x_perm", "gu", "h", "o", "gu_sh", "h_sh", "o_sh")]
+                                   "token_of", "x_perm", "gu", "h", "o", "gu_sh", "h_sh", "o_sh",
+                                   "router_probs", "aux_loss")]
 
 
 class moe_grads(ctypes.Structure):
@@ -153,11 +155,11 @@ def _stream(stream):
 
 def make_shape(T, d, E, k, f, router="softmax_topk", n_groups=1, topk_groups=1, n_shared=0,
                f_shared=0, route_scale=1.0, bias_mode="none", expert_bias=False, dtype="bf16",
-               renorm=1):
+               renorm=1, aux_coef=0.0):
     return moe_shape(T=T, d=d, E=E, k=k, f=f, n_groups=n_groups, topk_groups=topk_groups,
                      n_shared=n_shared, f_shared=f_shared, router=ROUTERS[router], renorm=renorm,
                      route_scale=route_scale, bias_mode=BIAS_MODES[bias_mode],
-                     expert_bias=int(bool(expert_bias)), dtype=DTYPES[dtype])
+                     expert_bias=int(bool(expert_bias)), dtype=DTYPES[dtype], aux_coef=aux_coef)
 
 
 def shape_from_config(cfg, T=None):
@@ -166,7 +168,7 @@ def shape_from_config(cfg, T=None):
                       topk_groups=cfg["topk_groups"], n_shared=cfg["n_shared"],
                       f_shared=cfg["f_shared"], route_scale=cfg["route_scale"],
                       bias_mode=cfg["bias_mode"], expert_bias=cfg["expert_bias"],
-                      dtype=cfg["dtype"])
+                      dtype=cfg["dtype"], aux_coef=cfg.get("aux_coef", 0.0))
 
 
 # ---------------------------------------------------------------------------

@@ -8,6 +8,8 @@
 
 #include <vector>
 
+#include <cstddef>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -75,7 +77,8 @@ const char* kernel_name(int id) {
       "route", "count_zero", "hist", "scan", "scatter", "gemm_gateup_fwd", "gemm_down_fwd",
       "combine_fwd", "combine_bwd", "route_dl", "route_dwr_partial", "route_dwr_reduce",
       "wr_transpose", "route_dx", "gemm_down_dgrad", "gemm_gateup_dgrad", "gemm_down_wgrad",
-      "gemm_gateup_wgrad", "unpermute", "rank", "wr_split", "route_select"};
+      "gemm_gateup_wgrad", "unpermute", "rank", "wr_split", "route_select", "aux_stats", "aux_grad",
+      "aux_dwr"};
   if (id < 0 || id >= K_NUM_KERNELS) return nullptr;
   return names[id];
 }
@@ -116,6 +119,10 @@ int check_shape(const moe_shape* sh) {
   if (s.n_shared && s.f_shared <= 0)
     return moe_set_error(MOE_ERR_INVALID_ARG, "f_shared must be positive with a shared expert");
   if (s.renorm != 1) return moe_set_error(MOE_ERR_UNSUPPORTED, "only renormalised top-k weights (renorm=1)");
+  if (!(s.aux_coef >= 0.f) || !isfinite(s.aux_coef))
+    return moe_set_error(MOE_ERR_INVALID_ARG, "aux_coef must be finite and non-negative");
+  if (s.aux_coef > 0.f && s.router == MOE_ROUTER_SIGMOID_GROUPED)
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "the auxiliary loss is defined for the softmax routers");
   if (s.E > 256) return moe_set_error(MOE_ERR_UNSUPPORTED, "E=%lld above 256", (long long)s.E);
   if (s.k > 16) return moe_set_error(MOE_ERR_UNSUPPORTED, "k=%lld above 16", (long long)s.k);
   if (s.d % 64 || s.f % 64 || (s.n_shared && s.f_shared % 64))
@@ -137,13 +144,22 @@ inline size_t act_bytes(const moe_shape& s) { return s.dtype == MOE_BF16 ? 2 : 4
 
 struct Plan {
   // forward
-  size_t hist, wsplit, lg;
+  size_t hist, wsplit, lg, aux_part;
   size_t fwd_total;
   // backward
   size_t d_o, dgu, dx_perm, dl, partial, w_rt, dgu_sh, dx_sh;
+  size_t aux_dl, aux_dx, aux_off, aux_wpart;
   size_t bwd_total;
   size_t saved_total;
 };
+
+// Auxiliary loss: experts padded to a multiple of 64 (the K of the router-dx
+// product), tokens in at most 256 chunks of a multiple of 256 rows (the groups
+// of the dW_r product).
+inline bool has_aux(const moe_shape& s) { return s.aux_coef > 0.f; }
+inline int aux_epad(const moe_shape& s) { return (int)((s.E + 63) / 64 * 64); }
+inline int64_t aux_chunk(const moe_shape& s) { return 256 * ((s.T + 256 * 256 - 1) / (256 * 256)); }
+inline int aux_groups(const moe_shape& s) { return s.T > 0 ? (int)((s.T + aux_chunk(s) - 1) / aux_chunk(s)) : 0; }
 
 Plan plan(const moe_shape& s) {
   Plan p{};
@@ -156,6 +172,8 @@ Plan plan(const moe_shape& s) {
   off += s.dtype == MOE_BF16 ? align_up((size_t)3 * s.E * s.d * 2) : 0;
   p.lg = off;
   off += s.dtype == MOE_BF16 ? align_up((size_t)s.T * s.E * 8) : 0;
+  p.aux_part = off;
+  off += has_aux(s) ? align_up((size_t)aux_blocks(s.T) * s.E * 8) : 0;
   p.fwd_total = off;
   off = 0;
   p.d_o = off; off += align_up((size_t)R * s.d * eb);
@@ -163,15 +181,21 @@ Plan plan(const moe_shape& s) {
   p.dx_perm = off; off += align_up((size_t)R * s.d * eb);
   p.dl = off; off += align_up((size_t)R * 4);
   p.partial = off; off += align_up((size_t)moe::route_dwr_tasks(R, s.E) * s.d * 4);
-  p.w_rt = off; off += align_up((size_t)s.E * s.d * 4);
+  p.w_rt = off; off += align_up((size_t)(has_aux(s) ? aux_epad(s) : s.E) * s.d * 4);
   p.dgu_sh = off; off += s.n_shared ? align_up((size_t)s.T * 2 * s.f_shared * eb) : 0;
   p.dx_sh = off; off += s.n_shared ? align_up((size_t)s.T * s.d * eb) : 0;
+  const bool aux = has_aux(s);
+  p.aux_dl = off; off += aux ? align_up((size_t)s.T * aux_epad(s) * eb) : 0;
+  p.aux_dx = off; off += aux ? align_up((size_t)s.T * s.d * eb) : 0;
+  p.aux_off = off; off += aux ? align_up((size_t)(aux_groups(s) + 1) * 4) : 0;
+  p.aux_wpart = off; off += aux ? align_up((size_t)aux_groups(s) * s.d * aux_epad(s) * eb) : 0;
   p.bwd_total = off;
   size_t sv = 0;
   sv += (size_t)R * (4 + 4 + 4 + 4 + 4);  // topk_idx, topk_w, s_sel, row_of, token_of
   sv += (size_t)(s.E + 1) * 4;
   sv += (size_t)R * (s.d + 2 * s.f + s.f + s.d) * eb;
   if (s.n_shared) sv += (size_t)s.T * (2 * s.f_shared + s.f_shared + s.d) * eb;
+  if (has_aux(s)) sv += (size_t)s.T * s.E * 4 + 4;
   p.saved_total = sv;
   return p;
 }
@@ -219,8 +243,9 @@ GemmArgs gemm_dense(const moe_shape& s, int mode) {
 }
 
 int do_route(const moe_shape& s, const void* x, const float* w_r, const float* bias, int32_t* topk_idx,
-             float* topk_w, float* s_sel, int32_t* counts, void* ws, hipStream_t st) {
+             float* topk_w, float* s_sel, int32_t* counts, void* ws, hipStream_t st, float* probs = nullptr) {
   RouteArgs a{};
+  a.probs = probs;
   a.wsplit = s.dtype == MOE_BF16 ? wsp(ws, plan(s).wsplit) : nullptr;
   a.lg = s.dtype == MOE_BF16 ? reinterpret_cast<double*>(wsp(ws, plan(s).lg)) : nullptr;
   a.x = x;
@@ -378,6 +403,19 @@ int do_shared_bwd(const moe_shape& s, const void* x, const void* dy, const void*
   return do_shared_wgrad(s, x, dy, h_sh, dgu_sh, dwsg, dwsu, dwsd, false, st);
 }
 
+AuxArgs aux_args(const moe_shape& s, const moe_params* prm, const moe_saved* sv) {
+  AuxArgs a{};
+  a.probs = sv->router_probs;
+  a.offsets = sv->expert_offsets;
+  a.aux_f = prm->aux_f;
+  a.T = s.T;
+  a.E = (int)s.E;
+  a.k = (int)s.k;
+  a.coef = s.aux_coef;
+  a.loss = sv->aux_loss;
+  return a;
+}
+
 RouteBwdArgs route_bwd_base(const moe_shape& s) {
   RouteBwdArgs a{};
   a.T = s.T;
@@ -394,6 +432,13 @@ RouteBwdArgs route_bwd_base(const moe_shape& s) {
 }  // namespace moe
 
 using namespace moe;
+
+// The Python binding mirrors these layouts field by field.
+static_assert(sizeof(moe_shape) == 96 && offsetof(moe_shape, f_shared) == 56 && offsetof(moe_shape, aux_coef) == 88,
+              "moe_shape layout");
+static_assert(sizeof(moe_params) == 12 * sizeof(void*) && sizeof(moe_saved) == 15 * sizeof(void*) &&
+                  sizeof(moe_grads) == 10 * sizeof(void*),
+              "pointer struct layouts");
 
 // ---------------------------------------------------------------------------
 // exported entry points
@@ -446,6 +491,7 @@ int check_layer_bwd(const moe_shape& s, const moe_params* prm, const void* x, co
       MOE_NEED(sv->o, "saved.o");
       if (s.router == MOE_ROUTER_SIGMOID_GROUPED) MOE_NEED(sv->s_sel, "saved.s_sel");
       if (s.n_shared) MOE_NEED(sv->gu_sh, "saved.gu_sh");
+      if (has_aux(s)) MOE_NEED(sv->router_probs, "saved.router_probs");
     }
     if (phase & 2) {
       MOE_NEED(sv->token_of, "saved.token_of");
@@ -486,8 +532,29 @@ int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const moe_saved* 
   // 2. expert dgrads
   MOE_TRY(do_gemm_bwd(s, MOE_DGRAD, nullptr, sv->expert_offsets, sv->gu, nullptr, d_o, prm->w_gate, prm->w_up,
                       prm->w_down, dgu, dx_perm, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, stream));
-  // 3. W_r^T for the router dx fused into the unpermute
-  MOE_TRY(launch_wr_transpose_act(prm->w_r, w_rt, (int)s.d, (int)s.E, s.dtype == MOE_BF16, stream));
+  // 3. W_r^T for the router dx fused into the unpermute (zero rows up to the
+  //    auxiliary loss's padded expert count)
+  const bool aux = has_aux(s) && s.T > 0;
+  const int E_rt = aux ? aux_epad(s) : (int)s.E;
+  MOE_TRY(launch_wr_transpose_act(prm->w_r, w_rt, (int)s.d, (int)s.E, E_rt, s.dtype == MOE_BF16, stream));
+  // 3b. auxiliary loss: its dense logit gradient, kept for the weight half,
+  //     and its router dx = dl_aux W_r^T (a dense down-projection product)
+  void* aux_dx = nullptr;
+  if (aux) {
+    void* aux_dl = wsp(ws, p.aux_dl);
+    aux_dx = wsp(ws, p.aux_dx);
+    MOE_TRY(launch_aux_grad(aux_args(s, prm, sv), aux_dl, E_rt, reinterpret_cast<int32_t*>(wsp(ws, p.aux_off)),
+                            aux_groups(s), aux_chunk(s), s.dtype == MOE_BF16, stream));
+    GemmArgs g = gemm_base(s, G_FWD_DOWN, nullptr);
+    g.ngroups = 1;
+    g.dense_rows = s.T;
+    g.max_rows = s.T;
+    g.f = E_rt;
+    g.a = aux_dl;
+    g.w0 = w_rt;
+    g.c0 = aux_dx;
+    MOE_TRY(launch_gemm(g, stream));
+  }
   // 4. shared expert input gradient
   void* dx_sh = nullptr;
   if (s.n_shared) {
@@ -501,6 +568,7 @@ int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const moe_saved* 
   u.row_of = sv->row_of;
   u.dx_router = nullptr;
   u.dx_shared = dx_sh;
+  u.dx_aux = aux_dx;
   u.dl = dl;
   u.topk_idx = sv->topk_idx;
   u.w_rt = w_rt;
@@ -535,6 +603,23 @@ int layer_bwd_wgrad(const moe_shape& s, const moe_params* prm, const void* x, co
   rb.partial = reinterpret_cast<float*>(wsp(ws, p.partial));
   rb.accumulate = accumulate;
   MOE_TRY(launch_route_bwd(rb, stream));
+  if (has_aux(s) && s.T > 0) {
+    // auxiliary loss: dW_r += x^T dl_aux, as per-chunk products of the grouped
+    // weight-gradient GEMM (chunks of tokens as the groups), summed in order
+    const int G = aux_groups(s), E_pad = aux_epad(s);
+    const int32_t* off = reinterpret_cast<const int32_t*>(wsp(ws, p.aux_off));  // written with dl_aux
+    void* part = wsp(ws, p.aux_wpart);
+    GemmArgs g = gemm_base(s, G_WGRAD_DOWN, off);
+    g.ngroups = G;
+    g.max_rows = s.T;
+    g.f = (int)s.d;
+    g.d = E_pad;
+    g.a = x;
+    g.b = wsp(ws, p.aux_dl);
+    g.c0 = part;
+    MOE_TRY(launch_gemm(g, stream));
+    MOE_TRY(launch_aux_dwr(part, G, (int)s.d, (int)s.E, E_pad, s.dtype == MOE_BF16, gr->dw_r, stream));
+  }
   if (s.n_shared)
     MOE_TRY(do_shared_wgrad(s, x, dy, sv->h_sh, wsp(ws, p.dgu_sh), gr->dws_gate, gr->dws_up, gr->dws_down,
                             accumulate, stream));
@@ -875,12 +960,22 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, 
       MOE_NEED(sv->o_sh, "saved.o_sh");
     }
   }
+  if (has_aux(s)) {
+    MOE_NEED(sv->aux_loss, "saved.aux_loss");
+    if (s.T > 0) MOE_NEED(sv->router_probs, "saved.router_probs");
+  }
   MOE_TRY(check_ws(ws, ws_bytes, plan(s).fwd_total));
   const void* bg = s.expert_bias ? prm->b_gate : nullptr;
   const void* bu = s.expert_bias ? prm->b_up : nullptr;
   const void* bd = s.expert_bias ? prm->b_down : nullptr;
-  MOE_TRY(do_route(s, x, prm->w_r, prm->router_bias, sv->topk_idx, sv->topk_w, sv->s_sel, nullptr, ws, stream));
+  MOE_TRY(do_route(s, x, prm->w_r, prm->router_bias, sv->topk_idx, sv->topk_w, sv->s_sel, nullptr, ws, stream,
+                   has_aux(s) ? sv->router_probs : nullptr));
   MOE_TRY(do_permute(s, x, sv->topk_idx, sv->expert_offsets, sv->row_of, sv->token_of, sv->x_perm, ws, stream));
+  if (has_aux(s)) {
+    AuxArgs aa = aux_args(s, prm, sv);
+    aa.part = reinterpret_cast<double*>(wsp(ws, plan(s).aux_part));
+    MOE_TRY(launch_aux_stats(aa, stream));
+  }
   MOE_TRY(do_gemm_fwd(s, sv->x_perm, sv->expert_offsets, prm->w_gate, prm->w_up, prm->w_down, bg, bu, bd, sv->gu,
                       sv->h, sv->o, stream));
   if (s.n_shared)

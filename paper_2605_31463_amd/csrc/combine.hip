@@ -174,6 +174,7 @@ __global__ __launch_bounds__(256) void unpermute_kernel(UnpermuteArgs a) {
   const int nch = a.d / V;
   const XT* dxp = reinterpret_cast<const XT*>(a.dx_perm);
   const XT* dxs = reinterpret_cast<const XT*>(a.dx_shared);
+  const XT* dxa = reinterpret_cast<const XT*>(a.dx_aux);
   const XT* wrt = reinterpret_cast<const XT*>(a.w_rt);
   XT* dx = reinterpret_cast<XT*>(a.dx);
   const int64_t R = a.T * a.k;
@@ -230,6 +231,12 @@ __global__ __launch_bounds__(256) void unpermute_kernel(UnpermuteArgs a) {
       if (dxs) {
         float vv[V];
         Vec16<XT>::load(dxs + t * a.d + (int64_t)c * V, vv);
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[v] += vv[v];
+      }
+      if (dxa) {
+        float vv[V];
+        Vec16<XT>::load(dxa + t * a.d + (int64_t)c * V, vv);
 #pragma unroll
         for (int v = 0; v < V; ++v) acc[v] += vv[v];
       }

@@ -32,6 +32,9 @@ enum KernelId {
   K_RANK,
   K_WR_SPLIT,
   K_ROUTE_SELECT,
+  K_AUX_STATS,
+  K_AUX_GRAD,
+  K_AUX_DWR,
   K_NUM_KERNELS
 };
 

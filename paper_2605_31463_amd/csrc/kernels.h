@@ -22,6 +22,7 @@ struct RouteArgs {
   int32_t* counts;  // may be null
   void* wsplit;      // bf16 [3][E][d] workspace for the MFMA path (bf16 x), or null
   double* lg;        // float64 [T][E] logits workspace for the MFMA path
+  float* probs;      // [T][E] softmax over all experts (auxiliary loss), or null
 };
 int launch_route(const RouteArgs& a, hipStream_t s);
 int zero_i32(int32_t* p, int64_t n, hipStream_t s);
@@ -102,14 +103,36 @@ constexpr int DWR_ROWS = 256;  // rows per partial-sum task of dW_r
 inline int64_t route_dwr_tasks(int64_t R, int64_t E) { return R / DWR_ROWS + E; }
 int launch_route_bwd(const RouteBwdArgs& a, hipStream_t s);
 int launch_wr_transpose(const float* w_r, float* w_rt, int d, int E, hipStream_t s);
+// W_r^T [Eo][d] in the activation type, rows E .. Eo-1 zero.
+int launch_wr_transpose_act(const float* w_r, void* w_rt, int d, int E, int Eo, bool bf16, hipStream_t s);
+
+// Global-level load-balancing loss: statistics and logit gradient.
+struct AuxArgs {
+  const float* probs;       // [T][E] softmax over all experts
+  const int32_t* offsets;   // [E+1] expert_offsets (this call's loads)
+  const float* aux_f;       // [E] given load fractions, or null
+  int64_t T;
+  int E, k;
+  float coef;
+  double* part;             // [aux_blocks(T)][E] workspace
+  float* loss;              // [1]
+};
+inline int64_t aux_blocks(int64_t T) { return (T + 255) / 256; }
+int launch_aux_stats(const AuxArgs& a, hipStream_t s);
+// dl [T][E_pad] in the activation type (columns E .. E_pad-1 zero), and the
+// row offsets [G+1] of the T tokens cut into chunks, for the grouped dW_r product
+int launch_aux_grad(const AuxArgs& a, void* dl, int E_pad, int32_t* chunk_off, int G, int64_t chunk, bool bf16,
+                    hipStream_t s);
+// dw_r[i][e] += sum over the G chunks of part[g][i][e]
+int launch_aux_dwr(const void* part, int G, int d, int E, int E_pad, bool bf16, float* dw_r, hipStream_t s);
 // W_r^T in the activation type (bf16 rounding for bf16 layers)
-int launch_wr_transpose_act(const float* w_r, void* w_rt, int d, int E, bool bf16, hipStream_t s);
 
 struct UnpermuteArgs {
   const void* dx_perm;
   const int32_t* row_of;
   const float* dx_router;   // may be null
   const void* dx_shared;    // may be null
+  const void* dx_aux;       // may be null: the auxiliary loss's router dx [T][d]
   // fused router dx: dx += sum_s dl[t][s] * w_rt[topk_idx[t][s]]
   const float* dl;          // may be null
   const int32_t* topk_idx;

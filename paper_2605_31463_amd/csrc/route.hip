@@ -98,6 +98,39 @@ __device__ void select_tokens(const RouteArgs& a, const double* lg, int ld, int6
         key[q] = isnan(kv) ? -INFINITY : kv;  // NaN orders below every number
       }
     }
+    if (a.probs) {
+      // the router's probabilities over all experts (auxiliary loss): softmax
+      // of the logits (+ bias when it is added to the logits)
+      double v[4];
+      double m = -INFINITY;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = lane * epl + q;
+        v[q] = -INFINITY;
+        if (q < epl && e < E) {
+          double l = lg[tl * EPAD + e];
+          if (logit_bias) l += (double)a.bias[e];
+          v[q] = l;
+          m = fmax(m, l);
+        }
+      }
+      m = wave_max_d(m, 64);
+      double z = 0.0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = lane * epl + q;
+        if (q < epl && e < E) {
+          v[q] = exp(v[q] - m);
+          z += v[q];
+        }
+      }
+      z = wave_sum_d(z, 64);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = lane * epl + q;
+        if (q < epl && e < E) a.probs[t * E + e] = (float)(v[q] / z);
+      }
+    }
     // group limit
     if (a.n_groups > 1) {
       double m1 = -INFINITY, m2 = -INFINITY;

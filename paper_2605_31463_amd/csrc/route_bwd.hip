@@ -109,8 +109,9 @@ __global__ __launch_bounds__(256) void dwr_reduce_kernel(RouteBwdArgs a) {
   *o = a.accumulate ? *o + acc : acc;
 }
 
+// wt [Eo][d] = w^T for rows e < E, zero for E <= e < Eo.
 template <class OT>
-__global__ void transpose_kernel(const float* __restrict__ w, OT* __restrict__ wt, int d, int E) {
+__global__ void transpose_kernel(const float* __restrict__ w, OT* __restrict__ wt, int d, int E, int Eo) {
   __shared__ float tile[32][33];
   const int e0 = blockIdx.x * 32, i0 = blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 256 threads: 32 x 8
@@ -121,7 +122,7 @@ __global__ void transpose_kernel(const float* __restrict__ w, OT* __restrict__ w
   __syncthreads();
   for (int r = ty; r < 32; r += 8) {
     const int e = e0 + r, i = i0 + tx;
-    if (e < E && i < d) Elem<OT>::store(wt, (int64_t)e * d + i, tile[tx][r]);
+    if (e < Eo && i < d) Elem<OT>::store(wt, (int64_t)e * d + i, tile[tx][r]);
   }
 }
 
@@ -148,14 +149,20 @@ __global__ __launch_bounds__(256) void dx_router_kernel(RouteBwdArgs a, const fl
 
 int launch_wr_transpose(const float* w_r, float* w_rt, int d, int E, hipStream_t s) {
   dim3 grid((E + 31) / 32, (d + 31) / 32);
-  return launch(K_WR_TRANSPOSE, s, "wr_transpose", [&] { transpose_kernel<float><<<grid, 256, 0, s>>>(w_r, w_rt, d, E); });
+  return launch(K_WR_TRANSPOSE, s, "wr_transpose",
+                [&] { transpose_kernel<float><<<grid, 256, 0, s>>>(w_r, w_rt, d, E, E); });
 }
 
-int launch_wr_transpose_act(const float* w_r, void* w_rt, int d, int E, bool bf16, hipStream_t s) {
-  if (!bf16) return launch_wr_transpose(w_r, reinterpret_cast<float*>(w_rt), d, E, s);
-  dim3 grid((E + 31) / 32, (d + 31) / 32);
+int launch_wr_transpose_act(const float* w_r, void* w_rt, int d, int E, int Eo, bool bf16, hipStream_t s) {
+  dim3 grid((Eo + 31) / 32, (d + 31) / 32);
+  if (!bf16) {
+    float* o = reinterpret_cast<float*>(w_rt);
+    return launch(K_WR_TRANSPOSE, s, "wr_transpose",
+                  [&] { transpose_kernel<float><<<grid, 256, 0, s>>>(w_r, o, d, E, Eo); });
+  }
   bf16_t* o = reinterpret_cast<bf16_t*>(w_rt);
-  return launch(K_WR_TRANSPOSE, s, "wr_transpose", [&] { transpose_kernel<bf16_t><<<grid, 256, 0, s>>>(w_r, o, d, E); });
+  return launch(K_WR_TRANSPOSE, s, "wr_transpose",
+                [&] { transpose_kernel<bf16_t><<<grid, 256, 0, s>>>(w_r, o, d, E, Eo); });
 }
 
 int launch_route_bwd(const RouteBwdArgs& a, hipStream_t s) {

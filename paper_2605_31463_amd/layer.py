@@ -30,6 +30,8 @@ class MoELayer:
             gu_sh=e(T, 2 * s.f_shared) if s.n_shared else None,
             h_sh=e(T, s.f_shared) if s.n_shared else None,
             o_sh=e(T, d) if s.n_shared else None,
+            router_probs=e(T, E, dt=f32) if s.aux_coef > 0 else None,
+            aux_loss=torch.zeros(1, dtype=f32, device=device) if s.aux_coef > 0 else None,
         )
         self.y = e(T, d)
         self.dx = e(T, d)

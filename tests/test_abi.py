@@ -56,6 +56,9 @@ def test_workspace_sizes_scale_with_shape():
     (dict(k=17, E=32), L.MOE_ERR_UNSUPPORTED),
     (dict(d=100), L.MOE_ERR_UNSUPPORTED),
     (dict(f=96), L.MOE_ERR_UNSUPPORTED),
+    (dict(aux_coef=-1.0), L.MOE_ERR_INVALID_ARG),
+    (dict(aux_coef=float("nan")), L.MOE_ERR_INVALID_ARG),
+    (dict(E=16, k=4, n_groups=4, topk_groups=2, router="sigmoid_grouped", aux_coef=1e-3), L.MOE_ERR_UNSUPPORTED),
 ])
 def test_bad_shapes_rejected(kw, status):
     base = dict(T=64, d=128, E=8, k=2, f=256)
@@ -101,9 +104,13 @@ def test_status_strings_and_kernel_names():
 
 
 def test_shape_struct_layout_matches_header():
-    # int64 x5, int32 x3 (+pad), int64, int32 x2, float, int32 x3 -> 88 bytes
-    assert ctypes.sizeof(L.moe_shape) == 88
+    # int64 x5, int32 x3 (+pad), int64, int32 x2, float, int32 x3, float (+pad) -> 96 bytes
+    assert ctypes.sizeof(L.moe_shape) == 96
     assert L.moe_shape.f_shared.offset == 56
+    assert L.moe_shape.aux_coef.offset == 88
+    # pointer structs: one pointer per field, in the header's order
+    assert ctypes.sizeof(L.moe_params) == 12 * 8 and L.moe_params.aux_f.offset == 88
+    assert ctypes.sizeof(L.moe_saved) == 15 * 8 and L.moe_saved.aux_loss.offset == 112
 
 
 def declared_arities():
