@@ -26,6 +26,7 @@
 // fp32 path: a plain kernel, one thread per output (or output pair), for the
 // fp32 workload; same modes, same epilogues.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -1048,7 +1049,11 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
     tile_dims<MODE>(a, tl, K, M, N);
     const int g = tl.g;
     const int nk = (K + BK - 1) / BK;
-    const bool wave_rows = tl.m0 + wm * C::TM < M;
+    // 32-row blocks of this wavefront that hold rows of the tile (a ragged
+    // last tile of an expert has fewer): the others skip their fragment reads
+    // and MFMAs (no rows at all: the SIMD partner has the matrix pipe alone)
+    const int live = __builtin_amdgcn_readfirstlane(max(0, min(MI, (M - (tl.m0 + wm * C::TM) + 31) / 32)));
+    const bool wave_rows = live > 0;
     const bool colsum = wgrad && a.db0 && tl.m0 == 0 && wm == 0;
     floatx16 acc[MI][NI];
 #pragma unroll
@@ -1061,6 +1066,9 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < NI; ++j) bsum[j] = 0.f;
 
+    // the k loop, in two copies: tiles whose wavefront rows are all live run
+    // the MFMA block without tests, ragged ones skip their dead row blocks
+    auto k_loop = [&](auto all_live) {
     for (int kt = 0; kt < nk; ++kt) {
       const int ahead = issued - consumed - 1;  // stages issued after this one
       if (S >= 5 && ahead >= 3) wait_vmcnt<(S >= 5 ? 3 : 0) * NL>();
@@ -1094,9 +1102,10 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < MI; ++i)
+          if (decltype(all_live)::value || i < live)
 #pragma unroll
-          for (int j = 0; j < NI; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
+            for (int j = 0; j < NI; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
         if (colsum) {
 #pragma unroll
@@ -1110,6 +1119,9 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
         }
       }
     }
+    };
+    if (live == MI) k_loop(std::true_type{});
+    else k_loop(std::false_type{});
 
     // ---- epilogue (this wavefront's rows only).  Block (i, j) holds the
     // transposed product: lane l has row 32i + l%32, register v = 4q + t
