@@ -847,7 +847,7 @@ __device__ __forceinline__ void tile_dims(const GemmArgs& a, const Tile& tl, int
 }
 
 template <int MODE, class C>
-__global__ __launch_bounds__(C::NT, 1) void gemm_bf16_persistent(GemmArgs a) {
+__global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persistent(GemmArgs a) {
   constexpr bool wgrad = is_wgrad<MODE>();
   constexpr bool a_mn = wgrad;
   constexpr bool b_mn = MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN || wgrad;
@@ -1535,12 +1535,13 @@ int launch_mode(const GemmArgs& a, hipStream_t s) {
   if (a.bf16) {
     const int G = a.offsets ? a.ngroups : 1;
     const int64_t rows_per_group = a.offsets ? a.max_rows / G : a.dense_rows;
-    if (MOE_GEMM_PERSISTENT) {
+    if constexpr (MOE_GEMM_PERSISTENT != 0) {
       if (!is_wgrad<MODE>() && rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall>(a, s);
       return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big>(a, s);
+    } else {
+      if (!is_wgrad<MODE>() && rows_per_group < 192) return launch_bf16<MODE, CfgSmall>(a, s);
+      return launch_bf16<MODE, typename GemmShape<MODE>::big>(a, s);
     }
-    if (!is_wgrad<MODE>() && rows_per_group < 192) return launch_bf16<MODE, CfgSmall>(a, s);
-    return launch_bf16<MODE, typename GemmShape<MODE>::big>(a, s);
   }
   constexpr bool wgrad = is_wgrad<MODE>();
   const int G = a.offsets ? a.ngroups : 1;
