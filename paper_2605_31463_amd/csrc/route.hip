@@ -458,8 +458,186 @@ __global__ __launch_bounds__(TT * 4) void route_logits_kernel(RouteArgs a) {
     }
 }
 
-// Selection over the float64 logits in the workspace: one wavefront per token,
-// 16 tokens per workgroup.
+// ---------------------------------------------------------------------------
+// Selection with one DPP row (16 lanes) per token: the same decisions as
+// select_tokens (float64 keys, ties to the lower index, NaN below every
+// number, group limit by the sum of a group's two best keys), with the
+// reductions as DPP moves inside the row instead of 64-lane shuffles through
+// LDS, and four tokens per wavefront side by side.
+// ---------------------------------------------------------------------------
+// DPP controls: quad permutations lane ^ 1 and lane ^ 2, the row half mirror
+// (lane i <-> 7 - i within each 8 lanes) and the row mirror (i <-> 15 - i).
+// Applied in this order they pair aligned groups of 2, 4, 8, 16 lanes.
+constexpr int DPP_QXOR1 = 0xB1, DPP_QXOR2 = 0x4E, DPP_HMIRROR = 0x141, DPP_MIRROR = 0x140;
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) { return __builtin_amdgcn_mov_dpp(v, CTRL, 0xf, 0xf, false); }
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = dpp_i<CTRL>((int)(b & 0xffffffffll));
+  const int hi = dpp_i<CTRL>((int)(b >> 32));
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+template <int CTRL>
+__device__ __forceinline__ void dpp_best_step(double& k, int& i) {
+  const double ok = dpp_d<CTRL>(k);
+  const int oi = dpp_i<CTRL>(i);
+  if (better(ok, oi, k, i)) {
+    k = ok;
+    i = oi;
+  }
+}
+// best (key, index) over aligned groups of 2^levels lanes of the row
+__device__ __forceinline__ void dpp_best(double& k, int& i, int levels) {
+  if (levels > 0) dpp_best_step<DPP_QXOR1>(k, i);
+  if (levels > 1) dpp_best_step<DPP_QXOR2>(k, i);
+  if (levels > 2) dpp_best_step<DPP_HMIRROR>(k, i);
+  if (levels > 3) dpp_best_step<DPP_MIRROR>(k, i);
+}
+__device__ __forceinline__ double dpp_row_sum(double v) {
+  v += dpp_d<DPP_QXOR1>(v);
+  v += dpp_d<DPP_QXOR2>(v);
+  v += dpp_d<DPP_HMIRROR>(v);
+  v += dpp_d<DPP_MIRROR>(v);
+  return v;
+}
+__device__ __forceinline__ double dpp_row_max(double v) {
+  v = fmax(v, dpp_d<DPP_QXOR1>(v));
+  v = fmax(v, dpp_d<DPP_QXOR2>(v));
+  v = fmax(v, dpp_d<DPP_HMIRROR>(v));
+  v = fmax(v, dpp_d<DPP_MIRROR>(v));
+  return v;
+}
+// top-2 of (m1, m2) pairs over aligned groups of 2^levels lanes
+template <int CTRL>
+__device__ __forceinline__ void dpp_top2_step(double& m1, double& m2) {
+  const double o1 = dpp_d<CTRL>(m1), o2 = dpp_d<CTRL>(m2);
+  const double n1 = fmax(m1, o1);
+  m2 = fmax(fmin(m1, o1), fmax(m2, o2));
+  m1 = n1;
+}
+
+// KPL = E / 16 experts per lane (contiguous); E <= 256.  Needs, with a group
+// limit, groups of a whole power-of-two number of lanes.
+template <int KPL>
+__device__ void select_tokens16(const RouteArgs& a, const double* lg, int ld, int64_t t0, int ntok, int* hist) {
+  const int tid = threadIdx.x;
+  const int E = a.E;
+  const int lane = tid & 63, sub = lane & 15;
+  const int tl = (tid >> 6) * 4 + (lane >> 4);  // this row's token within the block
+  const int64_t t = t0 + tl;
+  const bool valid = tl < ntok && t < a.T;   // rows past the end compute on -inf keys, store nothing
+  const bool sigm = a.router == MOE_ROUTER_SIGMOID_GROUPED;
+  const bool logit_bias = a.bias_mode == MOE_BIAS_LOGIT;
+  const bool select_bias = a.bias_mode == MOE_BIAS_SELECT_ONLY;
+  const int k = a.k;
+  const int e0 = sub * KPL;
+  double lv[KPL], key[KPL];
+  unsigned avail = 0;
+#pragma unroll
+  for (int q = 0; q < KPL; ++q) {
+    double l = valid ? lg[(int64_t)tl * ld + e0 + q] : 0.0;
+    if (logit_bias) l += (double)a.bias[e0 + q];
+    lv[q] = l;
+    const double sc = sigm ? 1.0 / (1.0 + exp(-l)) : l;
+    const double kv = select_bias ? sc + (double)a.bias[e0 + q] : sc;
+    key[q] = (!valid || isnan(kv)) ? -INFINITY : kv;  // NaN orders below every number
+    avail |= 1u << q;
+  }
+  if (a.probs) {
+    // the router's probabilities over all experts (auxiliary loss)
+    double m = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < KPL; ++q) m = fmax(m, lv[q]);
+    m = dpp_row_max(m);
+    double ex[KPL], z = 0.0;
+#pragma unroll
+    for (int q = 0; q < KPL; ++q) {
+      ex[q] = exp(lv[q] - m);
+      z += ex[q];
+    }
+    z = dpp_row_sum(z);
+    if (valid)
+#pragma unroll
+      for (int q = 0; q < KPL; ++q) a.probs[t * E + e0 + q] = (float)(ex[q] / z);
+  }
+  // group limit: keep the topk_groups groups with the best sums of two keys
+  if (a.n_groups > 1) {
+    const int gsize = E / a.n_groups;
+    const int lpg = gsize / KPL;
+    const int levels = lpg >= 16 ? 4 : lpg >= 8 ? 3 : lpg >= 4 ? 2 : lpg >= 2 ? 1 : 0;
+    double m1 = -INFINITY, m2 = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < KPL; ++q) {
+      if (key[q] > m1) {
+        m2 = m1;
+        m1 = key[q];
+      } else if (key[q] > m2) {
+        m2 = key[q];
+      }
+    }
+    if (levels > 0) dpp_top2_step<DPP_QXOR1>(m1, m2);
+    if (levels > 1) dpp_top2_step<DPP_QXOR2>(m1, m2);
+    if (levels > 2) dpp_top2_step<DPP_HMIRROR>(m1, m2);
+    if (levels > 3) dpp_top2_step<DPP_MIRROR>(m1, m2);
+    const int g = e0 / gsize;
+    double gscore = gsize >= 2 ? m1 + m2 : m1;
+    if (isnan(gscore)) gscore = -INFINITY;
+    bool kept = false;
+    for (int r = 0; r < a.topk_groups; ++r) {
+      double ck = kept ? -INFINITY : gscore;
+      int ci = kept ? 0x7fffffff : g;
+      dpp_best(ck, ci, 4);
+      if (ci == g) kept = true;
+    }
+    if (!kept) avail = 0;
+  }
+  // top-k: k rounds of a row argmax; lane s keeps the expert of slot s
+  int my_idx = -1;
+  for (int s = 0; s < k; ++s) {
+    double ck = -INFINITY;
+    int ci = 0x7fffffff;  // any available expert beats the empty slot (lower index)
+#pragma unroll
+    for (int q = 0; q < KPL; ++q)
+      if (((avail >> q) & 1u) && better(key[q], e0 + q, ck, ci)) {
+        ck = key[q];
+        ci = e0 + q;
+      }
+    dpp_best(ck, ci, 4);
+    if (ci >= e0 && ci < e0 + KPL) avail &= ~(1u << (ci - e0));
+    if (sub == s) my_idx = ci;
+  }
+  // weights over the k selected (lanes 0..k-1 of the row hold one slot each)
+  const bool holds = sub < k;
+  double sc = 0.0;
+  if (holds && valid && my_idx >= 0 && my_idx < E) {
+    double l = lg[(int64_t)tl * ld + my_idx];
+    if (logit_bias) l += (double)a.bias[my_idx];
+    sc = sigm ? 1.0 / (1.0 + exp(-l)) : l;
+  }
+  double w;
+  if (sigm) {
+    const double z = dpp_row_sum(holds ? sc : 0.0);
+    w = (double)a.route_scale * sc / z;
+  } else {
+    const double m = dpp_row_max(holds ? sc : -INFINITY);
+    const double p = holds ? exp(sc - m) : 0.0;
+    const double z = dpp_row_sum(p);
+    w = (double)a.route_scale * p / z;
+  }
+  if (holds && valid) {
+    a.topk_idx[t * k + sub] = my_idx;
+    a.topk_w[t * k + sub] = (float)w;
+    if (sigm && a.s_sel) a.s_sel[t * k + sub] = (float)sc;
+    atomicAdd(&hist[my_idx], 1);
+  }
+}
+
+// Selection over the float64 logits in the workspace, 16 tokens per
+// workgroup: KPL > 0, one DPP row per token (KPL = E / 16 experts per lane);
+// KPL = 0, one wavefront per token.
+template <int KPL>
 __global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a) {
   constexpr int TPB = 16;
   __shared__ int hist[256];
@@ -467,7 +645,10 @@ __global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a) {
   __syncthreads();
   const int64_t t0 = (int64_t)blockIdx.x * TPB;
   const int ntok = (int)min((int64_t)TPB, a.T - t0);
-  select_tokens(a, a.lg + t0 * a.E, a.E, t0, ntok, hist);
+  if constexpr (KPL > 0)
+    select_tokens16<KPL>(a, a.lg + t0 * a.E, a.E, t0, ntok, hist);
+  else
+    select_tokens(a, a.lg + t0 * a.E, a.E, t0, ntok, hist);
   __syncthreads();
   if (a.counts) {
     for (int e = threadIdx.x; e < a.E; e += 256)
@@ -497,8 +678,30 @@ int launch_route_gemm(const RouteArgs& a, hipStream_t s) {
   }
 #undef MOE_RL
   if (st) return st;
-  return launch(K_ROUTE_SELECT, s, "route_select",
-                [&] { route_select_kernel<<<(int)((a.T + 15) / 16), 256, 0, s>>>(a); });
+  // one DPP row per token when E / 16 experts per lane tile the groups into
+  // whole power-of-two lane sets (always without a group limit)
+  const int kpl = a.E / 16;
+  bool rows16 = a.E % 16 == 0 && a.E <= 256;
+  if (rows16 && a.n_groups > 1) {
+    const int gsize = a.E / a.n_groups, lpg = gsize / kpl;
+    rows16 = gsize % kpl == 0 && lpg >= 1 && lpg <= 16 && (lpg & (lpg - 1)) == 0;
+  }
+  const int nb = (int)((a.T + 15) / 16);
+#define MOE_SEL(KPL_) \
+  return launch(K_ROUTE_SELECT, s, "route_select", [&] { route_select_kernel<KPL_><<<nb, 256, 0, s>>>(a); });
+  if (rows16) switch (kpl) {
+      case 2: MOE_SEL(2)
+      case 4: MOE_SEL(4)
+      case 6: MOE_SEL(6)
+      case 8: MOE_SEL(8)
+      case 10: MOE_SEL(10)
+      case 12: MOE_SEL(12)
+      case 14: MOE_SEL(14)
+      case 16: MOE_SEL(16)
+      default: break;
+    }
+  MOE_SEL(0)
+#undef MOE_SEL
 }
 
 // NTW: 16-expert MFMA tiles per wavefront.  Without SPLIT a block is 64 tokens
