@@ -24,4 +24,10 @@ from .moe_oracle import (  # noqa: F401
     router_probs,
     aux_loss,
     aux_loss_backward,
+    ZeroComputeSpec,
+    zc_kind,
+    zc_aux_weights,
+    zc_const_alpha,
+    zc_forward,
+    zc_backward,
 )

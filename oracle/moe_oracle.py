@@ -22,7 +22,8 @@ index; slots are ordered by descending key; rows within an expert by
 ascending token; the DeepSeek group score is the sum of the top two keys of
 the group).
 
-Conventions.  x [T][d]; W_r [d][E]; expert e: W_gate, W_up [d][f],
+Conventions.  x [T][d]; W_r [d][E_pool] (E_pool = E plus any
+zero-computation experts, see the last section); expert e: W_gate, W_up [d][f],
 W_down [f][d], optional biases b_gate, b_up [f], b_down [d].
 Routing outputs topk_idx [T][k] (slot order = descending selection key,
 ties to the lower expert), topk_w [T][k].  Maps: row r of the permuted
@@ -171,23 +172,29 @@ def sort_maps(topk_idx, E):
     """Counts, offsets and the row maps of the expert-contiguous layout.
 
     counts[e] = number of (t, s) with topk_idx[t][s] == e;
-    offsets[e] = sum of counts of experts below e (offsets[E] = T*k);
+    offsets[e] = sum of counts of experts below e (offsets[E] = T*k when
+    every selected id is below E);
     the rows of expert e are offsets[e] .. offsets[e+1]-1, filled by
-    ascending token t (a token holds an expert in at most one slot).
+    ascending token t (a token holds an expert in at most one slot).  Slots
+    whose expert is not below E (zero-computation experts) get no row:
+    row_of = -1.
     """
     idx = np.asarray(topk_idx)
     T, k = idx.shape
     counts = np.zeros(E, dtype=np.int64)
     for e in idx.reshape(-1):
-        counts[e] += 1
+        if 0 <= e < E:
+            counts[e] += 1
     offsets = np.zeros(E + 1, dtype=np.int64)
     offsets[1:] = np.cumsum(counts)
     cursor = offsets[:-1].copy()
-    row_of = np.empty((T, k), dtype=np.int64)
-    token_of = np.empty(T * k, dtype=np.int64)
+    row_of = np.full((T, k), -1, dtype=np.int64)   # -1: a slot without a row
+    token_of = np.empty(int(offsets[E]), dtype=np.int64)
     for t in range(T):                       # ascending token: stable within expert
         for s in range(k):
             e = idx[t, s]
+            if not 0 <= e < E:
+                continue                     # an expert outside the E with rows
             r = cursor[e]
             cursor[e] += 1
             row_of[t, s] = r
@@ -276,34 +283,39 @@ def router_backward(spec, rt, omega):
 # ----------------------------------------------------------------------------
 
 def combine(o, topk_w, row_of, shared_o=None):
-    """y_t = sum_s w[t][s] * o[row_of[t][s]] (+ shared_o[t])."""
+    """y_t = sum_s w[t][s] * o[row_of[t][s]] (+ shared_o[t]); slots without a
+    row (row_of = -1) contribute nothing here."""
     T, k = topk_w.shape
     y = np.zeros((T, o.shape[1]))
     for s in range(k):
-        y += topk_w[:, s:s + 1] * o[row_of[:, s]]
+        has = row_of[:, s] >= 0
+        y[has] += topk_w[has, s:s + 1] * o[row_of[has, s]]
     if shared_o is not None:
         y = y + shared_o
     return y
 
 
 def combine_backward(dy, o, topk_w, row_of):
-    """d_o[row_of[t][s]] = w[t][s] dy_t and omega[t][s] = <dy_t, o[row_of[t][s]]>."""
+    """d_o[row_of[t][s]] = w[t][s] dy_t and omega[t][s] = <dy_t, o[row_of[t][s]]>
+    (omega = 0 for a slot without a row)."""
     T, k = topk_w.shape
     omega = np.zeros((T, k))
     do = np.zeros_like(o, dtype=np.float64)
     for s in range(k):
-        rows = row_of[:, s]
-        omega[:, s] = (dy * o[rows]).sum(axis=1)
-        do[rows] = topk_w[:, s:s + 1] * dy
+        has = row_of[:, s] >= 0
+        rows = row_of[has, s]
+        omega[has, s] = (dy[has] * o[rows]).sum(axis=1)
+        do[rows] = topk_w[has, s:s + 1] * dy[has]
     return do, omega
 
 
 def unpermute(dx_perm, row_of):
-    """dx_t = sum_s dx_perm[row_of[t][s]]."""
+    """dx_t = sum_s dx_perm[row_of[t][s]] over the slots that have a row."""
     T, k = row_of.shape
     dx = np.zeros((T, dx_perm.shape[1]))
     for s in range(k):
-        dx += dx_perm[row_of[:, s]]
+        has = row_of[:, s] >= 0
+        dx[has] += dx_perm[row_of[has, s]]
     return dx
 
 
@@ -311,19 +323,24 @@ def unpermute(dx_perm, row_of):
 # Whole layer
 # ----------------------------------------------------------------------------
 
-def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_f=None):
+def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_f=None, zc=None):
     """Forward of one MoE layer.
 
-    x [T][d] float64; w_r [d][E]; beta [E] or None;
+    x [T][d] float64; w_r [d][E_pool]; beta [E_pool] or None;
     expert_fn(e) -> (wg, wu, wd, bg, bu, bd) float64 (biases may be None);
     shared = (wsg, wsu, wsd) or None for an always-on expert of weight 1;
-    aux_coef > 0 adds the load-balancing loss (aux_f: the batch's fractions).
+    aux_coef > 0 adds the load-balancing loss (aux_f: the batch's fractions);
+    zc = (ZeroComputeSpec, v, wc) appends zero-computation experts to the pool
+    (E_pool = spec.E + their number), else None (E_pool = spec.E).
     Returns routing, maps and the per-row activations (permuted order) and y
     (and the auxiliary loss, its probabilities and fractions).
     """
     x = np.asarray(x, np.float64)
     T, d = x.shape
     E, k = spec.E, spec.k
+    E_pool = E + (zc[0].n if zc is not None else 0)
+    if np.asarray(w_r).shape[1] != E_pool:
+        raise ValueError("w_r must have one column per expert of the pool")
     l = router_logits(x, w_r)
     rt = route(spec, l, beta)
     mp = sort_maps(rt["topk_idx"], E)
@@ -346,29 +363,42 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
         g, u, h, osh = expert_forward(x, *shared)
         sh = dict(g=g, u=u, h=h, o=osh)
     y = combine(o, rt["topk_w"], mp["row_of"], None if sh is None else sh["o"])
+    zf = None
+    if zc is not None:
+        zf = zc_forward(x, rt["topk_idx"], rt["topk_w"], E, *zc)
+        y = y + zf["y"]
     aux = None
     if aux_coef:
         probs = router_probs(spec, l, beta)
-        aux = aux_loss(spec, probs, mp["counts"], aux_coef, aux_f)
-        aux.update(probs=probs, coef=aux_coef)
+        counts = np.bincount(rt["topk_idx"].reshape(-1), minlength=E_pool)
+        eta = None if zc is None else zc_aux_weights(E, zc[0])
+        aux = aux_loss(spec, probs, counts, aux_coef, aux_f, eta)
+        aux.update(probs=probs, coef=aux_coef, eta=eta)
     return dict(logits=l, route=rt, maps=mp, x_perm=x_perm, o=o, g=gs, u=us,
-                h=hs, y=y, shared=sh, f=fwidth, aux=aux)
+                h=hs, y=y, shared=sh, f=fwidth, aux=aux, zc=zf)
 
 
-def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bias=False):
-    """Backward of L = sum_t <dy_t, y_t> through the whole layer.
+def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bias=False, zc=None):
+    """Backward of L = sum_t <dy_t, y_t> (+ the auxiliary loss) through the
+    whole layer.
 
-    Returns dx [T][d], dw_r [d][E], per-expert dict of dW/db, shared-expert
-    grads, omega [T][k] and dl [T][k].
+    Returns dx [T][d], dw_r [d][E_pool], per-expert dict of dW/db,
+    shared-expert grads, omega [T][k], dl [T][k], and with zc the
+    zero-computation experts' dict (dv, dwc).
     """
     x = np.asarray(x, np.float64)
     dy = np.asarray(dy, np.float64)
     T, d = x.shape
     E, k = spec.E, spec.k
+    E_pool = np.asarray(w_r).shape[1]
     rt, mp = fwd["route"], fwd["maps"]
     w = rt["topk_w"]
     o = fwd["o"]
     do, omega = combine_backward(dy, o, w, mp["row_of"])
+    zb = None
+    if zc is not None:
+        zb = zc_backward(dy, x, rt["topk_idx"], w, E, *zc)
+        omega = omega + zb["omega"]
     # experts
     dx = np.zeros((T, d))
     dx_perm = np.zeros((T * k, d))
@@ -392,14 +422,16 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
     dx += unpermute(dx_perm, mp["row_of"])
     # router
     dl = router_backward(spec, rt, omega)
-    dl_dense = np.zeros((T, E))
+    dl_dense = np.zeros((T, E_pool))
     np.put_along_axis(dl_dense, rt["topk_idx"], dl, axis=1)
     aux = fwd.get("aux")
     if aux is not None:
-        dl_dense = dl_dense + aux_loss_backward(aux["probs"], aux["f"], aux["coef"])
+        dl_dense = dl_dense + aux_loss_backward(aux["probs"], aux["f"], aux["coef"], aux.get("eta"))
     dw_r = x.T @ dl_dense
     dx_router = dl_dense @ np.asarray(w_r, np.float64).T
     dx += dx_router
+    if zb is not None:
+        dx += zb["dx"]
     sh = None
     if shared is not None:
         wsg, wsu, wsd = shared
@@ -410,7 +442,8 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
         gsh.pop("du")
         sh = gsh
     return dict(dx=dx, dw_r=dw_r, experts=grads, shared=sh, omega=omega, dl=dl,
-                dx_perm=dx_perm, do=do, dx_router=dx_router)
+                dx_perm=dx_perm, do=do, dx_router=dx_router,
+                zc=None if zb is None else dict(dv=zb["dv"], dwc=zb["dwc"]))
 
 
 # ----------------------------------------------------------------------------
@@ -437,34 +470,40 @@ def router_probs(spec, logits, beta=None):
     return z / z.sum(axis=1, keepdims=True)
 
 
-def aux_loss(spec, p, counts, coef, f=None):
+def aux_loss(spec, p, counts, coef, f=None, eta=None):
     """Global-level load-balancing loss.  p [T][E] from router_probs; counts
     [E] routed slots per expert; f [E] the batch's fractions if given, else
-    counts / (T*k).  Returns dict(loss, P, f)."""
+    counts / (T*k); eta [E] per-expert weights of the balance terms (None:
+    all one), L = coef * E * sum_e eta_e f_e P_e.  Returns dict(loss, P, f)."""
     p = np.asarray(p, np.float64)
     T, E = p.shape
     if f is None:
         f = np.asarray(counts, np.float64) / float(T * spec.k)
     f = np.asarray(f, np.float64)
+    ef = f if eta is None else np.asarray(eta, np.float64) * f
     P = p.mean(axis=0)
-    return dict(loss=coef * E * float(np.dot(f, P)), P=P, f=f)
+    return dict(loss=coef * E * float(np.dot(ef, P)), P=P, f=f)
 
 
-def aux_loss_backward(p, f, coef):
+def aux_loss_backward(p, f, coef, eta=None):
     """dL/dlogit [T][E] of aux_loss with f held fixed: through P_e = mean_t
-    p[t][e] and the softmax Jacobian dp_e/dl_j = p_e (delta_ej - p_j),
-    dl[t][j] = coef * E / T * p[t][j] * (f_j - sum_e f_e p[t][e])."""
+    p[t][e] and the softmax Jacobian dp_e/dl_j = p_e (delta_ej - p_j), with
+    q = eta * f (q = f without weights),
+    dl[t][j] = coef * E / T * p[t][j] * (q_j - sum_e q_e p[t][e])."""
     p = np.asarray(p, np.float64)
     T, E = p.shape
-    F = p @ np.asarray(f, np.float64)
-    return coef * E / T * p * (np.asarray(f, np.float64)[None, :] - F[:, None])
+    q = np.asarray(f, np.float64)
+    if eta is not None:
+        q = np.asarray(eta, np.float64) * q
+    F = p @ q
+    return coef * E / T * p * (q[None, :] - F[:, None])
 
 
 # ----------------------------------------------------------------------------
 # Evaluation of a layer too large to run whole
 # ----------------------------------------------------------------------------
 
-def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None):
+def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=None):
     """Every per-token result of the layer for a batch of tokens: routing, y,
     omega, dl and dx (no weight gradients).
 
@@ -480,12 +519,20 @@ def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None):
     dy = np.asarray(dy, np.float64)
     T, d = x.shape
     E, k = spec.E, spec.k
+    E_pool = np.asarray(w_r).shape[1]
     rt = route(spec, router_logits(x, w_r), beta)
     idx, w = rt["topk_idx"], rt["topk_w"]
     y = np.zeros((T, d))
     dx = np.zeros((T, d))
     omega = np.zeros((T, k))
+    if zc is not None:
+        y += zc_forward(x, idx, w, E, *zc)["y"]
+        zb = zc_backward(dy, x, idx, w, E, *zc)
+        omega += zb["omega"]
+        dx += zb["dx"]
     for e in np.unique(idx):
+        if e >= E:
+            continue                         # zero-computation experts: above
         t, s = np.nonzero(idx == e)          # a token holds e in at most one slot
         wg, wu, wd, bg, bu, bd = expert_fn(int(e))
         g, u, h, o = expert_forward(x[t], wg, wu, wd, bg, bu, bd)
@@ -494,7 +541,7 @@ def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None):
         omega[t, s] = (dy[t] * o).sum(axis=1)
         dx[t] += expert_backward(x[t], g, u, h, we * dy[t], wg, wu, wd)["dx"]
     dl = router_backward(spec, rt, omega)
-    dl_dense = np.zeros((T, E))
+    dl_dense = np.zeros((T, E_pool))
     np.put_along_axis(dl_dense, idx, dl, axis=1)
     dx += dl_dense @ np.asarray(w_r, np.float64).T
     if shared is not None:
@@ -524,3 +571,125 @@ def expert_weight_grads_at(xe, do, wg, wu, wd, bg=None, bu=None, cols=None, with
     out.pop("dg")
     out.pop("du")
     return out
+
+
+# ----------------------------------------------------------------------------
+# Zero-computation experts (MoE++)
+# ----------------------------------------------------------------------------
+# Appendix B.3 describes the MoE++ task: the expert pool gains three kinds of
+# experts that do no feed-forward work (zero, copy, constant), the router's
+# output widens to cover them, and the load-balancing loss treats them
+# explicitly.  The expert functions are the ones of the MoE++ work it cites,
+# written out here:
+#   zero      out(x) = 0
+#   copy      out(x) = x
+#   constant  out(x) = a0 x + a1 v,  (a0, a1) = softmax(W_c x),
+#             with a trainable vector v [d] and matrix W_c [2][d] per expert.
+# Pool order: the E FFN experts (ids 0 .. E-1), then n_zero zero, n_copy copy
+# and n_const constant experts.  The router is the layer's softmax router
+# over the whole pool; a slot that picks a zero-computation expert adds
+# w * out(x_t) to y_t and gets no row in the permutation.  In the balance
+# loss every zero-computation expert's term carries the weight aux_weight
+# (1: the plain loss over the pool, 0: excluded), FFN experts weight 1.
+
+@dataclass
+class ZeroComputeSpec:
+    n_zero: int = 0
+    n_copy: int = 0
+    n_const: int = 0
+    aux_weight: float = 1.0
+
+    @property
+    def n(self):
+        return self.n_zero + self.n_copy + self.n_const
+
+
+def zc_kind(e, E, zs):
+    """('ffn' | 'zero' | 'copy' | 'const', index within its kind) of pool id e."""
+    if e < E:
+        return "ffn", e
+    j = e - E
+    if j < zs.n_zero:
+        return "zero", j
+    j -= zs.n_zero
+    if j < zs.n_copy:
+        return "copy", j
+    j -= zs.n_copy
+    if j < zs.n_const:
+        return "const", j
+    raise ValueError("expert id outside the pool")
+
+
+def zc_aux_weights(E, zs):
+    """eta [E_pool]: 1 for the FFN experts, aux_weight for the others."""
+    return np.concatenate([np.ones(E), np.full(zs.n, float(zs.aux_weight))])
+
+
+def zc_const_alpha(x_t, wc_c):
+    """(a0, a1) = softmax(W_c x_t) for one token and one constant expert."""
+    z = np.asarray(wc_c, np.float64) @ np.asarray(x_t, np.float64)
+    ez = np.exp(z - z.max())
+    return ez / ez.sum()
+
+
+def zc_forward(x, topk_idx, topk_w, E, zs, v, wc):
+    """y_zc[t] = sum over the slots s of token t whose expert is a
+    zero-computation one of w[t][s] * out(x_t).  v [n_const][d],
+    wc [n_const][2][d].  Returns dict(y, alpha [T][k][2], nan where the slot
+    is not a constant expert)."""
+    x = np.asarray(x, np.float64)
+    T, d = x.shape
+    k = topk_idx.shape[1]
+    y = np.zeros((T, d))
+    alpha = np.full((T, k, 2), np.nan)
+    for t in range(T):
+        for s in range(k):
+            kind, c = zc_kind(int(topk_idx[t, s]), E, zs)
+            wts = topk_w[t, s]
+            if kind == "copy":
+                y[t] += wts * x[t]
+            elif kind == "const":
+                a = zc_const_alpha(x[t], wc[c])
+                alpha[t, s] = a
+                y[t] += wts * (a[0] * x[t] + a[1] * np.asarray(v[c], np.float64))
+    return dict(y=y, alpha=alpha)
+
+
+def zc_backward(dy, x, topk_idx, topk_w, E, zs, v, wc):
+    """Gradients of sum_t <dy_t, y_zc[t]> with the gating weights held fixed,
+    and omega = dL/dw on the zero-computation slots.
+
+    Per slot with g = w dy_t:
+      copy:     omega = <dy_t, x_t>,  dx_t += g
+      constant: out = a0 x + a1 v, omega = <dy_t, out>;
+                da = (<g, x_t>, <g, v>), dz = a * (da - <a, da>) (softmax
+                Jacobian), dx_t += a0 g + W_c^T dz, dv += a1 g, dW_c += dz x_t^T
+      zero:     nothing.
+    Returns dict(omega [T][k] (zero on FFN slots), dx [T][d],
+    dv [n_const][d], dwc [n_const][2][d])."""
+    x = np.asarray(x, np.float64)
+    dy = np.asarray(dy, np.float64)
+    T, d = x.shape
+    k = topk_idx.shape[1]
+    omega = np.zeros((T, k))
+    dx = np.zeros((T, d))
+    dv = np.zeros((zs.n_const, d))
+    dwc = np.zeros((zs.n_const, 2, d))
+    for t in range(T):
+        for s in range(k):
+            kind, c = zc_kind(int(topk_idx[t, s]), E, zs)
+            g = topk_w[t, s] * dy[t]
+            if kind == "copy":
+                omega[t, s] = float(dy[t] @ x[t])
+                dx[t] += g
+            elif kind == "const":
+                vc = np.asarray(v[c], np.float64)
+                wcc = np.asarray(wc[c], np.float64)
+                a = zc_const_alpha(x[t], wcc)
+                omega[t, s] = float(dy[t] @ (a[0] * x[t] + a[1] * vc))
+                da = np.array([g @ x[t], g @ vc])
+                dz = a * (da - a @ da)
+                dx[t] += a[0] * g + wcc.T @ dz
+                dv[c] += a[1] * g
+                dwc[c] += np.outer(dz, x[t])
+    return dict(omega=omega, dx=dx, dv=dv, dwc=dwc)

@@ -583,3 +583,251 @@ def test_aux_loss_batch_fractions_are_used():
     fwd, _ = run_aux(spec, c, 0.3, f=f)
     assert fwd["aux"]["loss"] == pytest.approx(0.3, rel=1e-12)  # P sums to one
     assert np.array_equal(fwd["aux"]["f"], f)
+
+
+# ---------------------------------------------------------------------------
+# Zero-computation experts (MoE++; appendix B.3)
+# ---------------------------------------------------------------------------
+
+from oracle import ZeroComputeSpec, zc_backward, zc_forward  # noqa: E402
+
+ZC = ZeroComputeSpec(n_zero=2, n_copy=1, n_const=2, aux_weight=0.3)
+
+
+def make_zc_case(spec, zs, T=24, d=16, f=12, seed=0, wr_std=0.3):
+    """A case whose router covers the E FFN experts and zs.n more."""
+    rng = np.random.default_rng(seed)
+    Ep = spec.E + zs.n
+    c = make_case(spec, T=T, d=d, f=f, seed=seed, wr_std=wr_std)
+    c["w_r"] = rng.standard_normal((d, Ep)) * wr_std
+    c["beta"] = rng.standard_normal(Ep) * 0.1 if spec.bias_mode != "none" else None
+    c["v"] = rng.standard_normal((zs.n_const, d))
+    c["wc"] = rng.standard_normal((zs.n_const, 2, d)) * 0.4
+    return c
+
+
+def run_zc(spec, zs, c, coef=0.0):
+    zc = (zs, c["v"], c["wc"])
+    fwd = layer_forward(spec, c["x"], c["w_r"], c["beta"], efn(c), c["shared"], aux_coef=coef, zc=zc)
+    bwd = layer_backward(spec, c["x"], c["w_r"], c["beta"], efn(c), fwd, c["dy"], c["shared"], zc=zc)
+    return fwd, bwd
+
+
+def test_zc_maps_give_rows_to_ffn_slots_only():
+    """Slots of experts >= E get no row; the FFN slots are laid out as the
+    library stable sort by (expert, token) of the FFN slots alone."""
+    rng = np.random.default_rng(21)
+    T, E, Z, k = 150, 9, 5, 4
+    idx = np.stack([rng.permutation(E + Z)[:k] for _ in range(T)])
+    mp = sort_maps(idx, E)
+    flat = idx.reshape(-1)
+    ffn = flat < E
+    assert np.array_equal(mp["row_of"].reshape(-1) < 0, ~ffn)
+    t_of = np.repeat(np.arange(T), k)[ffn]
+    s_of = np.tile(np.arange(k), T)[ffn]
+    order = np.lexsort((t_of, flat[ffn]))
+    assert mp["token_of"].tolist() == (t_of[order] * k + s_of[order]).tolist()
+    assert mp["counts"].tolist() == np.bincount(flat[ffn], minlength=E).tolist()
+    assert mp["offsets"][E] == ffn.sum()
+
+
+def torch_zc_loss(spec, zs, c, params, coef):
+    """Independent dense formulation: every expert of the pool evaluated for
+    every token, the gate a masked softmax over the pool; returns
+    sum <dy, y> + the weighted balance loss, and the selection."""
+    x, w_r = params["x"], params["w_r"]
+    l = x @ w_r
+    T, Ep = l.shape
+    E = spec.E
+    key = l
+    sel = torch.topk(key.detach(), spec.k, dim=1).indices
+    mask = torch.zeros(T, Ep, dtype=torch.bool).scatter(1, sel, True)
+    gate = torch.softmax(l.masked_fill(~mask, float("-inf")), dim=1)
+    outs = []
+    for e in range(E):
+        g = x @ params["wg"][e]
+        u = x @ params["wu"][e]
+        outs.append((torch.nn.functional.silu(g) * u) @ params["wd"][e])
+    outs += [torch.zeros_like(x)] * zs.n_zero + [x] * zs.n_copy
+    for ci in range(zs.n_const):
+        a = torch.softmax(x @ params["wc"][ci].T, dim=1)          # [T][2]
+        outs.append(a[:, :1] * x + a[:, 1:] * params["v"][ci])
+    y = sum(gate[:, e:e + 1] * outs[e] for e in range(Ep))
+    loss = (torch.tensor(c["dy"]) * y).sum()
+    if coef:
+        cnt = torch.zeros(Ep, dtype=torch.float64).index_add_(
+            0, sel.reshape(-1), torch.ones(T * spec.k, dtype=torch.float64))
+        eta = torch.cat([torch.ones(E, dtype=torch.float64),
+                         torch.full((zs.n,), zs.aux_weight, dtype=torch.float64)])
+        loss = loss + coef * Ep * (eta * cnt / (T * spec.k) * torch.softmax(l, dim=1).mean(0)).sum()
+    return loss, sel
+
+
+@pytest.mark.parametrize("coef", [0.0, 0.4])
+def test_zc_layer_matches_torch_autograd(coef):
+    spec = RouterSpec("softmax_topk", E=6, k=3)
+    c = make_zc_case(spec, ZC, seed=22, wr_std=0.6)
+    fwd, bwd = run_zc(spec, ZC, c, coef)
+    idx = fwd["route"]["topk_idx"]
+    assert (idx >= spec.E).sum() >= 10 and (idx < spec.E).sum() >= 10   # both kinds exercised
+    for z in range(spec.E, spec.E + ZC.n):
+        assert (idx == z).any(), z
+    params = {n: torch.tensor(c[n], dtype=torch.float64, requires_grad=True)
+              for n in ("x", "w_r", "wg", "wu", "wd", "v", "wc")}
+    loss, sel = torch_zc_loss(spec, ZC, c, params, coef)
+    loss.backward()
+    assert [sorted(r) for r in sel.tolist()] == [sorted(r) for r in idx.tolist()]
+    ours = float((c["dy"] * fwd["y"]).sum()) + (fwd["aux"]["loss"] if coef else 0.0)
+    assert abs(loss.item() - ours) <= 1e-12 * abs(loss.item())
+    assert rel(bwd["dx"], params["x"].grad.numpy()) < 1e-11
+    assert rel(bwd["dw_r"], params["w_r"].grad.numpy()) < 1e-11
+    assert rel(bwd["zc"]["dv"], params["v"].grad.numpy()) < 1e-11
+    assert rel(bwd["zc"]["dwc"], params["wc"].grad.numpy()) < 1e-11
+    for e in range(spec.E):
+        for o_, t_ in (("dw_gate", "wg"), ("dw_up", "wu"), ("dw_down", "wd")):
+            want = params[t_].grad[e].numpy()
+            if np.linalg.norm(want) == 0:
+                assert np.linalg.norm(bwd["experts"][e][o_]) == 0
+            else:
+                assert rel(bwd["experts"][e][o_], want) < 1e-11
+
+
+def test_zc_gradients_match_finite_differences():
+    spec = RouterSpec("topk_softmax", E=5, k=2, bias_mode="logit")
+    zs = ZeroComputeSpec(n_zero=1, n_copy=2, n_const=2, aux_weight=0.0)
+    c = make_zc_case(spec, zs, T=14, d=8, f=6, seed=23, wr_std=0.7)
+    coef = 0.6
+    fwd, bwd = run_zc(spec, zs, c, coef)
+    assert (fwd["route"]["topk_idx"] >= spec.E).sum() >= 6
+
+    def total(cc):
+        fw = layer_forward(spec, cc["x"], cc["w_r"], cc["beta"], efn(cc), None, aux_coef=coef,
+                           zc=(zs, cc["v"], cc["wc"]))
+        return float((cc["dy"] * fw["y"]).sum()) + fw["aux"]["loss"], fw["route"]["topk_idx"]
+
+    rng = np.random.default_rng(7)
+    h = 1e-6
+    grads = {"x": bwd["dx"], "w_r": bwd["dw_r"], "v": bwd["zc"]["dv"], "wc": bwd["zc"]["dwc"],
+             "wd": np.stack([bwd["experts"][e]["dw_down"] for e in range(spec.E)])}
+    checked = 0
+    for key, gr in grads.items():
+        for _ in range(3):
+            v = rng.standard_normal(c[key].shape)
+            v /= np.linalg.norm(v)
+            lp, ip = total(dict(c, **{key: c[key] + h * v}))
+            lm, im = total(dict(c, **{key: c[key] - h * v}))
+            if not (np.array_equal(ip, fwd["route"]["topk_idx"]) and np.array_equal(im, fwd["route"]["topk_idx"])):
+                continue
+            fd = (lp - lm) / (2 * h)
+            an = float((gr * v).sum())
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (key, fd, an)
+            checked += 1
+    assert checked >= 12
+
+
+def test_zc_omega_is_the_derivative_in_the_gate_weight():
+    """y_zc is linear in each gating weight, so a unit step of w[t][s] changes
+    sum <dy, y_zc> by exactly omega[t][s]."""
+    rng = np.random.default_rng(24)
+    T, d, E, k = 7, 10, 3, 3
+    zs = ZeroComputeSpec(n_zero=1, n_copy=1, n_const=2)
+    idx = np.stack([rng.permutation(E + zs.n)[:k] for _ in range(T)])
+    w = rng.random((T, k))
+    x, dy = rng.standard_normal((T, d)), rng.standard_normal((T, d))
+    v, wc = rng.standard_normal((2, d)), rng.standard_normal((2, 2, d))
+    base = float((dy * zc_forward(x, idx, w, E, zs, v, wc)["y"]).sum())
+    om = zc_backward(dy, x, idx, w, E, zs, v, wc)["omega"]
+    for t in range(T):
+        for s in range(k):
+            w2 = w.copy()
+            w2[t, s] += 1.0
+            step = float((dy * zc_forward(x, idx, w2, E, zs, v, wc)["y"]).sum()) - base
+            assert step == pytest.approx(om[t, s], rel=1e-12, abs=1e-12)
+            if idx[t, s] < E + zs.n_zero:            # FFN (handled elsewhere) or zero expert
+                assert om[t, s] == 0.0
+
+
+def _forced_case(kind, zs, T=9, d=12):
+    """Router weights that send every token to k experts of one kind."""
+    spec = RouterSpec("softmax_topk", E=4, k=2)
+    c = make_zc_case(spec, zs, T=T, d=d, seed=25)
+    first = {"zero": spec.E, "copy": spec.E + zs.n_zero, "const": spec.E + zs.n_zero + zs.n_copy}[kind]
+    c["w_r"][:, :] = 0.0
+    c["beta"] = None
+    c["x"][:, 0] = np.abs(c["x"][:, 0]) + 1.0
+    c["w_r"][0, first] = 40.0
+    c["w_r"][0, first + 1] = 39.0
+    return spec, c
+
+
+def test_zc_all_copy_is_identity():
+    """Both slots on copy experts: y = x (the weights sum to one), and the
+    router gradient vanishes (equal omega on both slots), so dx = dy."""
+    zs = ZeroComputeSpec(n_zero=1, n_copy=2, n_const=1)
+    spec, c = _forced_case("copy", zs)
+    fwd, bwd = run_zc(spec, zs, c)
+    assert np.all(fwd["route"]["topk_idx"] >= spec.E + 1)
+    np.testing.assert_allclose(fwd["y"], c["x"], rtol=1e-14, atol=1e-14)
+    np.testing.assert_allclose(bwd["dx"], c["dy"], rtol=1e-12, atol=1e-12)
+    assert np.abs(bwd["dw_r"]).max() < 1e-12
+    assert all(np.abs(g["dw_gate"]).max() == 0 for g in bwd["experts"].values())
+
+
+def test_zc_all_zero_is_zero():
+    zs = ZeroComputeSpec(n_zero=2, n_copy=0, n_const=1)
+    spec, c = _forced_case("zero", zs)
+    fwd, bwd = run_zc(spec, zs, c)
+    assert np.all(fwd["y"] == 0.0)
+    assert np.all(bwd["dx"] == 0.0) and np.all(bwd["dw_r"] == 0.0)
+    assert np.all(bwd["zc"]["dv"] == 0.0) and np.all(bwd["zc"]["dwc"] == 0.0)
+
+
+def test_zc_constant_with_zero_projection_is_the_mean():
+    """W_c = 0: the two mixing weights are 1/2, so a constant expert returns
+    (x + v) / 2; with both slots on constant experts y = (x + w1 v1 + w2 v2) / 2."""
+    zs = ZeroComputeSpec(n_zero=0, n_copy=0, n_const=2)
+    spec, c = _forced_case("const", zs)
+    c["wc"][:] = 0.0
+    fwd, _ = run_zc(spec, zs, c)
+    w = fwd["route"]["topk_w"]
+    idx = fwd["route"]["topk_idx"] - spec.E
+    want = 0.5 * (c["x"] + w[:, :1] * c["v"][idx[:, 0]] + w[:, 1:] * c["v"][idx[:, 1]])
+    np.testing.assert_allclose(fwd["y"], want, rtol=1e-13, atol=1e-13)
+
+
+def test_zc_aux_weight_one_is_the_plain_pool_loss_and_zero_drops_the_terms():
+    """aux_weight = 1: the loss over the pool of E + Z experts; aux_weight = 0:
+    the same loss with every zero-computation expert's term removed (checked
+    by moving all their load onto them: the loss is then 0)."""
+    spec = RouterSpec("softmax_topk", E=4, k=2)
+    rng = np.random.default_rng(26)
+    p = router_probs(spec, rng.standard_normal((11, 7)))
+    counts = np.array([3, 5, 0, 2, 4, 6, 2])
+    base = aux_loss(spec, p, counts, 0.2)
+    one = aux_loss(spec, p, counts, 0.2, eta=np.ones(7))
+    assert one["loss"] == base["loss"]
+    only_zc = np.array([0, 0, 0, 0, 7, 8, 7])
+    assert aux_loss(spec, p, only_zc, 0.2, eta=[1, 1, 1, 1, 0, 0, 0])["loss"] == 0.0
+    dl = aux_loss_backward(p, only_zc / 22.0, 0.2, eta=[1, 1, 1, 1, 0, 0, 0])
+    assert np.all(dl == 0.0)
+
+
+def test_zc_token_subset_equals_whole_layer():
+    """The per-token evaluation used at full size gives the whole layer's y,
+    dx, omega and dl with zero-computation experts in the pool, and the
+    dW_r column of a zero-computation expert from the tokens that chose it."""
+    spec = RouterSpec("softmax_topk", E=6, k=3)
+    c = make_zc_case(spec, ZC, T=40, seed=27, wr_std=0.6)
+    fwd, bwd = run_zc(spec, ZC, c)
+    zc = (ZC, c["v"], c["wc"])
+    sub = np.array([39, 3, 17, 0, 22, 5, 30])
+    r = token_forward_backward(spec, c["x"][sub], c["dy"][sub], c["w_r"], c["beta"], efn(c), None, zc=zc)
+    assert np.array_equal(r["route"]["topk_idx"], fwd["route"]["topk_idx"][sub])
+    assert (r["route"]["topk_idx"] >= spec.E).any() and (r["route"]["topk_idx"] == spec.E).any()
+    for a, b in ((r["y"], fwd["y"][sub]), (r["dx"], bwd["dx"][sub]), (r["omega"], bwd["omega"][sub]),
+                 (r["dl"], bwd["dl"][sub])):
+        assert rel(a, b) < 1e-12
+    for e in (spec.E, spec.E + ZC.n - 1):
+        toks = np.nonzero((fwd["route"]["topk_idx"] == e).any(axis=1))[0]
+        r = token_forward_backward(spec, c["x"][toks], c["dy"][toks], c["w_r"], c["beta"], efn(c), None, zc=zc)
+        assert rel(c["x"][toks].T @ r["dl_dense"][:, e], bwd["dw_r"][:, e]) < 1e-12
