@@ -343,9 +343,12 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
         raise ValueError("w_r must have one column per expert of the pool")
     l = router_logits(x, w_r)
     rt = route(spec, l, beta)
-    mp = sort_maps(rt["topk_idx"], E)
+    # rows over the whole pool: the FFN experts' rows come first (lower ids),
+    # a zero-computation expert's rows carry no data
+    mp = sort_maps(rt["topk_idx"], E_pool)
+    mp["row_ffn"] = np.where(rt["topk_idx"] < E, mp["row_of"], -1)
     R = T * k
-    x_perm = permute_rows(x, mp["token_of"], k)
+    x_perm = permute_rows(x, mp["token_of"][:mp["offsets"][E]], k)
     fwidth = None
     o = np.zeros((R, d))
     gs, us, hs = {}, {}, {}
@@ -362,7 +365,7 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
     if shared is not None:
         g, u, h, osh = expert_forward(x, *shared)
         sh = dict(g=g, u=u, h=h, o=osh)
-    y = combine(o, rt["topk_w"], mp["row_of"], None if sh is None else sh["o"])
+    y = combine(o, rt["topk_w"], mp["row_ffn"], None if sh is None else sh["o"])
     zf = None
     if zc is not None:
         zf = zc_forward(x, rt["topk_idx"], rt["topk_w"], E, *zc)
@@ -370,9 +373,8 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
     aux = None
     if aux_coef:
         probs = router_probs(spec, l, beta)
-        counts = np.bincount(rt["topk_idx"].reshape(-1), minlength=E_pool)
         eta = None if zc is None else zc_aux_weights(E, zc[0])
-        aux = aux_loss(spec, probs, counts, aux_coef, aux_f, eta)
+        aux = aux_loss(spec, probs, mp["counts"], aux_coef, aux_f, eta)
         aux.update(probs=probs, coef=aux_coef, eta=eta)
     return dict(logits=l, route=rt, maps=mp, x_perm=x_perm, o=o, g=gs, u=us,
                 h=hs, y=y, shared=sh, f=fwidth, aux=aux, zc=zf)
@@ -394,7 +396,7 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
     rt, mp = fwd["route"], fwd["maps"]
     w = rt["topk_w"]
     o = fwd["o"]
-    do, omega = combine_backward(dy, o, w, mp["row_of"])
+    do, omega = combine_backward(dy, o, w, mp["row_ffn"])
     zb = None
     if zc is not None:
         zb = zc_backward(dy, x, rt["topk_idx"], w, E, *zc)
@@ -419,7 +421,7 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
         ge.pop("dg")
         ge.pop("du")
         grads[e] = ge
-    dx += unpermute(dx_perm, mp["row_of"])
+    dx += unpermute(dx_perm, mp["row_ffn"])
     # router
     dl = router_backward(spec, rt, omega)
     dl_dense = np.zeros((T, E_pool))
@@ -588,7 +590,9 @@ def expert_weight_grads_at(xe, do, wg, wu, wd, bg=None, bu=None, cols=None, with
 # Pool order: the E FFN experts (ids 0 .. E-1), then n_zero zero, n_copy copy
 # and n_const constant experts.  The router is the layer's softmax router
 # over the whole pool; a slot that picks a zero-computation expert adds
-# w * out(x_t) to y_t and gets no row in the permutation.  In the balance
+# w * out(x_t) to y_t.  The permutation sorts every slot of the pool by
+# (expert, token), so the FFN experts' rows come first; a zero-computation
+# expert's rows only list its tokens (no activations are copied there).  In the balance
 # loss every zero-computation expert's term carries the weight aux_weight
 # (1: the plain loss over the pool, 0: excluded), FFN experts weight 1.
 

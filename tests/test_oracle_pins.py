@@ -613,22 +613,26 @@ def run_zc(spec, zs, c, coef=0.0):
     return fwd, bwd
 
 
-def test_zc_maps_give_rows_to_ffn_slots_only():
-    """Slots of experts >= E get no row; the FFN slots are laid out as the
-    library stable sort by (expert, token) of the FFN slots alone."""
-    rng = np.random.default_rng(21)
-    T, E, Z, k = 150, 9, 5, 4
-    idx = np.stack([rng.permutation(E + Z)[:k] for _ in range(T)])
-    mp = sort_maps(idx, E)
+def test_zc_layer_rows_cover_the_pool_with_ffn_rows_first():
+    """The layer sorts every slot of the pool by (expert, token) (the library
+    stable sort); the FFN slots hold the first offsets[E] rows, whose x_perm
+    rows are their tokens' x, and only they reach the combine."""
+    spec = RouterSpec("softmax_topk", E=6, k=3)
+    c = make_zc_case(spec, ZC, T=40, seed=21, wr_std=0.6)
+    fwd = layer_forward(spec, c["x"], c["w_r"], None, efn(c), zc=(ZC, c["v"], c["wc"]))
+    idx, mp, k = fwd["route"]["topk_idx"], fwd["maps"], spec.k
+    T, Ep = idx.shape[0], spec.E + ZC.n
     flat = idx.reshape(-1)
-    ffn = flat < E
-    assert np.array_equal(mp["row_of"].reshape(-1) < 0, ~ffn)
-    t_of = np.repeat(np.arange(T), k)[ffn]
-    s_of = np.tile(np.arange(k), T)[ffn]
-    order = np.lexsort((t_of, flat[ffn]))
+    t_of = np.repeat(np.arange(T), k)
+    s_of = np.tile(np.arange(k), T)
+    order = np.lexsort((t_of, flat))
     assert mp["token_of"].tolist() == (t_of[order] * k + s_of[order]).tolist()
-    assert mp["counts"].tolist() == np.bincount(flat[ffn], minlength=E).tolist()
-    assert mp["offsets"][E] == ffn.sum()
+    assert mp["counts"].tolist() == np.bincount(flat, minlength=Ep).tolist()
+    n_ffn = int((flat < spec.E).sum())
+    assert 0 < n_ffn < T * k and mp["offsets"][spec.E] == n_ffn
+    assert np.array_equal(mp["row_ffn"] >= 0, idx < spec.E)
+    assert np.all(mp["row_ffn"][idx < spec.E] < n_ffn)
+    assert np.array_equal(fwd["x_perm"], c["x"][mp["token_of"][:n_ffn] // k])
 
 
 def torch_zc_loss(spec, zs, c, params, coef):
