@@ -30,19 +30,29 @@ GEMM_SOURCE = os.path.join(ROOT, "paper_2605_31463_amd", "csrc", "gemm.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
-def layer_flops(cfg):
-    """Algorithmic FLOPs (2 per multiply-add): fwd = 2TdE + 6Tkdf (+ 6Td f_shared), bwd = 2 fwd."""
-    T, d, E, k, f = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["f"]
-    fwd = 2 * T * d * E + 6 * T * k * d * f
+def pool(cfg):
+    return cfg["E"] + cfg.get("n_zero", 0) + cfg.get("n_copy", 0) + cfg.get("n_const", 0)
+
+
+def layer_flops(cfg, rows=None):
+    """Algorithmic FLOPs (2 per multiply-add): fwd = 2 T d E_pool + 6 R d f (+ 6 T d f_shared),
+    bwd = 2 fwd, with R = T k rows through the FFN experts (fewer when zero-computation
+    experts take some slots: then the routed FFN rows of the batch)."""
+    T, d, k, f = cfg["T"], cfg["d"], cfg["k"], cfg["f"]
+    R = T * k if rows is None else rows
+    fwd = 2 * T * d * pool(cfg) + 6 * R * d * f
     if cfg["n_shared"]:
         fwd += 6 * T * d * cfg["f_shared"]
     return fwd, 2 * fwd
 
 
-def kernel_work(cfg):
-    """Per-launch algorithmic work of the layer's main kernels: (bound, amount, unit)."""
-    T, d, E, k, f = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["f"]
-    R = T * k
+def kernel_work(cfg, rows=None):
+    """Per-launch algorithmic work of the layer's main kernels: (bound, amount, unit).
+    rows: routed FFN rows when zero-computation experts take some slots (the GEMMs
+    and the row gathers touch only those; the counts below are then lower bounds
+    for the gathers, which also read x or dy for such slots)."""
+    T, d, E, k, f = cfg["T"], cfg["d"], pool(cfg), cfg["k"], cfg["f"]
+    R = T * k if rows is None else rows
     eb = 2 if cfg["dtype"] == "bf16" else 4
     gu = 2.0 * R * d * 2 * f
     dn = 2.0 * R * f * d
@@ -53,11 +63,11 @@ def kernel_work(cfg):
         # router logits: bf16 x times the three bf16 parts of W_r
         "route": ("mfma", 2.0 * T * d * E * 3),
         # bytes: reads + writes of the HBM operands, once each
-        "route_select": ("hbm", T * E * 8 + R * 8),
-        "scatter": ("hbm", T * d * eb + R * d * eb + R * 4 * 3),
-        "combine_fwd": ("hbm", R * d * eb + T * d * eb + R * 8),
-        "combine_bwd": ("hbm", T * d * eb + 2 * R * d * eb + R * 12),
-        "unpermute": ("hbm", R * d * eb + T * d * eb + R * 12),
+        "route_select": ("hbm", T * E * 8 + T * k * 8),
+        "scatter": ("hbm", T * d * eb + R * d * eb + T * k * 4 * 3),
+        "combine_fwd": ("hbm", R * d * eb + T * d * eb + T * k * 8),
+        "combine_bwd": ("hbm", T * d * eb + 2 * R * d * eb + T * k * 12),
+        "unpermute": ("hbm", R * d * eb + T * d * eb + T * k * 12),
     }
 
 
@@ -88,7 +98,7 @@ def cpu_baseline(cfg, seed, tokens, reps=1):
     from threadpoolctl import threadpool_info
 
     from moe_inputs import layer_inputs, variant
-    from oracle import layer_backward, layer_forward, spec_from_config
+    from oracle import ZeroComputeSpec, layer_backward, layer_forward, spec_from_config
     from moe_inputs import to_f64
 
     scfg = variant(cfg["name"].split("[")[0], T=tokens)
@@ -109,12 +119,19 @@ def cpu_baseline(cfg, seed, tokens, reps=1):
     shared = None
     if scfg["n_shared"]:
         shared = tuple(to_f64(inp[n], dt) for n in ("ws_gate", "ws_up", "ws_down"))
+    zc = None
+    if pool(scfg) > scfg["E"]:
+        nc = scfg["n_const"]
+        zc = (ZeroComputeSpec(scfg["n_zero"], scfg["n_copy"], nc, scfg["zc_aux_weight"]),
+              inp["zc_v"].astype(np.float64) if nc else np.zeros((0, scfg["d"])),
+              inp["zc_wc"].astype(np.float64) if nc else np.zeros((0, 2, scfg["d"])))
+    coef = cfg.get("aux_coef", 0.0)
     t0 = time.perf_counter()
     for _ in range(reps):
-        fwd = layer_forward(spec, x, w_r, beta, efn, shared)
-        layer_backward(spec, x, w_r, beta, efn, fwd, dy, shared, with_bias=scfg["expert_bias"])
+        fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=coef, zc=zc)
+        layer_backward(spec, x, w_r, beta, efn, fwd, dy, shared, with_bias=scfg["expert_bias"], zc=zc)
     wall = time.perf_counter() - t0
-    _, fb = layer_flops(scfg)
+    _, fb = layer_flops(scfg, rows=int(fwd["maps"]["offsets"][scfg["E"]]))
     blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
     threads = max([p.get("num_threads", 1) for p in blas] or [1])
     cpu = "unknown"
@@ -248,7 +265,7 @@ def main():
         return torch.from_numpy(a).cuda()
 
     params = {n: dev(inp.get(n)) for n in ("w_r", "router_bias", "w_gate", "w_up", "w_down", "b_gate",
-                                           "b_up", "b_down", "ws_gate", "ws_up", "ws_down")}
+                                           "b_up", "b_down", "ws_gate", "ws_up", "ws_down", "zc_v", "zc_wc")}
     x = dev(inp["x"])
     dy = dev(inp["dy"])
     del inp
@@ -263,6 +280,13 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    zc = pool(cfg) > cfg["E"]
+    # routed FFN rows (every slot when the pool holds only FFN experts)
+    ffn_rows = int(layer.saved["expert_offsets"][cfg["E"]].item()) if zc else cfg["T"] * cfg["k"]
+    if args.memory_kernels and zc:
+        print("--memory-kernels drives the component entry points, which take no zero-computation "
+              "experts", file=sys.stderr)
+        sys.exit(2)
     if args.memory_kernels:
         workload = "%s moe layer T=%d d=%d E=%d k=%d f=%d" % (cfg["name"], cfg["T"], cfg["d"], cfg["E"],
                                                              cfg["k"], cfg["f"])
@@ -280,7 +304,7 @@ def main():
         del src, dst
 
     # per-kernel times over a few untimed steps, to pick the dominant kernel
-    work = kernel_work(cfg)
+    work = kernel_work(cfg, rows=ffn_rows)
     per_kernel = {}
     for name in work:
         L.moe_timing_select(L.kernel_id(name))
@@ -324,7 +348,7 @@ def main():
     s_ms = [e[0].elapsed_time(e[2]) for e in evs][-10:]
     med = lambda v: sorted(v)[len(v) // 2]  # noqa: E731
 
-    _, fb = layer_flops(cfg)
+    _, fb = layer_flops(cfg, rows=ffn_rows)
     tflops = fb / (ms_per_step / 1e3) / 1e12
     bound, amount = work[dominant]
     dom_avg_s = dom_ms / max(dom_n, 1) / 1e3
@@ -348,8 +372,10 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dt,
         "data": "synthetic (seeded; shapes and distributions of the workload)",
-        "config": {"workload": workload, "T": cfg["T"], "d": cfg["d"], "E": cfg["E"], "k": cfg["k"],
-                   "f": cfg["f"], "router": cfg["router"], "aux_coef": cfg.get("aux_coef", 0.0)},
+        "config": dict({"workload": workload, "T": cfg["T"], "d": cfg["d"], "E": cfg["E"], "k": cfg["k"],
+                        "f": cfg["f"], "router": cfg["router"], "aux_coef": cfg.get("aux_coef", 0.0)},
+                       **({"n_zero": cfg["n_zero"], "n_copy": cfg["n_copy"], "n_const": cfg["n_const"],
+                           "zc_aux_weight": cfg["zc_aux_weight"], "ffn_rows": ffn_rows} if zc else {})),
         "tokens_per_s": round(cfg["T"] / (ms_per_step / 1e3), 1),
         "phases_median_of_last_10": {"fwd_ms": round(med(f_ms), 4), "bwd_ms": round(med(b_ms), 4),
                                      "step_ms": round(med(s_ms), 4),

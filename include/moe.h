@@ -19,17 +19,19 @@
  *     library never allocates, frees or synchronises.  Every call only
  *     enqueues work on `stream` and returns; results are ready when the
  *     stream reaches that point.  Pointers must be 16-byte aligned.
- *   - Layouts are dense row-major.  T tokens, d hidden, E routed experts,
- *     k experts per token, f expert width, R = T*k routed rows.
+ *   - Layouts are dense row-major.  T tokens, d hidden, E routed (FFN)
+ *     experts, k experts per token, f expert width, R = T*k routed rows,
+ *     E_pool = E + n_zero + n_copy + n_const experts the router chooses from
+ *     (= E without zero-computation experts).
  *       x, y, dy, dx            [T][d]        activation dtype
- *       w_r, dw_r               [d][E]        float32
- *       router_bias             [E]           float32
+ *       w_r, dw_r               [d][E_pool]   float32
+ *       router_bias             [E_pool]      float32
  *       w_gate, w_up            [E][d][f]     activation dtype
  *       w_down                  [E][f][d]     activation dtype
  *       b_gate, b_up            [E][f];  b_down [E][d]
  *       topk_idx, row_of        [T][k]        int32
  *       topk_w, s_sel, d_topk_w [T][k]        float32
- *       expert_offsets          [E+1]         int32 (exclusive scan of counts)
+ *       expert_offsets          [E_pool+1]    int32 (exclusive scan of counts)
  *       token_of                [R]           int32 (= t*k + slot)
  *       x_perm, o, d_o, dx_perm [R][d]        activation dtype
  *       gu, dgu                 [R][2f]       columns [0,f) gate, [f,2f) up
@@ -40,7 +42,10 @@
  *   - Slot order: topk_idx[t][0..k-1] lists the chosen experts by
  *     descending selection key, equal keys to the lower expert index.
  *     Rows of expert e are expert_offsets[e] .. expert_offsets[e+1]-1, in
- *     ascending token order; row_of[t][s] is the row of (t, s).
+ *     ascending token order; row_of[t][s] is the row of (t, s).  Every slot
+ *     has a row; the rows of zero-computation experts (ids >= E, after the
+ *     FFN experts' rows) only list their tokens: x_perm, gu, h, o, d_o and
+ *     dx_perm hold nothing there.
  *   - Results are bitwise reproducible run to run: no floating-point atomics.
  *   - Gradients overwrite their outputs (no accumulation).
  *   - Return value: MOE_OK or a negative MOE_ERR_* code.  Argument checks run
@@ -49,8 +54,20 @@
  *   - T = 0 is valid: token outputs are empty, counts/offsets and gradients
  *     are written as zeros.
  *
- * Limits (MOE_ERR_UNSUPPORTED beyond them): 1 <= E <= 256, 1 <= k <= 16,
- * d and f multiples of 64, d <= 16384, renorm = 1.
+ * Limits (MOE_ERR_UNSUPPORTED beyond them): 1 <= E <= E_pool <= 256,
+ * 1 <= k <= 16, d and f multiples of 64, d <= 16384, renorm = 1.
+ *
+ * Zero-computation experts (MoE++; appendix B.3 of the paper lists it among
+ * the new-feature tasks: zero, copy and constant experts in the pool, the
+ * router widened over them, the balance loss treating them explicitly).
+ * Pool ids E .. E+n_zero-1 are zero experts (output 0), the next n_copy copy
+ * experts (output x_t), the next n_const constant experts (output
+ * a0 x_t + a1 v_c, (a0, a1) = softmax(W_c x_t), parameters zc_v [n_const][d]
+ * and zc_wc [n_const][2][d], float32).  A slot that picks one adds
+ * w * output to y_t and runs no GEMM.  Only the softmax routers support them,
+ * and only through the layer entry points (moe_combine_fwd, moe_combine_bwd
+ * and moe_unpermute_bwd refuse such shapes with MOE_ERR_UNSUPPORTED; route,
+ * permute, grouped GEMMs and route backward work on the pool as documented).
  */
 #ifndef MOE_H
 #define MOE_H
@@ -110,12 +127,18 @@ typedef struct moe_shape {
   float aux_coef;              /* > 0: the layer entry points add the global-level
                                   load-balancing loss of this coefficient (softmax
                                   routers); 0: none */
+  int32_t n_zero;              /* zero-computation experts in the pool: zero, */
+  int32_t n_copy;              /*   copy */
+  int32_t n_const;             /*   and constant experts (all 0: none) */
+  float zc_aux_weight;         /* weight of a zero-computation expert's term in
+                                  the load-balancing loss (FFN experts: 1; 0
+                                  drops their terms); must be finite, >= 0 */
 } moe_shape;
 
 /* Parameters of the layer (device pointers; unused ones may be NULL). */
 typedef struct moe_params {
-  const float* w_r;            /* [d][E] */
-  const float* router_bias;    /* [E], bias_mode != NONE */
+  const float* w_r;            /* [d][E_pool] */
+  const float* router_bias;    /* [E_pool], bias_mode != NONE */
   const void* w_gate;          /* [E][d][f] */
   const void* w_up;            /* [E][d][f] */
   const void* w_down;          /* [E][f][d] */
@@ -125,9 +148,11 @@ typedef struct moe_params {
   const void* ws_gate;         /* [d][f_shared], n_shared */
   const void* ws_up;           /* [d][f_shared], n_shared */
   const void* ws_down;         /* [f_shared][d], n_shared */
-  const float* aux_f;          /* [E] expert load fractions of the whole batch for the
-                                  auxiliary loss (may be NULL: this call's routed-slot
-                                  fractions counts / (T k)) */
+  const float* aux_f;          /* [E_pool] expert load fractions of the whole batch for
+                                  the auxiliary loss (may be NULL: this call's
+                                  routed-slot fractions counts / (T k)) */
+  const float* zc_v;           /* [n_const][d] constant experts' vectors */
+  const float* zc_wc;          /* [n_const][2][d] constant experts' mixing weights */
 } moe_params;
 
 /* Tensors the forward writes and the backward reads (caller-allocated). */
@@ -135,7 +160,7 @@ typedef struct moe_saved {
   int32_t* topk_idx;           /* [T][k] */
   float* topk_w;               /* [T][k] */
   float* s_sel;                /* [T][k], SIGMOID_GROUPED only (else may be NULL) */
-  int32_t* expert_offsets;     /* [E+1] */
+  int32_t* expert_offsets;     /* [E_pool+1] */
   int32_t* row_of;             /* [T][k] */
   int32_t* token_of;           /* [R] */
   void* x_perm;                /* [R][d] */
@@ -145,13 +170,13 @@ typedef struct moe_saved {
   void* gu_sh;                 /* [T][2 f_shared], n_shared */
   void* h_sh;                  /* [T][f_shared], n_shared */
   void* o_sh;                  /* [T][d], n_shared */
-  float* router_probs;         /* [T][E] softmax over all experts, aux_coef > 0 */
+  float* router_probs;         /* [T][E_pool] softmax over all experts, aux_coef > 0 */
   float* aux_loss;             /* [1] the auxiliary loss value, aux_coef > 0 */
 } moe_saved;
 
 /* Gradients of the parameters (overwritten). */
 typedef struct moe_grads {
-  float* dw_r;                 /* [d][E] float32 */
+  float* dw_r;                 /* [d][E_pool] float32 */
   void* dw_gate;               /* [E][d][f] */
   void* dw_up;                 /* [E][d][f] */
   void* dw_down;               /* [E][f][d] */
@@ -161,6 +186,8 @@ typedef struct moe_grads {
   void* dws_gate;              /* [d][f_shared], n_shared */
   void* dws_up;                /* [d][f_shared], n_shared */
   void* dws_down;              /* [f_shared][d], n_shared */
+  float* dzc_v;                /* [n_const][d], n_const > 0 */
+  float* dzc_wc;               /* [n_const][2][d], n_const > 0 */
 } moe_grads;
 
 /* Workspace bytes.  fwd_ws: enough for moe_route, moe_permute and
@@ -175,7 +202,7 @@ int moe_workspace_size(const moe_shape* shape, size_t* fwd_ws, size_t* saved_byt
  * Logits are accumulated with float32 partial sums of 16 products folded
  * into a float64 total, and selection compares float64 keys.
  * out: topk_idx, topk_w [T][k]; s_sel [T][k] (SIGMOID_GROUPED, else may be
- * NULL); expert_counts [E] int32 (may be NULL).  ws: fwd_ws bytes. */
+ * NULL); expert_counts [E_pool] int32 (may be NULL).  ws: fwd_ws bytes. */
 int moe_route(const moe_shape* shape, const void* x, const float* w_r, const float* router_bias,
               int32_t* topk_idx, float* topk_w, float* s_sel, int32_t* expert_counts,
               void* ws, size_t ws_bytes, hipStream_t stream);
@@ -275,7 +302,10 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* params, const void* 
 
 /* Whole layer backward of L = sum_t <dy_t, y_t>: combine backward, expert
  * dgrad and wgrad, router backward, shared expert backward, unpermute.
- * dx includes the expert, router and shared-expert paths.  ws: bwd_ws bytes. */
+ * dx includes the expert, router and shared-expert paths (and the
+ * zero-computation experts': copy slots w dy_t, constant slots
+ * a0 w dy_t + W_c^T dz; their parameter gradients go to dzc_v, dzc_wc).
+ * ws: bwd_ws bytes. */
 int moe_layer_bwd(const moe_shape* shape, const moe_params* params, const void* x,
                   const moe_saved* saved, const void* dy, void* dx, const moe_grads* grads,
                   void* ws, size_t ws_bytes, hipStream_t stream);
@@ -289,11 +319,13 @@ int moe_layer_bwd(const moe_shape* shape, const moe_params* params, const void* 
  * moe_layer_bwd_dgrad: combine backward with the router's dl, expert dgrad
  *   (fused SwiGLU backward), shared-expert dgrad, unpermute -> dx (with the
  *   router and shared-expert paths).  Leaves d_o, dgu, dl (and the shared
- *   expert's dgu) in ws, which the caller must keep unchanged until the
- *   matching moe_layer_bwd_wgrad call.  Pointers of *saved read: topk_idx,
- *   topk_w, s_sel (SIGMOID_GROUPED), expert_offsets, row_of, gu, o, gu_sh.
+ *   expert's dgu, the zero-computation slots' coefficients) in ws, which the
+ *   caller must keep unchanged until the matching moe_layer_bwd_wgrad call.
+ *   Pointers of *saved read: topk_idx, topk_w, s_sel (SIGMOID_GROUPED),
+ *   expert_offsets, row_of, gu, o, gu_sh.
  * moe_layer_bwd_wgrad: expert wgrads (+ biases), dW_r, shared-expert wgrads
- *   into *grads, from what the dgrad half left in ws.  accumulate = 1 adds
+ *   and the constant experts' dzc_v, dzc_wc into *grads, from what the dgrad
+ *   half left in ws.  accumulate = 1 adds
  *   every gradient to the buffer's current value (gradient accumulation over
  *   micro-batches), 0 overwrites.  Pointers of *saved read: topk_idx,
  *   expert_offsets, token_of, x_perm, h, h_sh.

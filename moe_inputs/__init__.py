@@ -14,6 +14,7 @@ from .gen import (  # noqa: F401
     gen_expert_tensor,
     gen_expert_stack,
     layer_inputs,
+    pool_size,
     stress_router_bias,
     to_f64,
 )

@@ -15,6 +15,11 @@ those models' MoE layers on one GPU:
   4 stress    Qwen3 dims at T=32768 with a per-expert logit bias that makes the
               expert token counts follow a capped Zipf(1.2) law, 8 experts
               receive no token
+  5 moepp     Qwen3 dims with MoE++ zero-computation experts added to the pool
+              (appendix B.3 lists MoE++ among the new-feature tasks): 128 FFN
+              experts plus 8 zero, 8 copy and 16 constant experts, one
+              zero-computation expert per four FFN experts and zero : copy :
+              constant = 1 : 1 : 2 as in the MoE++ work's configurations
 
 Fields:
   T, d, E, k, f          tokens, hidden, routed experts, top-k, expert width
@@ -26,6 +31,9 @@ Fields:
   expert_bias            experts carry b_gate, b_up (f) and b_down (d)
   n_shared, f_shared     always-on shared expert and its width
   dtype                  'f32' or 'bf16' storage of x, weights, activations
+  n_zero, n_copy, n_const  zero-computation experts after the E FFN experts
+                         (the router covers E + their number)
+  zc_aux_weight          their weight in the load-balancing loss
 """
 import copy
 
@@ -33,13 +41,14 @@ import copy
 TENSOR_IDS = {
     "x": 0, "w_r": 1, "w_gate": 2, "w_up": 3, "w_down": 4,
     "b_gate": 5, "b_up": 6, "b_down": 7, "router_bias": 8, "dy": 9,
-    "ws_gate": 10, "ws_up": 11, "ws_down": 12,
+    "ws_gate": 10, "ws_up": 11, "ws_down": 12, "zc_v": 13, "zc_wc": 14,
 }
 
 _BASE = dict(
     n_groups=1, topk_groups=1, route_scale=1.0, bias_mode="none",
     expert_bias=False, n_shared=0, f_shared=0,
     x_std=1.0, w_r_std=0.02, w_std=0.02, b_std=0.02, beta_std=0.1, dy_std=1.0,
+    n_zero=0, n_copy=0, n_const=0, zc_aux_weight=1.0, zc_v_std=1.0, zc_wc_std=0.02,
 )
 
 
@@ -62,11 +71,13 @@ CONFIGS = [
     _mk(cfg_id=4, name="stress", T=32768, d=2048, E=128, k=8, f=768,
         router="softmax_topk", bias_mode="logit", dtype="bf16",
         zipf_s=1.2, n_empty=8),
+    _mk(cfg_id=5, name="moepp", T=8192, d=2048, E=128, k=8, f=768,
+        router="softmax_topk", dtype="bf16", n_zero=8, n_copy=8, n_const=16, zc_aux_weight=0.5),
 ]
 
 
 def config(name_or_id):
-    """A copy of one of the five workload configs, by name or id."""
+    """A copy of one of the workload configs, by name or id."""
     for c in CONFIGS:
         if c["name"] == name_or_id or c["cfg_id"] == name_or_id:
             return copy.deepcopy(c)

@@ -13,7 +13,8 @@ Recipe (one child stream per tensor slice):
 Distributions follow the workload statement: x ~ N(0,1), W_r ~ N(0,0.02),
 expert weights and biases ~ N(0,0.02), DeepSeek-style selection bias
 ~ N(0,0.1), upstream gradient dy ~ N(0,1) (the second argument of N is the
-standard deviation).  The stress config's logit bias is stored data (see
+standard deviation); constant zero-computation experts: v ~ N(0,1),
+W_c ~ N(0,0.02), both float32.  The stress config's logit bias is stored data (see
 ``stress_router_bias``).
 """
 import os
@@ -148,11 +149,16 @@ def stress_router_bias(cfg):
     return b
 
 
+def pool_size(cfg):
+    """Experts the router covers: E plus any zero-computation experts."""
+    return cfg["E"] + cfg.get("n_zero", 0) + cfg.get("n_copy", 0) + cfg.get("n_const", 0)
+
+
 def router_bias(seed, cfg):
     if cfg["bias_mode"] == "none":
         return None
     if cfg["bias_mode"] == "select":
-        return _draw(seed, cfg["cfg_id"], "router_bias", 0, (cfg["E"],), cfg["beta_std"])
+        return _draw(seed, cfg["cfg_id"], "router_bias", 0, (pool_size(cfg),), cfg["beta_std"])
     if cfg["bias_mode"] == "logit":
         return stress_router_bias(cfg)
     raise ValueError(cfg["bias_mode"])
@@ -161,16 +167,17 @@ def router_bias(seed, cfg):
 def layer_inputs(cfg, seed=0, experts=True, with_dy=True, threads=None):
     """Every input of one layer forward+backward, in storage format.
 
-    Returns a dict: x [T][d], w_r [d][E] (f32), router_bias [E] (f32 or None),
+    Returns a dict: x [T][d], w_r [d][E_pool] (f32), router_bias [E_pool] (f32 or None),
     w_gate/w_up [E][d][f], w_down [E][f][d], b_gate/b_up [E][f] and
     b_down [E][d] (or None), ws_gate/ws_up [d][fs], ws_down [fs][d] (or None),
-    dy [T][d].  bf16 tensors are uint16 bit patterns.  With experts=False the
+    dy [T][d], and with constant experts zc_v [n_const][d], zc_wc [n_const][2][d]
+    (f32).  bf16 tensors are uint16 bit patterns.  With experts=False the
     per-expert stacks are omitted (generate them with gen_expert_stack).
     """
     T, d, E, dt = cfg["T"], cfg["d"], cfg["E"], cfg["dtype"]
     out = {"cfg": cfg, "seed": seed}
     out["x"] = gen_rows(seed, cfg, "x", T, d, cfg["x_std"], dt, threads)
-    out["w_r"] = _draw(seed, cfg["cfg_id"], "w_r", 0, (d, E), cfg["w_r_std"])
+    out["w_r"] = _draw(seed, cfg["cfg_id"], "w_r", 0, (d, pool_size(cfg)), cfg["w_r_std"])
     out["router_bias"] = router_bias(seed, cfg)
     if experts:
         for t in ("w_gate", "w_up", "w_down"):
@@ -184,6 +191,9 @@ def layer_inputs(cfg, seed=0, experts=True, with_dy=True, threads=None):
         out["ws_down"] = gen_tensor(seed, cfg, "ws_down", (fs, d), cfg["w_std"], dt)
     else:
         out["ws_gate"] = out["ws_up"] = out["ws_down"] = None
+    nc = cfg.get("n_const", 0)
+    out["zc_v"] = _draw(seed, cfg["cfg_id"], "zc_v", 0, (nc, d), cfg["zc_v_std"]) if nc else None
+    out["zc_wc"] = _draw(seed, cfg["cfg_id"], "zc_wc", 0, (nc, 2, d), cfg["zc_wc_std"]) if nc else None
     if with_dy:
         out["dy"] = gen_rows(seed, cfg, "dy", T, d, cfg["dy_std"], dt, threads)
     return out

@@ -50,6 +50,8 @@ class moe_shape(ctypes.Structure):
         ("route_scale", ctypes.c_float), ("bias_mode", ctypes.c_int32),
         ("expert_bias", ctypes.c_int32), ("dtype", ctypes.c_int32),
         ("aux_coef", ctypes.c_float),
+        ("n_zero", ctypes.c_int32), ("n_copy", ctypes.c_int32), ("n_const", ctypes.c_int32),
+        ("zc_aux_weight", ctypes.c_float),
     ]
 
 
@@ -58,7 +60,8 @@ _VP = ctypes.c_void_p
 
 class moe_params(ctypes.Structure):
     _fields_ = [(n, _VP) for n in ("w_r", "router_bias", "w_gate", "w_up", "w_down", "b_gate",
-                                   "b_up", "b_down", "ws_gate", "ws_up", "ws_down", "aux_f")]
+                                   "b_up", "b_down", "ws_gate", "ws_up", "ws_down", "aux_f",
+                                   "zc_v", "zc_wc")]
 
 
 class moe_saved(ctypes.Structure):
@@ -69,7 +72,7 @@ class moe_saved(ctypes.Structure):
 
 class moe_grads(ctypes.Structure):
     _fields_ = [(n, _VP) for n in ("dw_r", "dw_gate", "dw_up", "dw_down", "db_gate", "db_up",
-                                   "db_down", "dws_gate", "dws_up", "dws_down")]
+                                   "db_down", "dws_gate", "dws_up", "dws_down", "dzc_v", "dzc_wc")]
 
 
 def _load():
@@ -155,11 +158,17 @@ def _stream(stream):
 
 def make_shape(T, d, E, k, f, router="softmax_topk", n_groups=1, topk_groups=1, n_shared=0,
                f_shared=0, route_scale=1.0, bias_mode="none", expert_bias=False, dtype="bf16",
-               renorm=1, aux_coef=0.0):
+               renorm=1, aux_coef=0.0, n_zero=0, n_copy=0, n_const=0, zc_aux_weight=1.0):
     return moe_shape(T=T, d=d, E=E, k=k, f=f, n_groups=n_groups, topk_groups=topk_groups,
                      n_shared=n_shared, f_shared=f_shared, router=ROUTERS[router], renorm=renorm,
                      route_scale=route_scale, bias_mode=BIAS_MODES[bias_mode],
-                     expert_bias=int(bool(expert_bias)), dtype=DTYPES[dtype], aux_coef=aux_coef)
+                     expert_bias=int(bool(expert_bias)), dtype=DTYPES[dtype], aux_coef=aux_coef,
+                     n_zero=n_zero, n_copy=n_copy, n_const=n_const, zc_aux_weight=zc_aux_weight)
+
+
+def pool_size(shape):
+    """Experts the router chooses from: E plus the zero-computation experts."""
+    return shape.E + shape.n_zero + shape.n_copy + shape.n_const
 
 
 def shape_from_config(cfg, T=None):
@@ -168,7 +177,9 @@ def shape_from_config(cfg, T=None):
                       topk_groups=cfg["topk_groups"], n_shared=cfg["n_shared"],
                       f_shared=cfg["f_shared"], route_scale=cfg["route_scale"],
                       bias_mode=cfg["bias_mode"], expert_bias=cfg["expert_bias"],
-                      dtype=cfg["dtype"], aux_coef=cfg.get("aux_coef", 0.0))
+                      dtype=cfg["dtype"], aux_coef=cfg.get("aux_coef", 0.0),
+                      n_zero=cfg.get("n_zero", 0), n_copy=cfg.get("n_copy", 0),
+                      n_const=cfg.get("n_const", 0), zc_aux_weight=cfg.get("zc_aux_weight", 1.0))
 
 
 # ---------------------------------------------------------------------------

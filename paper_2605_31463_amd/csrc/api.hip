@@ -78,7 +78,7 @@ const char* kernel_name(int id) {
       "combine_fwd", "combine_bwd", "route_dl", "route_dwr_partial", "route_dwr_reduce",
       "wr_transpose", "route_dx", "gemm_down_dgrad", "gemm_gateup_dgrad", "gemm_down_wgrad",
       "gemm_gateup_wgrad", "unpermute", "rank", "wr_split", "route_select", "aux_stats", "aux_grad",
-      "aux_dwr"};
+      "aux_dwr", "zc_param_partial", "zc_param_reduce"};
   if (id < 0 || id >= K_NUM_KERNELS) return nullptr;
   return names[id];
 }
@@ -91,13 +91,26 @@ namespace {
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// Experts the router chooses from: the E FFN experts and any zero-computation
+// experts after them.
+inline int64_t epool(const moe_shape& s) { return s.E + s.n_zero + s.n_copy + s.n_const; }
+inline bool has_zc(const moe_shape& s) { return s.n_zero + s.n_copy + s.n_const > 0; }
+
 int check_shape(const moe_shape* sh) {
   if (!sh) return moe_set_error(MOE_ERR_INVALID_ARG, "shape is NULL");
   const moe_shape& s = *sh;
+  if (s.n_zero < 0 || s.n_copy < 0 || s.n_const < 0)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "negative zero-computation expert count");
+  if (!(s.zc_aux_weight >= 0.f) || !isfinite(s.zc_aux_weight))
+    return moe_set_error(MOE_ERR_INVALID_ARG, "zc_aux_weight must be finite and non-negative");
+  if (has_zc(s) && s.router == MOE_ROUTER_SIGMOID_GROUPED)
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "zero-computation experts need a softmax router");
   if (s.T < 0 || s.d <= 0 || s.E <= 0 || s.k <= 0 || s.f <= 0)
     return moe_set_error(MOE_ERR_INVALID_ARG, "sizes must be positive (T >= 0): T=%lld d=%lld E=%lld k=%lld f=%lld",
                          (long long)s.T, (long long)s.d, (long long)s.E, (long long)s.k, (long long)s.f);
-  if (s.k > s.E) return moe_set_error(MOE_ERR_INVALID_ARG, "k=%lld exceeds E=%lld", (long long)s.k, (long long)s.E);
+  if (s.k > epool(s))
+    return moe_set_error(MOE_ERR_INVALID_ARG, "k=%lld exceeds the %lld experts of the pool", (long long)s.k,
+                         (long long)epool(s));
   if (s.router < MOE_ROUTER_SOFTMAX_TOPK || s.router > MOE_ROUTER_SIGMOID_GROUPED)
     return moe_set_error(MOE_ERR_INVALID_ARG, "unknown router %d", s.router);
   if (s.bias_mode < MOE_BIAS_NONE || s.bias_mode > MOE_BIAS_LOGIT)
@@ -123,7 +136,7 @@ int check_shape(const moe_shape* sh) {
     return moe_set_error(MOE_ERR_INVALID_ARG, "aux_coef must be finite and non-negative");
   if (s.aux_coef > 0.f && s.router == MOE_ROUTER_SIGMOID_GROUPED)
     return moe_set_error(MOE_ERR_UNSUPPORTED, "the auxiliary loss is defined for the softmax routers");
-  if (s.E > 256) return moe_set_error(MOE_ERR_UNSUPPORTED, "E=%lld above 256", (long long)s.E);
+  if (epool(s) > 256) return moe_set_error(MOE_ERR_UNSUPPORTED, "E_pool=%lld above 256", (long long)epool(s));
   if (s.k > 16) return moe_set_error(MOE_ERR_UNSUPPORTED, "k=%lld above 16", (long long)s.k);
   if (s.d % 64 || s.f % 64 || (s.n_shared && s.f_shared % 64))
     return moe_set_error(MOE_ERR_UNSUPPORTED, "d, f and f_shared must be multiples of 64");
@@ -149,6 +162,7 @@ struct Plan {
   // backward
   size_t d_o, dgu, dx_perm, dl, partial, w_rt, dgu_sh, dx_sh;
   size_t aux_dl, aux_dx, aux_off, aux_wpart;
+  size_t zc_coef, zc_part;
   size_t bwd_total;
   size_t saved_total;
 };
@@ -157,7 +171,7 @@ struct Plan {
 // product), tokens in at most 256 chunks of a multiple of 256 rows (the groups
 // of the dW_r product).
 inline bool has_aux(const moe_shape& s) { return s.aux_coef > 0.f; }
-inline int aux_epad(const moe_shape& s) { return (int)((s.E + 63) / 64 * 64); }
+inline int aux_epad(const moe_shape& s) { return (int)((epool(s) + 63) / 64 * 64); }
 inline int64_t aux_chunk(const moe_shape& s) { return 256 * ((s.T + 256 * 256 - 1) / (256 * 256)); }
 inline int aux_groups(const moe_shape& s) { return s.T > 0 ? (int)((s.T + aux_chunk(s) - 1) / aux_chunk(s)) : 0; }
 
@@ -166,22 +180,23 @@ Plan plan(const moe_shape& s) {
   const size_t eb = act_bytes(s);
   const int64_t R = s.T * s.k;
   size_t off = 0;
+  const int64_t Ep = epool(s);
   p.hist = off;
-  off += align_up((size_t)moe::perm_blocks(s.T) * s.E * 4);
+  off += align_up((size_t)moe::perm_blocks(s.T) * Ep * 4);
   p.wsplit = off;
-  off += s.dtype == MOE_BF16 ? align_up((size_t)3 * s.E * s.d * 2) : 0;
+  off += s.dtype == MOE_BF16 ? align_up((size_t)3 * Ep * s.d * 2) : 0;
   p.lg = off;
-  off += s.dtype == MOE_BF16 ? align_up((size_t)s.T * s.E * 8) : 0;
+  off += s.dtype == MOE_BF16 ? align_up((size_t)s.T * Ep * 8) : 0;
   p.aux_part = off;
-  off += has_aux(s) ? align_up((size_t)aux_blocks(s.T) * s.E * 8) : 0;
+  off += has_aux(s) ? align_up((size_t)aux_blocks(s.T) * Ep * 8) : 0;
   p.fwd_total = off;
   off = 0;
   p.d_o = off; off += align_up((size_t)R * s.d * eb);
   p.dgu = off; off += align_up((size_t)R * 2 * s.f * eb);
   p.dx_perm = off; off += align_up((size_t)R * s.d * eb);
   p.dl = off; off += align_up((size_t)R * 4);
-  p.partial = off; off += align_up((size_t)moe::route_dwr_tasks(R, s.E) * s.d * 4);
-  p.w_rt = off; off += align_up((size_t)(has_aux(s) ? aux_epad(s) : s.E) * s.d * 4);
+  p.partial = off; off += align_up((size_t)moe::route_dwr_tasks(R, Ep) * s.d * 4);
+  p.w_rt = off; off += align_up((size_t)(has_aux(s) ? aux_epad(s) : Ep) * s.d * 4);
   p.dgu_sh = off; off += s.n_shared ? align_up((size_t)s.T * 2 * s.f_shared * eb) : 0;
   p.dx_sh = off; off += s.n_shared ? align_up((size_t)s.T * s.d * eb) : 0;
   const bool aux = has_aux(s);
@@ -189,13 +204,15 @@ Plan plan(const moe_shape& s) {
   p.aux_dx = off; off += aux ? align_up((size_t)s.T * s.d * eb) : 0;
   p.aux_off = off; off += aux ? align_up((size_t)(aux_groups(s) + 1) * 4) : 0;
   p.aux_wpart = off; off += aux ? align_up((size_t)aux_groups(s) * s.d * aux_epad(s) * eb) : 0;
+  p.zc_coef = off; off += has_zc(s) ? align_up((size_t)R * 16) : 0;
+  p.zc_part = off; off += s.n_const > 0 ? align_up((size_t)moe::route_dwr_tasks(R, s.n_const) * 3 * s.d * 4) : 0;
   p.bwd_total = off;
   size_t sv = 0;
   sv += (size_t)R * (4 + 4 + 4 + 4 + 4);  // topk_idx, topk_w, s_sel, row_of, token_of
-  sv += (size_t)(s.E + 1) * 4;
+  sv += (size_t)(Ep + 1) * 4;
   sv += (size_t)R * (s.d + 2 * s.f + s.f + s.d) * eb;
   if (s.n_shared) sv += (size_t)s.T * (2 * s.f_shared + s.f_shared + s.d) * eb;
-  if (has_aux(s)) sv += (size_t)s.T * s.E * 4 + 4;
+  if (has_aux(s)) sv += (size_t)s.T * Ep * 4 + 4;
   p.saved_total = sv;
   return p;
 }
@@ -253,7 +270,7 @@ int do_route(const moe_shape& s, const void* x, const float* w_r, const float* b
   a.bias = bias;
   a.T = s.T;
   a.d = (int)s.d;
-  a.E = (int)s.E;
+  a.E = (int)epool(s);
   a.k = (int)s.k;
   a.router = s.router;
   a.bias_mode = s.bias_mode;
@@ -275,7 +292,8 @@ int do_permute(const moe_shape& s, const void* x, const int32_t* topk_idx, int32
   a.topk_idx = topk_idx;
   a.T = s.T;
   a.d = (int)s.d;
-  a.E = (int)s.E;
+  a.E = (int)epool(s);
+  a.E_rows = (int)s.E;
   a.k = (int)s.k;
   a.bf16 = s.dtype == MOE_BF16;
   a.hist = reinterpret_cast<int32_t*>(wsp(ws, plan(s).hist));
@@ -409,18 +427,36 @@ AuxArgs aux_args(const moe_shape& s, const moe_params* prm, const moe_saved* sv)
   a.offsets = sv->expert_offsets;
   a.aux_f = prm->aux_f;
   a.T = s.T;
-  a.E = (int)s.E;
+  a.E = (int)epool(s);
   a.k = (int)s.k;
   a.coef = s.aux_coef;
+  a.E_ffn = has_zc(s) ? (int)s.E : (int)epool(s);
+  a.zc_weight = s.zc_aux_weight;
   a.loss = sv->aux_loss;
   return a;
+}
+
+// Zero-computation experts' arguments of the gather-side kernels.
+ZcArgs zc_args(const moe_shape& s, const moe_params* prm, const void* x, const void* dy, void* coef) {
+  ZcArgs z{};
+  z.on = has_zc(s);
+  z.E_ffn = (int)s.E;
+  z.n_zero = s.n_zero;
+  z.n_copy = s.n_copy;
+  z.n_const = s.n_const;
+  z.x = x;
+  z.v = prm->zc_v;
+  z.wc = prm->zc_wc;
+  z.coef = reinterpret_cast<float4*>(coef);
+  z.dy = dy;
+  return z;
 }
 
 RouteBwdArgs route_bwd_base(const moe_shape& s) {
   RouteBwdArgs a{};
   a.T = s.T;
   a.d = (int)s.d;
-  a.E = (int)s.E;
+  a.E = (int)epool(s);
   a.k = (int)s.k;
   a.router = s.router;
   a.route_scale = s.route_scale;
@@ -434,10 +470,11 @@ RouteBwdArgs route_bwd_base(const moe_shape& s) {
 using namespace moe;
 
 // The Python binding mirrors these layouts field by field.
-static_assert(sizeof(moe_shape) == 96 && offsetof(moe_shape, f_shared) == 56 && offsetof(moe_shape, aux_coef) == 88,
+static_assert(sizeof(moe_shape) == 112 && offsetof(moe_shape, f_shared) == 56 &&
+                  offsetof(moe_shape, aux_coef) == 88 && offsetof(moe_shape, zc_aux_weight) == 104,
               "moe_shape layout");
-static_assert(sizeof(moe_params) == 12 * sizeof(void*) && sizeof(moe_saved) == 15 * sizeof(void*) &&
-                  sizeof(moe_grads) == 10 * sizeof(void*),
+static_assert(sizeof(moe_params) == 14 * sizeof(void*) && sizeof(moe_saved) == 15 * sizeof(void*) &&
+                  sizeof(moe_grads) == 12 * sizeof(void*),
               "pointer struct layouts");
 
 // ---------------------------------------------------------------------------
@@ -452,6 +489,15 @@ int check_layer_bwd(const moe_shape& s, const moe_params* prm, const void* x, co
   MOE_NEED(sv, "saved");
   MOE_NEED(prm->w_r, "params.w_r");
   MOE_NEED(sv->expert_offsets, "saved.expert_offsets");
+  if (s.n_const > 0 && (phase & 1)) {
+    MOE_NEED(prm->zc_v, "params.zc_v");
+    MOE_NEED(prm->zc_wc, "params.zc_wc");
+  }
+  if (s.n_const > 0 && (phase & 2)) {
+    MOE_NEED(gr, "grads");
+    MOE_NEED(gr->dzc_v, "grads.dzc_v");
+    MOE_NEED(gr->dzc_wc, "grads.dzc_wc");
+  }
   if (phase & 1) {
     MOE_NEED(prm->w_gate, "params.w_gate");
     MOE_NEED(prm->w_up, "params.w_up");
@@ -505,8 +551,8 @@ int check_layer_bwd(const moe_shape& s, const moe_params* prm, const void* x, co
 
 // Input-gradient half: combine backward with the router's dl, expert dgrads,
 // shared-expert dgrad, and dx.  Leaves d_o, dgu, dl (and dgu_sh) in ws.
-int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const moe_saved* sv, const void* dy, void* dx,
-                    const Plan& p, void* ws, hipStream_t stream) {
+int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const void* x, const moe_saved* sv, const void* dy,
+                    void* dx, const Plan& p, void* ws, hipStream_t stream) {
   void* d_o = wsp(ws, p.d_o);
   void* dgu = wsp(ws, p.dgu);
   void* dx_perm = wsp(ws, p.dx_perm);
@@ -528,6 +574,8 @@ int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const moe_saved* 
   cb.s_sel = sv->s_sel;
   cb.router = s.router;
   cb.route_scale = s.route_scale;
+  cb.topk_idx = sv->topk_idx;
+  cb.zc = zc_args(s, prm, x, dy, wsp(ws, p.zc_coef));
   MOE_TRY(launch_combine_bwd(cb, stream));
   // 2. expert dgrads
   MOE_TRY(do_gemm_bwd(s, MOE_DGRAD, nullptr, sv->expert_offsets, sv->gu, nullptr, d_o, prm->w_gate, prm->w_up,
@@ -535,8 +583,9 @@ int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const moe_saved* 
   // 3. W_r^T for the router dx fused into the unpermute (zero rows up to the
   //    auxiliary loss's padded expert count)
   const bool aux = has_aux(s) && s.T > 0;
-  const int E_rt = aux ? aux_epad(s) : (int)s.E;
-  MOE_TRY(launch_wr_transpose_act(prm->w_r, w_rt, (int)s.d, (int)s.E, E_rt, s.dtype == MOE_BF16, stream));
+  const int Ep = (int)epool(s);
+  const int E_rt = aux ? aux_epad(s) : Ep;
+  MOE_TRY(launch_wr_transpose_act(prm->w_r, w_rt, (int)s.d, Ep, E_rt, s.dtype == MOE_BF16, stream));
   // 3b. auxiliary loss: its dense logit gradient, kept for the weight half,
   //     and its router dx = dl_aux W_r^T (a dense down-projection product)
   void* aux_dx = nullptr;
@@ -577,6 +626,7 @@ int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const moe_saved* 
   u.d = (int)s.d;
   u.k = (int)s.k;
   u.bf16 = s.dtype == MOE_BF16;
+  u.zc = zc_args(s, prm, x, dy, wsp(ws, p.zc_coef));
   return launch_unpermute(u, stream);
 }
 
@@ -618,7 +668,27 @@ int layer_bwd_wgrad(const moe_shape& s, const moe_params* prm, const void* x, co
     g.b = wsp(ws, p.aux_dl);
     g.c0 = part;
     MOE_TRY(launch_gemm(g, stream));
-    MOE_TRY(launch_aux_dwr(part, G, (int)s.d, (int)s.E, E_pad, s.dtype == MOE_BF16, gr->dw_r, stream));
+    MOE_TRY(launch_aux_dwr(part, G, (int)s.d, (int)epool(s), E_pad, s.dtype == MOE_BF16, gr->dw_r, stream));
+  }
+  if (s.n_const > 0) {
+    // constant experts' dv and dW_c over their rows
+    ZcParamArgs z{};
+    z.x = x;
+    z.dy = dy;
+    z.coef = reinterpret_cast<const float4*>(wsp(ws, p.zc_coef));
+    z.offsets = sv->expert_offsets;
+    z.token_of = sv->token_of;
+    z.T = s.T;
+    z.d = (int)s.d;
+    z.k = (int)s.k;
+    z.e0 = (int)(s.E + s.n_zero + s.n_copy);
+    z.n_const = s.n_const;
+    z.bf16 = s.dtype == MOE_BF16;
+    z.partial = reinterpret_cast<float*>(wsp(ws, p.zc_part));
+    z.dwc = gr->dzc_wc;
+    z.dv = gr->dzc_v;
+    z.accumulate = accumulate;
+    MOE_TRY(launch_zc_param_grads(z, stream));
   }
   if (s.n_shared)
     MOE_TRY(do_shared_wgrad(s, x, dy, sv->h_sh, wsp(ws, p.dgu_sh), gr->dws_gate, gr->dws_up, gr->dws_down,
@@ -781,13 +851,15 @@ int moe_combine_fwd(const moe_shape* shape, const void* o, const float* topk_w, 
                     const void* shared_o, void* y, hipStream_t stream) {
   MOE_TRY(check_shape(shape));
   const moe_shape& s = *shape;
+  if (has_zc(s))
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "moe_combine_fwd: zero-computation experts need the layer entry points");
   if (s.T > 0) {
     MOE_NEED(o, "o");
     MOE_NEED(topk_w, "topk_w");
     MOE_NEED(row_of, "row_of");
     MOE_NEED(y, "y");
   }
-  CombineFwdArgs a{o, topk_w, row_of, shared_o, y, s.T, (int)s.d, (int)s.k, s.dtype == MOE_BF16};
+  CombineFwdArgs a{o, topk_w, row_of, shared_o, y, s.T, (int)s.d, (int)s.k, s.dtype == MOE_BF16, nullptr, ZcArgs{}};
   return launch_combine_fwd(a, stream);
 }
 
@@ -795,6 +867,8 @@ int moe_combine_bwd(const moe_shape* shape, const void* dy, const void* o, const
                     const int32_t* row_of, void* d_o, float* d_topk_w, hipStream_t stream) {
   MOE_TRY(check_shape(shape));
   const moe_shape& s = *shape;
+  if (has_zc(s))
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "moe_combine_bwd: zero-computation experts need the layer entry points");
   if (s.T > 0) {
     MOE_NEED(dy, "dy");
     MOE_NEED(o, "o");
@@ -859,6 +933,8 @@ int moe_unpermute_bwd(const moe_shape* shape, const void* dx_perm, const int32_t
                       const void* dx_shared, void* dx, hipStream_t stream) {
   MOE_TRY(check_shape(shape));
   const moe_shape& s = *shape;
+  if (has_zc(s))
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "moe_unpermute_bwd: zero-computation experts need the layer entry points");
   if (s.T > 0) {
     MOE_NEED(dx_perm, "dx_perm");
     MOE_NEED(row_of, "row_of");
@@ -964,6 +1040,10 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, 
     MOE_NEED(sv->aux_loss, "saved.aux_loss");
     if (s.T > 0) MOE_NEED(sv->router_probs, "saved.router_probs");
   }
+  if (s.n_const > 0) {
+    MOE_NEED(prm->zc_v, "params.zc_v");
+    MOE_NEED(prm->zc_wc, "params.zc_wc");
+  }
   MOE_TRY(check_ws(ws, ws_bytes, plan(s).fwd_total));
   const void* bg = s.expert_bias ? prm->b_gate : nullptr;
   const void* bu = s.expert_bias ? prm->b_up : nullptr;
@@ -981,7 +1061,7 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, 
   if (s.n_shared)
     MOE_TRY(do_shared_fwd(s, x, prm->ws_gate, prm->ws_up, prm->ws_down, sv->gu_sh, sv->h_sh, sv->o_sh, stream));
   CombineFwdArgs c{sv->o, sv->topk_w, sv->row_of, s.n_shared ? sv->o_sh : nullptr, y, s.T, (int)s.d, (int)s.k,
-                   s.dtype == MOE_BF16};
+                   s.dtype == MOE_BF16, sv->topk_idx, zc_args(s, prm, x, nullptr, nullptr)};
   return launch_combine_fwd(c, stream);
 }
 
@@ -992,7 +1072,7 @@ int moe_layer_bwd(const moe_shape* shape, const moe_params* prm, const void* x, 
   MOE_TRY(check_layer_bwd(s, prm, x, sv, dy, dx, gr, 3));
   const Plan p = plan(s);
   MOE_TRY(check_ws(ws, ws_bytes, p.bwd_total));
-  MOE_TRY(layer_bwd_dgrad(s, prm, sv, dy, dx, p, ws, stream));
+  MOE_TRY(layer_bwd_dgrad(s, prm, x, sv, dy, dx, p, ws, stream));
   return layer_bwd_wgrad(s, prm, x, sv, dy, gr, false, p, ws, stream);
 }
 
@@ -1003,7 +1083,7 @@ int moe_layer_bwd_dgrad(const moe_shape* shape, const moe_params* prm, const voi
   MOE_TRY(check_layer_bwd(s, prm, x, sv, dy, dx, nullptr, 1));
   const Plan p = plan(s);
   MOE_TRY(check_ws(ws, ws_bytes, p.bwd_total));
-  return layer_bwd_dgrad(s, prm, sv, dy, dx, p, ws, stream);
+  return layer_bwd_dgrad(s, prm, x, sv, dy, dx, p, ws, stream);
 }
 
 int moe_layer_bwd_wgrad(const moe_shape* shape, const moe_params* prm, const void* x, const moe_saved* sv,

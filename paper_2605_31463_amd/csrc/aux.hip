@@ -1,10 +1,12 @@
 // Global-level load-balancing loss of the router (the paper pretrains with
 // one of coefficient 1e-3, appendix A.1 training configuration):
-//   L = coef * E * sum_e f_e P_e,  P_e = mean over tokens of p[t][e],
-// p the softmax over all E logits (written by the route kernels), f_e the
-// fraction of the T*k routed slots that chose e (or fractions of the whole
-// batch given by the caller).  f carries no gradient, so
-//   dL/dl[t][j] = coef * E / T * p[t][j] * (f_j - sum_e f_e p[t][e]),
+//   L = coef * E * sum_e eta_e f_e P_e,  P_e = mean over tokens of p[t][e],
+// p the softmax over all E logits of the pool (written by the route kernels),
+// f_e the fraction of the T*k routed slots that chose e (or fractions of the
+// whole batch given by the caller), eta_e = 1 for FFN experts and the given
+// weight for zero-computation experts (appendix B.3, MoE++: the loss treats
+// them explicitly).  f carries no gradient, so with q = eta f
+//   dL/dl[t][j] = coef * E / T * p[t][j] * (q_j - sum_e q_e p[t][e]),
 // a dense [T][E] term added to the router's logit gradient; its products
 // with x (dW_r) and W_r^T (dx) run on the grouped GEMM kernels.
 // Deterministic: every sum has a fixed order, no floating-point atomics.
@@ -14,9 +16,11 @@
 namespace moe {
 namespace {
 
+// eta_e f_e: zero-computation experts (e >= E_ffn) weigh zc_weight
 __device__ __forceinline__ double aux_frac(const AuxArgs& a, int e) {
-  if (a.aux_f) return (double)a.aux_f[e];
-  return (double)(a.offsets[e + 1] - a.offsets[e]) / ((double)a.T * (double)a.k);
+  const double f = a.aux_f ? (double)a.aux_f[e]
+                           : (double)(a.offsets[e + 1] - a.offsets[e]) / ((double)a.T * (double)a.k);
+  return e >= a.E_ffn ? (double)a.zc_weight * f : f;
 }
 
 // Column sums of p over each block of 256 tokens: 64 experts (blockIdx.y

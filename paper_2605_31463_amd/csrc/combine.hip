@@ -1,6 +1,7 @@
 // Gather-side kernels of the layer: weighted combine, its backward (with the
 // first step of the router backward fused in), and the unpermute-reduce of
-// the data gradient (with the router's dx fused in).
+// the data gradient (with the router's dx fused in); each also in a variant
+// for pools with zero-computation experts (MoE++, appendix B.3).
 //
 // All three run one wavefront per token over 16-byte chunks of the hidden
 // dimension, keep the k slot rows' loads in flight together, accumulate in
@@ -245,6 +246,413 @@ __global__ __launch_bounds__(256) void unpermute_kernel(UnpermuteArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Zero-computation experts (MoE++).  A slot whose pool id is E_ffn or above
+// has no expert row: a zero expert adds nothing, a copy expert w x_t, a
+// constant expert w (a0 x_t + a1 v_c) with (a0, a1) = softmax(W_c x_t).  Per
+// token the wave first takes the dot products W_c x_t of its constant slots
+// (one pass over x_t), then runs the combine with them.
+// ---------------------------------------------------------------------------
+enum { ZK_FFN = 0, ZK_ZERO = 1, ZK_COPY = 2, ZK_CONST = 3 };
+
+// Kind of pool id e (c: index among the constant experts).  An id outside
+// the pool (not produced by the router) is taken as a zero expert, so that
+// no load leaves the parameter arrays.
+__device__ __forceinline__ int zc_kind(const ZcArgs& z, int e, int& c) {
+  c = 0;
+  if (e < 0) return ZK_ZERO;
+  const int j = e - z.E_ffn;
+  if (j < 0) return ZK_FFN;
+  if (j < z.n_zero) return ZK_ZERO;
+  if (j < z.n_zero + z.n_copy) return ZK_COPY;
+  c = j - z.n_zero - z.n_copy;
+  return c < z.n_const ? ZK_CONST : ZK_ZERO;
+}
+
+__device__ __forceinline__ bool zc_in_pool(const ZcArgs& z, int64_t e) {
+  return (uint64_t)e < (uint64_t)(z.E_ffn + z.n_zero + z.n_copy + z.n_const);
+}
+
+// (a0, a1) = softmax(z0, z1)
+__device__ __forceinline__ void softmax2(float z0, float z1, float& a0, float& a1) {
+  const float m = fmaxf(z0, z1);
+  const float e0 = __expf(z0 - m), e1 = __expf(z1 - m);
+  const float r = 1.0f / (e0 + e1);
+  a0 = e0 * r;
+  a1 = e1 * r;
+}
+
+// Slot kinds of token t, and z = W_c x_t for its constant slots (every lane
+// ends with the sums).  Returns whether the token has a constant slot.
+template <class XT, int KM>
+__device__ __forceinline__ bool zc_slots(const ZcArgs& z, const int32_t* topk_idx, int64_t t, int k, int d,
+                                         int lane, int* kind, int* cid, float* z0, float* z1) {
+  constexpr int V = Vec16<XT>::N;
+  bool any_const = false;
+#pragma unroll
+  for (int s = 0; s < KM; ++s) {
+    kind[s] = ZK_ZERO;
+    cid[s] = 0;
+    z0[s] = z1[s] = 0.f;
+    if (s < k) {
+      const int e = __builtin_amdgcn_readfirstlane(topk_idx[t * k + s]);
+      kind[s] = zc_kind(z, e, cid[s]);
+      any_const |= kind[s] == ZK_CONST;
+    }
+  }
+  if (!any_const) return false;
+  const XT* x = reinterpret_cast<const XT*>(z.x) + t * d;
+  const int nch = d / V;
+  for (int c = lane; c < nch; c += 64) {
+    float xv[V];
+    Vec16<XT>::load(x + (int64_t)c * V, xv);
+#pragma unroll
+    for (int s = 0; s < KM; ++s) {
+      if (s >= k || kind[s] != ZK_CONST) continue;
+      const float* w0 = z.wc + (int64_t)cid[s] * 2 * d + (int64_t)c * V;
+      const float* w1 = w0 + d;
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        z0[s] = __builtin_fmaf(w0[v], xv[v], z0[s]);
+        z1[s] = __builtin_fmaf(w1[v], xv[v], z1[s]);
+      }
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < KM; ++s) {
+    if (s >= k || kind[s] != ZK_CONST) continue;
+    z0[s] = wave_sum(z0[s]);
+    z1[s] = wave_sum(z1[s]);
+  }
+  return true;
+}
+
+template <class XT, int KT>
+__global__ __launch_bounds__(256) void combine_fwd_zc_kernel(CombineFwdArgs a) {
+  constexpr int V = Vec16<XT>::N;
+  constexpr int KM = KT > 0 ? KT : KMAX;
+  const int lane = threadIdx.x & 63;
+  const int64_t t = uniform_token((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6));
+  if (t >= a.T) return;
+  const int k = KT > 0 ? KT : a.k;
+  const int nch = a.d / V;
+  const ZcArgs& z = a.zc;
+  const XT* o = reinterpret_cast<const XT*>(a.o);
+  const XT* sh = reinterpret_cast<const XT*>(a.shared_o);
+  const XT* x = reinterpret_cast<const XT*>(z.x) + t * a.d;
+  XT* y = reinterpret_cast<XT*>(a.y);
+  int kind[KM], cid[KM];
+  float z0[KM], z1[KM];
+  zc_slots<XT, KM>(z, a.topk_idx, t, a.k, a.d, lane, kind, cid, z0, z1);
+  int64_t rows[KM];
+  float w[KM], bv[KM];
+  float ax = 0.f;  // factor of x_t: copy slots w, constant slots w a0
+#pragma unroll
+  for (int s = 0; s < KM; ++s) {
+    rows[s] = 0;
+    w[s] = bv[s] = 0.f;
+    if (s >= k) continue;
+    const float ws = a.topk_w[t * a.k + s];
+    if (kind[s] == ZK_FFN) {
+      rows[s] = a.row_of[t * a.k + s];
+      w[s] = ws;
+      if ((uint64_t)rows[s] >= (uint64_t)(a.T * a.k)) {  // no row: contributes nothing
+        kind[s] = ZK_ZERO;
+        rows[s] = 0;
+      }
+    } else if (kind[s] == ZK_COPY) {
+      ax += ws;
+    } else if (kind[s] == ZK_CONST) {
+      float a0, a1;
+      softmax2(z0[s], z1[s], a0, a1);
+      ax += ws * a0;
+      bv[s] = ws * a1;
+    }
+  }
+  const bool use_x = ax != 0.f;
+  for (int c0 = 0; c0 < nch; c0 += 64 * CPL) {
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+      const int c = c0 + j * 64 + lane;
+      if (c >= nch) break;
+      uint4 raw[KM];
+#pragma unroll
+      for (int s = 0; s < KM; ++s)
+        raw[s] = (s < k && kind[s] == ZK_FFN) ? *reinterpret_cast<const uint4*>(o + rows[s] * a.d + (int64_t)c * V)
+                                              : make_uint4(0, 0, 0, 0);
+      float acc[V];
+#pragma unroll
+      for (int v = 0; v < V; ++v) acc[v] = 0.f;
+#pragma unroll
+      for (int s = 0; s < KM; ++s) {
+        if (s >= k) break;
+        if (kind[s] == ZK_FFN) {
+          float vv[V];
+          Vec16<XT>::load(reinterpret_cast<const XT*>(&raw[s]), vv);
+#pragma unroll
+          for (int v = 0; v < V; ++v) acc[v] = __builtin_fmaf(w[s], vv[v], acc[v]);
+        } else if (kind[s] == ZK_CONST) {
+          const float* vc = z.v + (int64_t)cid[s] * a.d + (int64_t)c * V;
+#pragma unroll
+          for (int v = 0; v < V; ++v) acc[v] = __builtin_fmaf(bv[s], vc[v], acc[v]);
+        }
+      }
+      if (use_x) {
+        float xv[V];
+        Vec16<XT>::load(x + (int64_t)c * V, xv);
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[v] = __builtin_fmaf(ax, xv[v], acc[v]);
+      }
+      if (sh) {
+        float vv[V];
+        Vec16<XT>::load(sh + t * a.d + (int64_t)c * V, vv);
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[v] += vv[v];
+      }
+      Vec16<XT>::store(y + t * a.d + (int64_t)c * V, acc);
+    }
+  }
+}
+
+// Combine backward with zero-computation slots.  One pass over d takes, per
+// slot, omega = <dy, out>: FFN slots from their row (and d_o = w dy), copy
+// slots <dy, x>, constant slots a0 <dy, x> + a1 <dy, v_c> (with z = W_c x
+// taken in the same pass); then dl as for the FFN-only combine, and per slot
+// the coefficients of the zero-computation gradients:
+//   constant: da = w (<dy, x>, <dy, v_c>), dz = a * (da - <a, da>),
+//             coef = (dz0, dz1, w a1, w a0)
+//   copy:     coef = (0, 0, 0, w);  zero and FFN slots: 0.
+template <class XT, int KT>
+__global__ __launch_bounds__(256) void combine_bwd_zc_kernel(CombineBwdArgs a) {
+  constexpr int V = Vec16<XT>::N;
+  constexpr int KM = KT > 0 ? KT : KMAX;
+  const int lane = threadIdx.x & 63;
+  const int64_t t = uniform_token((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6));
+  if (t >= a.T) return;
+  const int k = KT > 0 ? KT : a.k;
+  const int nch = a.d / V;
+  const ZcArgs& z = a.zc;
+  const XT* dy = reinterpret_cast<const XT*>(a.dy);
+  const XT* o = reinterpret_cast<const XT*>(a.o);
+  const XT* x = reinterpret_cast<const XT*>(z.x) + t * a.d;
+  XT* d_o = reinterpret_cast<XT*>(a.d_o);
+  int kind[KM], cid[KM];
+  int64_t rows[KM];
+  float w[KM], om[KM], dyv[KM], z0[KM], z1[KM];
+  bool need_x = false;
+#pragma unroll
+  for (int s = 0; s < KM; ++s) {
+    kind[s] = ZK_ZERO;
+    cid[s] = 0;
+    rows[s] = 0;
+    w[s] = om[s] = dyv[s] = z0[s] = z1[s] = 0.f;
+    if (s < k) {
+      const int e = __builtin_amdgcn_readfirstlane(a.topk_idx[t * a.k + s]);
+      kind[s] = zc_kind(z, e, cid[s]);
+      w[s] = a.topk_w[t * a.k + s];
+      if (kind[s] == ZK_FFN) {
+        rows[s] = a.row_of[t * a.k + s];
+        if ((uint64_t)rows[s] >= (uint64_t)(a.T * a.k)) {
+          kind[s] = ZK_ZERO;
+          rows[s] = 0;
+        }
+      }
+      need_x |= kind[s] == ZK_COPY || kind[s] == ZK_CONST;
+    }
+  }
+  float dyx = 0.f;
+  for (int c0 = 0; c0 < nch; c0 += 64 * CPL) {
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+      const int c = c0 + j * 64 + lane;
+      if (c >= nch) break;
+      const uint4 graw = *reinterpret_cast<const uint4*>(dy + t * a.d + (int64_t)c * V);
+      uint4 raw[KM];
+#pragma unroll
+      for (int s = 0; s < KM; ++s)
+        raw[s] = (s < k && kind[s] == ZK_FFN) ? *reinterpret_cast<const uint4*>(o + rows[s] * a.d + (int64_t)c * V)
+                                              : make_uint4(0, 0, 0, 0);
+      float g[V], xv[V];
+      Vec16<XT>::load(reinterpret_cast<const XT*>(&graw), g);
+#pragma unroll
+      for (int v = 0; v < V; ++v) xv[v] = 0.f;
+      if (need_x) {
+        Vec16<XT>::load(x + (int64_t)c * V, xv);
+#pragma unroll
+        for (int v = 0; v < V; ++v) dyx = __builtin_fmaf(g[v], xv[v], dyx);
+      }
+#pragma unroll
+      for (int s = 0; s < KM; ++s) {
+        if (s >= k) break;
+        if (kind[s] == ZK_FFN) {
+          float vv[V], out[V];
+          Vec16<XT>::load(reinterpret_cast<const XT*>(&raw[s]), vv);
+#pragma unroll
+          for (int v = 0; v < V; ++v) {
+            om[s] = __builtin_fmaf(g[v], vv[v], om[s]);
+            out[v] = w[s] * g[v];
+          }
+          Vec16<XT>::store(d_o + rows[s] * a.d + (int64_t)c * V, out);
+        } else if (kind[s] == ZK_CONST) {
+          const float* vc = z.v + (int64_t)cid[s] * a.d + (int64_t)c * V;
+          const float* w0 = z.wc + (int64_t)cid[s] * 2 * a.d + (int64_t)c * V;
+          const float* w1 = w0 + a.d;
+#pragma unroll
+          for (int v = 0; v < V; ++v) {
+            dyv[s] = __builtin_fmaf(g[v], vc[v], dyv[s]);
+            z0[s] = __builtin_fmaf(w0[v], xv[v], z0[s]);
+            z1[s] = __builtin_fmaf(w1[v], xv[v], z1[s]);
+          }
+        }
+      }
+    }
+  }
+  if (need_x) dyx = wave_sum(dyx);
+  float4 cf[KM];
+  float wo = 0.f;
+#pragma unroll
+  for (int s = 0; s < KM; ++s) {
+    if (s >= k) break;
+    cf[s] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (kind[s] == ZK_FFN) {
+      om[s] = wave_sum(om[s]);
+    } else if (kind[s] == ZK_COPY) {
+      om[s] = dyx;
+      cf[s].w = w[s];
+    } else if (kind[s] == ZK_CONST) {
+      dyv[s] = wave_sum(dyv[s]);
+      float a0, a1;
+      softmax2(wave_sum(z0[s]), wave_sum(z1[s]), a0, a1);
+      om[s] = a0 * dyx + a1 * dyv[s];
+      const float da0 = w[s] * dyx, da1 = w[s] * dyv[s];
+      const float ad = a0 * da0 + a1 * da1;
+      cf[s] = make_float4(a0 * (da0 - ad), a1 * (da1 - ad), w[s] * a1, w[s] * a0);
+    }
+    wo += w[s] * om[s];
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int s = 0; s < KM; ++s) {
+      if (s >= k) break;
+      z.coef[t * a.k + s] = cf[s];
+      if (a.d_topk_w) a.d_topk_w[t * a.k + s] = om[s];
+      // softmax families only (zero-computation experts need a softmax router)
+      if (a.dl) a.dl[t * a.k + s] = w[s] * (om[s] - wo / a.route_scale);
+    }
+  }
+}
+
+// Unpermute with zero-computation slots: dx_t = sum over FFN slots of their
+// dx_perm rows + sum over all slots of dl W_r[:, e] + (sum of the slots' dy
+// factors) dy_t + sum over constant slots of W_c^T dz (+ shared, auxiliary).
+template <class XT, int KT>
+__global__ __launch_bounds__(256) void unpermute_zc_kernel(UnpermuteArgs a) {
+  constexpr int V = Vec16<XT>::N;
+  constexpr int KM = KT > 0 ? KT : KMAX;
+  const int lane = threadIdx.x & 63;
+  const int64_t t = uniform_token((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6));
+  if (t >= a.T) return;
+  const int k = KT > 0 ? KT : a.k;
+  const int nch = a.d / V;
+  const ZcArgs& z = a.zc;
+  const XT* dxp = reinterpret_cast<const XT*>(a.dx_perm);
+  const XT* dxs = reinterpret_cast<const XT*>(a.dx_shared);
+  const XT* dxa = reinterpret_cast<const XT*>(a.dx_aux);
+  const XT* wrt = reinterpret_cast<const XT*>(a.w_rt);
+  const XT* dyt = reinterpret_cast<const XT*>(z.dy) + t * a.d;
+  XT* dx = reinterpret_cast<XT*>(a.dx);
+  int64_t rows[KM], ex[KM];
+  int kind[KM], cid[KM];
+  float dl[KM], dz0[KM], dz1[KM];
+  float gdy = 0.f;  // factor of dy_t
+#pragma unroll
+  for (int s = 0; s < KM; ++s) {
+    rows[s] = ex[s] = 0;
+    kind[s] = ZK_ZERO;
+    cid[s] = 0;
+    dl[s] = dz0[s] = dz1[s] = 0.f;
+    if (s >= k) continue;
+    const int e = __builtin_amdgcn_readfirstlane(a.topk_idx[t * a.k + s]);
+    ex[s] = e;
+    kind[s] = zc_kind(z, e, cid[s]);
+    dl[s] = a.dl ? a.dl[t * a.k + s] : 0.f;
+    if (kind[s] == ZK_FFN) {
+      rows[s] = a.row_of[t * a.k + s];
+      if ((uint64_t)rows[s] >= (uint64_t)(a.T * a.k)) {
+        kind[s] = ZK_ZERO;
+        rows[s] = 0;
+      }
+    } else {
+      const float4 cf = z.coef[t * a.k + s];
+      dz0[s] = cf.x;
+      dz1[s] = cf.y;
+      gdy += cf.w;
+    }
+  }
+  const bool use_dy = gdy != 0.f;
+  for (int c0 = 0; c0 < nch; c0 += 64 * CPL) {
+#pragma unroll
+    for (int j = 0; j < CPL; ++j) {
+      const int c = c0 + j * 64 + lane;
+      if (c >= nch) break;
+      uint4 raw[KM], rw[KM];
+#pragma unroll
+      for (int s = 0; s < KM; ++s) {
+        raw[s] = make_uint4(0, 0, 0, 0);
+        rw[s] = make_uint4(0, 0, 0, 0);
+        if (s < k && kind[s] == ZK_FFN) raw[s] = *reinterpret_cast<const uint4*>(dxp + rows[s] * a.d + (int64_t)c * V);
+        if (s < k && a.dl && zc_in_pool(z, ex[s]))
+          rw[s] = *reinterpret_cast<const uint4*>(wrt + ex[s] * a.d + (int64_t)c * V);
+      }
+      float acc[V], r[V];
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        acc[v] = 0.f;
+        r[v] = 0.f;
+      }
+#pragma unroll
+      for (int s = 0; s < KM; ++s) {
+        if (s >= k) break;
+        float vv[V], ww[V];
+        Vec16<XT>::load(reinterpret_cast<const XT*>(&raw[s]), vv);
+        Vec16<XT>::load(reinterpret_cast<const XT*>(&rw[s]), ww);
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          acc[v] += vv[v];
+          r[v] = __builtin_fmaf(dl[s], ww[v], r[v]);
+        }
+        if (kind[s] == ZK_CONST) {
+          const float* w0 = z.wc + (int64_t)cid[s] * 2 * a.d + (int64_t)c * V;
+          const float* w1 = w0 + a.d;
+#pragma unroll
+          for (int v = 0; v < V; ++v) r[v] = __builtin_fmaf(dz0[s], w0[v], __builtin_fmaf(dz1[s], w1[v], r[v]));
+        }
+      }
+      if (use_dy) {
+        float g[V];
+        Vec16<XT>::load(dyt + (int64_t)c * V, g);
+#pragma unroll
+        for (int v = 0; v < V; ++v) r[v] = __builtin_fmaf(gdy, g[v], r[v]);
+      }
+#pragma unroll
+      for (int v = 0; v < V; ++v) acc[v] += r[v];
+      if (dxs) {
+        float vv[V];
+        Vec16<XT>::load(dxs + t * a.d + (int64_t)c * V, vv);
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[v] += vv[v];
+      }
+      if (dxa) {
+        float vv[V];
+        Vec16<XT>::load(dxa + t * a.d + (int64_t)c * V, vv);
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[v] += vv[v];
+      }
+      Vec16<XT>::store(dx + t * a.d + (int64_t)c * V, acc);
+    }
+  }
+}
+
 }  // namespace
 
 #define MOE_BY_K(NAME, KID, KERNEL, XT)                                                   \
@@ -258,6 +666,10 @@ __global__ __launch_bounds__(256) void unpermute_kernel(UnpermuteArgs a) {
 int launch_combine_fwd(const CombineFwdArgs& a, hipStream_t s) {
   if (a.T == 0) return MOE_OK;
   const int nb = (int)((a.T + 3) / 4);
+  if (a.zc.on) {
+    if (a.bf16) { MOE_BY_K("combine_fwd", K_COMBINE_FWD, combine_fwd_zc_kernel, bf16_t) }
+    MOE_BY_K("combine_fwd", K_COMBINE_FWD, combine_fwd_zc_kernel, float)
+  }
   if (a.bf16) { MOE_BY_K("combine_fwd", K_COMBINE_FWD, combine_fwd_kernel, bf16_t) }
   MOE_BY_K("combine_fwd", K_COMBINE_FWD, combine_fwd_kernel, float)
 }
@@ -265,6 +677,10 @@ int launch_combine_fwd(const CombineFwdArgs& a, hipStream_t s) {
 int launch_combine_bwd(const CombineBwdArgs& a, hipStream_t s) {
   if (a.T == 0) return MOE_OK;
   const int nb = (int)((a.T + 3) / 4);
+  if (a.zc.on) {
+    if (a.bf16) { MOE_BY_K("combine_bwd", K_COMBINE_BWD, combine_bwd_zc_kernel, bf16_t) }
+    MOE_BY_K("combine_bwd", K_COMBINE_BWD, combine_bwd_zc_kernel, float)
+  }
   if (a.bf16) { MOE_BY_K("combine_bwd", K_COMBINE_BWD, combine_bwd_kernel, bf16_t) }
   MOE_BY_K("combine_bwd", K_COMBINE_BWD, combine_bwd_kernel, float)
 }
@@ -272,6 +688,7 @@ int launch_combine_bwd(const CombineBwdArgs& a, hipStream_t s) {
 template <class XT>
 int launch_unpermute_t(const UnpermuteArgs& a, hipStream_t s) {
   const int nb = (int)((a.T + 3) / 4);
+  if (a.zc.on) { MOE_BY_K("unpermute", K_UNPERMUTE, unpermute_zc_kernel, XT) }
 #define MOE_UNP(KT_) \
   return launch(K_UNPERMUTE, s, "unpermute", [&] { unpermute_kernel<XT, KT_><<<nb, 256, 0, s>>>(a); });
   switch (a.k) {

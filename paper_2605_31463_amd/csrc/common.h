@@ -35,6 +35,8 @@ enum KernelId {
   K_AUX_STATS,
   K_AUX_GRAD,
   K_AUX_DWR,
+  K_ZC_PARAM_PARTIAL,
+  K_ZC_PARAM_REDUCE,
   K_NUM_KERNELS
 };
 

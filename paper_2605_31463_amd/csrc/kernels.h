@@ -34,7 +34,8 @@ struct PermArgs {
   const void* x;
   const int32_t* topk_idx;
   int64_t T;
-  int d, E, k;
+  int d, E, k;       // E: experts ranked (the whole pool)
+  int E_rows;        // the first E_rows experts' rows receive x (FFN experts)
   bool bf16;
   int32_t* hist;     // [nblk][E] workspace
   int32_t* offsets;  // [E+1]
@@ -43,6 +44,20 @@ struct PermArgs {
   void* x_perm;      // [R][d]
 };
 int launch_permute(const PermArgs& a, hipStream_t s);
+
+// Zero-computation experts of the pool (MoE++): pool ids E_ffn .. are n_zero
+// zero experts (out = 0), then n_copy copy experts (out = x), then n_const
+// constant experts (out = a0 x + a1 v_c, (a0, a1) = softmax(W_c x)).
+struct ZcArgs {
+  bool on;                // false: no such experts (every slot is an FFN slot)
+  int E_ffn, n_zero, n_copy, n_const;
+  const void* x;          // [T][d] layer input, activation type
+  const float* v;         // [n_const][d]
+  const float* wc;        // [n_const][2][d]
+  float4* coef;           // [T*k] per slot: (dz0, dz1, w a1, dy's factor in dx);
+                          // written by the combine backward
+  const void* dy;         // [T][d] (unpermute)
+};
 
 struct CombineFwdArgs {
   const void* o;
@@ -53,6 +68,8 @@ struct CombineFwdArgs {
   int64_t T;
   int d, k;
   bool bf16;
+  const int32_t* topk_idx;  // read with zero-computation experts
+  ZcArgs zc;
 };
 int launch_combine_fwd(const CombineFwdArgs& a, hipStream_t s);
 
@@ -73,6 +90,8 @@ struct CombineBwdArgs {
   const float* s_sel;
   int router;
   float route_scale;
+  const int32_t* topk_idx;  // read with zero-computation experts
+  ZcArgs zc;
 };
 int launch_combine_bwd(const CombineBwdArgs& a, hipStream_t s);
 
@@ -114,6 +133,8 @@ struct AuxArgs {
   int64_t T;
   int E, k;
   float coef;
+  int E_ffn;                // experts E_ffn .. E-1 (zero-computation ones) weigh
+  float zc_weight;          //   zc_weight in the loss, the others 1
   double* part;             // [aux_blocks(T)][E] workspace
   float* loss;              // [1]
 };
@@ -141,8 +162,30 @@ struct UnpermuteArgs {
   int64_t T;
   int d, k;
   bool bf16;
+  ZcArgs zc;                // zero-computation slots: no dx_perm row, dx from coef
 };
 int launch_unpermute(const UnpermuteArgs& a, hipStream_t s);
+
+// Gradients of the constant experts' parameters: over the rows of each
+// constant expert (the permutation lists its tokens), in tasks of DWR_ROWS rows,
+//   dW_c[c][j] = sum_rows dz_j x_token,  dv[c] = sum_rows (w a1) dy_token,
+// per-task float32 partials summed in task order.
+struct ZcParamArgs {
+  const void* x;            // [T][d]
+  const void* dy;           // [T][d]
+  const float4* coef;       // [T*k] from the combine backward
+  const int32_t* offsets;   // [E_pool+1]
+  const int32_t* token_of;  // [T*k]
+  int64_t T;
+  int d, k;
+  int e0, n_const;          // pool id of the first constant expert, their number
+  bool bf16;
+  float* partial;           // [route_dwr_tasks(T*k, n_const)][3][d] workspace
+  float* dwc;               // [n_const][2][d]
+  float* dv;                // [n_const][d]
+  bool accumulate;
+};
+int launch_zc_param_grads(const ZcParamArgs& a, hipStream_t s);
 
 // Grouped GEMMs.
 enum GemmMode {

@@ -10,7 +10,9 @@
 //            ascending token order from per-wave 64-bit membership masks
 //            (popcount below the lane) and writes row_of / token_of;
 //   copy     one wavefront per token reads its x row once from HBM and writes
-//            it to the token's k rows with 16-byte vector loads and stores.
+//            it to the token's k rows with 16-byte vector loads and stores
+//            (rows of the FFN experts only: a zero-computation expert's rows
+//            just list its tokens).
 // No atomics touch the row layout, so the permutation is the stable counting
 // sort by (expert, token) on every run.
 #include "common.h"
@@ -144,9 +146,15 @@ __global__ __launch_bounds__(256) void permute_copy_kernel(PermArgs a) {
   const int nch = a.d / V;
   const XT* x = reinterpret_cast<const XT*>(a.x) + t * a.d;
   XT* xp = reinterpret_cast<XT*>(a.x_perm);
+  // rows at or past the FFN experts' end belong to zero-computation experts
+  // (no activations): not written
+  const int64_t r_end = a.offsets[a.E_rows];
   int64_t rows[16];
 #pragma unroll
-  for (int s = 0; s < 16; ++s) rows[s] = s < k ? a.row_of[t * k + s] : -1;
+  for (int s = 0; s < 16; ++s) {
+    rows[s] = s < k ? a.row_of[t * k + s] : -1;
+    if (rows[s] >= r_end) rows[s] = -1;
+  }
   for (int c0 = 0; c0 < nch; c0 += 64 * CPL) {
     uint4 v[CPL];
 #pragma unroll

@@ -15,6 +15,7 @@ class MoELayer:
         self.device = device
         s = shape
         T, d, E, k, f = s.T, s.d, s.E, s.k, s.f
+        Ep = L.pool_size(s)
         R = T * k
         self.act = torch.bfloat16 if s.dtype == L.MOE_BF16 else torch.float32
         fwd, _, bwd = L.moe_workspace_size(shape)
@@ -25,12 +26,12 @@ class MoELayer:
         self.saved = dict(
             topk_idx=e(T, k, dt=i32), topk_w=e(T, k, dt=f32),
             s_sel=e(T, k, dt=f32) if s.router == L.MOE_ROUTER_SIGMOID_GROUPED else None,
-            expert_offsets=e(E + 1, dt=i32), row_of=e(T, k, dt=i32), token_of=e(R, dt=i32),
+            expert_offsets=e(Ep + 1, dt=i32), row_of=e(T, k, dt=i32), token_of=e(R, dt=i32),
             x_perm=e(R, d), gu=e(R, 2 * f), h=e(R, f), o=e(R, d),
             gu_sh=e(T, 2 * s.f_shared) if s.n_shared else None,
             h_sh=e(T, s.f_shared) if s.n_shared else None,
             o_sh=e(T, d) if s.n_shared else None,
-            router_probs=e(T, E, dt=f32) if s.aux_coef > 0 else None,
+            router_probs=e(T, Ep, dt=f32) if s.aux_coef > 0 else None,
             aux_loss=torch.zeros(1, dtype=f32, device=device) if s.aux_coef > 0 else None,
         )
         self.y = e(T, d)
@@ -40,12 +41,14 @@ class MoELayer:
         s = self.shape
         a = self.act
         e = lambda *shp, dt=a: torch.empty(*shp, dtype=dt, device=self.device)  # noqa: E731
-        g = dict(dw_r=e(s.d, s.E, dt=torch.float32), dw_gate=e(s.E, s.d, s.f), dw_up=e(s.E, s.d, s.f),
-                 dw_down=e(s.E, s.f, s.d))
+        g = dict(dw_r=e(s.d, L.pool_size(s), dt=torch.float32), dw_gate=e(s.E, s.d, s.f),
+                 dw_up=e(s.E, s.d, s.f), dw_down=e(s.E, s.f, s.d))
         if s.expert_bias:
             g.update(db_gate=e(s.E, s.f), db_up=e(s.E, s.f), db_down=e(s.E, s.d))
         if s.n_shared:
             g.update(dws_gate=e(s.d, s.f_shared), dws_up=e(s.d, s.f_shared), dws_down=e(s.f_shared, s.d))
+        if s.n_const:
+            g.update(dzc_v=e(s.n_const, s.d, dt=torch.float32), dzc_wc=e(s.n_const, 2, s.d, dt=torch.float32))
         return g
 
     def forward(self, params, x, stream=None):

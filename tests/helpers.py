@@ -4,7 +4,7 @@ top-k margin)."""
 import numpy as np
 
 from moe_inputs import f32_from_bf16_bits, layer_inputs, to_f64
-from oracle import layer_backward, layer_forward, spec_from_config
+from oracle import ZeroComputeSpec, layer_backward, layer_forward, spec_from_config
 
 MARGIN = 1e-6
 TOL = {"bf16": 2e-2, "f32": 1e-4}
@@ -61,6 +61,18 @@ def shared_of(inp, cfg):
     return (to_f64(inp["ws_gate"], dt), to_f64(inp["ws_up"], dt), to_f64(inp["ws_down"], dt))
 
 
+def zc_of(inp, cfg):
+    """(ZeroComputeSpec, v, W_c) of a config with zero-computation experts, else None."""
+    nz, ncp, nc = cfg.get("n_zero", 0), cfg.get("n_copy", 0), cfg.get("n_const", 0)
+    if nz + ncp + nc == 0:
+        return None
+    zs = ZeroComputeSpec(n_zero=nz, n_copy=ncp, n_const=nc, aux_weight=cfg.get("zc_aux_weight", 1.0))
+    d = cfg["d"]
+    v = inp["zc_v"].astype(np.float64) if nc else np.zeros((0, d))
+    wc = inp["zc_wc"].astype(np.float64) if nc else np.zeros((0, 2, d))
+    return (zs, v, wc)
+
+
 def oracle_run(cfg, inp, aux_coef=0.0, aux_f=None):
     spec = spec_from_config(cfg)
     dt = cfg["dtype"]
@@ -69,9 +81,10 @@ def oracle_run(cfg, inp, aux_coef=0.0, aux_f=None):
     beta = None if inp["router_bias"] is None else inp["router_bias"].astype(np.float64)
     efn = expert_fn(inp, cfg)
     shared = shared_of(inp, cfg)
-    fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=aux_coef, aux_f=aux_f)
+    zc = zc_of(inp, cfg)
+    fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=aux_coef, aux_f=aux_f, zc=zc)
     bwd = layer_backward(spec, x, w_r, beta, efn, fwd, to_f64(inp["dy"], dt), shared,
-                         with_bias=cfg["expert_bias"])
+                         with_bias=cfg["expert_bias"], zc=zc)
     return fwd, bwd
 
 
@@ -84,6 +97,8 @@ def device_params(inp, cfg):
         w_gate=dev(inp["w_gate"], dt), w_up=dev(inp["w_up"], dt), w_down=dev(inp["w_down"], dt),
         b_gate=dev(inp.get("b_gate"), dt), b_up=dev(inp.get("b_up"), dt), b_down=dev(inp.get("b_down"), dt),
         ws_gate=dev(inp.get("ws_gate"), dt), ws_up=dev(inp.get("ws_up"), dt), ws_down=dev(inp.get("ws_down"), dt),
+        zc_v=None if inp.get("zc_v") is None else torch.from_numpy(inp["zc_v"]).cuda(),
+        zc_wc=None if inp.get("zc_wc") is None else torch.from_numpy(inp["zc_wc"]).cuda(),
     )
     return p
 

@@ -59,6 +59,12 @@ def test_workspace_sizes_scale_with_shape():
     (dict(aux_coef=-1.0), L.MOE_ERR_INVALID_ARG),
     (dict(aux_coef=float("nan")), L.MOE_ERR_INVALID_ARG),
     (dict(E=16, k=4, n_groups=4, topk_groups=2, router="sigmoid_grouped", aux_coef=1e-3), L.MOE_ERR_UNSUPPORTED),
+    (dict(n_zero=-1), L.MOE_ERR_INVALID_ARG),
+    (dict(n_const=2, zc_aux_weight=-0.5), L.MOE_ERR_INVALID_ARG),
+    (dict(n_const=2, zc_aux_weight=float("inf")), L.MOE_ERR_INVALID_ARG),
+    (dict(E=16, k=4, n_groups=4, topk_groups=2, router="sigmoid_grouped", n_copy=1), L.MOE_ERR_UNSUPPORTED),
+    (dict(E=250, k=8, n_zero=4, n_copy=4), L.MOE_ERR_UNSUPPORTED),     # pool of 258
+    (dict(E=2, k=5, n_zero=1, n_copy=1), L.MOE_ERR_INVALID_ARG),       # k above the pool of 4
 ])
 def test_bad_shapes_rejected(kw, status):
     base = dict(T=64, d=128, E=8, k=2, f=256)
@@ -104,13 +110,16 @@ def test_status_strings_and_kernel_names():
 
 
 def test_shape_struct_layout_matches_header():
-    # int64 x5, int32 x3 (+pad), int64, int32 x2, float, int32 x3, float (+pad) -> 96 bytes
-    assert ctypes.sizeof(L.moe_shape) == 96
+    # int64 x5, int32 x3 (+pad), int64, int32 x2, float, int32 x3, float, int32 x3,
+    # float (+pad) -> 112 bytes
+    assert ctypes.sizeof(L.moe_shape) == 112
     assert L.moe_shape.f_shared.offset == 56
     assert L.moe_shape.aux_coef.offset == 88
+    assert L.moe_shape.zc_aux_weight.offset == 104
     # pointer structs: one pointer per field, in the header's order
-    assert ctypes.sizeof(L.moe_params) == 12 * 8 and L.moe_params.aux_f.offset == 88
+    assert ctypes.sizeof(L.moe_params) == 14 * 8 and L.moe_params.zc_wc.offset == 104
     assert ctypes.sizeof(L.moe_saved) == 15 * 8 and L.moe_saved.aux_loss.offset == 112
+    assert ctypes.sizeof(L.moe_grads) == 12 * 8 and L.moe_grads.dzc_wc.offset == 88
 
 
 def declared_arities():
@@ -154,3 +163,27 @@ def test_accumulate_arguments_rejected_on_the_host():
     assert st == L.MOE_ERR_INVALID_ARG
     st = L.LIB.moe_layer_bwd_dgrad(ctypes.byref(s), None, None, None, None, None, None, 0, None)
     assert st == L.MOE_ERR_INVALID_ARG
+
+
+def test_zero_computation_shapes_on_the_host():
+    """The pool (E plus zero-computation experts) sizes the router's
+    workspaces; the gather-side component entry points refuse such shapes;
+    the layer entry points ask for the constant experts' parameters."""
+    base = dict(T=512, d=256, E=16, k=4, f=128)
+    f0, v0, b0 = L.moe_workspace_size(L.make_shape(**base))
+    f1, v1, b1 = L.moe_workspace_size(L.make_shape(**base, n_zero=2, n_copy=2, n_const=4))
+    assert f1 > f0 and v1 > v0 and b1 > b0
+    s = L.make_shape(**base, n_copy=1)
+    assert L.LIB.moe_combine_fwd(ctypes.byref(s), None, None, None, None, None, None) == L.MOE_ERR_UNSUPPORTED
+    assert L.LIB.moe_combine_bwd(ctypes.byref(s), *([None] * 6), None) == L.MOE_ERR_UNSUPPORTED
+    assert L.LIB.moe_unpermute_bwd(ctypes.byref(s), *([None] * 5), None) == L.MOE_ERR_UNSUPPORTED
+    s = L.make_shape(**base, n_const=2)
+    fake = ctypes.c_void_p(16)   # never dereferenced: validation fails first
+    pr = L.moe_params(w_r=fake, w_gate=fake, w_up=fake, w_down=fake)
+    sv = L.moe_saved(**{n: fake for n, _ in L.moe_saved._fields_})
+    st = L.LIB.moe_layer_fwd(ctypes.byref(s), ctypes.byref(pr), fake, ctypes.byref(sv), fake, fake, 1 << 40, None)
+    assert st == L.MOE_ERR_INVALID_ARG and "zc_v" in L.last_error()
+    gr = L.moe_grads(**{n: fake for n, _ in L.moe_grads._fields_ if not n.startswith("dzc")})
+    st = L.LIB.moe_layer_bwd_wgrad(ctypes.byref(s), ctypes.byref(pr), fake, ctypes.byref(sv), fake,
+                                   ctypes.byref(gr), 0, fake, 1 << 40, None)
+    assert st == L.MOE_ERR_INVALID_ARG and "dzc_v" in L.last_error()
