@@ -11,6 +11,7 @@ from .moe_oracle import (  # noqa: F401
     route,
     sort_maps,
     permute_rows,
+    glu,
     expert_forward,
     expert_backward,
     layer_forward,

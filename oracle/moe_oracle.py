@@ -211,34 +211,58 @@ def permute_rows(x, token_of, k):
 # SwiGLU expert
 # ----------------------------------------------------------------------------
 
-def expert_forward(xe, wg, wu, wd, bg=None, bu=None, bd=None):
-    """g = x W_gate (+b_gate), u = x W_up (+b_up), h = silu(g) * u,
-    o = h W_down (+b_down), for the rows xe [M][d]."""
+def glu(g, u, act=None):
+    """The expert's gated activation h(g, u) and its partial derivatives.
+
+    act None: SwiGLU, h = silu(g) u.
+    act ("clamped_glu", alpha, limit): the GPT-OSS release's variant (the paper
+      trains GPT-OSS-20B, section 5.1, without naming it): gc = min(g, limit),
+      uc = clip(u, -limit, limit), h = gc sig(alpha gc) (uc + 1).  The clamps
+      pass the gradient where the value lies inside them, bounds included.
+    Returns h, dh/dg, dh/du (elementwise)."""
+    if act is None:
+        sg = sigmoid(g)
+        return g * sg * u, u * sg * (1.0 + g * (1.0 - sg)), g * sg
+    kind, alpha, limit = act
+    if kind != "clamped_glu":
+        raise ValueError("unknown activation " + str(kind))
+    gc = np.minimum(g, limit)
+    uc = np.clip(u, -limit, limit)
+    s = sigmoid(alpha * gc)
+    h = gc * s * (uc + 1.0)
+    dgc = (uc + 1.0) * s * (1.0 + alpha * gc * (1.0 - s))
+    return h, np.where(g <= limit, dgc, 0.0), np.where(np.abs(u) <= limit, gc * s, 0.0)
+
+
+def expert_forward(xe, wg, wu, wd, bg=None, bu=None, bd=None, act=None):
+    """g = x W_gate (+b_gate), u = x W_up (+b_up), h = act(g, u) (SwiGLU:
+    silu(g) * u), o = h W_down (+b_down), for the rows xe [M][d]."""
     g = xe @ wg
     u = xe @ wu
     if bg is not None:
         g = g + bg
     if bu is not None:
         u = u + bu
-    h = silu(g) * u
+    h = glu(g, u, act)[0]
     o = h @ wd
     if bd is not None:
         o = o + bd
     return g, u, h, o
 
 
-def expert_backward(xe, g, u, h, do, wg, wu, wd, with_bias=False):
+def expert_backward(xe, g, u, h, do, wg, wu, wd, with_bias=False, act=None):
     """Gradients of sum(<do, o>) for one expert's rows.
 
     dh = do W_down^T; dW_down = h^T do; db_down = sum_rows do
-    dg = dh * u * sig(g) * (1 + g (1 - sig(g)));  du = dh * silu(g)
+    dg = dh * dh/dg, du = dh * dh/du (SwiGLU: dh/dg = u sig(g) (1 + g (1 - sig(g))),
+    dh/du = silu(g));
     dW_gate = x^T dg; dW_up = x^T du; db_gate, db_up = row sums
     dx = dg W_gate^T + du W_up^T
     """
-    sg = sigmoid(g)
     dh = do @ wd.T
-    dg = dh * u * sg * (1.0 + g * (1.0 - sg))
-    du = dh * g * sg
+    _, hg, hu = glu(g, u, act)
+    dg = dh * hg
+    du = dh * hu
     out = dict(
         dw_down=h.T @ do,
         dw_gate=xe.T @ dg,
@@ -323,7 +347,7 @@ def unpermute(dx_perm, row_of):
 # Whole layer
 # ----------------------------------------------------------------------------
 
-def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_f=None, zc=None):
+def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_f=None, zc=None, act=None):
     """Forward of one MoE layer.
 
     x [T][d] float64; w_r [d][E_pool]; beta [E_pool] or None;
@@ -331,7 +355,8 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
     shared = (wsg, wsu, wsd) or None for an always-on expert of weight 1;
     aux_coef > 0 adds the load-balancing loss (aux_f: the batch's fractions);
     zc = (ZeroComputeSpec, v, wc) appends zero-computation experts to the pool
-    (E_pool = spec.E + their number), else None (E_pool = spec.E).
+    (E_pool = spec.E + their number), else None (E_pool = spec.E);
+    act: the routed experts' activation (None: SwiGLU; see glu).
     Returns routing, maps and the per-row activations (permuted order) and y
     (and the auxiliary loss, its probabilities and fractions).
     """
@@ -357,7 +382,7 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
         if r1 == r0:
             continue
         wg, wu, wd, bg, bu, bd = expert_fn(e)
-        g, u, h, oe = expert_forward(x_perm[r0:r1], wg, wu, wd, bg, bu, bd)
+        g, u, h, oe = expert_forward(x_perm[r0:r1], wg, wu, wd, bg, bu, bd, act=act)
         gs[e], us[e], hs[e] = g, u, h
         o[r0:r1] = oe
         fwidth = wg.shape[1]
@@ -380,7 +405,7 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
                 h=hs, y=y, shared=sh, f=fwidth, aux=aux, zc=zf)
 
 
-def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bias=False, zc=None):
+def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bias=False, zc=None, act=None):
     """Backward of L = sum_t <dy_t, y_t> (+ the auxiliary loss) through the
     whole layer.
 
@@ -416,7 +441,7 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
                                 db_down=np.zeros(wd.shape[1]))
             continue
         ge = expert_backward(fwd["x_perm"][r0:r1], fwd["g"][e], fwd["u"][e], fwd["h"][e],
-                             do[r0:r1], wg, wu, wd, with_bias=with_bias)
+                             do[r0:r1], wg, wu, wd, with_bias=with_bias, act=act)
         dx_perm[r0:r1] = ge.pop("dx")
         ge.pop("dg")
         ge.pop("du")
@@ -505,7 +530,7 @@ def aux_loss_backward(p, f, coef, eta=None):
 # Evaluation of a layer too large to run whole
 # ----------------------------------------------------------------------------
 
-def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=None):
+def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=None, act=None):
     """Every per-token result of the layer for a batch of tokens: routing, y,
     omega, dl and dx (no weight gradients).
 
@@ -537,11 +562,11 @@ def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=No
             continue                         # zero-computation experts: above
         t, s = np.nonzero(idx == e)          # a token holds e in at most one slot
         wg, wu, wd, bg, bu, bd = expert_fn(int(e))
-        g, u, h, o = expert_forward(x[t], wg, wu, wd, bg, bu, bd)
+        g, u, h, o = expert_forward(x[t], wg, wu, wd, bg, bu, bd, act=act)
         we = w[t, s][:, None]
         y[t] += we * o
         omega[t, s] = (dy[t] * o).sum(axis=1)
-        dx[t] += expert_backward(x[t], g, u, h, we * dy[t], wg, wu, wd)["dx"]
+        dx[t] += expert_backward(x[t], g, u, h, we * dy[t], wg, wu, wd, act=act)["dx"]
     dl = router_backward(spec, rt, omega)
     dl_dense = np.zeros((T, E_pool))
     np.put_along_axis(dl_dense, idx, dl, axis=1)
@@ -553,7 +578,7 @@ def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=No
     return dict(route=rt, y=y, dx=dx, omega=omega, dl=dl, dl_dense=dl_dense)
 
 
-def expert_weight_grads_at(xe, do, wg, wu, wd, bg=None, bu=None, cols=None, with_bias=False):
+def expert_weight_grads_at(xe, do, wg, wu, wd, bg=None, bu=None, cols=None, with_bias=False, act=None):
     """Weight gradients of one expert restricted to the intermediate indices
     `cols`: dW_gate[:, cols], dW_up[:, cols], dW_down[cols, :] (and db_gate,
     db_up at cols, db_down whole).
@@ -567,8 +592,8 @@ def expert_weight_grads_at(xe, do, wg, wu, wd, bg=None, bu=None, cols=None, with
     cols = np.asarray(cols)
     wg_c, wu_c, wd_c = wg[:, cols], wu[:, cols], wd[cols, :]
     g, u, h, _ = expert_forward(xe, wg_c, wu_c, wd_c,
-                                None if bg is None else bg[cols], None if bu is None else bu[cols])
-    out = expert_backward(xe, g, u, h, do, wg_c, wu_c, wd_c, with_bias=with_bias)
+                                None if bg is None else bg[cols], None if bu is None else bu[cols], act=act)
+    out = expert_backward(xe, g, u, h, do, wg_c, wu_c, wd_c, with_bias=with_bias, act=act)
     out.pop("dx")
     out.pop("dg")
     out.pop("du")

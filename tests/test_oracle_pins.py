@@ -835,3 +835,111 @@ def test_zc_token_subset_equals_whole_layer():
         toks = np.nonzero((fwd["route"]["topk_idx"] == e).any(axis=1))[0]
         r = token_forward_backward(spec, c["x"][toks], c["dy"][toks], c["w_r"], c["beta"], efn(c), None, zc=zc)
         assert rel(c["x"][toks].T @ r["dl_dense"][:, e], bwd["dw_r"][:, e]) < 1e-12
+
+
+# ---------------------------------------------------------------------------
+# Clamped GLU expert activation (the GPT-OSS release's variant)
+# ---------------------------------------------------------------------------
+
+from oracle import glu  # noqa: E402
+
+CLAMPED = ("clamped_glu", 1.702, 7.0)
+
+
+def _clamp_case(seed, scale=12.0, T=30):
+    """Expert weights scaled so that a large share of g and u fall outside +-7."""
+    spec = RouterSpec("topk_softmax", E=6, k=2)
+    c = make_case(spec, T=T, d=16, f=12, seed=seed, expert_bias=True)
+    for n in ("wg", "wu"):
+        c[n] = c[n] * scale
+    return spec, c
+
+
+def test_clamped_glu_layer_matches_torch_autograd():
+    spec, c = _clamp_case(31)
+    fwd = layer_forward(spec, c["x"], c["w_r"], c["beta"], efn(c), act=CLAMPED)
+    bwd = layer_backward(spec, c["x"], c["w_r"], c["beta"], efn(c), fwd, c["dy"], with_bias=True, act=CLAMPED)
+    g = np.concatenate([fwd["g"][e] for e in fwd["g"]])
+    u = np.concatenate([fwd["u"][e] for e in fwd["u"]])
+    assert 0.15 < (g > 7.0).mean() < 0.6 and 0.15 < (np.abs(u) > 7.0).mean() < 0.8   # both clamps active
+    P = {n: torch.tensor(c[n], dtype=torch.float64, requires_grad=True)
+         for n in ("x", "w_r", "wg", "wu", "wd", "bg", "bu", "bd")}
+    l = P["x"] @ P["w_r"]
+    sel = torch.topk(l.detach(), spec.k, dim=1).indices
+    mask = torch.zeros_like(l, dtype=torch.bool).scatter(1, sel, True)
+    gate = torch.softmax(l.masked_fill(~mask, float("-inf")), dim=1)
+    y = 0
+    for e in range(spec.E):
+        ge = P["x"] @ P["wg"][e] + P["bg"][e]
+        ue = P["x"] @ P["wu"][e] + P["bu"][e]
+        gc = torch.clamp(ge, max=7.0)
+        he = gc * torch.sigmoid(1.702 * gc) * (torch.clamp(ue, -7.0, 7.0) + 1.0)
+        y = y + gate[:, e:e + 1] * (he @ P["wd"][e] + P["bd"][e])
+    loss = (torch.tensor(c["dy"]) * y).sum()
+    loss.backward()
+    assert abs(loss.item() - float((c["dy"] * fwd["y"]).sum())) <= 1e-12 * abs(loss.item())
+    assert rel(bwd["dx"], P["x"].grad.numpy()) < 1e-11
+    assert rel(bwd["dw_r"], P["w_r"].grad.numpy()) < 1e-11
+    for ours, theirs in (("dw_gate", "wg"), ("dw_up", "wu"), ("dw_down", "wd"), ("db_gate", "bg"),
+                         ("db_up", "bu"), ("db_down", "bd")):
+        got = np.stack([bwd["experts"][e][ours] for e in range(spec.E)])
+        assert rel(got, P[theirs].grad.numpy()) < 1e-11, ours
+
+
+def test_clamped_glu_gradients_match_finite_differences():
+    spec, c = _clamp_case(32, T=16)
+    fwd = layer_forward(spec, c["x"], c["w_r"], c["beta"], efn(c), act=CLAMPED)
+    bwd = layer_backward(spec, c["x"], c["w_r"], c["beta"], efn(c), fwd, c["dy"], with_bias=True, act=CLAMPED)
+
+    def total(cc):
+        fw = layer_forward(spec, cc["x"], cc["w_r"], cc["beta"], efn(cc), act=CLAMPED)
+        return float((cc["dy"] * fw["y"]).sum()), fw["route"]["topk_idx"]
+
+    rng = np.random.default_rng(8)
+    h = 1e-7
+    checked = 0
+    for key, gr in (("x", bwd["dx"]), ("wg", np.stack([bwd["experts"][e]["dw_gate"] for e in range(spec.E)])),
+                    ("wu", np.stack([bwd["experts"][e]["dw_up"] for e in range(spec.E)])),
+                    ("bu", np.stack([bwd["experts"][e]["db_up"] for e in range(spec.E)]))):
+        for _ in range(3):
+            v = rng.standard_normal(c[key].shape)
+            v /= np.linalg.norm(v)
+            lp, ip = total(dict(c, **{key: c[key] + h * v}))
+            lm, im = total(dict(c, **{key: c[key] - h * v}))
+            if not (np.array_equal(ip, fwd["route"]["topk_idx"]) and np.array_equal(im, fwd["route"]["topk_idx"])):
+                continue
+            fd = (lp - lm) / (2 * h)
+            an = float((gr * v).sum())
+            assert abs(fd - an) <= 1e-5 * max(1.0, abs(an)), (key, fd, an)
+            checked += 1
+    assert checked >= 8
+
+
+def test_clamped_glu_without_clamps_is_swiglu_of_u_plus_one():
+    """alpha = 1 and no clamping: h = silu(g) (u + 1), the SwiGLU layer with b_up
+    raised by one."""
+    spec = RouterSpec("softmax_topk", E=5, k=2)
+    c = make_case(spec, T=20, seed=33, expert_bias=True)
+    fwd = layer_forward(spec, c["x"], c["w_r"], None, efn(c), act=("clamped_glu", 1.0, 1e300))
+    bwd = layer_backward(spec, c["x"], c["w_r"], None, efn(c), fwd, c["dy"], with_bias=True,
+                         act=("clamped_glu", 1.0, 1e300))
+    c1 = dict(c, bu=c["bu"] + 1.0)
+    fwd1 = layer_forward(spec, c1["x"], c1["w_r"], None, efn(c1))
+    bwd1 = layer_backward(spec, c1["x"], c1["w_r"], None, efn(c1), fwd1, c1["dy"], with_bias=True)
+    assert rel(fwd["y"], fwd1["y"]) < 1e-14 and rel(bwd["dx"], bwd1["dx"]) < 1e-13
+    for e in range(spec.E):
+        for n in ("dw_gate", "dw_up", "dw_down", "db_up"):
+            assert rel(bwd["experts"][e][n], bwd1["experts"][e][n]) < 1e-13
+
+
+def test_clamped_glu_saturated_gate_passes_no_gradient():
+    """g above the limit everywhere: h = L sig(alpha L) (clip(u) + 1), no gradient
+    reaches the gate; u beyond the limits: none reaches the up projection."""
+    g = np.array([[7.5, 9.0, 100.0]])
+    u = np.array([[-8.0, 0.5, 7.0]])
+    h, hg, hu = glu(g, u, CLAMPED)
+    L, a = 7.0, 1.702
+    s = 1.0 / (1.0 + np.exp(-a * L))
+    np.testing.assert_allclose(h, L * s * (np.clip(u, -L, L) + 1.0), rtol=1e-15)
+    assert np.all(hg == 0.0)
+    assert hu[0, 0] == 0.0 and hu[0, 1] == pytest.approx(L * s) and hu[0, 2] == pytest.approx(L * s)
