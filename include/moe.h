@@ -106,6 +106,17 @@ enum { MOE_BIAS_NONE = 0, MOE_BIAS_SELECT_ONLY = 1, MOE_BIAS_LOGIT = 2 };
 
 enum { MOE_F32 = 0, MOE_BF16 = 1 };
 
+/* Activation of the routed experts.  SWIGLU: h = silu(g) * u.  CLAMPED_GLU:
+ * the GPT-OSS release's variant, gc = min(g, act_limit),
+ * uc = clamp(u, -act_limit, act_limit), h = gc * sigmoid(act_alpha * gc) * (uc + 1)
+ * (that release uses act_alpha = 1.702, act_limit = 7); in the backward the
+ * clamps pass the gradient where the value lies inside them, bounds included.
+ * With bf16 storage, a g or u value that rounding would carry across a clamp
+ * bound is stored one bf16 step back on its own side, so that the backward's
+ * clamp decisions (taken on the stored gu) are the forward's.
+ * The shared expert always uses SwiGLU. */
+enum { MOE_ACT_SWIGLU = 0, MOE_ACT_CLAMPED_GLU = 1 };
+
 /* passes of moe_grouped_gemm_bwd (bit mask).  MOE_ACCUMULATE (with
  * MOE_WGRAD): add the weight and bias gradients to what the output buffers
  * hold instead of overwriting them (bf16 gradients: the sum is taken in
@@ -133,6 +144,9 @@ typedef struct moe_shape {
   float zc_aux_weight;         /* weight of a zero-computation expert's term in
                                   the load-balancing loss (FFN experts: 1; 0
                                   drops their terms); must be finite, >= 0 */
+  int32_t act;                 /* MOE_ACT_* of the routed experts */
+  float act_alpha;             /* CLAMPED_GLU: slope inside the sigmoid (> 0) */
+  float act_limit;             /* CLAMPED_GLU: clamp bound (> 0) */
 } moe_shape;
 
 /* Parameters of the layer (device pointers; unused ones may be NULL). */
@@ -219,7 +233,7 @@ int moe_permute(const moe_shape* shape, const void* x, const int32_t* topk_idx,
 
 /* Grouped SwiGLU expert forward (section 3.2, fused SwiGLU forward):
  *   [g|u] = x_perm_e [W_gate,e | W_up,e] (+ b_gate,e | b_up,e),
- *   h = silu(g) * u  (from the float32 accumulators),
+ *   h = silu(g) * u  (or the shape's MOE_ACT_*; from the float32 accumulators),
  *   o = h W_down,e (+ b_down,e),
  * for every expert e over its rows expert_offsets[e] .. expert_offsets[e+1]-1,
  * scheduled on the device from expert_offsets (no host synchronisation).
@@ -232,7 +246,8 @@ int moe_grouped_gemm_fwd(const moe_shape* shape, const void* x_perm, const int32
 /* Grouped expert backward, as one or both passes (section 3.2, wgrad delay):
  *  MOE_DGRAD: dh = d_o W_down^T with the fused SwiGLU backward
  *             dg = dh * u * sig(g) * (1 + g (1 - sig(g))), du = dh * silu(g)
- *             (g, u read from gu) -> dgu; then dx_perm = [dg|du] [W_gate|W_up]^T.
+ *             (or that of the shape's MOE_ACT_*; g, u read from gu) -> dgu;
+ *             then dx_perm = [dg|du] [W_gate|W_up]^T.
  *  MOE_WGRAD: dW_down = h^T d_o, dW_gate = x_perm^T dg, dW_up = x_perm^T du
  *             per expert, and with expert_bias the column sums db_down, db_gate,
  *             db_up.  Reads dgu, so it runs after a DGRAD pass.  With

@@ -34,6 +34,9 @@ Fields:
   n_zero, n_copy, n_const  zero-computation experts after the E FFN experts
                          (the router covers E + their number)
   zc_aux_weight          their weight in the load-balancing loss
+  act, act_alpha, act_limit  routed experts' activation: 'swiglu' or
+                         'clamped_glu' (the GPT-OSS release's variant; its
+                         slope and clamp bound)
 """
 import copy
 
@@ -49,6 +52,7 @@ _BASE = dict(
     expert_bias=False, n_shared=0, f_shared=0,
     x_std=1.0, w_r_std=0.02, w_std=0.02, b_std=0.02, beta_std=0.1, dy_std=1.0,
     n_zero=0, n_copy=0, n_const=0, zc_aux_weight=1.0, zc_v_std=1.0, zc_wc_std=0.02,
+    act="swiglu", act_alpha=1.702, act_limit=7.0,
 )
 
 

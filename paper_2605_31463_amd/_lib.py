@@ -29,6 +29,9 @@ BIAS_MODES = {"none": MOE_BIAS_NONE, "select": MOE_BIAS_SELECT_ONLY, "logit": MO
 MOE_F32 = 0
 MOE_BF16 = 1
 DTYPES = {"f32": MOE_F32, "bf16": MOE_BF16}
+MOE_ACT_SWIGLU = 0
+MOE_ACT_CLAMPED_GLU = 1
+ACTS = {"swiglu": MOE_ACT_SWIGLU, "clamped_glu": MOE_ACT_CLAMPED_GLU}
 MOE_DGRAD = 1
 MOE_WGRAD = 2
 MOE_ACCUMULATE = 4
@@ -52,6 +55,7 @@ class moe_shape(ctypes.Structure):
         ("aux_coef", ctypes.c_float),
         ("n_zero", ctypes.c_int32), ("n_copy", ctypes.c_int32), ("n_const", ctypes.c_int32),
         ("zc_aux_weight", ctypes.c_float),
+        ("act", ctypes.c_int32), ("act_alpha", ctypes.c_float), ("act_limit", ctypes.c_float),
     ]
 
 
@@ -158,12 +162,14 @@ def _stream(stream):
 
 def make_shape(T, d, E, k, f, router="softmax_topk", n_groups=1, topk_groups=1, n_shared=0,
                f_shared=0, route_scale=1.0, bias_mode="none", expert_bias=False, dtype="bf16",
-               renorm=1, aux_coef=0.0, n_zero=0, n_copy=0, n_const=0, zc_aux_weight=1.0):
+               renorm=1, aux_coef=0.0, n_zero=0, n_copy=0, n_const=0, zc_aux_weight=1.0,
+               act="swiglu", act_alpha=1.702, act_limit=7.0):
     return moe_shape(T=T, d=d, E=E, k=k, f=f, n_groups=n_groups, topk_groups=topk_groups,
                      n_shared=n_shared, f_shared=f_shared, router=ROUTERS[router], renorm=renorm,
                      route_scale=route_scale, bias_mode=BIAS_MODES[bias_mode],
                      expert_bias=int(bool(expert_bias)), dtype=DTYPES[dtype], aux_coef=aux_coef,
-                     n_zero=n_zero, n_copy=n_copy, n_const=n_const, zc_aux_weight=zc_aux_weight)
+                     n_zero=n_zero, n_copy=n_copy, n_const=n_const, zc_aux_weight=zc_aux_weight,
+                     act=ACTS[act], act_alpha=act_alpha, act_limit=act_limit)
 
 
 def pool_size(shape):
@@ -179,7 +185,9 @@ def shape_from_config(cfg, T=None):
                       bias_mode=cfg["bias_mode"], expert_bias=cfg["expert_bias"],
                       dtype=cfg["dtype"], aux_coef=cfg.get("aux_coef", 0.0),
                       n_zero=cfg.get("n_zero", 0), n_copy=cfg.get("n_copy", 0),
-                      n_const=cfg.get("n_const", 0), zc_aux_weight=cfg.get("zc_aux_weight", 1.0))
+                      n_const=cfg.get("n_const", 0), zc_aux_weight=cfg.get("zc_aux_weight", 1.0),
+                      act=cfg.get("act", "swiglu"), act_alpha=cfg.get("act_alpha", 1.702),
+                      act_limit=cfg.get("act_limit", 7.0))
 
 
 # ---------------------------------------------------------------------------

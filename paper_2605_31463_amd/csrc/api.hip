@@ -105,6 +105,11 @@ int check_shape(const moe_shape* sh) {
     return moe_set_error(MOE_ERR_INVALID_ARG, "zc_aux_weight must be finite and non-negative");
   if (has_zc(s) && s.router == MOE_ROUTER_SIGMOID_GROUPED)
     return moe_set_error(MOE_ERR_UNSUPPORTED, "zero-computation experts need a softmax router");
+  if (s.act != MOE_ACT_SWIGLU && s.act != MOE_ACT_CLAMPED_GLU)
+    return moe_set_error(MOE_ERR_INVALID_ARG, "unknown activation %d", s.act);
+  if (s.act == MOE_ACT_CLAMPED_GLU &&
+      (!(s.act_alpha > 0.f) || !isfinite(s.act_alpha) || !(s.act_limit > 0.f) || !isfinite(s.act_limit)))
+    return moe_set_error(MOE_ERR_INVALID_ARG, "clamped GLU needs finite positive act_alpha and act_limit");
   if (s.T < 0 || s.d <= 0 || s.E <= 0 || s.k <= 0 || s.f <= 0)
     return moe_set_error(MOE_ERR_INVALID_ARG, "sizes must be positive (T >= 0): T=%lld d=%lld E=%lld k=%lld f=%lld",
                          (long long)s.T, (long long)s.d, (long long)s.E, (long long)s.k, (long long)s.f);
@@ -247,15 +252,20 @@ GemmArgs gemm_base(const moe_shape& s, int mode, const int32_t* offsets) {
   g.max_rows = s.T * s.k;
   g.d = (int)s.d;
   g.f = (int)s.f;
+  g.act = s.act;
+  g.act_alpha = s.act_alpha;
+  g.act_limit = s.act_limit;
   return g;
 }
 
+// The shared expert (and the dense products of the auxiliary loss): SwiGLU.
 GemmArgs gemm_dense(const moe_shape& s, int mode) {
   GemmArgs g = gemm_base(s, mode, nullptr);
   g.ngroups = 1;
   g.dense_rows = s.T;
   g.max_rows = s.T;
   g.f = (int)s.f_shared;
+  g.act = MOE_ACT_SWIGLU;
   return g;
 }
 
@@ -470,8 +480,9 @@ RouteBwdArgs route_bwd_base(const moe_shape& s) {
 using namespace moe;
 
 // The Python binding mirrors these layouts field by field.
-static_assert(sizeof(moe_shape) == 112 && offsetof(moe_shape, f_shared) == 56 &&
-                  offsetof(moe_shape, aux_coef) == 88 && offsetof(moe_shape, zc_aux_weight) == 104,
+static_assert(sizeof(moe_shape) == 120 && offsetof(moe_shape, f_shared) == 56 &&
+                  offsetof(moe_shape, aux_coef) == 88 && offsetof(moe_shape, zc_aux_weight) == 104 &&
+                  offsetof(moe_shape, act_limit) == 116,
               "moe_shape layout");
 static_assert(sizeof(moe_params) == 14 * sizeof(void*) && sizeof(moe_saved) == 15 * sizeof(void*) &&
                   sizeof(moe_grads) == 12 * sizeof(void*),

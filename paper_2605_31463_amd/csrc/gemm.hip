@@ -46,6 +46,78 @@ typedef __attribute__((address_space(3))) v4i16* lds_v4_t;
 
 __device__ __forceinline__ float silu_f(float z) { return z / (1.0f + __expf(-z)); }
 
+// The experts' gated activation h = act(g, u) and its backward:
+//   SwiGLU:      h = silu(g) u;
+//   clamped GLU: gc = min(g, L), uc = clamp(u, -L, L), h = gc sig(alpha gc) (uc + 1)
+//                (the GPT-OSS release's variant); the clamps pass the gradient
+//                inside their bounds, bounds included.
+// CL selects the clamped GLU at compile time (the bf16 epilogues are compiled
+// for both and pick one per launch); the runtime forms below serve the others.
+template <bool CL>
+__device__ __forceinline__ float act_h_t(const GemmArgs& a, float g, float u) {
+  if constexpr (CL) {
+    const float L = a.act_limit;
+    const float gc = fminf(g, L);
+    const float uc = fminf(fmaxf(u, -L), L);
+    return gc / (1.0f + __expf(-a.act_alpha * gc)) * (uc + 1.0f);
+  } else {
+    return silu_f(g) * u;
+  }
+}
+
+// dg = dh * dact/dg, du = dh * dact/du at (g, u)
+template <bool CL>
+__device__ __forceinline__ void act_grad_t(const GemmArgs& a, float g, float u, float dh, float& dg, float& du) {
+  if constexpr (CL) {
+    const float L = a.act_limit, al = a.act_alpha;
+    const float gc = fminf(g, L);
+    const float uc = fminf(fmaxf(u, -L), L);
+    const float s = 1.0f / (1.0f + __expf(-al * gc));
+    dg = g <= L ? dh * (uc + 1.0f) * s * (1.0f + al * gc * (1.0f - s)) : 0.f;
+    du = (u >= -L && u <= L) ? dh * gc * s : 0.f;
+  } else {
+    const float sgm = 1.0f / (1.0f + __expf(-g));
+    dg = dh * u * sgm * (1.0f + g * (1.0f - sgm));
+    du = dh * g * sgm;
+  }
+}
+
+// bf16 storage of g and u for the clamped GLU: rounded to nearest even, but
+// a value that rounding would carry across a clamp bound keeps the bound's side
+// (one bf16 step back toward the value), so that the backward's clamp masks,
+// taken on the stored values, decide as the forward did on the float32 ones.
+__device__ __forceinline__ float bf16_keep_above(float v, float b) {  // side of v > b
+  const float r = bf2f(f2bf(v));
+  if ((v > b) == (r > b)) return r;
+  const uint32_t bits = __float_as_uint(r);
+  const bool up = v > r, pos = !(bits >> 31);
+  return __uint_as_float(pos == up ? bits + 0x10000u : bits - 0x10000u);
+}
+template <bool CL>
+__device__ __forceinline__ float act_store_g_t(const GemmArgs& a, float g) {
+  if constexpr (CL) return bf16_keep_above(g, a.act_limit);
+  else return g;
+}
+template <bool CL>
+__device__ __forceinline__ float act_store_u_t(const GemmArgs& a, float u) {
+  if constexpr (CL) return u >= 0.f ? bf16_keep_above(u, a.act_limit) : -bf16_keep_above(-u, a.act_limit);
+  else return u;
+}
+
+__device__ __forceinline__ float act_h(const GemmArgs& a, float g, float u) {
+  return a.act == MOE_ACT_CLAMPED_GLU ? act_h_t<true>(a, g, u) : act_h_t<false>(a, g, u);
+}
+__device__ __forceinline__ void act_grad(const GemmArgs& a, float g, float u, float dh, float& dg, float& du) {
+  if (a.act == MOE_ACT_CLAMPED_GLU) act_grad_t<true>(a, g, u, dh, dg, du);
+  else act_grad_t<false>(a, g, u, dh, dg, du);
+}
+__device__ __forceinline__ float act_store_g(const GemmArgs& a, float g) {
+  return a.act == MOE_ACT_CLAMPED_GLU ? act_store_g_t<true>(a, g) : g;
+}
+__device__ __forceinline__ float act_store_u(const GemmArgs& a, float u) {
+  return a.act == MOE_ACT_CLAMPED_GLU ? act_store_u_t<true>(a, u) : u;
+}
+
 template <int MODE>
 __host__ __device__ constexpr bool is_wgrad() { return MODE == G_WGRAD_DOWN || MODE == G_WGRAD_GATEUP; }
 
@@ -542,11 +614,12 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
             gv[t] = acc[i][j][4 * q + t] + bgv[t];
             uv[t] = acc[i][j + NI / 2][4 * q + t] + buv[t];
           }
-          put4(sg, r, c, gv[0], gv[1], gv[2], gv[3]);
-          put4(sg + C::TM * TN_OUT, r, c, uv[0], uv[1], uv[2], uv[3]);
+          put4(sg, r, c, act_store_g(a, gv[0]), act_store_g(a, gv[1]), act_store_g(a, gv[2]), act_store_g(a, gv[3]));
+          put4(sg + C::TM * TN_OUT, r, c, act_store_u(a, uv[0]), act_store_u(a, uv[1]), act_store_u(a, uv[2]),
+               act_store_u(a, uv[3]));
           // h overwrites the accumulators of the gate block (already staged)
 #pragma unroll
-          for (int t = 0; t < 4; ++t) acc[i][j][4 * q + t] = silu_f(gv[t]) * uv[t];
+          for (int t = 0; t < 4; ++t) acc[i][j][4 * q + t] = act_h(a, gv[t], uv[t]);
         }
       }
     auto dst_gu = [&](int half) {
@@ -613,9 +686,9 @@ __global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
               }
 #pragma unroll
               for (int t = 0; t < 4; ++t) {
-                const float sgm = 1.0f / (1.0f + __expf(-gv[t]));
-                o[t] = pass == 0 ? o[t] * uv[t] * sgm * (1.0f + gv[t] * (1.0f - sgm))   // dg
-                                 : o[t] * gv[t] * sgm;                                    // du
+                float dg, du;
+                act_grad(a, gv[t], uv[t], o[t], dg, du);
+                o[t] = pass == 0 ? dg : du;
               }
             }
             put4(stg, r, c, o[0], o[1], o[2], o[3]);
@@ -846,7 +919,9 @@ __device__ __forceinline__ void tile_dims(const GemmArgs& a, const Tile& tl, int
   else { K = tl.rows; M = d; N = 2 * f; }
 }
 
-template <int MODE, class C>
+// CL: the clamped GLU activation (gate/up forward and down dgrad epilogues);
+// compiled as its own kernel so that the SwiGLU kernels carry none of its code.
+template <int MODE, class C, bool CL = false>
 __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persistent(GemmArgs a) {
   constexpr bool wgrad = is_wgrad<MODE>();
   constexpr bool a_mn = wgrad;
@@ -1128,103 +1203,106 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
     // column 32j + 8q + 4(l/32) + t.
     const int mrow0 = tl.m0 + wm * C::TM;
     if (MODE == G_FWD_GATEUP) {
-      bf16_t* gu = reinterpret_cast<bf16_t*>(a.c0);
-      bf16_t* h = reinterpret_cast<bf16_t*>(a.c1);
-      const bf16_t* bgp = reinterpret_cast<const bf16_t*>(a.bias0);
-      const bf16_t* bup = reinterpret_cast<const bf16_t*>(a.bias1);
-      const int jbase = tl.n0 + wn * (C::TN / 2);
-#pragma unroll
-      for (int j = 0; j < NI / 2; ++j) {
-        const int jj0 = jbase + 32 * j;
-        const int ncols = min(32, N - jj0);
-        float bgv[16], buv[16];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int c = jj0 + 8 * (v >> 2) + 4 * hh + (v & 3);
-          bgv[v] = (bgp && c < N) ? bf2f(bgp[(int64_t)g * f + c]) : 0.f;
-          buv[v] = (bup && c < N) ? bf2f(bup[(int64_t)g * f + c]) : 0.f;
+      auto epi = [&](auto) {
+        bf16_t* gu = reinterpret_cast<bf16_t*>(a.c0);
+        bf16_t* h = reinterpret_cast<bf16_t*>(a.c1);
+        const bf16_t* bgp = reinterpret_cast<const bf16_t*>(a.bias0);
+        const bf16_t* bup = reinterpret_cast<const bf16_t*>(a.bias1);
+        const int jbase = tl.n0 + wn * (C::TN / 2);
+  #pragma unroll
+        for (int j = 0; j < NI / 2; ++j) {
+          const int jj0 = jbase + 32 * j;
+          const int ncols = min(32, N - jj0);
+          float bgv[16], buv[16];
+  #pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int c = jj0 + 8 * (v >> 2) + 4 * hh + (v & 3);
+            bgv[v] = (bgp && c < N) ? bf2f(bgp[(int64_t)g * f + c]) : 0.f;
+            buv[v] = (bup && c < N) ? bf2f(bup[(int64_t)g * f + c]) : 0.f;
+          }
+  #pragma unroll
+          for (int i = 0; i < MI; ++i) {
+            const int m0 = mrow0 + 32 * i;
+            if (m0 >= M || ncols <= 0) continue;
+            float gv[16], uv[16], hv[16];
+  #pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              gv[v] = acc[i][j][v] + bgv[v];
+              uv[v] = acc[i][j + NI / 2][v] + buv[v];
+              hv[v] = act_h_t<CL>(a, gv[v], uv[v]);
+              gv[v] = act_store_g_t<CL>(a, gv[v]);
+              uv[v] = act_store_u_t<CL>(a, uv[v]);
+            }
+            auto row_gu = [&](int half) {
+              return [&, half](int r) -> bf16_t* {
+                return m0 + r < M ? gu + (int64_t)(tl.row_base + m0 + r) * 2 * f + half * f + jj0 : nullptr;
+              };
+            };
+            put_block(gv, row_gu(0), ncols);
+            put_block(uv, row_gu(1), ncols);
+            put_block(hv, [&](int r) -> bf16_t* {
+              return m0 + r < M ? h + (int64_t)(tl.row_base + m0 + r) * f + jj0 : nullptr;
+            }, ncols);
+          }
         }
-#pragma unroll
+      };
+      epi(0);
+    } else if (MODE == G_DGRAD_DOWN) {
+      auto epi = [&](auto) {
+        // dSwiGLU with the saved gate/up values: for each 32-row block, every
+        // gate/up load of the wavefront's columns is issued before any math
+        const int nbase = tl.n0 + wn * C::TN;
+        const bf16_t* gup = reinterpret_cast<const bf16_t*>(a.aux);
+        bf16_t* out = reinterpret_cast<bf16_t*>(a.c0);
+        constexpr int JB = NI > 2 ? 2 : NI;  // column blocks per batch of loads
+  #pragma unroll
         for (int i = 0; i < MI; ++i) {
           const int m0 = mrow0 + 32 * i;
-          if (m0 >= M || ncols <= 0) continue;
-          float gv[16], uv[16], hv[16];
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            gv[v] = acc[i][j][v] + bgv[v];
-            uv[v] = acc[i][j + NI / 2][v] + buv[v];
-            hv[v] = silu_f(gv[v]) * uv[v];
-          }
-          auto row_gu = [&](int half) {
-            return [&, half](int r) -> bf16_t* {
-              return m0 + r < M ? gu + (int64_t)(tl.row_base + m0 + r) * 2 * f + half * f + jj0 : nullptr;
-            };
-          };
-          put_block(gv, row_gu(0), ncols);
-          put_block(uv, row_gu(1), ncols);
-          put_block(hv, [&](int r) -> bf16_t* {
-            return m0 + r < M ? h + (int64_t)(tl.row_base + m0 + r) * f + jj0 : nullptr;
-          }, ncols);
-        }
-      }
-    } else if (MODE == G_DGRAD_DOWN) {
-      // dSwiGLU with the saved gate/up values: for each 32-row block, every
-      // gate/up load of the wavefront's columns is issued before any math
-      const int nbase = tl.n0 + wn * C::TN;
-      const bf16_t* gup = reinterpret_cast<const bf16_t*>(a.aux);
-      bf16_t* out = reinterpret_cast<bf16_t*>(a.c0);
-      constexpr int JB = NI > 2 ? 2 : NI;  // column blocks per batch of loads
-#pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        const int m0 = mrow0 + 32 * i;
-        if (m0 >= M) continue;
-        const int m = m0 + r32;
-        const int64_t row = tl.row_base + (m < M ? m : M - 1);
-#pragma unroll
-        for (int jb = 0; jb < NI; jb += JB) {
-          uint2 gr[JB][4], ur[JB][4];
-#pragma unroll
-          for (int jj = 0; jj < JB; ++jj)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int c = nbase + 32 * (jb + jj) + 8 * q + 4 * hh;
-              gr[jj][q] = make_uint2(0, 0);
-              ur[jj][q] = make_uint2(0, 0);
-              if (m < M && c < N) {
-                gr[jj][q] = *reinterpret_cast<const uint2*>(gup + row * 2 * f + c);
-                ur[jj][q] = *reinterpret_cast<const uint2*>(gup + row * 2 * f + f + c);
+          if (m0 >= M) continue;
+          const int m = m0 + r32;
+          const int64_t row = tl.row_base + (m < M ? m : M - 1);
+  #pragma unroll
+          for (int jb = 0; jb < NI; jb += JB) {
+            uint2 gr[JB][4], ur[JB][4];
+  #pragma unroll
+            for (int jj = 0; jj < JB; ++jj)
+  #pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int c = nbase + 32 * (jb + jj) + 8 * q + 4 * hh;
+                gr[jj][q] = make_uint2(0, 0);
+                ur[jj][q] = make_uint2(0, 0);
+                if (m < M && c < N) {
+                  gr[jj][q] = *reinterpret_cast<const uint2*>(gup + row * 2 * f + c);
+                  ur[jj][q] = *reinterpret_cast<const uint2*>(gup + row * 2 * f + f + c);
+                }
               }
-            }
-#pragma unroll
-          for (int jj = 0; jj < JB; ++jj) {
-            const int j = jb + jj;
-            const int n0 = nbase + 32 * j;
-            const int ncols = min(32, N - n0);
-            if (ncols <= 0) continue;
-            float dg[16], du[16];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const float gv[4] = {__uint_as_float(gr[jj][q].x << 16), __uint_as_float(gr[jj][q].x & 0xffff0000u),
-                                   __uint_as_float(gr[jj][q].y << 16), __uint_as_float(gr[jj][q].y & 0xffff0000u)};
-              const float uv[4] = {__uint_as_float(ur[jj][q].x << 16), __uint_as_float(ur[jj][q].x & 0xffff0000u),
-                                   __uint_as_float(ur[jj][q].y << 16), __uint_as_float(ur[jj][q].y & 0xffff0000u)};
-#pragma unroll
-              for (int t = 0; t < 4; ++t) {
-                const float o = acc[i][j][4 * q + t];
-                const float sgm = 1.0f / (1.0f + __expf(-gv[t]));
-                dg[4 * q + t] = o * uv[t] * sgm * (1.0f + gv[t] * (1.0f - sgm));
-                du[4 * q + t] = o * gv[t] * sgm;
+  #pragma unroll
+            for (int jj = 0; jj < JB; ++jj) {
+              const int j = jb + jj;
+              const int n0 = nbase + 32 * j;
+              const int ncols = min(32, N - n0);
+              if (ncols <= 0) continue;
+              float dg[16], du[16];
+  #pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const float gv[4] = {__uint_as_float(gr[jj][q].x << 16), __uint_as_float(gr[jj][q].x & 0xffff0000u),
+                                     __uint_as_float(gr[jj][q].y << 16), __uint_as_float(gr[jj][q].y & 0xffff0000u)};
+                const float uv[4] = {__uint_as_float(ur[jj][q].x << 16), __uint_as_float(ur[jj][q].x & 0xffff0000u),
+                                     __uint_as_float(ur[jj][q].y << 16), __uint_as_float(ur[jj][q].y & 0xffff0000u)};
+  #pragma unroll
+                for (int t = 0; t < 4; ++t) act_grad_t<CL>(a, gv[t], uv[t], acc[i][j][4 * q + t], dg[4 * q + t], du[4 * q + t]);
               }
+              put_block(dg, [&](int r) -> bf16_t* {
+                return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + n0 : nullptr;
+              }, ncols);
+              put_block(du, [&](int r) -> bf16_t* {
+                return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + f + n0 : nullptr;
+              }, ncols);
             }
-            put_block(dg, [&](int r) -> bf16_t* {
-              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + n0 : nullptr;
-            }, ncols);
-            put_block(du, [&](int r) -> bf16_t* {
-              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + f + n0 : nullptr;
-            }, ncols);
           }
         }
-      }
+      };
+      epi(0);
     } else if (MODE == G_FWD_DOWN || MODE == G_DGRAD_GATEUP) {
       const int nbase = tl.n0 + wn * C::TN;
       const bf16_t* bdp = MODE == G_FWD_DOWN ? reinterpret_cast<const bf16_t*>(a.bias0) : nullptr;
@@ -1265,11 +1343,7 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
               const float uv[4] = {__uint_as_float(ur.x << 16), __uint_as_float(ur.x & 0xffff0000u),
                                    __uint_as_float(ur.y << 16), __uint_as_float(ur.y & 0xffff0000u)};
 #pragma unroll
-              for (int t = 0; t < 4; ++t) {
-                const float sgm = 1.0f / (1.0f + __expf(-gv[t]));
-                dg[4 * q + t] = o[4 * q + t] * uv[t] * sgm * (1.0f + gv[t] * (1.0f - sgm));
-                du[4 * q + t] = o[4 * q + t] * gv[t] * sgm;
-              }
+              for (int t = 0; t < 4; ++t) act_grad(a, gv[t], uv[t], o[4 * q + t], dg[4 * q + t], du[4 * q + t]);
             }
             put_block(dg, [&](int r) -> bf16_t* {
               return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + n0 : nullptr;
@@ -1423,7 +1497,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     float* gu = reinterpret_cast<float*>(a.c0);
     gu[row * 2 * f + n] = ag;
     gu[row * 2 * f + f + n] = au;
-    reinterpret_cast<float*>(a.c1)[row * f + n] = silu_f(ag) * au;
+    reinterpret_cast<float*>(a.c1)[row * f + n] = act_h(a, ag, au);
   } else if (MODE == G_FWD_DOWN) {
     float acc = 0.f;
     const float* w = W0 + (int64_t)g * f * d + n;
@@ -1436,10 +1510,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
     for (int k = 0; k < d; ++k) dh = __builtin_fmaf(A[row * d + k], w[k], dh);
     const float* gu = reinterpret_cast<const float*>(a.aux);
     const float gv = gu[row * 2 * f + n], uv = gu[row * 2 * f + f + n];
-    const float sg = 1.0f / (1.0f + __expf(-gv));
     float* dgu = reinterpret_cast<float*>(a.c0);
-    dgu[row * 2 * f + n] = dh * uv * sg * (1.0f + gv * (1.0f - sg));
-    dgu[row * 2 * f + f + n] = dh * gv * sg;
+    act_grad(a, gv, uv, dh, dgu[row * 2 * f + n], dgu[row * 2 * f + f + n]);
   } else {  // G_DGRAD_GATEUP
     float acc = 0.f;
     const float* wg = W0 + (int64_t)g * d * f + (int64_t)n * f;
@@ -1501,7 +1573,7 @@ inline int cu_count() {
   return n;
 }
 
-template <int MODE, class C>
+template <int MODE, class C, bool CL = false>
 int launch_bf16_persistent(const GemmArgs& a, hipStream_t s) {
   const int G = a.offsets ? a.ngroups : 1;
   const int nt = n_tiles<MODE, C::BN>(a.d, a.f);
@@ -1519,7 +1591,7 @@ int launch_bf16_persistent(const GemmArgs& a, hipStream_t s) {
   constexpr int kOcc = (160 * 1024) / kLdsPerBlock > 0 ? (160 * 1024) / kLdsPerBlock : 1;
   const int64_t grid = std::min<int64_t>((cu_count() * kOcc / 8) * 8, (nb + 7) / 8 * 8);
   return launch(kGemmKernelId[MODE], s, kGemmName[MODE],
-                [&] { gemm_bf16_persistent<MODE, C><<<(int)grid, C::NT, 0, s>>>(a); });
+                [&] { gemm_bf16_persistent<MODE, C, CL><<<(int)grid, C::NT, 0, s>>>(a); });
 }
 
 #ifndef MOE_GEMM_PERSISTENT
@@ -1536,6 +1608,12 @@ int launch_mode(const GemmArgs& a, hipStream_t s) {
     const int G = a.offsets ? a.ngroups : 1;
     const int64_t rows_per_group = a.offsets ? a.max_rows / G : a.dense_rows;
     if constexpr (MOE_GEMM_PERSISTENT != 0) {
+      if constexpr (MODE == G_FWD_GATEUP || MODE == G_DGRAD_DOWN) {
+        if (a.act == MOE_ACT_CLAMPED_GLU) {
+          if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, true>(a, s);
+          return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big, true>(a, s);
+        }
+      }
       if (!is_wgrad<MODE>() && rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall>(a, s);
       return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big>(a, s);
     } else {

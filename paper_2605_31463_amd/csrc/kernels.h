@@ -218,6 +218,8 @@ struct GemmArgs {
   void* db0;               // db_down | db_gate
   void* db1;               // db_up
   bool accumulate;         // wgrad passes: add into c0/c1/db0/db1 instead of overwriting
+  int act;                 // MOE_ACT_*: activation of the gate/up forward and down dgrad epilogues
+  float act_alpha, act_limit;
 };
 int launch_gemm(const GemmArgs& a, hipStream_t s);
 

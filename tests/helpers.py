@@ -82,10 +82,18 @@ def oracle_run(cfg, inp, aux_coef=0.0, aux_f=None):
     efn = expert_fn(inp, cfg)
     shared = shared_of(inp, cfg)
     zc = zc_of(inp, cfg)
-    fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=aux_coef, aux_f=aux_f, zc=zc)
+    act = act_of(cfg)
+    fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=aux_coef, aux_f=aux_f, zc=zc, act=act)
     bwd = layer_backward(spec, x, w_r, beta, efn, fwd, to_f64(inp["dy"], dt), shared,
-                         with_bias=cfg["expert_bias"], zc=zc)
+                         with_bias=cfg["expert_bias"], zc=zc, act=act)
     return fwd, bwd
+
+
+def act_of(cfg):
+    """The oracle's activation argument for a config (None: SwiGLU)."""
+    if cfg.get("act", "swiglu") == "swiglu":
+        return None
+    return (cfg["act"], float(np.float32(cfg["act_alpha"])), float(np.float32(cfg["act_limit"])))
 
 
 def device_params(inp, cfg):

@@ -65,6 +65,8 @@ def test_workspace_sizes_scale_with_shape():
     (dict(E=16, k=4, n_groups=4, topk_groups=2, router="sigmoid_grouped", n_copy=1), L.MOE_ERR_UNSUPPORTED),
     (dict(E=250, k=8, n_zero=4, n_copy=4), L.MOE_ERR_UNSUPPORTED),     # pool of 258
     (dict(E=2, k=5, n_zero=1, n_copy=1), L.MOE_ERR_INVALID_ARG),       # k above the pool of 4
+    (dict(act="clamped_glu", act_alpha=0.0), L.MOE_ERR_INVALID_ARG),
+    (dict(act="clamped_glu", act_limit=float("inf")), L.MOE_ERR_INVALID_ARG),
 ])
 def test_bad_shapes_rejected(kw, status):
     base = dict(T=64, d=128, E=8, k=2, f=256)
@@ -111,11 +113,12 @@ def test_status_strings_and_kernel_names():
 
 def test_shape_struct_layout_matches_header():
     # int64 x5, int32 x3 (+pad), int64, int32 x2, float, int32 x3, float, int32 x3,
-    # float (+pad) -> 112 bytes
-    assert ctypes.sizeof(L.moe_shape) == 112
+    # float, int32, float x2 -> 120 bytes
+    assert ctypes.sizeof(L.moe_shape) == 120
     assert L.moe_shape.f_shared.offset == 56
     assert L.moe_shape.aux_coef.offset == 88
     assert L.moe_shape.zc_aux_weight.offset == 104
+    assert L.moe_shape.act_limit.offset == 116
     # pointer structs: one pointer per field, in the header's order
     assert ctypes.sizeof(L.moe_params) == 14 * 8 and L.moe_params.zc_wc.offset == 104
     assert ctypes.sizeof(L.moe_saved) == 15 * 8 and L.moe_saved.aux_loss.offset == 112
