@@ -17,6 +17,7 @@ from .moe_oracle import (  # noqa: F401
     layer_forward,
     layer_backward,
     router_backward,
+    threshold_backward,
     combine,
     combine_backward,
     unpermute,

@@ -46,6 +46,11 @@ class RouterSpec:
                   'topk_softmax'  top k logits, softmax over those k
                   'sigmoid_grouped'  s = sigmoid(logit), selection key s+beta,
                                   group-limited top-k, w = scale*s/sum(s)
+                  'sigmoid_threshold'  DynMoE-style gating: s = sigmoid(logit),
+                                  expert e active when logit - theta_e > 0 (a
+                                  learned threshold per expert), at least the
+                                  best one and at most k (the slot capacity),
+                                  w = scale*s/sum(s) over the active ones
     k, n_groups, topk_groups, route_scale as in the workload configs;
     bias_mode:    'none', 'select' (bias in the selection key only) or
                   'logit' (bias added to the logits, for selection and weights).
@@ -96,7 +101,7 @@ def _adjacent_gap_min(sorted_keys, upto):
     return gaps.min(axis=1)
 
 
-def route(spec, logits, beta=None):
+def route(spec, logits, beta=None, theta=None):
     """Expert selection and gating weights for every token.
 
     Returns a dict with
@@ -108,7 +113,11 @@ def route(spec, logits, beta=None):
       margin   [T]            smallest gap between consecutive keys among the
                               top k+1 candidates (and, for the grouped router,
                               between the kept and the first dropped group
-                              score); a token is ambiguous when it is < 1e-6
+                              score; for the threshold router, between a
+                              candidate's key and 0); a token is ambiguous
+                              when it is < 1e-6
+    The threshold router (theta [E] required) fills slots past the token's
+    active experts with topk_idx = -1 and zero weight and score.
     """
     l = np.asarray(logits, np.float64)
     T, E = l.shape
@@ -159,6 +168,23 @@ def route(spec, logits, beta=None):
         margin = np.minimum(_adjacent_gap_min(sk, k), gmargin)
         ssel = np.take_along_axis(s, idx, axis=1)
         w = spec.route_scale * ssel / ssel.sum(axis=1, keepdims=True)
+        return dict(topk_idx=idx, topk_w=w, s_sel=ssel, keys=keys, margin=margin)
+
+    if spec.router == "sigmoid_threshold":
+        if theta is None:
+            raise ValueError("the threshold router needs theta")
+        s = sigmoid(l)
+        keys = l - np.asarray(theta, np.float64)[None, :]
+        order = _desc_order(keys)
+        cand = order[:, :k]
+        sk = np.take_along_axis(keys, cand, axis=1)
+        active = sk > 0.0
+        active[:, 0] = True                  # the best expert even below its threshold
+        idx = np.where(active, cand, -1)
+        ssel = np.where(active, np.take_along_axis(s, cand, axis=1), 0.0)
+        w = spec.route_scale * ssel / ssel.sum(axis=1, keepdims=True)
+        sorted_keys = np.take_along_axis(keys, order, axis=1)
+        margin = np.minimum(_adjacent_gap_min(sorted_keys, k), np.abs(sk).min(axis=1))
         return dict(topk_idx=idx, topk_w=w, s_sel=ssel, keys=keys, margin=margin)
 
     raise ValueError("unknown router " + spec.router)
@@ -287,9 +313,10 @@ def router_backward(spec, rt, omega):
     omega[t][j] = dL/dw[t][j] = <dy_t, o_j(x_t)>.
     Softmax families, w_j = c * p_j with p the softmax over the selected
     (weight) logits:  dl_j = w_j * (omega_j - sum_i w_i omega_i / c).
-    Sigmoid family, w_j = c * s_j / Z, Z = sum_S s:
-        ds_j = (c * omega_j - sum_i w_i omega_i) / Z,  dl_j = ds_j s_j (1 - s_j).
-    The bias has no gradient.
+    Sigmoid families, w_j = c * s_j / Z, Z = sum_S s over the selected (for
+    the threshold router: active) slots:
+        ds_j = (c * omega_j - sum_i w_i omega_i) / Z,  dl_j = ds_j s_j (1 - s_j)
+    (an empty slot, s = 0, gets 0).  The bias has no gradient.
     """
     w = rt["topk_w"]
     c = spec.route_scale
@@ -300,6 +327,27 @@ def router_backward(spec, rt, omega):
     Z = s.sum(axis=1, keepdims=True)
     ds = (c * omega - wo) / Z
     return ds * s * (1.0 - s)
+
+
+def threshold_backward(spec, rt, omega, E):
+    """dL/dtheta [E] of the threshold router, through a straight-through
+    estimator of the activation indicator a_e = [logit_e - theta_e > 0]: the
+    layer's output written as sum_e a_e c s_e o_e / sum_j a_j s_j gives
+    dL/da_e = s_e (c omega_e - sum_j w_j omega_j) / Z on an active expert, and
+    the estimator takes da_e/dtheta_e = -1 there.  Inactive experts, whose
+    outputs are never computed, contribute nothing; the logits keep their exact
+    gradient (router_backward)."""
+    w, ssel, idx = rt["topk_w"], rt["s_sel"], rt["topk_idx"]
+    c = spec.route_scale
+    Z = ssel.sum(axis=1, keepdims=True)
+    wo = (w * omega).sum(axis=1, keepdims=True)
+    g = -ssel * (c * omega - wo) / Z
+    dtheta = np.zeros(E)
+    for t in range(idx.shape[0]):
+        for j in range(idx.shape[1]):
+            if idx[t, j] >= 0:
+                dtheta[idx[t, j]] += g[t, j]
+    return dtheta
 
 
 # ----------------------------------------------------------------------------
@@ -347,7 +395,8 @@ def unpermute(dx_perm, row_of):
 # Whole layer
 # ----------------------------------------------------------------------------
 
-def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_f=None, zc=None, act=None):
+def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_f=None, zc=None, act=None,
+                  theta=None):
     """Forward of one MoE layer.
 
     x [T][d] float64; w_r [d][E_pool]; beta [E_pool] or None;
@@ -356,7 +405,8 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
     aux_coef > 0 adds the load-balancing loss (aux_f: the batch's fractions);
     zc = (ZeroComputeSpec, v, wc) appends zero-computation experts to the pool
     (E_pool = spec.E + their number), else None (E_pool = spec.E);
-    act: the routed experts' activation (None: SwiGLU; see glu).
+    act: the routed experts' activation (None: SwiGLU; see glu);
+    theta [E]: the threshold router's per-expert thresholds.
     Returns routing, maps and the per-row activations (permuted order) and y
     (and the auxiliary loss, its probabilities and fractions).
     """
@@ -367,7 +417,7 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
     if np.asarray(w_r).shape[1] != E_pool:
         raise ValueError("w_r must have one column per expert of the pool")
     l = router_logits(x, w_r)
-    rt = route(spec, l, beta)
+    rt = route(spec, l, beta, theta)
     # rows over the whole pool: the FFN experts' rows come first (lower ids),
     # a zero-computation expert's rows carry no data
     mp = sort_maps(rt["topk_idx"], E_pool)
@@ -400,7 +450,8 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
         probs = router_probs(spec, l, beta)
         eta = None if zc is None else zc_aux_weights(E, zc[0])
         aux = aux_loss(spec, probs, mp["counts"], aux_coef, aux_f, eta)
-        aux.update(probs=probs, coef=aux_coef, eta=eta)
+        aux.update(probs=probs, coef=aux_coef, eta=eta,
+                   sig=sigmoid(l) if spec.router == "sigmoid_threshold" else None)
     return dict(logits=l, route=rt, maps=mp, x_perm=x_perm, o=o, g=gs, u=us,
                 h=hs, y=y, shared=sh, f=fwidth, aux=aux, zc=zf)
 
@@ -410,8 +461,9 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
     whole layer.
 
     Returns dx [T][d], dw_r [d][E_pool], per-expert dict of dW/db,
-    shared-expert grads, omega [T][k], dl [T][k], and with zc the
-    zero-computation experts' dict (dv, dwc).
+    shared-expert grads, omega [T][k], dl [T][k], with zc the
+    zero-computation experts' dict (dv, dwc), and for the threshold router
+    dtheta [E].
     """
     x = np.asarray(x, np.float64)
     dy = np.asarray(dy, np.float64)
@@ -449,11 +501,11 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
     dx += unpermute(dx_perm, mp["row_ffn"])
     # router
     dl = router_backward(spec, rt, omega)
-    dl_dense = np.zeros((T, E_pool))
-    np.put_along_axis(dl_dense, rt["topk_idx"], dl, axis=1)
+    dl_dense = _scatter_slots(dl, rt["topk_idx"], E_pool)
     aux = fwd.get("aux")
     if aux is not None:
-        dl_dense = dl_dense + aux_loss_backward(aux["probs"], aux["f"], aux["coef"], aux.get("eta"))
+        dl_dense = dl_dense + aux_loss_backward(aux["probs"], aux["f"], aux["coef"], aux.get("eta"),
+                                                aux.get("sig"))
     dw_r = x.T @ dl_dense
     dx_router = dl_dense @ np.asarray(w_r, np.float64).T
     dx += dx_router
@@ -468,9 +520,18 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
         gsh.pop("dg")
         gsh.pop("du")
         sh = gsh
+    dtheta = threshold_backward(spec, rt, omega, E) if spec.router == "sigmoid_threshold" else None
     return dict(dx=dx, dw_r=dw_r, experts=grads, shared=sh, omega=omega, dl=dl,
                 dx_perm=dx_perm, do=do, dx_router=dx_router,
-                zc=None if zb is None else dict(dv=zb["dv"], dwc=zb["dwc"]))
+                zc=None if zb is None else dict(dv=zb["dv"], dwc=zb["dwc"]), dtheta=dtheta)
+
+
+def _scatter_slots(v, idx, E):
+    """dense [T][E] with v[t][s] at column idx[t][s] (empty slots, idx < 0, dropped)."""
+    out = np.zeros((idx.shape[0], E))
+    t, s = np.nonzero(idx >= 0)
+    out[t, idx[t, s]] = v[t, s]
+    return out
 
 
 # ----------------------------------------------------------------------------
@@ -487,9 +548,14 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
 
 def router_probs(spec, logits, beta=None):
     """p [T][E]: softmax over all E experts of the logits (plus beta when the
-    bias is added to the logits)."""
+    bias is added to the logits); for the threshold router the sigmoid scores
+    normalised over all experts, p_e = s_e / sum_j s_j (its variable-k form:
+    the gates are independent sigmoids, their shares are what balance)."""
     if spec.router == "sigmoid_grouped":
-        raise ValueError("the auxiliary loss is defined for the softmax routers")
+        raise ValueError("the auxiliary loss is defined for the softmax and threshold routers")
+    if spec.router == "sigmoid_threshold":
+        sg = sigmoid(np.asarray(logits, np.float64))
+        return sg / sg.sum(axis=1, keepdims=True)
     v = np.asarray(logits, np.float64)
     if beta is not None and spec.bias_mode == "logit":
         v = v + np.asarray(beta, np.float64)[None, :]
@@ -505,32 +571,39 @@ def aux_loss(spec, p, counts, coef, f=None, eta=None):
     p = np.asarray(p, np.float64)
     T, E = p.shape
     if f is None:
-        f = np.asarray(counts, np.float64) / float(T * spec.k)
+        # the routed slots: T*k, or for the threshold router (a variable number
+        # of experts per token) the slots actually filled
+        n = float(np.sum(counts)) if spec.router == "sigmoid_threshold" else float(T * spec.k)
+        f = np.asarray(counts, np.float64) / max(n, 1.0)
     f = np.asarray(f, np.float64)
     ef = f if eta is None else np.asarray(eta, np.float64) * f
     P = p.mean(axis=0)
     return dict(loss=coef * E * float(np.dot(ef, P)), P=P, f=f)
 
 
-def aux_loss_backward(p, f, coef, eta=None):
+def aux_loss_backward(p, f, coef, eta=None, sig=None):
     """dL/dlogit [T][E] of aux_loss with f held fixed: through P_e = mean_t
     p[t][e] and the softmax Jacobian dp_e/dl_j = p_e (delta_ej - p_j), with
     q = eta * f (q = f without weights),
-    dl[t][j] = coef * E / T * p[t][j] * (q_j - sum_e q_e p[t][e])."""
+    dl[t][j] = coef * E / T * p[t][j] * (q_j - sum_e q_e p[t][e]).
+    sig: the sigmoid scores of the threshold router, whose p = s / sum s has
+    dp_e/dl_j = p_e (delta_ej - p_j) (1 - s_j), so the same expression carries
+    the factor (1 - s_j)."""
     p = np.asarray(p, np.float64)
     T, E = p.shape
     q = np.asarray(f, np.float64)
     if eta is not None:
         q = np.asarray(eta, np.float64) * q
     F = p @ q
-    return coef * E / T * p * (q[None, :] - F[:, None])
+    dl = coef * E / T * p * (q[None, :] - F[:, None])
+    return dl if sig is None else dl * (1.0 - np.asarray(sig, np.float64))
 
 
 # ----------------------------------------------------------------------------
 # Evaluation of a layer too large to run whole
 # ----------------------------------------------------------------------------
 
-def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=None, act=None):
+def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=None, act=None, theta=None):
     """Every per-token result of the layer for a batch of tokens: routing, y,
     omega, dl and dx (no weight gradients).
 
@@ -547,7 +620,7 @@ def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=No
     T, d = x.shape
     E, k = spec.E, spec.k
     E_pool = np.asarray(w_r).shape[1]
-    rt = route(spec, router_logits(x, w_r), beta)
+    rt = route(spec, router_logits(x, w_r), beta, theta)
     idx, w = rt["topk_idx"], rt["topk_w"]
     y = np.zeros((T, d))
     dx = np.zeros((T, d))
@@ -558,8 +631,8 @@ def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=No
         omega += zb["omega"]
         dx += zb["dx"]
     for e in np.unique(idx):
-        if e >= E:
-            continue                         # zero-computation experts: above
+        if e >= E or e < 0:
+            continue                         # zero-computation experts (above), empty slots
         t, s = np.nonzero(idx == e)          # a token holds e in at most one slot
         wg, wu, wd, bg, bu, bd = expert_fn(int(e))
         g, u, h, o = expert_forward(x[t], wg, wu, wd, bg, bu, bd, act=act)
@@ -568,8 +641,7 @@ def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=No
         omega[t, s] = (dy[t] * o).sum(axis=1)
         dx[t] += expert_backward(x[t], g, u, h, we * dy[t], wg, wu, wd, act=act)["dx"]
     dl = router_backward(spec, rt, omega)
-    dl_dense = np.zeros((T, E_pool))
-    np.put_along_axis(dl_dense, idx, dl, axis=1)
+    dl_dense = _scatter_slots(dl, idx, E_pool)
     dx += dl_dense @ np.asarray(w_r, np.float64).T
     if shared is not None:
         g, u, h, osh = expert_forward(x, *shared)

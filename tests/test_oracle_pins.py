@@ -943,3 +943,156 @@ def test_clamped_glu_saturated_gate_passes_no_gradient():
     np.testing.assert_allclose(h, L * s * (np.clip(u, -L, L) + 1.0), rtol=1e-15)
     assert np.all(hg == 0.0)
     assert hu[0, 0] == 0.0 and hu[0, 1] == pytest.approx(L * s) and hu[0, 2] == pytest.approx(L * s)
+
+
+# ---------------------------------------------------------------------------
+# Threshold router (DynMoE-style: sigmoid gates, learned thresholds, variable k)
+# ---------------------------------------------------------------------------
+
+from oracle import threshold_backward  # noqa: E402,F401
+
+THR = RouterSpec("sigmoid_threshold", E=8, k=4)
+
+
+def _thr_case(seed, T=40, theta_mean=0.6):
+    c = make_case(THR, T=T, seed=seed, wr_std=0.4, expert_bias=False)
+    c["theta"] = theta_mean + 0.2 * np.random.default_rng(seed + 100).standard_normal(THR.E)
+    return c
+
+
+def run_thr(spec, c, coef=0.0):
+    fwd = layer_forward(spec, c["x"], c["w_r"], None, efn(c), aux_coef=coef, theta=c["theta"])
+    bwd = layer_backward(spec, c["x"], c["w_r"], None, efn(c), fwd, c["dy"])
+    return fwd, bwd
+
+
+def test_threshold_routing_invariants():
+    c = _thr_case(41, T=200)
+    fwd, _ = run_thr(THR, c)
+    rt = fwd["route"]
+    idx, w, keys = rt["topk_idx"], rt["topk_w"], rt["keys"]
+    n = (idx >= 0).sum(1)
+    assert n.min() >= 1 and n.max() <= THR.k and len(set(n.tolist())) >= 3   # the count varies
+    for t in range(idx.shape[0]):
+        act = idx[t][idx[t] >= 0]
+        assert np.all(idx[t][n[t]:] == -1)                        # active slots first
+        kk = keys[t, act]
+        assert np.all(np.diff(kk) <= 0)                           # descending key
+        above = np.nonzero(keys[t] > 0)[0]
+        if len(above) == 0:
+            assert len(act) == 1 and act[0] == int(np.argmax(keys[t]))   # the best one
+        else:
+            assert set(act.tolist()) <= set(above.tolist()) and len(act) == min(len(above), THR.k)
+    np.testing.assert_allclose(w.sum(1), 1.0, rtol=1e-14)
+    assert np.all(w[idx < 0] == 0) and np.all(w[idx >= 0] > 0)
+
+
+def torch_threshold_loss(spec, c, P, coef):
+    """Dense formulation: every expert for every token, the active mask from
+    detached keys, a straight-through indicator a = M + M (theta_d - theta) for
+    the thresholds, gates a s / sum(a s); plus the variable-k balance loss with
+    p = s / sum s and f the share of the filled slots."""
+    x, w_r, th = P["x"], P["w_r"], P["theta"]
+    l = x @ w_r
+    T, E = l.shape
+    s = torch.sigmoid(l)
+    key = (l - th).detach()
+    order = torch.argsort(-key, dim=1, stable=True)[:, :spec.k]
+    M = torch.zeros(T, E, dtype=torch.bool)
+    for t in range(T):
+        for j, e in enumerate(order[t].tolist()):
+            if j == 0 or key[t, e] > 0:
+                M[t, e] = True
+    Mf = M.double()
+    a = Mf + Mf * (th.detach() - th)
+    gate = a * s / (a * s).sum(1, keepdim=True)
+    y = 0
+    for e in range(E):
+        he = torch.nn.functional.silu(x @ P["wg"][e]) * (x @ P["wu"][e])
+        y = y + gate[:, e:e + 1] * (he @ P["wd"][e])
+    loss = (torch.tensor(c["dy"]) * y).sum()
+    if coef:
+        cnt = Mf.sum(0)
+        p = s / s.sum(1, keepdim=True)
+        loss = loss + coef * E * (cnt / cnt.sum() * p.mean(0)).sum()
+    return loss, M
+
+
+@pytest.mark.parametrize("coef", [0.0, 0.7])
+def test_threshold_router_matches_torch_autograd(coef):
+    c = _thr_case(42)
+    fwd = layer_forward(THR, c["x"], c["w_r"], None, efn(c), aux_coef=coef, theta=c["theta"])
+    bwd = layer_backward(THR, c["x"], c["w_r"], None, efn(c), fwd, c["dy"])
+    P = {n: torch.tensor(c[n], dtype=torch.float64, requires_grad=True)
+         for n in ("x", "w_r", "wg", "wu", "wd", "theta")}
+    loss, M = torch_threshold_loss(THR, c, P, coef)
+    loss.backward()
+    idx = fwd["route"]["topk_idx"]
+    mine = np.zeros_like(M.numpy())
+    for t in range(idx.shape[0]):
+        mine[t, idx[t][idx[t] >= 0]] = True
+    assert np.array_equal(mine, M.numpy())
+    ours = float((c["dy"] * fwd["y"]).sum()) + (fwd["aux"]["loss"] if coef else 0.0)
+    assert abs(loss.item() - ours) <= 1e-12 * abs(loss.item())
+    assert rel(bwd["dx"], P["x"].grad.numpy()) < 1e-11
+    assert rel(bwd["dw_r"], P["w_r"].grad.numpy()) < 1e-11
+    assert rel(bwd["dtheta"], P["theta"].grad.numpy()) < 1e-11
+    for e in range(THR.E):
+        for o_, t_ in (("dw_gate", "wg"), ("dw_up", "wu"), ("dw_down", "wd")):
+            want = P[t_].grad[e].numpy()
+            if np.linalg.norm(want) == 0:
+                assert np.linalg.norm(bwd["experts"][e][o_]) == 0
+            else:
+                assert rel(bwd["experts"][e][o_], want) < 1e-11
+
+
+def test_threshold_router_gradients_match_finite_differences():
+    c = _thr_case(43, T=16)
+    coef = 0.5
+    fwd = layer_forward(THR, c["x"], c["w_r"], None, efn(c), aux_coef=coef, theta=c["theta"])
+    bwd = layer_backward(THR, c["x"], c["w_r"], None, efn(c), fwd, c["dy"])
+
+    def total(cc):
+        fw = layer_forward(THR, cc["x"], cc["w_r"], None, efn(cc), aux_coef=coef, theta=cc["theta"])
+        return float((cc["dy"] * fw["y"]).sum()) + fw["aux"]["loss"], fw["route"]["topk_idx"]
+
+    rng = np.random.default_rng(9)
+    h = 1e-6
+    checked = 0
+    for key, gr in (("x", bwd["dx"]), ("w_r", bwd["dw_r"]),
+                    ("wd", np.stack([bwd["experts"][e]["dw_down"] for e in range(THR.E)]))):
+        for _ in range(3):
+            v = rng.standard_normal(c[key].shape)
+            v /= np.linalg.norm(v)
+            lp, ip = total(dict(c, **{key: c[key] + h * v}))
+            lm, im = total(dict(c, **{key: c[key] - h * v}))
+            if not (np.array_equal(ip, fwd["route"]["topk_idx"]) and np.array_equal(im, fwd["route"]["topk_idx"])):
+                continue
+            fd = (lp - lm) / (2 * h)
+            an = float((gr * v).sum())
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (key, fd, an)
+            checked += 1
+    assert checked >= 6
+
+
+def test_threshold_router_limits_reduce_to_fixed_k_routers():
+    """Thresholds far above every logit: only the best expert, weight 1 (the
+    top-1 softmax router).  Far below: every expert passes and the capacity
+    keeps the k largest logits, weights s / sum s (the sigmoid router without
+    groups or bias).  Outputs and gradients equal those routers' bit for bit
+    up to rounding."""
+    c = _thr_case(44)
+    for theta, ref_spec in ((1e9, RouterSpec("softmax_topk", E=8, k=1)),
+                            (-1e9, RouterSpec("sigmoid_grouped", E=8, k=4))):
+        c1 = dict(c, theta=np.full(THR.E, theta))
+        fwd, bwd = run_thr(THR, c1)
+        spec_k = ref_spec
+        fr = layer_forward(spec_k, c["x"], c["w_r"], None, efn(c))
+        br = layer_backward(spec_k, c["x"], c["w_r"], None, efn(c), fr, c["dy"])
+        act = fwd["route"]["topk_idx"][:, :spec_k.k]
+        assert np.array_equal(act, fr["route"]["topk_idx"])
+        assert rel(fwd["y"], fr["y"]) < 1e-14 and rel(bwd["dx"], br["dx"]) < 1e-13
+        assert rel(bwd["dw_r"], br["dw_r"]) < 1e-13 if np.linalg.norm(br["dw_r"]) else np.abs(bwd["dw_r"]).max() < 1e-15
+        for e in range(THR.E):
+            assert rel(bwd["experts"][e]["dw_gate"], br["experts"][e]["dw_gate"]) < 1e-13 or \
+                np.linalg.norm(br["experts"][e]["dw_gate"]) == 0
