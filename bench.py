@@ -126,9 +126,10 @@ def cpu_baseline(cfg, seed, tokens, reps=1):
               inp["zc_v"].astype(np.float64) if nc else np.zeros((0, scfg["d"])),
               inp["zc_wc"].astype(np.float64) if nc else np.zeros((0, 2, scfg["d"])))
     coef = cfg.get("aux_coef", 0.0)
+    theta = None if inp.get("gate_threshold") is None else inp["gate_threshold"].astype(np.float64)
     t0 = time.perf_counter()
     for _ in range(reps):
-        fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=coef, zc=zc)
+        fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=coef, zc=zc, theta=theta)
         layer_backward(spec, x, w_r, beta, efn, fwd, dy, shared, with_bias=scfg["expert_bias"], zc=zc)
     wall = time.perf_counter() - t0
     _, fb = layer_flops(scfg, rows=int(fwd["maps"]["offsets"][scfg["E"]]))
@@ -265,7 +266,8 @@ def main():
         return torch.from_numpy(a).cuda()
 
     params = {n: dev(inp.get(n)) for n in ("w_r", "router_bias", "w_gate", "w_up", "w_down", "b_gate",
-                                           "b_up", "b_down", "ws_gate", "ws_up", "ws_down", "zc_v", "zc_wc")}
+                                           "b_up", "b_down", "ws_gate", "ws_up", "ws_down", "zc_v", "zc_wc",
+                                           "gate_threshold")}
     x = dev(inp["x"])
     dy = dev(inp["dy"])
     del inp
@@ -281,11 +283,12 @@ def main():
         step()
     torch.cuda.synchronize()
     zc = pool(cfg) > cfg["E"]
-    # routed FFN rows (every slot when the pool holds only FFN experts)
-    ffn_rows = int(layer.saved["expert_offsets"][cfg["E"]].item()) if zc else cfg["T"] * cfg["k"]
-    if args.memory_kernels and zc:
-        print("--memory-kernels drives the component entry points, which take no zero-computation "
-              "experts", file=sys.stderr)
+    variable = zc or cfg["router"] == "sigmoid_threshold"
+    # routed FFN rows (every slot when every slot holds an FFN expert)
+    ffn_rows = int(layer.saved["expert_offsets"][cfg["E"]].item()) if variable else cfg["T"] * cfg["k"]
+    if args.memory_kernels and variable:
+        print("--memory-kernels drives the component entry points, which take neither zero-computation "
+              "experts nor the threshold router", file=sys.stderr)
         sys.exit(2)
     if args.memory_kernels:
         workload = "%s moe layer T=%d d=%d E=%d k=%d f=%d" % (cfg["name"], cfg["T"], cfg["d"], cfg["E"],
@@ -375,7 +378,8 @@ def main():
         "config": dict({"workload": workload, "T": cfg["T"], "d": cfg["d"], "E": cfg["E"], "k": cfg["k"],
                         "f": cfg["f"], "router": cfg["router"], "aux_coef": cfg.get("aux_coef", 0.0)},
                        **({"n_zero": cfg["n_zero"], "n_copy": cfg["n_copy"], "n_const": cfg["n_const"],
-                           "zc_aux_weight": cfg["zc_aux_weight"], "ffn_rows": ffn_rows} if zc else {})),
+                           "zc_aux_weight": cfg["zc_aux_weight"]} if zc else {}),
+                       **({"ffn_rows": ffn_rows} if variable else {})),
         "tokens_per_s": round(cfg["T"] / (ms_per_step / 1e3), 1),
         "phases_median_of_last_10": {"fwd_ms": round(med(f_ms), 4), "bwd_ms": round(med(b_ms), 4),
                                      "step_ms": round(med(s_ms), 4),

@@ -97,8 +97,26 @@ enum {
  *   experts form n_groups contiguous groups, a group scores the sum of its two
  *   largest keys, the topk_groups best groups are kept and the top-k keys
  *   among their experts selected; weight = route_scale * s / sum of the
- *   selected s (DeepSeek-V3). */
-enum { MOE_ROUTER_SOFTMAX_TOPK = 0, MOE_ROUTER_TOPK_SOFTMAX = 1, MOE_ROUTER_SIGMOID_GROUPED = 2 };
+ *   selected s (DeepSeek-V3).
+ * SIGMOID_THRESHOLD: the DynMoE task of the paper's appendix B.3 (per-expert
+ *   sigmoid gates and a learned threshold, so the number of active experts
+ *   varies per token).  Expert e is active for token t when
+ *   logit - gate_threshold[e] > 0; the active experts fill the slots in
+ *   descending order of that key, at most k of them (k is the slot capacity)
+ *   and at least one (the best key, even when none passes); weights
+ *   route_scale * s / sum of the active s, s = sigmoid(logit).  Empty slots
+ *   hold topk_idx = -1, topk_w = s_sel = 0.  The thresholds get a gradient
+ *   through a straight-through estimator of the activation indicator on the
+ *   active experts: dL/dtheta_e = -sum over the slots holding e of
+ *   s (route_scale omega - sum_j w_j omega_j) / sum of the active s.
+ *   Needs n_groups = 1, bias_mode = NONE and no zero-computation experts;
+ *   runs through the layer entry points (moe_route refuses it). */
+enum {
+  MOE_ROUTER_SOFTMAX_TOPK = 0,
+  MOE_ROUTER_TOPK_SOFTMAX = 1,
+  MOE_ROUTER_SIGMOID_GROUPED = 2,
+  MOE_ROUTER_SIGMOID_THRESHOLD = 3
+};
 
 /* Router bias: none; added to the selection key only; added to the logits
  * (selection and weights).  The bias never receives a gradient. */
@@ -167,13 +185,14 @@ typedef struct moe_params {
                                   routed-slot fractions counts / (T k)) */
   const float* zc_v;           /* [n_const][d] constant experts' vectors */
   const float* zc_wc;          /* [n_const][2][d] constant experts' mixing weights */
+  const float* gate_threshold; /* [E] thresholds of MOE_ROUTER_SIGMOID_THRESHOLD */
 } moe_params;
 
 /* Tensors the forward writes and the backward reads (caller-allocated). */
 typedef struct moe_saved {
   int32_t* topk_idx;           /* [T][k] */
   float* topk_w;               /* [T][k] */
-  float* s_sel;                /* [T][k], SIGMOID_GROUPED only (else may be NULL) */
+  float* s_sel;                /* [T][k], the sigmoid routers only (else may be NULL) */
   int32_t* expert_offsets;     /* [E_pool+1] */
   int32_t* row_of;             /* [T][k] */
   int32_t* token_of;           /* [R] */
@@ -184,7 +203,8 @@ typedef struct moe_saved {
   void* gu_sh;                 /* [T][2 f_shared], n_shared */
   void* h_sh;                  /* [T][f_shared], n_shared */
   void* o_sh;                  /* [T][d], n_shared */
-  float* router_probs;         /* [T][E_pool] softmax over all experts, aux_coef > 0 */
+  float* router_probs;         /* [T][E_pool] softmax over all experts, aux_coef > 0
+                                  (threshold router: the sigmoid scores of all experts) */
   float* aux_loss;             /* [1] the auxiliary loss value, aux_coef > 0 */
 } moe_saved;
 
@@ -202,6 +222,7 @@ typedef struct moe_grads {
   void* dws_down;              /* [f_shared][d], n_shared */
   float* dzc_v;                /* [n_const][d], n_const > 0 */
   float* dzc_wc;               /* [n_const][2][d], n_const > 0 */
+  float* d_threshold;          /* [E], MOE_ROUTER_SIGMOID_THRESHOLD */
 } moe_grads;
 
 /* Workspace bytes.  fwd_ws: enough for moe_route, moe_permute and
@@ -310,7 +331,7 @@ int moe_shared_expert_bwd(const moe_shape* shape, const void* x, const void* dy,
                           void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Whole layer forward: route, permute, grouped SwiGLU experts, shared expert,
- * combine.  Fills every pointer of *saved (s_sel only for SIGMOID_GROUPED,
+ * combine.  Fills every pointer of *saved (s_sel only for the sigmoid routers,
  * the *_sh tensors only with a shared expert) and y.  ws: fwd_ws bytes. */
 int moe_layer_fwd(const moe_shape* shape, const moe_params* params, const void* x,
                   const moe_saved* saved, void* y, void* ws, size_t ws_bytes, hipStream_t stream);
@@ -336,7 +357,7 @@ int moe_layer_bwd(const moe_shape* shape, const moe_params* params, const void* 
  *   router and shared-expert paths).  Leaves d_o, dgu, dl (and the shared
  *   expert's dgu, the zero-computation slots' coefficients) in ws, which the
  *   caller must keep unchanged until the matching moe_layer_bwd_wgrad call.
- *   Pointers of *saved read: topk_idx, topk_w, s_sel (SIGMOID_GROUPED),
+ *   Pointers of *saved read: topk_idx, topk_w, s_sel (sigmoid routers),
  *   expert_offsets, row_of, gu, o, gu_sh.
  * moe_layer_bwd_wgrad: expert wgrads (+ biases), dW_r, shared-expert wgrads
  *   and the constant experts' dzc_v, dzc_wc into *grads, from what the dgrad

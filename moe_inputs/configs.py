@@ -20,10 +20,15 @@ those models' MoE layers on one GPU:
               experts plus 8 zero, 8 copy and 16 constant experts, one
               zero-computation expert per four FFN experts and zero : copy :
               constant = 1 : 1 : 2 as in the MoE++ work's configurations
+  6 dynmoe    Qwen3 dims with DynMoE-style threshold gating (appendix B.3
+              lists DynMoE among the new-feature tasks): sigmoid gates on the
+              128 experts, per-expert thresholds ~ N(1.8, 0.1) on the logits,
+              at most k = 8 active experts per token (on average about 3)
 
 Fields:
   T, d, E, k, f          tokens, hidden, routed experts, top-k, expert width
-  router                 'softmax_topk' | 'topk_softmax' | 'sigmoid_grouped'
+  router                 'softmax_topk' | 'topk_softmax' | 'sigmoid_grouped' |
+                         'sigmoid_threshold'
   n_groups, topk_groups  expert groups and groups kept (1, 1 = no group limit)
   route_scale            factor on the renormalised weights
   bias_mode              'none' | 'select' (selection key only) | 'logit'
@@ -34,6 +39,7 @@ Fields:
   n_zero, n_copy, n_const  zero-computation experts after the E FFN experts
                          (the router covers E + their number)
   zc_aux_weight          their weight in the load-balancing loss
+  theta_mean, theta_std  thresholds of the 'sigmoid_threshold' router
   act, act_alpha, act_limit  routed experts' activation: 'swiglu' or
                          'clamped_glu' (the GPT-OSS release's variant; its
                          slope and clamp bound)
@@ -44,7 +50,7 @@ import copy
 TENSOR_IDS = {
     "x": 0, "w_r": 1, "w_gate": 2, "w_up": 3, "w_down": 4,
     "b_gate": 5, "b_up": 6, "b_down": 7, "router_bias": 8, "dy": 9,
-    "ws_gate": 10, "ws_up": 11, "ws_down": 12, "zc_v": 13, "zc_wc": 14,
+    "ws_gate": 10, "ws_up": 11, "ws_down": 12, "zc_v": 13, "zc_wc": 14, "gate_threshold": 15,
 }
 
 _BASE = dict(
@@ -52,7 +58,7 @@ _BASE = dict(
     expert_bias=False, n_shared=0, f_shared=0,
     x_std=1.0, w_r_std=0.02, w_std=0.02, b_std=0.02, beta_std=0.1, dy_std=1.0,
     n_zero=0, n_copy=0, n_const=0, zc_aux_weight=1.0, zc_v_std=1.0, zc_wc_std=0.02,
-    act="swiglu", act_alpha=1.702, act_limit=7.0,
+    act="swiglu", act_alpha=1.702, act_limit=7.0, theta_mean=1.8, theta_std=0.1,
 )
 
 
@@ -77,6 +83,8 @@ CONFIGS = [
         zipf_s=1.2, n_empty=8),
     _mk(cfg_id=5, name="moepp", T=8192, d=2048, E=128, k=8, f=768,
         router="softmax_topk", dtype="bf16", n_zero=8, n_copy=8, n_const=16, zc_aux_weight=0.5),
+    _mk(cfg_id=6, name="dynmoe", T=8192, d=2048, E=128, k=8, f=768,
+        router="sigmoid_threshold", dtype="bf16"),
 ]
 
 

@@ -14,7 +14,8 @@ Distributions follow the workload statement: x ~ N(0,1), W_r ~ N(0,0.02),
 expert weights and biases ~ N(0,0.02), DeepSeek-style selection bias
 ~ N(0,0.1), upstream gradient dy ~ N(0,1) (the second argument of N is the
 standard deviation); constant zero-computation experts: v ~ N(0,1),
-W_c ~ N(0,0.02), both float32.  The stress config's logit bias is stored data (see
+W_c ~ N(0,0.02), both float32; the threshold router's thresholds
+~ N(theta_mean, theta_std) float32.  The stress config's logit bias is stored data (see
 ``stress_router_bias``).
 """
 import os
@@ -191,6 +192,10 @@ def layer_inputs(cfg, seed=0, experts=True, with_dy=True, threads=None):
         out["ws_down"] = gen_tensor(seed, cfg, "ws_down", (fs, d), cfg["w_std"], dt)
     else:
         out["ws_gate"] = out["ws_up"] = out["ws_down"] = None
+    out["gate_threshold"] = None
+    if cfg["router"] == "sigmoid_threshold":
+        th = _draw(seed, cfg["cfg_id"], "gate_threshold", 0, (E,), cfg["theta_std"])
+        out["gate_threshold"] = (th + np.float32(cfg["theta_mean"])).astype(np.float32)
     nc = cfg.get("n_const", 0)
     out["zc_v"] = _draw(seed, cfg["cfg_id"], "zc_v", 0, (nc, d), cfg["zc_v_std"]) if nc else None
     out["zc_wc"] = _draw(seed, cfg["cfg_id"], "zc_wc", 0, (nc, 2, d), cfg["zc_wc_std"]) if nc else None

@@ -20,8 +20,9 @@ MOE_ERR_WORKSPACE = -4
 MOE_ROUTER_SOFTMAX_TOPK = 0
 MOE_ROUTER_TOPK_SOFTMAX = 1
 MOE_ROUTER_SIGMOID_GROUPED = 2
+MOE_ROUTER_SIGMOID_THRESHOLD = 3
 ROUTERS = {"softmax_topk": MOE_ROUTER_SOFTMAX_TOPK, "topk_softmax": MOE_ROUTER_TOPK_SOFTMAX,
-           "sigmoid_grouped": MOE_ROUTER_SIGMOID_GROUPED}
+           "sigmoid_grouped": MOE_ROUTER_SIGMOID_GROUPED, "sigmoid_threshold": MOE_ROUTER_SIGMOID_THRESHOLD}
 MOE_BIAS_NONE = 0
 MOE_BIAS_SELECT_ONLY = 1
 MOE_BIAS_LOGIT = 2
@@ -65,7 +66,7 @@ _VP = ctypes.c_void_p
 class moe_params(ctypes.Structure):
     _fields_ = [(n, _VP) for n in ("w_r", "router_bias", "w_gate", "w_up", "w_down", "b_gate",
                                    "b_up", "b_down", "ws_gate", "ws_up", "ws_down", "aux_f",
-                                   "zc_v", "zc_wc")]
+                                   "zc_v", "zc_wc", "gate_threshold")]
 
 
 class moe_saved(ctypes.Structure):
@@ -76,7 +77,8 @@ class moe_saved(ctypes.Structure):
 
 class moe_grads(ctypes.Structure):
     _fields_ = [(n, _VP) for n in ("dw_r", "dw_gate", "dw_up", "dw_down", "db_gate", "db_up",
-                                   "db_down", "dws_gate", "dws_up", "dws_down", "dzc_v", "dzc_wc")]
+                                   "db_down", "dws_gate", "dws_up", "dws_down", "dzc_v", "dzc_wc",
+                                   "d_threshold")]
 
 
 def _load():

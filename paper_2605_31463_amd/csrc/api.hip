@@ -78,7 +78,7 @@ const char* kernel_name(int id) {
       "combine_fwd", "combine_bwd", "route_dl", "route_dwr_partial", "route_dwr_reduce",
       "wr_transpose", "route_dx", "gemm_down_dgrad", "gemm_gateup_dgrad", "gemm_down_wgrad",
       "gemm_gateup_wgrad", "unpermute", "rank", "wr_split", "route_select", "aux_stats", "aux_grad",
-      "aux_dwr", "zc_param_partial", "zc_param_reduce"};
+      "aux_dwr", "zc_param_partial", "zc_param_reduce", "threshold_grad", "aux_partial_rows"};
   if (id < 0 || id >= K_NUM_KERNELS) return nullptr;
   return names[id];
 }
@@ -95,6 +95,8 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // experts after them.
 inline int64_t epool(const moe_shape& s) { return s.E + s.n_zero + s.n_copy + s.n_const; }
 inline bool has_zc(const moe_shape& s) { return s.n_zero + s.n_copy + s.n_const > 0; }
+inline bool is_thr(const moe_shape& s) { return s.router == MOE_ROUTER_SIGMOID_THRESHOLD; }
+inline bool is_sigm(const moe_shape& s) { return s.router == MOE_ROUTER_SIGMOID_GROUPED || is_thr(s); }
 
 int check_shape(const moe_shape* sh) {
   if (!sh) return moe_set_error(MOE_ERR_INVALID_ARG, "shape is NULL");
@@ -103,8 +105,10 @@ int check_shape(const moe_shape* sh) {
     return moe_set_error(MOE_ERR_INVALID_ARG, "negative zero-computation expert count");
   if (!(s.zc_aux_weight >= 0.f) || !isfinite(s.zc_aux_weight))
     return moe_set_error(MOE_ERR_INVALID_ARG, "zc_aux_weight must be finite and non-negative");
-  if (has_zc(s) && s.router == MOE_ROUTER_SIGMOID_GROUPED)
+  if (has_zc(s) && (s.router == MOE_ROUTER_SIGMOID_GROUPED || s.router == MOE_ROUTER_SIGMOID_THRESHOLD))
     return moe_set_error(MOE_ERR_UNSUPPORTED, "zero-computation experts need a softmax router");
+  if (s.router == MOE_ROUTER_SIGMOID_THRESHOLD && s.bias_mode != MOE_BIAS_NONE)
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "the threshold router takes no router bias");
   if (s.act != MOE_ACT_SWIGLU && s.act != MOE_ACT_CLAMPED_GLU)
     return moe_set_error(MOE_ERR_INVALID_ARG, "unknown activation %d", s.act);
   if (s.act == MOE_ACT_CLAMPED_GLU &&
@@ -116,7 +120,7 @@ int check_shape(const moe_shape* sh) {
   if (s.k > epool(s))
     return moe_set_error(MOE_ERR_INVALID_ARG, "k=%lld exceeds the %lld experts of the pool", (long long)s.k,
                          (long long)epool(s));
-  if (s.router < MOE_ROUTER_SOFTMAX_TOPK || s.router > MOE_ROUTER_SIGMOID_GROUPED)
+  if (s.router < MOE_ROUTER_SOFTMAX_TOPK || s.router > MOE_ROUTER_SIGMOID_THRESHOLD)
     return moe_set_error(MOE_ERR_INVALID_ARG, "unknown router %d", s.router);
   if (s.bias_mode < MOE_BIAS_NONE || s.bias_mode > MOE_BIAS_LOGIT)
     return moe_set_error(MOE_ERR_INVALID_ARG, "unknown bias_mode %d", s.bias_mode);
@@ -167,7 +171,7 @@ struct Plan {
   // backward
   size_t d_o, dgu, dx_perm, dl, partial, w_rt, dgu_sh, dx_sh;
   size_t aux_dl, aux_dx, aux_off, aux_wpart;
-  size_t zc_coef, zc_part;
+  size_t zc_coef, zc_part, dth;
   size_t bwd_total;
   size_t saved_total;
 };
@@ -211,6 +215,7 @@ Plan plan(const moe_shape& s) {
   p.aux_wpart = off; off += aux ? align_up((size_t)aux_groups(s) * s.d * aux_epad(s) * eb) : 0;
   p.zc_coef = off; off += has_zc(s) ? align_up((size_t)R * 16) : 0;
   p.zc_part = off; off += s.n_const > 0 ? align_up((size_t)moe::route_dwr_tasks(R, s.n_const) * 3 * s.d * 4) : 0;
+  p.dth = off; off += is_thr(s) ? align_up((size_t)R * 4) : 0;
   p.bwd_total = off;
   size_t sv = 0;
   sv += (size_t)R * (4 + 4 + 4 + 4 + 4);  // topk_idx, topk_w, s_sel, row_of, token_of
@@ -270,9 +275,11 @@ GemmArgs gemm_dense(const moe_shape& s, int mode) {
 }
 
 int do_route(const moe_shape& s, const void* x, const float* w_r, const float* bias, int32_t* topk_idx,
-             float* topk_w, float* s_sel, int32_t* counts, void* ws, hipStream_t st, float* probs = nullptr) {
+             float* topk_w, float* s_sel, int32_t* counts, void* ws, hipStream_t st, float* probs = nullptr,
+             const float* threshold = nullptr) {
   RouteArgs a{};
   a.probs = probs;
+  a.threshold = threshold;
   a.wsplit = s.dtype == MOE_BF16 ? wsp(ws, plan(s).wsplit) : nullptr;
   a.lg = s.dtype == MOE_BF16 ? reinterpret_cast<double*>(wsp(ws, plan(s).lg)) : nullptr;
   a.x = x;
@@ -442,6 +449,7 @@ AuxArgs aux_args(const moe_shape& s, const moe_params* prm, const moe_saved* sv)
   a.coef = s.aux_coef;
   a.E_ffn = has_zc(s) ? (int)s.E : (int)epool(s);
   a.zc_weight = s.zc_aux_weight;
+  a.thr = is_thr(s);
   a.loss = sv->aux_loss;
   return a;
 }
@@ -484,8 +492,8 @@ static_assert(sizeof(moe_shape) == 120 && offsetof(moe_shape, f_shared) == 56 &&
                   offsetof(moe_shape, aux_coef) == 88 && offsetof(moe_shape, zc_aux_weight) == 104 &&
                   offsetof(moe_shape, act_limit) == 116,
               "moe_shape layout");
-static_assert(sizeof(moe_params) == 14 * sizeof(void*) && sizeof(moe_saved) == 15 * sizeof(void*) &&
-                  sizeof(moe_grads) == 12 * sizeof(void*),
+static_assert(sizeof(moe_params) == 15 * sizeof(void*) && sizeof(moe_saved) == 15 * sizeof(void*) &&
+                  sizeof(moe_grads) == 13 * sizeof(void*),
               "pointer struct layouts");
 
 // ---------------------------------------------------------------------------
@@ -508,6 +516,10 @@ int check_layer_bwd(const moe_shape& s, const moe_params* prm, const void* x, co
     MOE_NEED(gr, "grads");
     MOE_NEED(gr->dzc_v, "grads.dzc_v");
     MOE_NEED(gr->dzc_wc, "grads.dzc_wc");
+  }
+  if (is_thr(s) && (phase & 2)) {
+    MOE_NEED(gr, "grads");
+    MOE_NEED(gr->d_threshold, "grads.d_threshold");
   }
   if (phase & 1) {
     MOE_NEED(prm->w_gate, "params.w_gate");
@@ -546,7 +558,7 @@ int check_layer_bwd(const moe_shape& s, const moe_params* prm, const void* x, co
       MOE_NEED(sv->row_of, "saved.row_of");
       MOE_NEED(sv->gu, "saved.gu");
       MOE_NEED(sv->o, "saved.o");
-      if (s.router == MOE_ROUTER_SIGMOID_GROUPED) MOE_NEED(sv->s_sel, "saved.s_sel");
+      if (is_sigm(s)) MOE_NEED(sv->s_sel, "saved.s_sel");
       if (s.n_shared) MOE_NEED(sv->gu_sh, "saved.gu_sh");
       if (has_aux(s)) MOE_NEED(sv->router_probs, "saved.router_probs");
     }
@@ -587,6 +599,7 @@ int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const void* x, co
   cb.route_scale = s.route_scale;
   cb.topk_idx = sv->topk_idx;
   cb.zc = zc_args(s, prm, x, dy, wsp(ws, p.zc_coef));
+  cb.dth = is_thr(s) ? reinterpret_cast<float*>(wsp(ws, p.dth)) : nullptr;
   MOE_TRY(launch_combine_bwd(cb, stream));
   // 2. expert dgrads
   MOE_TRY(do_gemm_bwd(s, MOE_DGRAD, nullptr, sv->expert_offsets, sv->gu, nullptr, d_o, prm->w_gate, prm->w_up,
@@ -681,6 +694,9 @@ int layer_bwd_wgrad(const moe_shape& s, const moe_params* prm, const void* x, co
     MOE_TRY(launch_gemm(g, stream));
     MOE_TRY(launch_aux_dwr(part, G, (int)s.d, (int)epool(s), E_pad, s.dtype == MOE_BF16, gr->dw_r, stream));
   }
+  if (is_thr(s))
+    MOE_TRY(launch_threshold_grad(sv->expert_offsets, sv->token_of, reinterpret_cast<const float*>(wsp(ws, p.dth)),
+                                  (int)s.E, gr->d_threshold, accumulate, stream));
   if (s.n_const > 0) {
     // constant experts' dv and dW_c over their rows
     ZcParamArgs z{};
@@ -761,6 +777,8 @@ int moe_route(const moe_shape* shape, const void* x, const float* w_r, const flo
               float* topk_w, float* s_sel, int32_t* expert_counts, void* ws, size_t ws_bytes, hipStream_t stream) {
   MOE_TRY(check_shape(shape));
   const moe_shape& s = *shape;
+  if (is_thr(s))
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "moe_route: the threshold router needs the layer entry points");
   if (s.T > 0) {
     MOE_NEED(x, "x");
     MOE_NEED(topk_idx, "topk_idx");
@@ -919,7 +937,7 @@ int moe_route_bwd(const moe_shape* shape, const void* x, const float* w_r, const
     MOE_NEED(topk_w, "topk_w");
     MOE_NEED(d_topk_w, "d_topk_w");
     MOE_NEED(token_of, "token_of");
-    if (s.router == MOE_ROUTER_SIGMOID_GROUPED) MOE_NEED(s_sel, "s_sel");
+    if (is_sigm(s)) MOE_NEED(s_sel, "s_sel");
   }
   const Plan p = plan(s);
   MOE_TRY(check_ws(ws, ws_bytes, p.bwd_total));
@@ -1040,7 +1058,7 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, 
     MOE_NEED(sv->gu, "saved.gu");
     MOE_NEED(sv->h, "saved.h");
     MOE_NEED(sv->o, "saved.o");
-    if (s.router == MOE_ROUTER_SIGMOID_GROUPED) MOE_NEED(sv->s_sel, "saved.s_sel");
+    if (is_sigm(s)) MOE_NEED(sv->s_sel, "saved.s_sel");
     if (s.n_shared) {
       MOE_NEED(sv->gu_sh, "saved.gu_sh");
       MOE_NEED(sv->h_sh, "saved.h_sh");
@@ -1055,12 +1073,13 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, 
     MOE_NEED(prm->zc_v, "params.zc_v");
     MOE_NEED(prm->zc_wc, "params.zc_wc");
   }
+  if (is_thr(s)) MOE_NEED(prm->gate_threshold, "params.gate_threshold");
   MOE_TRY(check_ws(ws, ws_bytes, plan(s).fwd_total));
   const void* bg = s.expert_bias ? prm->b_gate : nullptr;
   const void* bu = s.expert_bias ? prm->b_up : nullptr;
   const void* bd = s.expert_bias ? prm->b_down : nullptr;
   MOE_TRY(do_route(s, x, prm->w_r, prm->router_bias, sv->topk_idx, sv->topk_w, sv->s_sel, nullptr, ws, stream,
-                   has_aux(s) ? sv->router_probs : nullptr));
+                   has_aux(s) ? sv->router_probs : nullptr, prm->gate_threshold));
   MOE_TRY(do_permute(s, x, sv->topk_idx, sv->expert_offsets, sv->row_of, sv->token_of, sv->x_perm, ws, stream));
   if (has_aux(s)) {
     AuxArgs aa = aux_args(s, prm, sv);

@@ -16,10 +16,12 @@
 namespace moe {
 namespace {
 
-// eta_e f_e: zero-computation experts (e >= E_ffn) weigh zc_weight
+// eta_e f_e: zero-computation experts (e >= E_ffn) weigh zc_weight.  The
+// threshold router fills a variable number of slots: f is the share of the
+// filled ones.
 __device__ __forceinline__ double aux_frac(const AuxArgs& a, int e) {
-  const double f = a.aux_f ? (double)a.aux_f[e]
-                           : (double)(a.offsets[e + 1] - a.offsets[e]) / ((double)a.T * (double)a.k);
+  const double n = a.thr ? (double)max(a.offsets[a.E], 1) : (double)a.T * (double)a.k;
+  const double f = a.aux_f ? (double)a.aux_f[e] : (double)(a.offsets[e + 1] - a.offsets[e]) / n;
   return e >= a.E_ffn ? (double)a.zc_weight * f : f;
 }
 
@@ -85,6 +87,36 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
+// Threshold router: column sums of p = s / sum_e s (s the sigmoid scores in
+// probs) over blocks of 256 tokens; each wavefront takes 64 tokens in order
+// (the per-token sum over experts is a wave sum), expert e = lane + 64 q, and
+// the four wavefronts' sums are added in order.
+__global__ __launch_bounds__(256) void aux_partial_rows_kernel(AuxArgs a) {
+  __shared__ double red[4][256];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  const int64_t tb = (int64_t)blockIdx.x * 256 + w * 64;
+  for (int j = 0; j < 64; ++j) {
+    const int64_t t = tb + j;
+    if (t >= a.T) break;
+    double sv[4], S = 0.0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = lane + 64 * q;
+      sv[q] = e < a.E ? (double)a.probs[t * a.E + e] : 0.0;
+      S += sv[q];
+    }
+    S = wave_sum(S);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[q] += sv[q] / S;
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) red[w][lane + 64 * q] = acc[q];
+  __syncthreads();
+  for (int e = threadIdx.x; e < a.E; e += 256)
+    a.part[(int64_t)blockIdx.x * a.E + e] = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
+}
+
 // One wavefront per token, expert e = lane + 64 q.  Block 0 also writes the
 // token-chunk offsets [G+1] of the grouped dW_r product.
 template <class OT>
@@ -98,25 +130,40 @@ __global__ __launch_bounds__(256) void aux_grad_kernel(AuxArgs a, OT* __restrict
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= a.T) return;
-  double p[4], fe[4];
+  double p[4], fe[4], sg[4];
   double F = 0.0;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = lane + 64 * q;
     p[q] = 0.0;
     fe[q] = 0.0;
+    sg[q] = 0.0;
     if (e < a.E) {
       p[q] = (double)a.probs[t * a.E + e];
       fe[q] = aux_frac(a, e);
-      F += p[q] * fe[q];
     }
   }
+  if (a.thr) {
+    // p = s / sum s; dp/dl carries the factor (1 - s)
+    double S = 0.0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) S += p[q];
+    S = wave_sum(S);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      sg[q] = p[q];
+      p[q] = p[q] / S;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) F += p[q] * fe[q];
   F = wave_sum(F);
   const double c = (double)a.coef * (double)a.E / (double)a.T;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = lane + 64 * q;
-    if (e < E_pad) Elem<OT>::store(dl, t * E_pad + e, e < a.E ? (float)(c * p[q] * (fe[q] - F)) : 0.f);
+    const double g = c * p[q] * (fe[q] - F) * (a.thr ? 1.0 - sg[q] : 1.0);
+    if (e < E_pad) Elem<OT>::store(dl, t * E_pad + e, e < a.E ? (float)g : 0.f);
   }
 }
 
@@ -142,7 +189,11 @@ __global__ __launch_bounds__(256) void aux_dwr_kernel(const IT* __restrict__ par
 
 int launch_aux_stats(const AuxArgs& a, hipStream_t s) {
   const int nb = (int)aux_blocks(a.T);
-  if (nb > 0) {
+  if (nb > 0 && a.thr) {
+    const int st =
+        launch(K_AUX_PARTIAL_ROWS, s, "aux_partial_rows", [&] { aux_partial_rows_kernel<<<nb, 256, 0, s>>>(a); });
+    if (st) return st;
+  } else if (nb > 0) {
     const dim3 grid(nb, (a.E + 63) / 64);
     const int st = launch(K_AUX_STATS, s, "aux_stats", [&] { aux_partial_kernel<<<grid, 256, 0, s>>>(a); });
     if (st) return st;

@@ -36,11 +36,13 @@ __global__ __launch_bounds__(256) void combine_fwd_kernel(CombineFwdArgs a) {
   const int64_t R = a.T * a.k;
   int64_t rows[KM];
   float w[KM];
+  bool ok[KM];
 #pragma unroll
   for (int s = 0; s < KM; ++s) {
     rows[s] = s < k ? a.row_of[t * a.k + s] : 0;
     w[s] = s < k ? a.topk_w[t * a.k + s] : 0.f;
-    if ((uint64_t)rows[s] >= (uint64_t)R) {  // a dropped slot contributes nothing
+    ok[s] = s < k && (uint64_t)rows[s] < (uint64_t)R;
+    if (!ok[s]) {  // an empty or dropped slot contributes nothing (and loads nothing)
       rows[s] = 0;
       w[s] = 0.f;
     }
@@ -53,7 +55,7 @@ __global__ __launch_bounds__(256) void combine_fwd_kernel(CombineFwdArgs a) {
       uint4 raw[KM];
 #pragma unroll
       for (int s = 0; s < KM; ++s)
-        raw[s] = s < k ? *reinterpret_cast<const uint4*>(o + rows[s] * a.d + (int64_t)c * V) : make_uint4(0, 0, 0, 0);
+        raw[s] = ok[s] ? *reinterpret_cast<const uint4*>(o + rows[s] * a.d + (int64_t)c * V) : make_uint4(0, 0, 0, 0);
       uint4 rs = make_uint4(0, 0, 0, 0);
       if (sh) rs = *reinterpret_cast<const uint4*>(sh + t * a.d + (int64_t)c * V);
       float acc[V];
@@ -143,7 +145,8 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(CombineBwdArgs a) {
   }
   if (a.dl && lane == 0) {
     const float c = a.route_scale;
-    if (a.router == MOE_ROUTER_SIGMOID_GROUPED) {
+    if (a.router == MOE_ROUTER_SIGMOID_GROUPED || a.router == MOE_ROUTER_SIGMOID_THRESHOLD) {
+      // (an empty slot of the threshold router has s = 0 and gets 0)
 #pragma unroll
       for (int s = 0; s < KM; ++s)
         if (s < k) z += a.s_sel[t * a.k + s];
@@ -151,7 +154,9 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(CombineBwdArgs a) {
       for (int s = 0; s < KM; ++s)
         if (s < k) {
           const float sv = a.s_sel[t * a.k + s];
-          a.dl[t * a.k + s] = (c * om[s] - wo) / z * sv * (1.f - sv);
+          const float gs = (c * om[s] - wo) / z * sv;
+          a.dl[t * a.k + s] = gs * (1.f - sv);
+          if (a.dth) a.dth[t * a.k + s] = -gs;  // straight-through threshold gradient
         }
     } else {
 #pragma unroll

@@ -37,6 +37,8 @@ enum KernelId {
   K_AUX_DWR,
   K_ZC_PARAM_PARTIAL,
   K_ZC_PARAM_REDUCE,
+  K_THRESHOLD_GRAD,
+  K_AUX_PARTIAL_ROWS,
   K_NUM_KERNELS
 };
 

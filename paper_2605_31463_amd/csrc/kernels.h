@@ -22,7 +22,9 @@ struct RouteArgs {
   int32_t* counts;  // may be null
   void* wsplit;      // bf16 [3][E][d] workspace for the MFMA path (bf16 x), or null
   double* lg;        // float64 [T][E] logits workspace for the MFMA path
-  float* probs;      // [T][E] softmax over all experts (auxiliary loss), or null
+  float* probs;      // [T][E] softmax over all experts (auxiliary loss), or null;
+                     // the threshold router writes its sigmoid scores there
+  const float* threshold;  // [E] thresholds of the threshold router
 };
 int launch_route(const RouteArgs& a, hipStream_t s);
 int zero_i32(int32_t* p, int64_t n, hipStream_t s);
@@ -92,6 +94,7 @@ struct CombineBwdArgs {
   float route_scale;
   const int32_t* topk_idx;  // read with zero-computation experts
   ZcArgs zc;
+  float* dth;        // threshold router: per slot -s (c omega - sum w omega) / sum s, or null
 };
 int launch_combine_bwd(const CombineBwdArgs& a, hipStream_t s);
 
@@ -122,6 +125,10 @@ constexpr int DWR_ROWS = 256;  // rows per partial-sum task of dW_r
 inline int64_t route_dwr_tasks(int64_t R, int64_t E) { return R / DWR_ROWS + E; }
 int launch_route_bwd(const RouteBwdArgs& a, hipStream_t s);
 int launch_wr_transpose(const float* w_r, float* w_rt, int d, int E, hipStream_t s);
+// Threshold router: dtheta[e] (+)= sum over expert e's rows of g[token_of[row]]
+// (g [T*k] per slot, from the combine backward).
+int launch_threshold_grad(const int32_t* offsets, const int32_t* token_of, const float* g, int E, float* dtheta,
+                          bool accumulate, hipStream_t s);
 // W_r^T [Eo][d] in the activation type, rows E .. Eo-1 zero.
 int launch_wr_transpose_act(const float* w_r, void* w_rt, int d, int E, int Eo, bool bf16, hipStream_t s);
 
@@ -135,6 +142,8 @@ struct AuxArgs {
   float coef;
   int E_ffn;                // experts E_ffn .. E-1 (zero-computation ones) weigh
   float zc_weight;          //   zc_weight in the loss, the others 1
+  bool thr;                 // threshold router: probs hold sigmoid scores s, the loss
+                            // uses p = s / sum s and fractions of the filled slots
   double* part;             // [aux_blocks(T)][E] workspace
   float* loss;              // [1]
 };

@@ -73,7 +73,9 @@ __device__ void select_tokens(const RouteArgs& a, const double* lg, int ld, int6
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int epl = (E + 63) / 64;              // experts per lane, contiguous
-  const bool sigm = a.router == MOE_ROUTER_SIGMOID_GROUPED;
+  // threshold router: key l - theta_e, weights from sigmoid scores
+  const bool thr = a.router == MOE_ROUTER_SIGMOID_THRESHOLD;
+  const bool sigm = a.router == MOE_ROUTER_SIGMOID_GROUPED || thr;
   const bool logit_bias = a.bias_mode == MOE_BIAS_LOGIT;
   const bool select_bias = a.bias_mode == MOE_BIAS_SELECT_ONLY;
   const int gsize = E / a.n_groups;           // experts per group
@@ -93,12 +95,20 @@ __device__ void select_tokens(const RouteArgs& a, const double* lg, int ld, int6
       if (avail[q]) {
         double l = lg[tl * EPAD + e];
         if (logit_bias) l += (double)a.bias[e];
-        double sc = sigm ? 1.0 / (1.0 + exp(-l)) : l;
-        const double kv = select_bias ? sc + (double)a.bias[e] : sc;
+        double sc = (sigm && !thr) ? 1.0 / (1.0 + exp(-l)) : l;
+        const double kv = thr ? l - (double)a.threshold[e] : select_bias ? sc + (double)a.bias[e] : sc;
         key[q] = isnan(kv) ? -INFINITY : kv;  // NaN orders below every number
       }
     }
-    if (a.probs) {
+    if (a.probs && thr) {
+      // threshold router: the sigmoid scores of all experts (the auxiliary
+      // loss normalises them per token)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = lane * epl + q;
+        if (q < epl && e < E) a.probs[t * E + e] = (float)(1.0 / (1.0 + exp(-lg[tl * EPAD + e])));
+      }
+    } else if (a.probs) {
       // the router's probabilities over all experts (auxiliary loss): softmax
       // of the logits (+ bias when it is added to the logits)
       double v[4];
@@ -173,6 +183,7 @@ __device__ void select_tokens(const RouteArgs& a, const double* lg, int ld, int6
     }
     // top-k
     int my_idx = -1;
+    double my_key = -INFINITY;
     for (int s = 0; s < k; ++s) {
       Cand c{-INFINITY, 0x7fffffff};  // any available expert beats the empty slot (lower index)
 #pragma unroll
@@ -189,19 +200,25 @@ __device__ void select_tokens(const RouteArgs& a, const double* lg, int ld, int6
         for (int q = 0; q < 4; ++q)
           if (lane * epl + q == c.idx) avail[q] = false;
       }
-      if (lane == s) my_idx = c.idx;
+      if (lane == s) {
+        my_idx = c.idx;
+        my_key = c.key;
+      }
     }
-    // weights over the k selected (lanes 0..k-1 hold one slot each)
+    // weights over the k selected (lanes 0..k-1 hold one slot each); the
+    // threshold router keeps the slots whose key is positive, and always the
+    // first: the rest become empty (-1)
     const bool holds = lane < k;
+    const bool active = holds && (!thr || lane == 0 || my_key > 0.0);
     double sc = 0.0;
-    if (holds) {
+    if (active) {
       double l = lg[tl * EPAD + my_idx];
       if (logit_bias) l += (double)a.bias[my_idx];
       sc = sigm ? 1.0 / (1.0 + exp(-l)) : l;
     }
     double w;
     if (sigm) {
-      const double z = wave_sum_d(holds ? sc : 0.0, 64);
+      const double z = wave_sum_d(active ? sc : 0.0, 64);
       w = (double)a.route_scale * sc / z;
     } else {
       const double m = wave_max_d(holds ? sc : -INFINITY, 64);
@@ -209,11 +226,15 @@ __device__ void select_tokens(const RouteArgs& a, const double* lg, int ld, int6
       const double z = wave_sum_d(p, 64);
       w = (double)a.route_scale * p / z;
     }
-    if (holds) {
+    if (active) {
       a.topk_idx[t * k + lane] = my_idx;
       a.topk_w[t * k + lane] = (float)w;
       if (sigm && a.s_sel) a.s_sel[t * k + lane] = (float)sc;
       atomicAdd(&hist[my_idx], 1);
+    } else if (holds) {
+      a.topk_idx[t * k + lane] = -1;
+      a.topk_w[t * k + lane] = 0.f;
+      if (a.s_sel) a.s_sel[t * k + lane] = 0.f;
     }
   }
 }
@@ -681,7 +702,7 @@ int launch_route_gemm(const RouteArgs& a, hipStream_t s) {
   // one DPP row per token when E / 16 experts per lane tile the groups into
   // whole power-of-two lane sets (always without a group limit)
   const int kpl = a.E / 16;
-  bool rows16 = a.E % 16 == 0 && a.E <= 256;
+  bool rows16 = a.E % 16 == 0 && a.E <= 256 && a.router != MOE_ROUTER_SIGMOID_THRESHOLD;
   if (rows16 && a.n_groups > 1) {
     const int gsize = a.E / a.n_groups, lpg = gsize / kpl;
     rows16 = gsize % kpl == 0 && lpg >= 1 && lpg <= 16 && (lpg & (lpg - 1)) == 0;

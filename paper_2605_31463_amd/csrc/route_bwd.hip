@@ -38,7 +38,7 @@ __global__ void dl_kernel(RouteBwdArgs a) {
   const float c = a.route_scale;
   float wo = 0.f;
   for (int s = 0; s < k; ++s) wo += a.topk_w[t * k + s] * a.d_topk_w[t * k + s];
-  if (a.router == MOE_ROUTER_SIGMOID_GROUPED) {
+  if (a.router == MOE_ROUTER_SIGMOID_GROUPED || a.router == MOE_ROUTER_SIGMOID_THRESHOLD) {
     float z = 0.f;
     for (int s = 0; s < k; ++s) z += a.s_sel[t * k + s];
     for (int s = 0; s < k; ++s) {
@@ -145,6 +145,27 @@ __global__ __launch_bounds__(256) void dx_router_kernel(RouteBwdArgs a, const fl
   }
 }
 
+// dtheta[e] (+)= sum over the rows of expert e of g[token_of[row]], each
+// expert's rows summed by one block in a fixed order (strided per thread,
+// then a fixed tree).
+__global__ __launch_bounds__(256) void threshold_reduce_kernel(const int32_t* __restrict__ offsets,
+                                                              const int32_t* __restrict__ token_of,
+                                                              const float* __restrict__ g, float* dtheta,
+                                                              bool accumulate) {
+  __shared__ float red[256];
+  const int e = blockIdx.x;
+  const int r0 = offsets[e], r1 = offsets[e + 1];
+  float acc = 0.f;
+  for (int r = r0 + (int)threadIdx.x; r < r1; r += 256) acc += g[token_of[r]];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) dtheta[e] = accumulate ? dtheta[e] + red[0] : red[0];
+}
+
 }  // namespace
 
 int launch_wr_transpose(const float* w_r, float* w_rt, int d, int E, hipStream_t s) {
@@ -163,6 +184,13 @@ int launch_wr_transpose_act(const float* w_r, void* w_rt, int d, int E, int Eo, 
   bf16_t* o = reinterpret_cast<bf16_t*>(w_rt);
   return launch(K_WR_TRANSPOSE, s, "wr_transpose",
                 [&] { transpose_kernel<bf16_t><<<grid, 256, 0, s>>>(w_r, o, d, E, Eo); });
+}
+
+int launch_threshold_grad(const int32_t* offsets, const int32_t* token_of, const float* g, int E, float* dtheta,
+                          bool accumulate, hipStream_t s) {
+  return launch(K_THRESHOLD_GRAD, s, "threshold_grad", [&] {
+    threshold_reduce_kernel<<<E, 256, 0, s>>>(offsets, token_of, g, dtheta, accumulate);
+  });
 }
 
 int launch_route_bwd(const RouteBwdArgs& a, hipStream_t s) {

@@ -25,7 +25,8 @@ class MoELayer:
         e = lambda *shp, dt=a: torch.empty(*shp, dtype=dt, device=device)  # noqa: E731
         self.saved = dict(
             topk_idx=e(T, k, dt=i32), topk_w=e(T, k, dt=f32),
-            s_sel=e(T, k, dt=f32) if s.router == L.MOE_ROUTER_SIGMOID_GROUPED else None,
+            s_sel=e(T, k, dt=f32) if s.router in (L.MOE_ROUTER_SIGMOID_GROUPED, L.MOE_ROUTER_SIGMOID_THRESHOLD)
+            else None,
             expert_offsets=e(Ep + 1, dt=i32), row_of=e(T, k, dt=i32), token_of=e(R, dt=i32),
             x_perm=e(R, d), gu=e(R, 2 * f), h=e(R, f), o=e(R, d),
             gu_sh=e(T, 2 * s.f_shared) if s.n_shared else None,
@@ -49,6 +50,8 @@ class MoELayer:
             g.update(dws_gate=e(s.d, s.f_shared), dws_up=e(s.d, s.f_shared), dws_down=e(s.f_shared, s.d))
         if s.n_const:
             g.update(dzc_v=e(s.n_const, s.d, dt=torch.float32), dzc_wc=e(s.n_const, 2, s.d, dt=torch.float32))
+        if s.router == L.MOE_ROUTER_SIGMOID_THRESHOLD:
+            g.update(d_threshold=e(s.E, dt=torch.float32))
         return g
 
     def forward(self, params, x, stream=None):

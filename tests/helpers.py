@@ -83,7 +83,9 @@ def oracle_run(cfg, inp, aux_coef=0.0, aux_f=None):
     shared = shared_of(inp, cfg)
     zc = zc_of(inp, cfg)
     act = act_of(cfg)
-    fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=aux_coef, aux_f=aux_f, zc=zc, act=act)
+    theta = None if inp.get("gate_threshold") is None else inp["gate_threshold"].astype(np.float64)
+    fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=aux_coef, aux_f=aux_f, zc=zc, act=act,
+                        theta=theta)
     bwd = layer_backward(spec, x, w_r, beta, efn, fwd, to_f64(inp["dy"], dt), shared,
                          with_bias=cfg["expert_bias"], zc=zc, act=act)
     return fwd, bwd
@@ -107,6 +109,7 @@ def device_params(inp, cfg):
         ws_gate=dev(inp.get("ws_gate"), dt), ws_up=dev(inp.get("ws_up"), dt), ws_down=dev(inp.get("ws_down"), dt),
         zc_v=None if inp.get("zc_v") is None else torch.from_numpy(inp["zc_v"]).cuda(),
         zc_wc=None if inp.get("zc_wc") is None else torch.from_numpy(inp["zc_wc"]).cuda(),
+        gate_threshold=None if inp.get("gate_threshold") is None else torch.from_numpy(inp["gate_threshold"]).cuda(),
     )
     return p
 
@@ -124,19 +127,25 @@ def check_routing(cfg, fwd, topk_idx_gpu):
 
 
 def check_maps_valid(topk_idx, offsets, row_of, token_of, E):
-    """Maps are the stable (expert, token) counting sort of the given topk_idx."""
+    """Maps are the stable (expert, token) counting sort of the given topk_idx
+    (empty slots, id -1, get no row)."""
     T, k = topk_idx.shape
-    counts = np.bincount(topk_idx.reshape(-1), minlength=E)
+    flat = topk_idx.reshape(-1)
+    filled = np.nonzero(flat >= 0)[0]
+    n = filled.size
+    counts = np.bincount(flat[filled], minlength=E)
     assert np.array_equal(np.diff(offsets), counts)
-    assert offsets[0] == 0 and offsets[E] == T * k
-    assert np.array_equal(np.sort(token_of), np.arange(T * k))
+    assert offsets[0] == 0 and offsets[E] == n
+    token_of = token_of[:n]
+    assert np.array_equal(np.sort(token_of), filled)
     t_of = token_of // k
     s_of = token_of % k
     assert np.array_equal(topk_idx[t_of, s_of], np.repeat(np.arange(E), counts))
     for e in range(E):
         seg = t_of[offsets[e]:offsets[e + 1]]
         assert np.all(np.diff(seg) > 0)
-    assert np.array_equal(row_of[t_of, s_of], np.arange(T * k))
+    assert np.array_equal(row_of[t_of, s_of], np.arange(n))
+    assert np.all(row_of.reshape(-1)[flat < 0] == -1)
 
 
 def small_inputs(cfg, seed=0):

@@ -65,6 +65,9 @@ def test_workspace_sizes_scale_with_shape():
     (dict(E=16, k=4, n_groups=4, topk_groups=2, router="sigmoid_grouped", n_copy=1), L.MOE_ERR_UNSUPPORTED),
     (dict(E=250, k=8, n_zero=4, n_copy=4), L.MOE_ERR_UNSUPPORTED),     # pool of 258
     (dict(E=2, k=5, n_zero=1, n_copy=1), L.MOE_ERR_INVALID_ARG),       # k above the pool of 4
+    (dict(router="sigmoid_threshold", n_copy=1), L.MOE_ERR_UNSUPPORTED),
+    (dict(router="sigmoid_threshold", bias_mode="select"), L.MOE_ERR_UNSUPPORTED),
+    (dict(router="sigmoid_threshold", E=16, n_groups=4, topk_groups=2), L.MOE_ERR_INVALID_ARG),
     (dict(act="clamped_glu", act_alpha=0.0), L.MOE_ERR_INVALID_ARG),
     (dict(act="clamped_glu", act_limit=float("inf")), L.MOE_ERR_INVALID_ARG),
 ])
@@ -120,9 +123,9 @@ def test_shape_struct_layout_matches_header():
     assert L.moe_shape.zc_aux_weight.offset == 104
     assert L.moe_shape.act_limit.offset == 116
     # pointer structs: one pointer per field, in the header's order
-    assert ctypes.sizeof(L.moe_params) == 14 * 8 and L.moe_params.zc_wc.offset == 104
+    assert ctypes.sizeof(L.moe_params) == 15 * 8 and L.moe_params.gate_threshold.offset == 112
     assert ctypes.sizeof(L.moe_saved) == 15 * 8 and L.moe_saved.aux_loss.offset == 112
-    assert ctypes.sizeof(L.moe_grads) == 12 * 8 and L.moe_grads.dzc_wc.offset == 88
+    assert ctypes.sizeof(L.moe_grads) == 13 * 8 and L.moe_grads.d_threshold.offset == 96
 
 
 def declared_arities():
@@ -190,3 +193,20 @@ def test_zero_computation_shapes_on_the_host():
     st = L.LIB.moe_layer_bwd_wgrad(ctypes.byref(s), ctypes.byref(pr), fake, ctypes.byref(sv), fake,
                                    ctypes.byref(gr), 0, fake, 1 << 40, None)
     assert st == L.MOE_ERR_INVALID_ARG and "dzc_v" in L.last_error()
+
+
+def test_threshold_router_on_the_host():
+    """moe_route refuses the threshold router; the layer asks for the
+    thresholds and their gradient buffer."""
+    s = L.make_shape(T=64, d=128, E=8, k=4, f=128, router="sigmoid_threshold")
+    fake = ctypes.c_void_p(16)   # never dereferenced: validation fails first
+    st = L.LIB.moe_route(ctypes.byref(s), fake, fake, None, fake, fake, fake, None, fake, 1 << 40, None)
+    assert st == L.MOE_ERR_UNSUPPORTED and "threshold" in L.last_error()
+    pr = L.moe_params(w_r=fake, w_gate=fake, w_up=fake, w_down=fake)
+    sv = L.moe_saved(**{n: fake for n, _ in L.moe_saved._fields_})
+    st = L.LIB.moe_layer_fwd(ctypes.byref(s), ctypes.byref(pr), fake, ctypes.byref(sv), fake, fake, 1 << 40, None)
+    assert st == L.MOE_ERR_INVALID_ARG and "gate_threshold" in L.last_error()
+    gr = L.moe_grads(**{n: fake for n, _ in L.moe_grads._fields_ if n != "d_threshold"})
+    st = L.LIB.moe_layer_bwd_wgrad(ctypes.byref(s), ctypes.byref(pr), fake, ctypes.byref(sv), fake,
+                                   ctypes.byref(gr), 0, fake, 1 << 40, None)
+    assert st == L.MOE_ERR_INVALID_ARG and "d_threshold" in L.last_error()
