@@ -297,12 +297,14 @@ int moe_combine_bwd(const moe_shape* shape, const void* dy, const void* o, const
 
 /* Router backward.  dl on the selected experts only:
  *   softmax families: dl_j = w_j (omega_j - sum_i w_i omega_i / route_scale)
- *   SIGMOID_GROUPED:  dl_j = (route_scale omega_j - sum_i w_i omega_i) / sum_i s_i
- *                            * s_j (1 - s_j)
+ *   SIGMOID_GROUPED, SIGMOID_THRESHOLD:
+ *                     dl_j = (route_scale omega_j - sum_i w_i omega_i) / sum_i s_i
+ *                            * s_j (1 - s_j)   (an empty slot has s = 0: dl = 0)
  * with omega = d_topk_w; then dw_r[:, e] = sum over the rows of expert e of
  * x[token] * dl (using expert_offsets and token_of from moe_permute, in row
- * order), and dx_router[t] = sum_s dl[t][s] * W_r[:, topk_idx[t][s]] (float32,
- * may be NULL to skip).  ws: bwd_ws bytes. */
+ * order), and dx_router[t] = sum_s dl[t][s] * W_r[:, topk_idx[t][s]] over the
+ * filled slots (float32, may be NULL to skip).  The thresholds' gradient
+ * comes from the layer entry points only.  ws: bwd_ws bytes. */
 int moe_route_bwd(const moe_shape* shape, const void* x, const float* w_r,
                   const int32_t* topk_idx, const float* topk_w, const float* s_sel,
                   const float* d_topk_w, const int32_t* expert_offsets, const int32_t* token_of,

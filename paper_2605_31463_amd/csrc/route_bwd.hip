@@ -134,8 +134,10 @@ __global__ __launch_bounds__(256) void dx_router_kernel(RouteBwdArgs a, const fl
   for (int i = lane * 4; i < a.d; i += 256) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int s = 0; s < k; ++s) {
+      const int e = a.topk_idx[t * k + s];
+      if ((unsigned)e >= (unsigned)a.E) continue;  // an empty slot (threshold router)
       const float g = dl[t * k + s];
-      const float4 w = *reinterpret_cast<const float4*>(a.w_rt + (int64_t)a.topk_idx[t * k + s] * a.d + i);
+      const float4 w = *reinterpret_cast<const float4*>(a.w_rt + (int64_t)e * a.d + i);
       acc.x = __builtin_fmaf(g, w.x, acc.x);
       acc.y = __builtin_fmaf(g, w.y, acc.y);
       acc.z = __builtin_fmaf(g, w.z, acc.z);

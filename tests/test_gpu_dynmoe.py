@@ -153,3 +153,26 @@ def test_threshold_fullsize_whole_oracle():
           {n: "%.2e" % v for n, v in errs.items()}, flush=True)
     bad = {n: v for n, v in errs.items() if not v <= tol}
     assert not bad, bad
+
+
+def test_threshold_route_bwd_entry_point():
+    """moe_route_bwd on the oracle's omega with the threshold router's empty
+    slots (id -1): dW_r and the router dx skip them."""
+    import torch
+    from paper_2605_31463_amd import _lib as L
+    for name in ("tiny", "qwen3"):
+        cfg, coef, inp, fwd, bwd = case(name)
+        layer, p, x, dy, y, dx, grads = run_layer(cfg, inp)
+        sv = layer.saved
+        assert np.array_equal(host(sv["topk_idx"]), fwd["route"]["topk_idx"])
+        assert (host(sv["topk_idx"]) < 0).any()
+        omt = torch.from_numpy(bwd["omega"].astype(np.float32)).cuda()
+        dwr = torch.empty(cfg["d"], cfg["E"], dtype=torch.float32, device="cuda")
+        dxr = torch.empty(cfg["T"], cfg["d"], dtype=torch.float32, device="cuda")
+        L.moe_route_bwd(layer.shape, x, p["w_r"], sv["topk_idx"], sv["topk_w"], sv["s_sel"], omt,
+                        sv["expert_offsets"], sv["token_of"], dwr, dxr, layer.ws_bwd)
+        torch.cuda.synchronize()
+        tol = TOL[cfg["dtype"]]
+        e1, e2 = rel(host(dwr), bwd["dw_r"]), rel(host(dxr), bwd["dx_router"])
+        print(name, "route_bwd entry point: dw_r %.2e, dx_router %.2e" % (e1, e2), flush=True)
+        assert e1 <= tol and e2 <= tol
