@@ -32,4 +32,9 @@ from .moe_oracle import (  # noqa: F401
     zc_const_alpha,
     zc_forward,
     zc_backward,
+    e4m3_values,
+    e4m3_round,
+    quantize_rows,
+    quantize_cols,
+    fp8_expert_forward,
 )

@@ -396,7 +396,7 @@ def unpermute(dx_perm, row_of):
 # ----------------------------------------------------------------------------
 
 def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_f=None, zc=None, act=None,
-                  theta=None):
+                  theta=None, fp8=False):
     """Forward of one MoE layer.
 
     x [T][d] float64; w_r [d][E_pool]; beta [E_pool] or None;
@@ -406,7 +406,8 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
     zc = (ZeroComputeSpec, v, wc) appends zero-computation experts to the pool
     (E_pool = spec.E + their number), else None (E_pool = spec.E);
     act: the routed experts' activation (None: SwiGLU; see glu);
-    theta [E]: the threshold router's per-expert thresholds.
+    theta [E]: the threshold router's per-expert thresholds;
+    fp8: the routed experts' GEMMs on E4M3 operands (see fp8_expert_forward).
     Returns routing, maps and the per-row activations (permuted order) and y
     (and the auxiliary loss, its probabilities and fractions).
     """
@@ -432,7 +433,8 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
         if r1 == r0:
             continue
         wg, wu, wd, bg, bu, bd = expert_fn(e)
-        g, u, h, oe = expert_forward(x_perm[r0:r1], wg, wu, wd, bg, bu, bd, act=act)
+        fwd_fn = fp8_expert_forward if fp8 else expert_forward
+        g, u, h, oe = fwd_fn(x_perm[r0:r1], wg, wu, wd, bg, bu, bd, act=act)
         gs[e], us[e], hs[e] = g, u, h
         o[r0:r1] = oe
         fwidth = wg.shape[1]
@@ -794,3 +796,111 @@ def zc_backward(dy, x, topk_idx, topk_w, E, zs, v, wc):
                 dv[c] += a[1] * g
                 dwc[c] += np.outer(dz, x[t])
     return dict(omega=omega, dx=dx, dv=dv, dwc=dwc)
+
+
+# ----------------------------------------------------------------------------
+# FP8 forward of the expert GEMMs
+# ----------------------------------------------------------------------------
+# The paper trains with FP8 GEMMs (the Qwen3 FP8 row of its B200 results; its
+# framework fuses the quantisation and caches quantised weights across
+# micro-batches) without stating the scaling recipe.  Reading written out
+# here: OCP FP8 E4M3 (1 sign, 4 exponent bits of bias 7, 3 mantissa bits, no
+# infinities, largest finite 448); each row of an activation operand (a token
+# row of x_perm, or of h) gets the scale amax_row / 448 and each output column
+# of a weight matrix the scale amax_column / 448; a value v of a row with
+# largest magnitude amax is stored as the E4M3 value nearest to
+# min(max(v * (448 / amax), -448), 448), ties to the even mantissa, where
+# 448 / amax and the product are float32 operations (the quantised codes are
+# decided in float32 on both sides); an all-zero row or column gets scale 1.
+# The GEMMs multiply the dequantised operands (code value times scale).  The
+# backward uses the bf16 operands and weights as if the quantisation were the
+# identity (straight-through), with the activations gu and h of the FP8
+# forward.
+
+_E4M3_MAX = 448.0
+
+
+def e4m3_values():
+    """The 256 E4M3 codes' values (NaN for the two NaN codes), float64."""
+    out = np.empty(256)
+    for code in range(256):
+        s = -1.0 if code & 0x80 else 1.0
+        e = (code >> 3) & 0xF
+        m = code & 0x7
+        if e == 0xF and m == 0x7:
+            out[code] = np.nan
+        elif e == 0:
+            out[code] = s * m * 2.0 ** -9
+        else:
+            out[code] = s * (1.0 + m / 8.0) * 2.0 ** (e - 7)
+    return out
+
+
+_E4M3 = None
+
+
+def e4m3_round(v):
+    """Codes (uint8) of the E4M3 values nearest to v (|v| <= 448 assumed),
+    ties to the even code (the even mantissa), the sign of v kept (a negative
+    value that rounds to zero gives -0)."""
+    global _E4M3
+    if _E4M3 is None:
+        _E4M3 = e4m3_values()
+    v = np.asarray(v, np.float64)
+    pos = np.arange(0, 127)                      # finite non-negative codes 0x00..0x7e
+    pv = _E4M3[pos]
+    a = np.abs(v).reshape(-1)
+    # nearest by distance; ties to the even code
+    idx = np.searchsorted(pv, a)                 # pv ascending
+    lo = np.clip(idx - 1, 0, len(pv) - 1)
+    hi = np.clip(idx, 0, len(pv) - 1)
+    dlo = a - pv[lo]
+    dhi = pv[hi] - a
+    pick = np.where(dlo < dhi, lo, np.where(dhi < dlo, hi, np.where(pos[lo] % 2 == 0, lo, hi)))
+    code = pos[pick].astype(np.uint8)
+    neg = np.signbit(v.reshape(-1))              # the sign is kept, also on a zero result
+    code = np.where(neg, code | 0x80, code).astype(np.uint8)
+    return code.reshape(np.shape(v))
+
+
+def quantize_rows(a):
+    """Row-wise E4M3 quantisation: (codes [M][K] uint8, scale [M] float64 of the
+    float32 scale amax/448, dequantised values [M][K])."""
+    a32 = np.asarray(a, np.float32)
+    amax = np.abs(a32).max(axis=1) if a32.shape[1] else np.zeros(a32.shape[0], np.float32)
+    amax = np.where(amax > 0, amax, np.float32(_E4M3_MAX)).astype(np.float32)   # all-zero row: scale 1
+    inv = (np.float32(_E4M3_MAX) / amax).astype(np.float32)
+    x = (a32 * inv[:, None]).astype(np.float32)
+    x = np.clip(x, np.float32(-_E4M3_MAX), np.float32(_E4M3_MAX))
+    codes = e4m3_round(x.astype(np.float64))
+    scale = (amax / np.float32(_E4M3_MAX)).astype(np.float32).astype(np.float64)
+    vals = e4m3_values()[codes] * scale[:, None]
+    return codes, scale, vals
+
+
+def quantize_cols(w):
+    """Column-wise quantisation of a weight [K][N] (each output column its scale):
+    (codes [K][N], scale [N], dequantised [K][N])."""
+    c, s, v = quantize_rows(np.asarray(w).T)
+    return c.T, s, v.T
+
+
+def fp8_expert_forward(xe, wg, wu, wd, bg=None, bu=None, bd=None, act=None):
+    """expert_forward with both GEMMs on E4M3 operands: x rows and h rows
+    quantised per row, the weights per output column."""
+    _, _, xq = quantize_rows(xe)
+    _, _, wgq = quantize_cols(wg)
+    _, _, wuq = quantize_cols(wu)
+    _, _, wdq = quantize_cols(wd)
+    g = xq @ wgq
+    u = xq @ wuq
+    if bg is not None:
+        g = g + bg
+    if bu is not None:
+        u = u + bu
+    h = glu(g, u, act)[0]
+    _, _, hq = quantize_rows(h)
+    o = hq @ wdq
+    if bd is not None:
+        o = o + bd
+    return g, u, h, o

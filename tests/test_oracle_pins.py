@@ -1096,3 +1096,74 @@ def test_threshold_router_limits_reduce_to_fixed_k_routers():
         for e in range(THR.E):
             assert rel(bwd["experts"][e]["dw_gate"], br["experts"][e]["dw_gate"]) < 1e-13 or \
                 np.linalg.norm(br["experts"][e]["dw_gate"]) == 0
+
+
+# ---------------------------------------------------------------------------
+# FP8 (E4M3) forward of the expert GEMMs
+# ---------------------------------------------------------------------------
+
+from oracle import e4m3_round, e4m3_values, fp8_expert_forward, quantize_rows  # noqa: E402
+
+
+def test_e4m3_values_and_rounding_match_torch():
+    """The format's 256 values and the round-to-nearest-even of float32 values
+    against torch's float8_e4m3fn (an independent implementation)."""
+    v = e4m3_values()
+    t = torch.arange(256, dtype=torch.uint8).view(torch.float8_e4m3fn).double().numpy()
+    assert np.array_equal(np.isnan(v), np.isnan(t)) and np.array_equal(v[~np.isnan(v)], t[~np.isnan(t)])
+    assert np.nanmax(v) == 448.0 and np.nanmin(np.abs(v[v != 0])) == 2.0 ** -9
+    rng = np.random.default_rng(51)
+    x = np.concatenate([rng.uniform(-448, 448, 100000), rng.uniform(-1, 1, 100000),
+                        rng.uniform(-0.02, 0.02, 50000), [0.0, -0.0, 448.0, -448.0, 2.0 ** -10, 3 * 2.0 ** -11]])
+    x = x.astype(np.float32)
+    assert np.array_equal(e4m3_round(x.astype(np.float64)), torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy())
+
+
+def test_row_quantisation_properties():
+    """Every non-zero row reaches +-448 at its largest element; the dequantised
+    values are within half an E4M3 step of the inputs; a zero row stays zero."""
+    rng = np.random.default_rng(52)
+    a = rng.standard_normal((40, 96)) * rng.uniform(0.01, 50, (40, 1))
+    a[7] = 0.0
+    a = a.astype(np.float32).astype(np.float64)
+    codes, scale, vals = quantize_rows(a)
+    ev = e4m3_values()
+    for r in range(40):
+        if r == 7:
+            assert np.all(vals[r] == 0) and scale[r] == 1.0
+            continue
+        assert np.abs(ev[codes[r]]).max() == 448.0
+        # relative step of E4M3 normals is 2^-3: rounding error <= 2^-4 relative, or
+        # half the smallest subnormal step (2^-10) times the scale
+        err = np.abs(vals[r] - a[r])
+        assert np.all(err <= np.maximum(2.0 ** -4 * np.abs(a[r]), 2.0 ** -10 * scale[r]) * (1 + 1e-6))
+
+
+def test_fp8_forward_exact_on_representable_operands():
+    """Operands that are E4M3 values times a power of two, with each row's and
+    column's largest magnitude at 448 times that power: quantisation is exact,
+    so the first GEMM of the FP8 expert equals the plain one."""
+    rng = np.random.default_rng(53)
+    ev = e4m3_values()
+    fin = ev[np.isfinite(ev) & (np.abs(ev) <= 448)]
+    x = rng.choice(fin, (12, 16)) * 2.0 ** -6
+    x[:, 0] = 448 * 2.0 ** -6
+    wg = rng.choice(fin, (16, 8)) * 2.0 ** -9
+    wg[0, :] = 448 * 2.0 ** -9
+    wu = rng.choice(fin, (16, 8)) * 2.0 ** -8
+    wu[0, :] = -448 * 2.0 ** -8
+    wd = rng.standard_normal((8, 16))
+    g, u, h, o = fp8_expert_forward(x, wg, wu, wd)
+    assert np.array_equal(g, x @ wg) and np.array_equal(u, x @ wu)
+
+
+def test_fp8_layer_close_to_bf16_layer():
+    """The FP8 forward differs from the plain one by quantisation noise only
+    (a few percent normwise), and the backward is the plain backward of the
+    FP8 forward's activations."""
+    spec = RouterSpec("softmax_topk", E=6, k=2)
+    c = make_case(spec, T=48, d=64, f=48, seed=54)
+    f0 = layer_forward(spec, c["x"], c["w_r"], None, efn(c))
+    f1 = layer_forward(spec, c["x"], c["w_r"], None, efn(c), fp8=True)
+    assert 1e-3 < rel(f1["y"], f0["y"]) < 0.1
+    assert np.array_equal(f1["route"]["topk_idx"], f0["route"]["topk_idx"])
