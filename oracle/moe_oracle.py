@@ -812,10 +812,12 @@ def zc_backward(dy, x, topk_idx, topk_w, E, zs, v, wc):
 # min(max(v * (448 / amax), -448), 448), ties to the even mantissa, where
 # 448 / amax and the product are float32 operations (the quantised codes are
 # decided in float32 on both sides); an all-zero row or column gets scale 1.
-# The GEMMs multiply the dequantised operands (code value times scale).  The
-# backward uses the bf16 operands and weights as if the quantisation were the
-# identity (straight-through), with the activations gu and h of the FP8
-# forward.
+# The activations are quantised from their stored bf16 values (FP8 runs bf16
+# layers): x is stored bf16 already, h is rounded to float32 and then to bf16
+# (nearest even) before its row is quantised.  The GEMMs multiply the
+# dequantised operands (code value times scale).  The backward uses the bf16
+# operands and weights as if the quantisation were the identity
+# (straight-through), with the activations gu and h of the FP8 forward.
 
 _E4M3_MAX = 448.0
 
@@ -885,9 +887,17 @@ def quantize_cols(w):
     return c.T, s, v.T
 
 
+def round_bf16(a):
+    """float64 values rounded to float32, then to bfloat16 (nearest, ties to
+    even), returned as float64."""
+    u = np.ascontiguousarray(np.asarray(a, np.float32)).view(np.uint32)
+    r = ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)) << np.uint32(16)
+    return r.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
 def fp8_expert_forward(xe, wg, wu, wd, bg=None, bu=None, bd=None, act=None):
-    """expert_forward with both GEMMs on E4M3 operands: x rows and h rows
-    quantised per row, the weights per output column."""
+    """expert_forward with both GEMMs on E4M3 operands: x rows and the stored
+    (bf16) h rows quantised per row, the weights per output column."""
     _, _, xq = quantize_rows(xe)
     _, _, wgq = quantize_cols(wg)
     _, _, wuq = quantize_cols(wu)
@@ -899,7 +909,7 @@ def fp8_expert_forward(xe, wg, wu, wd, bg=None, bu=None, bd=None, act=None):
     if bu is not None:
         u = u + bu
     h = glu(g, u, act)[0]
-    _, _, hq = quantize_rows(h)
+    _, _, hq = quantize_rows(round_bf16(h))
     o = hq @ wdq
     if bd is not None:
         o = o + bd

@@ -1167,3 +1167,11 @@ def test_fp8_layer_close_to_bf16_layer():
     f1 = layer_forward(spec, c["x"], c["w_r"], None, efn(c), fp8=True)
     assert 1e-3 < rel(f1["y"], f0["y"]) < 0.1
     assert np.array_equal(f1["route"]["topk_idx"], f0["route"]["topk_idx"])
+
+
+def test_round_bf16_matches_torch():
+    from oracle.moe_oracle import round_bf16
+    rng = np.random.default_rng(55)
+    a = np.concatenate([rng.standard_normal(100000) * 10.0 ** rng.integers(-8, 8, 100000), [0.0, -0.0, 1.0]])
+    want = torch.from_numpy(a).to(torch.float32).to(torch.bfloat16).double().numpy()
+    assert np.array_equal(round_bf16(a), want)
