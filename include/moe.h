@@ -165,6 +165,8 @@ typedef struct moe_shape {
   int32_t act;                 /* MOE_ACT_* of the routed experts */
   float act_alpha;             /* CLAMPED_GLU: slope inside the sigmoid (> 0) */
   float act_limit;             /* CLAMPED_GLU: clamp bound (> 0) */
+  int32_t fp8;                 /* 1: the routed experts' forward GEMMs take FP8
+                                  operands (see the FP8 section below); 0: bf16 */
 } moe_shape;
 
 /* Parameters of the layer (device pointers; unused ones may be NULL). */
@@ -186,6 +188,7 @@ typedef struct moe_params {
   const float* zc_v;           /* [n_const][d] constant experts' vectors */
   const float* zc_wc;          /* [n_const][2][d] constant experts' mixing weights */
   const float* gate_threshold; /* [E] thresholds of MOE_ROUTER_SIGMOID_THRESHOLD */
+  const void* fp8_cache;       /* shape->fp8: the weight cache moe_fp8_cache_build wrote */
 } moe_params;
 
 /* Tensors the forward writes and the backward reads (caller-allocated). */
@@ -258,7 +261,8 @@ int moe_permute(const moe_shape* shape, const void* x, const int32_t* topk_idx,
  *   o = h W_down,e (+ b_down,e),
  * for every expert e over its rows expert_offsets[e] .. expert_offsets[e+1]-1,
  * scheduled on the device from expert_offsets (no host synchronisation).
- * b_* may be NULL when shape->expert_bias is 0.  out: gu, h, o. */
+ * b_* may be NULL when shape->expert_bias is 0.  out: gu, h, o.
+ * (bf16 operands: a shape with fp8 = 1 is refused; moe_layer_fwd runs it.) */
 int moe_grouped_gemm_fwd(const moe_shape* shape, const void* x_perm, const int32_t* expert_offsets,
                          const void* w_gate, const void* w_up, const void* w_down,
                          const void* b_gate, const void* b_up, const void* b_down,
@@ -376,6 +380,31 @@ int moe_layer_bwd_dgrad(const moe_shape* shape, const moe_params* params, const 
 int moe_layer_bwd_wgrad(const moe_shape* shape, const moe_params* params, const void* x,
                         const moe_saved* saved, const void* dy, const moe_grads* grads,
                         int32_t accumulate, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* FP8 forward of the routed experts (the paper's FP8 training: fused
+ * quantisation, quantised weights cached across micro-batches; it states no
+ * scaling recipe, so this one is the library's).  With shape->fp8 = 1 (bf16
+ * layers, d and f multiples of 128) moe_layer_fwd runs both expert GEMMs on
+ * OCP FP8 E4M3 operands: the permutation also writes every routed row of x in
+ * E4M3 with one scale per token, h is quantised per row after the gate/up
+ * GEMM, and the weights come from the cache.  A value v of a row (column)
+ * whose largest magnitude is amax is stored as the E4M3 value nearest to
+ * clamp(v * (448 / amax), -448, 448) (float32 product, ties to even) with
+ * scale amax / 448 (1 for an all-zero row); the GEMMs accumulate the code
+ * products in float32 and multiply by the row and column scales.  gu, h and o
+ * stay bf16; the backward is the bf16 backward of those activations and of the
+ * bf16 weights (quantisation taken as the identity).  The shared expert stays
+ * bf16.
+ *
+ * moe_fp8_cache_size: bytes of the cache for the shape.  moe_fp8_cache_build:
+ * quantises w_gate, w_up [E][d][f] and w_down [E][f][d] (bf16) per output
+ * column into the caller's cache (codes stored transposed, K-contiguous, with
+ * the scales); call it again whenever the weights change, and reuse it for
+ * every micro-batch in between.  Errors: MOE_ERR_UNSUPPORTED without
+ * shape->fp8, MOE_ERR_WORKSPACE for a cache below the size. */
+int moe_fp8_cache_size(const moe_shape* shape, size_t* bytes);
+int moe_fp8_cache_build(const moe_shape* shape, const void* w_gate, const void* w_up, const void* w_down,
+                        void* cache, size_t cache_bytes, hipStream_t stream);
 
 /* Status code -> static string. */
 const char* moe_status_string(int status);

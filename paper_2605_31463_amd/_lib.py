@@ -57,6 +57,7 @@ class moe_shape(ctypes.Structure):
         ("n_zero", ctypes.c_int32), ("n_copy", ctypes.c_int32), ("n_const", ctypes.c_int32),
         ("zc_aux_weight", ctypes.c_float),
         ("act", ctypes.c_int32), ("act_alpha", ctypes.c_float), ("act_limit", ctypes.c_float),
+        ("fp8", ctypes.c_int32),
     ]
 
 
@@ -66,7 +67,7 @@ _VP = ctypes.c_void_p
 class moe_params(ctypes.Structure):
     _fields_ = [(n, _VP) for n in ("w_r", "router_bias", "w_gate", "w_up", "w_down", "b_gate",
                                    "b_up", "b_down", "ws_gate", "ws_up", "ws_down", "aux_f",
-                                   "zc_v", "zc_wc", "gate_threshold")]
+                                   "zc_v", "zc_wc", "gate_threshold", "fp8_cache")]
 
 
 class moe_saved(ctypes.Structure):
@@ -116,6 +117,8 @@ def _load():
                                 _VP, sz, _VP],
         "moe_layer_bwd_wgrad": [S, ctypes.POINTER(moe_params), _VP, ctypes.POINTER(moe_saved), _VP,
                                 ctypes.POINTER(moe_grads), i32, _VP, sz, _VP],
+        "moe_fp8_cache_size": [S, szp],
+        "moe_fp8_cache_build": [S, _VP, _VP, _VP, _VP, sz, _VP],
         "moe_kernel_count": [],
         "moe_kernel_name": [ctypes.c_int],
         "moe_timing_select": [ctypes.c_int],
@@ -165,13 +168,13 @@ def _stream(stream):
 def make_shape(T, d, E, k, f, router="softmax_topk", n_groups=1, topk_groups=1, n_shared=0,
                f_shared=0, route_scale=1.0, bias_mode="none", expert_bias=False, dtype="bf16",
                renorm=1, aux_coef=0.0, n_zero=0, n_copy=0, n_const=0, zc_aux_weight=1.0,
-               act="swiglu", act_alpha=1.702, act_limit=7.0):
+               act="swiglu", act_alpha=1.702, act_limit=7.0, fp8=False):
     return moe_shape(T=T, d=d, E=E, k=k, f=f, n_groups=n_groups, topk_groups=topk_groups,
                      n_shared=n_shared, f_shared=f_shared, router=ROUTERS[router], renorm=renorm,
                      route_scale=route_scale, bias_mode=BIAS_MODES[bias_mode],
                      expert_bias=int(bool(expert_bias)), dtype=DTYPES[dtype], aux_coef=aux_coef,
                      n_zero=n_zero, n_copy=n_copy, n_const=n_const, zc_aux_weight=zc_aux_weight,
-                     act=ACTS[act], act_alpha=act_alpha, act_limit=act_limit)
+                     act=ACTS[act], act_alpha=act_alpha, act_limit=act_limit, fp8=int(bool(fp8)))
 
 
 def pool_size(shape):
@@ -189,7 +192,7 @@ def shape_from_config(cfg, T=None):
                       n_zero=cfg.get("n_zero", 0), n_copy=cfg.get("n_copy", 0),
                       n_const=cfg.get("n_const", 0), zc_aux_weight=cfg.get("zc_aux_weight", 1.0),
                       act=cfg.get("act", "swiglu"), act_alpha=cfg.get("act_alpha", 1.702),
-                      act_limit=cfg.get("act_limit", 7.0))
+                      act_limit=cfg.get("act_limit", 7.0), fp8=cfg.get("fp8", False))
 
 
 # ---------------------------------------------------------------------------
@@ -338,3 +341,15 @@ def kernel_id(name):
         if moe_kernel_name(i) == name:
             return i
     raise KeyError(name)
+
+
+def moe_fp8_cache_size(shape):
+    b = ctypes.c_size_t()
+    _check("moe_fp8_cache_size", LIB.moe_fp8_cache_size(ctypes.byref(shape), ctypes.byref(b)))
+    return b.value
+
+
+def moe_fp8_cache_build(shape, w_gate, w_up, w_down, cache, stream=None):
+    cp, cb = _ws(cache)
+    return _check("moe_fp8_cache_build", LIB.moe_fp8_cache_build(ctypes.byref(shape), P(w_gate), P(w_up),
+                                                                 P(w_down), cp, cb, _stream(stream)))

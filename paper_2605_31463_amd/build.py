@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libmoe.so")
 BUILD = os.path.join(ROOT, "_build")
-SOURCES = ["api.hip", "route.hip", "route_bwd.hip", "permute.hip", "combine.hip", "gemm.hip", "aux.hip", "zc.hip"]
+SOURCES = ["api.hip", "route.hip", "route_bwd.hip", "permute.hip", "combine.hip", "gemm.hip", "aux.hip", "zc.hip", "fp8.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",

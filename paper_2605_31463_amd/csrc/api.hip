@@ -78,7 +78,8 @@ const char* kernel_name(int id) {
       "combine_fwd", "combine_bwd", "route_dl", "route_dwr_partial", "route_dwr_reduce",
       "wr_transpose", "route_dx", "gemm_down_dgrad", "gemm_gateup_dgrad", "gemm_down_wgrad",
       "gemm_gateup_wgrad", "unpermute", "rank", "wr_split", "route_select", "aux_stats", "aux_grad",
-      "aux_dwr", "zc_param_partial", "zc_param_reduce", "threshold_grad", "aux_partial_rows"};
+      "aux_dwr", "zc_param_partial", "zc_param_reduce", "threshold_grad", "aux_partial_rows", "quant_rows",
+      "weight_quant"};
   if (id < 0 || id >= K_NUM_KERNELS) return nullptr;
   return names[id];
 }
@@ -109,6 +110,9 @@ int check_shape(const moe_shape* sh) {
     return moe_set_error(MOE_ERR_UNSUPPORTED, "zero-computation experts need a softmax router");
   if (s.router == MOE_ROUTER_SIGMOID_THRESHOLD && s.bias_mode != MOE_BIAS_NONE)
     return moe_set_error(MOE_ERR_UNSUPPORTED, "the threshold router takes no router bias");
+  if (s.fp8 != 0 && s.fp8 != 1) return moe_set_error(MOE_ERR_INVALID_ARG, "fp8 must be 0 or 1");
+  if (s.fp8 && (s.dtype != MOE_BF16 || s.d % 128 || s.f % 128))
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "fp8 needs bf16 layers with d and f multiples of 128");
   if (s.act != MOE_ACT_SWIGLU && s.act != MOE_ACT_CLAMPED_GLU)
     return moe_set_error(MOE_ERR_INVALID_ARG, "unknown activation %d", s.act);
   if (s.act == MOE_ACT_CLAMPED_GLU &&
@@ -166,7 +170,7 @@ inline size_t act_bytes(const moe_shape& s) { return s.dtype == MOE_BF16 ? 2 : 4
 
 struct Plan {
   // forward
-  size_t hist, wsplit, lg, aux_part;
+  size_t hist, wsplit, lg, aux_part, xq, sx, hq, sh;
   size_t fwd_total;
   // backward
   size_t d_o, dgu, dx_perm, dl, partial, w_rt, dgu_sh, dx_sh;
@@ -198,6 +202,11 @@ Plan plan(const moe_shape& s) {
   off += s.dtype == MOE_BF16 ? align_up((size_t)s.T * Ep * 8) : 0;
   p.aux_part = off;
   off += has_aux(s) ? align_up((size_t)aux_blocks(s.T) * Ep * 8) : 0;
+  // FP8 forward: E4M3 rows of x_perm and h, and their scales
+  p.xq = off; off += s.fp8 ? align_up((size_t)R * s.d) : 0;
+  p.sx = off; off += s.fp8 ? align_up((size_t)R * 4) : 0;
+  p.hq = off; off += s.fp8 ? align_up((size_t)R * s.f) : 0;
+  p.sh = off; off += s.fp8 ? align_up((size_t)R * 4) : 0;
   p.fwd_total = off;
   off = 0;
   p.d_o = off; off += align_up((size_t)R * s.d * eb);
@@ -264,6 +273,28 @@ GemmArgs gemm_base(const moe_shape& s, int mode, const int32_t* offsets) {
 }
 
 // The shared expert (and the dense products of the auxiliary loss): SwiGLU.
+// FP8 weight cache regions: codes of gate, up [E][f][d] and down [E][d][f],
+// then the column maxima and scales of each (float32).
+struct CachePlan {
+  size_t qg, qu, qd, ag, au, ad, sg, su, sd, total;
+};
+CachePlan cache_plan(const moe_shape& s) {
+  CachePlan c{};
+  size_t off = 0;
+  const size_t efd = (size_t)s.E * s.f * s.d;
+  c.qg = off; off += align_up(efd);
+  c.qu = off; off += align_up(efd);
+  c.qd = off; off += align_up(efd);
+  c.ag = off; off += align_up((size_t)s.E * s.f * 4);
+  c.au = off; off += align_up((size_t)s.E * s.f * 4);
+  c.ad = off; off += align_up((size_t)s.E * s.d * 4);
+  c.sg = off; off += align_up((size_t)s.E * s.f * 4);
+  c.su = off; off += align_up((size_t)s.E * s.f * 4);
+  c.sd = off; off += align_up((size_t)s.E * s.d * 4);
+  c.total = off;
+  return c;
+}
+
 GemmArgs gemm_dense(const moe_shape& s, int mode) {
   GemmArgs g = gemm_base(s, mode, nullptr);
   g.ngroups = 1;
@@ -271,6 +302,7 @@ GemmArgs gemm_dense(const moe_shape& s, int mode) {
   g.max_rows = s.T;
   g.f = (int)s.f_shared;
   g.act = MOE_ACT_SWIGLU;
+  g.fp8 = false;
   return g;
 }
 
@@ -303,7 +335,7 @@ int do_route(const moe_shape& s, const void* x, const float* w_r, const float* b
 }
 
 int do_permute(const moe_shape& s, const void* x, const int32_t* topk_idx, int32_t* offsets, int32_t* row_of,
-               int32_t* token_of, void* x_perm, void* ws, hipStream_t st) {
+               int32_t* token_of, void* x_perm, void* ws, hipStream_t st, bool fp8_rows = false) {
   PermArgs a{};
   a.x = x;
   a.topk_idx = topk_idx;
@@ -318,7 +350,45 @@ int do_permute(const moe_shape& s, const void* x, const int32_t* topk_idx, int32
   a.row_of = row_of;
   a.token_of = token_of;
   a.x_perm = x_perm;
+  if (fp8_rows) {
+    a.xq = reinterpret_cast<uint8_t*>(wsp(ws, plan(s).xq));
+    a.sx = reinterpret_cast<float*>(wsp(ws, plan(s).sx));
+  }
   return launch_permute(a, st);
+}
+
+// FP8 forward of the routed experts: E4M3 x rows (written by the permutation)
+// and cached weights through the gate/up GEMM, E4M3 h rows through the down GEMM.
+int do_gemm_fwd_fp8(const moe_shape& s, const int32_t* offsets, const void* cache, const void* b_gate,
+                    const void* b_up, const void* b_down, void* gu, void* h, void* o, void* ws, hipStream_t st) {
+  const Plan p = plan(s);
+  const CachePlan c = cache_plan(s);
+  const char* cb = static_cast<const char*>(cache);
+  GemmArgs g = gemm_base(s, G_FWD_GATEUP, offsets);
+  g.fp8 = true;
+  g.a = wsp(ws, p.xq);
+  g.a_scale = reinterpret_cast<const float*>(wsp(ws, p.sx));
+  g.w0 = cb + c.qg;
+  g.w1 = cb + c.qu;
+  g.b_scale0 = reinterpret_cast<const float*>(cb + c.sg);
+  g.b_scale1 = reinterpret_cast<const float*>(cb + c.su);
+  g.bias0 = b_gate;
+  g.bias1 = b_up;
+  g.c0 = gu;
+  g.c1 = h;
+  MOE_TRY(launch_gemm(g, st));
+  uint8_t* hq = reinterpret_cast<uint8_t*>(wsp(ws, p.hq));
+  float* sh = reinterpret_cast<float*>(wsp(ws, p.sh));
+  MOE_TRY(launch_quant_rows(h, offsets, (int)s.E, s.T * s.k, (int)s.f, hq, sh, st));
+  g = gemm_base(s, G_FWD_DOWN, offsets);
+  g.fp8 = true;
+  g.a = hq;
+  g.a_scale = sh;
+  g.w0 = cb + c.qd;
+  g.b_scale0 = reinterpret_cast<const float*>(cb + c.sd);
+  g.bias0 = b_down;
+  g.c0 = o;
+  return launch_gemm(g, st);
 }
 
 int do_gemm_fwd(const moe_shape& s, const void* x_perm, const int32_t* offsets, const void* w_gate, const void* w_up,
@@ -488,11 +558,11 @@ RouteBwdArgs route_bwd_base(const moe_shape& s) {
 using namespace moe;
 
 // The Python binding mirrors these layouts field by field.
-static_assert(sizeof(moe_shape) == 120 && offsetof(moe_shape, f_shared) == 56 &&
+static_assert(sizeof(moe_shape) == 128 && offsetof(moe_shape, f_shared) == 56 &&
                   offsetof(moe_shape, aux_coef) == 88 && offsetof(moe_shape, zc_aux_weight) == 104 &&
-                  offsetof(moe_shape, act_limit) == 116,
+                  offsetof(moe_shape, act_limit) == 116 && offsetof(moe_shape, fp8) == 120,
               "moe_shape layout");
-static_assert(sizeof(moe_params) == 15 * sizeof(void*) && sizeof(moe_saved) == 15 * sizeof(void*) &&
+static_assert(sizeof(moe_params) == 16 * sizeof(void*) && sizeof(moe_saved) == 15 * sizeof(void*) &&
                   sizeof(moe_grads) == 13 * sizeof(void*),
               "pointer struct layouts");
 
@@ -764,6 +834,33 @@ int moe_timing_read(double* total_ms, int* launches) {
   return MOE_OK;
 }
 
+int moe_fp8_cache_size(const moe_shape* shape, size_t* bytes) {
+  MOE_TRY(check_shape(shape));
+  if (!shape->fp8) return moe_set_error(MOE_ERR_UNSUPPORTED, "moe_fp8_cache_size: shape->fp8 is 0");
+  MOE_NEED(bytes, "bytes");
+  *bytes = cache_plan(*shape).total;
+  return MOE_OK;
+}
+
+int moe_fp8_cache_build(const moe_shape* shape, const void* w_gate, const void* w_up, const void* w_down, void* cache,
+                        size_t cache_bytes, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  if (!s.fp8) return moe_set_error(MOE_ERR_UNSUPPORTED, "moe_fp8_cache_build: shape->fp8 is 0");
+  MOE_NEED(w_gate, "w_gate");
+  MOE_NEED(w_up, "w_up");
+  MOE_NEED(w_down, "w_down");
+  const CachePlan c = cache_plan(s);
+  MOE_TRY(check_ws(cache, cache_bytes, c.total));
+  char* cb = static_cast<char*>(cache);
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(cb + off); };
+  auto Q = [&](size_t off) { return reinterpret_cast<uint8_t*>(cb + off); };
+  const int E = (int)s.E, d = (int)s.d, f = (int)s.f;
+  MOE_TRY(launch_weight_quant(w_gate, E, d, f, F(c.ag), F(c.sg), Q(c.qg), stream));
+  MOE_TRY(launch_weight_quant(w_up, E, d, f, F(c.au), F(c.su), Q(c.qu), stream));
+  return launch_weight_quant(w_down, E, f, d, F(c.ad), F(c.sd), Q(c.qd), stream);
+}
+
 int moe_workspace_size(const moe_shape* shape, size_t* fwd_ws, size_t* saved_bytes, size_t* bwd_ws) {
   MOE_TRY(check_shape(shape));
   const Plan p = plan(*shape);
@@ -812,6 +909,8 @@ int moe_grouped_gemm_fwd(const moe_shape* shape, const void* x_perm, const int32
                          const void* b_up, const void* b_down, void* gu, void* h, void* o, hipStream_t stream) {
   MOE_TRY(check_shape(shape));
   const moe_shape& s = *shape;
+  if (s.fp8)
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "moe_grouped_gemm_fwd: FP8 operands come from moe_layer_fwd");
   MOE_NEED(expert_offsets, "expert_offsets");
   MOE_NEED(w_gate, "w_gate");
   MOE_NEED(w_up, "w_up");
@@ -1074,20 +1173,25 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, 
     MOE_NEED(prm->zc_wc, "params.zc_wc");
   }
   if (is_thr(s)) MOE_NEED(prm->gate_threshold, "params.gate_threshold");
+  if (s.fp8) MOE_NEED(prm->fp8_cache, "params.fp8_cache");
   MOE_TRY(check_ws(ws, ws_bytes, plan(s).fwd_total));
   const void* bg = s.expert_bias ? prm->b_gate : nullptr;
   const void* bu = s.expert_bias ? prm->b_up : nullptr;
   const void* bd = s.expert_bias ? prm->b_down : nullptr;
   MOE_TRY(do_route(s, x, prm->w_r, prm->router_bias, sv->topk_idx, sv->topk_w, sv->s_sel, nullptr, ws, stream,
                    has_aux(s) ? sv->router_probs : nullptr, prm->gate_threshold));
-  MOE_TRY(do_permute(s, x, sv->topk_idx, sv->expert_offsets, sv->row_of, sv->token_of, sv->x_perm, ws, stream));
+  MOE_TRY(do_permute(s, x, sv->topk_idx, sv->expert_offsets, sv->row_of, sv->token_of, sv->x_perm, ws, stream,
+                     s.fp8 != 0));
   if (has_aux(s)) {
     AuxArgs aa = aux_args(s, prm, sv);
     aa.part = reinterpret_cast<double*>(wsp(ws, plan(s).aux_part));
     MOE_TRY(launch_aux_stats(aa, stream));
   }
-  MOE_TRY(do_gemm_fwd(s, sv->x_perm, sv->expert_offsets, prm->w_gate, prm->w_up, prm->w_down, bg, bu, bd, sv->gu,
-                      sv->h, sv->o, stream));
+  if (s.fp8)
+    MOE_TRY(do_gemm_fwd_fp8(s, sv->expert_offsets, prm->fp8_cache, bg, bu, bd, sv->gu, sv->h, sv->o, ws, stream));
+  else
+    MOE_TRY(do_gemm_fwd(s, sv->x_perm, sv->expert_offsets, prm->w_gate, prm->w_up, prm->w_down, bg, bu, bd, sv->gu,
+                        sv->h, sv->o, stream));
   if (s.n_shared)
     MOE_TRY(do_shared_fwd(s, x, prm->ws_gate, prm->ws_up, prm->ws_down, sv->gu_sh, sv->h_sh, sv->o_sh, stream));
   CombineFwdArgs c{sv->o, sv->topk_w, sv->row_of, s.n_shared ? sv->o_sh : nullptr, y, s.T, (int)s.d, (int)s.k,

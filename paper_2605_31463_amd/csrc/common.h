@@ -39,6 +39,8 @@ enum KernelId {
   K_ZC_PARAM_REDUCE,
   K_THRESHOLD_GRAD,
   K_AUX_PARTIAL_ROWS,
+  K_QUANT_ROWS,
+  K_WEIGHT_QUANT,
   K_NUM_KERNELS
 };
 
@@ -118,6 +120,25 @@ template <> struct Vec16<bf16_t> {
 };
 
 __device__ __forceinline__ float sigmoidf_(float z) { return 1.0f / (1.0f + __expf(-z)); }
+
+// OCP FP8 E4M3 codes (round to nearest even) of four float32 values, clamped
+// to +-448 first, packed little-endian into one dword.
+__device__ __forceinline__ float e4m3_clamp(float v) { return fminf(fmaxf(v, -448.f), 448.f); }
+__device__ __forceinline__ uint32_t e4m3x4(float a, float b, float c, float d) {
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_clamp(a), e4m3_clamp(b), 0, false);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(e4m3_clamp(c), e4m3_clamp(d), lo, true);
+}
+// Row / column quantisation scale of the largest magnitude amax: values are
+// multiplied by 448 / amax before rounding and the products carry amax / 448
+// (an all-zero row or column: 1 and 1).
+__device__ __forceinline__ float e4m3_inv(float amax) { return amax > 0.f ? 448.f / amax : 1.f; }
+__device__ __forceinline__ float e4m3_scale(float amax) { return amax > 0.f ? amax / 448.f : 1.f; }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  return v;
+}
 
 // Wave-wide float sum (64 lanes), result in every lane.
 __device__ __forceinline__ float wave_sum(float v) {

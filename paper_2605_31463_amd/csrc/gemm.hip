@@ -36,6 +36,7 @@ namespace moe {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef int v4i32 __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -282,6 +283,36 @@ struct KOperand {
   }
 };
 
+// FP8 gate/up weights: a K-contiguous ROWS x BK tile whose rows 0 .. ROWS/2-1
+// are rows n0.. of the gate matrix and rows ROWS/2 .. of the same rows of the
+// up matrix (each 1 KB copy lies in one half: the copy, wave-uniform, picks
+// its descriptor).
+template <int ROWS, int NW, int BK>
+struct KOperandGU {
+  static constexpr int CPR = BK / 8;
+  static constexpr int NIW = ROWS * BK * 2 / 1024 / NW;
+  static constexpr int RPC = 1024 / (2 * BK);              // rows per copy
+  static_assert((ROWS / 2) % RPC == 0, "a copy never straddles the gate/up halves");
+  int32x4_t rg, ru;
+  uint32_t voff[NIW];
+  __device__ __forceinline__ void init(int wave, int lane, int n0, int ld) {
+#pragma unroll
+    for (int j = 0; j < NIW; ++j) {
+      const int q = (NIW * wave + j) * 64 + lane;
+      const int row = q / CPR, phys = q % CPR;
+      const int src_row = n0 + (row < ROWS / 2 ? row : row - ROWS / 2);
+      voff[j] = (uint32_t)(((int64_t)src_row * ld + 8 * (phys ^ kswz<BK>(row))) * 2);
+    }
+  }
+  __device__ __forceinline__ void issue(uint32_t tile, int wave, uint32_t soff) const {
+#pragma unroll
+    for (int j = 0; j < NIW; ++j) {
+      const bool up = (NIW * wave + j) * RPC >= ROWS / 2;
+      dma16(up ? ru : rg, tile + (NIW * wave + j) * 1024, voff[j], soff);
+    }
+  }
+};
+
 // This wave's share of one MN-contiguous BK x (64*NSUB) tile.  Copy t covers
 // k-rows 8 (t % (BK/8)) .. +7 of sub-tile t / (BK/8); sub-tile s comes from
 // descriptor src[s] starting at column col0[s].  The descriptors of this
@@ -333,6 +364,12 @@ __device__ __forceinline__ uint4 add_bf16x8(uint4 a, uint4 b) {
 template <int BK>
 __device__ __forceinline__ bf16x8 frag_k(const bf16_t* tile, int rb, int ks, int lane) {
   return *reinterpret_cast<const bf16x8*>(tile + k_off<BK>(rb * 32 + (lane & 31), 2 * ks + (lane >> 5)));
+}
+typedef int v8i __attribute__((ext_vector_type(8)));
+// two 16-byte fragments as the 32-byte operand of the FP8 MFMA
+__device__ __forceinline__ v8i pair8(bf16x8 lo, bf16x8 hi) {
+  const v4i32 a = __builtin_bit_cast(v4i32, lo), b = __builtin_bit_cast(v4i32, hi);
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 // MN-contiguous: columns cb*32 + lane%32, same k.
 template <int BK>
@@ -921,11 +958,18 @@ __device__ __forceinline__ void tile_dims(const GemmArgs& a, const Tile& tl, int
 
 // CL: the clamped GLU activation (gate/up forward and down dgrad epilogues);
 // compiled as its own kernel so that the SwiGLU kernels carry none of its code.
-template <int MODE, class C, bool CL = false>
+// FP8 (forward passes only): E4M3 operands, both K-contiguous (activation rows
+// and the weight cache's transposed weights), staged exactly like bf16 data of
+// half the K (a 16-byte chunk holds 16 codes); v_mfma_f32_32x32x64_f8f6f4 takes
+// two bf16-sized fragments per operand (the same k subset on both sides); the
+// epilogue first scales the float32 accumulators by the row's and the
+// column's quantisation scales.
+template <int MODE, class C, bool CL = false, bool FP8 = false>
 __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persistent(GemmArgs a) {
+  static_assert(!FP8 || MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN, "FP8 forward passes only");
   constexpr bool wgrad = is_wgrad<MODE>();
   constexpr bool a_mn = wgrad;
-  constexpr bool b_mn = MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN || wgrad;
+  constexpr bool b_mn = !FP8 && (MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN || wgrad);
   constexpr int BM = C::BM, BN = C::BN, MI = C::MI, NI = C::NI, S = C::S, NW = C::NW, BK = C::BK;
   static_assert(MODE != G_FWD_GATEUP || NI % 2 == 0, "gate/up pairs need an even number of column blocks");
   __shared__ __align__(16) bf16_t lds[S][C::STAGE_ELEMS];
@@ -965,6 +1009,7 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
   KOperand<BM, NW, BK> ka;
   MNOperand<BM / 64, NW, BK> ma;
   KOperand<BN, NW, BK> kb;
+  KOperandGU<BN, NW, BK> kgu;
   MNOperand<BN / 64, NW, BK> mb;
   int32x4_t b_up = make_rsrc(W0, 0);
   int64_t a_kstride = 0, b_kstride = 0;
@@ -974,7 +1019,8 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
     tile_dims<MODE>(a, tl, K, M, N);
     const int g = tl.g;
     if (!a_mn) {
-      const int lda = MODE == G_FWD_DOWN ? f : (MODE == G_DGRAD_GATEUP ? 2 * f : d);
+      // (FP8 rows: K codes = K/2 two-byte units)
+      const int lda = (MODE == G_FWD_DOWN ? f : (MODE == G_DGRAD_GATEUP ? 2 * f : d)) / (FP8 ? 2 : 1);
       ka.rsrc = make_rsrc(A + (int64_t)tl.row_base * lda, (int64_t)M * lda * 2);
       ka.init(wave, lane, tl.m0, lda);
       a_kstride = 2;
@@ -991,7 +1037,20 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
       ma.init(wave, lane, src, col0, lda);
       a_kstride = (int64_t)lda * 2;
     }
-    if (MODE == G_FWD_GATEUP) {
+    if (FP8 && MODE == G_FWD_GATEUP) {
+      // cache rows: [E][f][d] codes of the gate and of the up weights
+      const uint8_t* qg = reinterpret_cast<const uint8_t*>(a.w0) + (int64_t)g * f * d;
+      const uint8_t* qu = reinterpret_cast<const uint8_t*>(a.w1) + (int64_t)g * f * d;
+      kgu.rg = make_rsrc(qg, (int64_t)f * d);
+      kgu.ru = make_rsrc(qu, (int64_t)f * d);
+      kgu.init(wave, lane, tl.n0, d / 2);
+      b_kstride = 2;
+    } else if (FP8 && MODE == G_FWD_DOWN) {
+      // cache rows: [E][d][f] codes of the down weights
+      kb.rsrc = make_rsrc(reinterpret_cast<const uint8_t*>(a.w0) + (int64_t)g * d * f, (int64_t)d * f);
+      kb.init(wave, lane, tl.n0, f / 2);
+      b_kstride = 2;
+    } else if (MODE == G_FWD_GATEUP) {
       const int32x4_t rg = make_rsrc(W0 + (int64_t)g * d * f, (int64_t)d * f * 2);
       const int32x4_t ru = make_rsrc(W1 + (int64_t)g * d * f, (int64_t)d * f * 2);
       int32x4_t src[BN / 64];
@@ -1045,6 +1104,7 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
       const Tile tl = tile_at<MODE, BM, BN>(a, p_t, pre, tord);
       int K, M, N;
       tile_dims<MODE>(a, tl, K, M, N);
+      if constexpr (FP8) K >>= 1;  // two-byte units of codes
       p_nk = (K + BK - 1) / BK;
       if (p_nk > 0) {
         setup(tl);
@@ -1060,11 +1120,13 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
     const uint32_t Bs = As + C::A_ELEMS * 2;
     if (!a_mn) ka.issue(As, wave, (uint32_t)(k0 * a_kstride));
     else ma.issue(As, wave, (uint32_t)(k0 * a_kstride));
-    if (MODE == G_DGRAD_GATEUP) {
+    if (FP8 && MODE == G_FWD_GATEUP) {
+      kgu.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
+    } else if (MODE == G_DGRAD_GATEUP) {
       KOperand<BN, NW, BK> kk = kb;
       if (k0 >= f) kk.rsrc = b_up;
       kk.issue(Bs, wave, (uint32_t)((k0 >= f ? k0 - f : k0) * b_kstride));
-    } else if (MODE == G_DGRAD_DOWN) {
+    } else if (MODE == G_DGRAD_DOWN || (FP8 && MODE == G_FWD_DOWN)) {
       kb.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
     } else {
       mb.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
@@ -1122,6 +1184,7 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
     const Tile tl = tile_at<MODE, BM, BN>(a, c_t, pre, tord);
     int K, M, N;
     tile_dims<MODE>(a, tl, K, M, N);
+    if constexpr (FP8) K >>= 1;
     const int g = tl.g;
     const int nk = (K + BK - 1) / BK;
     // 32-row blocks of this wavefront that hold rows of the tile (a ragged
@@ -1159,6 +1222,26 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
       const bf16_t* Bs = As + C::A_ELEMS;
       ++consumed;
       if (!wave_rows) continue;
+      if constexpr (FP8) {
+        // 64 codes of k per instruction: chunks 2ks, 2ks+1 of the bf16 layout
+#pragma unroll
+        for (int ks = 0; ks < BK / 32; ++ks) {
+          v8i b8[NI];
+#pragma unroll
+          for (int j = 0; j < NI; ++j)
+            b8[j] = pair8(frag_k<BK>(Bs, bcol(j), 2 * ks, lane), frag_k<BK>(Bs, bcol(j), 2 * ks + 1, lane));
+#pragma unroll
+          for (int i = 0; i < MI; ++i)
+            if (decltype(all_live)::value || i < live) {
+              const v8i a8 =
+                  pair8(frag_k<BK>(As, wm * MI + i, 2 * ks, lane), frag_k<BK>(As, wm * MI + i, 2 * ks + 1, lane));
+#pragma unroll
+              for (int j = 0; j < NI; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(b8[j], a8, acc[i][j], 0, 0, 0, 127, 0,
+                                                                            127);
+            }
+        }
+      } else {
       bf16x8 af[2][MI], bfr[2][NI];
       auto load_frags = [&](int ks, int slot) {
 #pragma unroll
@@ -1193,6 +1276,7 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
           }
         }
       }
+      }  // bf16
     }
     };
     if (live == MI) k_loop(std::true_type{});
@@ -1202,6 +1286,33 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
     // transposed product: lane l has row 32i + l%32, register v = 4q + t
     // column 32j + 8q + 4(l/32) + t.
     const int mrow0 = tl.m0 + wm * C::TM;
+    if constexpr (FP8) {
+      // dequantise: row scale (activation row) times column scale (weight
+      // column); the column scales are loaded once per column block
+      float sr[MI];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const int m = mrow0 + 32 * i + r32;
+        sr[i] = m < M ? a.a_scale[tl.row_base + m] : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const bool up = MODE == G_FWD_GATEUP && j >= NI / 2;
+        const int c0 = MODE == G_FWD_GATEUP ? tl.n0 + wn * (C::TN / 2) + 32 * (up ? j - NI / 2 : j)
+                                            : tl.n0 + wn * C::TN + 32 * j;
+        const float* sc = (up ? a.b_scale1 : a.b_scale0) + (int64_t)g * N;
+        float cs[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int c = c0 + 8 * (v >> 2) + 4 * hh + (v & 3);
+          cs[v] = c < N ? sc[c] : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < MI; ++i)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) acc[i][j][v] *= sr[i] * cs[v];
+      }
+    }
     if (MODE == G_FWD_GATEUP) {
       auto epi = [&](auto) {
         bf16_t* gu = reinterpret_cast<bf16_t*>(a.c0);
@@ -1573,7 +1684,7 @@ inline int cu_count() {
   return n;
 }
 
-template <int MODE, class C, bool CL = false>
+template <int MODE, class C, bool CL = false, bool FP8 = false>
 int launch_bf16_persistent(const GemmArgs& a, hipStream_t s) {
   const int G = a.offsets ? a.ngroups : 1;
   const int nt = n_tiles<MODE, C::BN>(a.d, a.f);
@@ -1591,7 +1702,7 @@ int launch_bf16_persistent(const GemmArgs& a, hipStream_t s) {
   constexpr int kOcc = (160 * 1024) / kLdsPerBlock > 0 ? (160 * 1024) / kLdsPerBlock : 1;
   const int64_t grid = std::min<int64_t>((cu_count() * kOcc / 8) * 8, (nb + 7) / 8 * 8);
   return launch(kGemmKernelId[MODE], s, kGemmName[MODE],
-                [&] { gemm_bf16_persistent<MODE, C, CL><<<(int)grid, C::NT, 0, s>>>(a); });
+                [&] { gemm_bf16_persistent<MODE, C, CL, FP8><<<(int)grid, C::NT, 0, s>>>(a); });
 }
 
 #ifndef MOE_GEMM_PERSISTENT
@@ -1600,6 +1711,8 @@ int launch_bf16_persistent(const GemmArgs& a, hipStream_t s) {
 
 template <int MODE>
 int launch_mode(const GemmArgs& a, hipStream_t s) {
+  if (a.fp8 && !(a.bf16 && MOE_GEMM_PERSISTENT && (MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN)))
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "gemm: FP8 runs the bf16 forward passes only");
   if (a.accumulate && !is_wgrad<MODE>())
     return moe_set_error(MOE_ERR_INVALID_ARG, "gemm: accumulate applies to the weight-gradient passes only");
   if (a.bf16 && a.accumulate && !MOE_GEMM_PERSISTENT)
@@ -1608,6 +1721,18 @@ int launch_mode(const GemmArgs& a, hipStream_t s) {
     const int G = a.offsets ? a.ngroups : 1;
     const int64_t rows_per_group = a.offsets ? a.max_rows / G : a.dense_rows;
     if constexpr (MOE_GEMM_PERSISTENT != 0) {
+      if constexpr (MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN) {
+        if (a.fp8) {
+          if constexpr (MODE == G_FWD_GATEUP) {
+            if (a.act == MOE_ACT_CLAMPED_GLU) {
+              if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, true, true>(a, s);
+              return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big, true, true>(a, s);
+            }
+          }
+          if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, false, true>(a, s);
+          return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big, false, true>(a, s);
+        }
+      }
       if constexpr (MODE == G_FWD_GATEUP || MODE == G_DGRAD_DOWN) {
         if (a.act == MOE_ACT_CLAMPED_GLU) {
           if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, true>(a, s);

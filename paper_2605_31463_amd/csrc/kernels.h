@@ -44,8 +44,17 @@ struct PermArgs {
   int32_t* row_of;   // [T][k]
   int32_t* token_of; // [R]
   void* x_perm;      // [R][d]
+  uint8_t* xq;       // [R][d] E4M3 rows of the FFN experts (FP8 forward), or null
+  float* sx;         // [R] their row scales
 };
 int launch_permute(const PermArgs& a, hipStream_t s);
+
+// FP8 forward: E4M3 rows of h [R][f] (rows below offsets[E]) and their scales.
+int launch_quant_rows(const void* h, const int32_t* offsets, int E, int64_t R, int f, uint8_t* hq, float* sh,
+                      hipStream_t s);
+// FP8 weight cache of one expert weight W [E][K][N] (bf16): column maxima
+// amax [E][N], scales [E][N] = amax / 448, codes Q [E][N][K] (transposed).
+int launch_weight_quant(const void* w, int E, int K, int N, float* amax, float* scale, uint8_t* q, hipStream_t s);
 
 // Zero-computation experts of the pool (MoE++): pool ids E_ffn .. are n_zero
 // zero experts (out = 0), then n_copy copy experts (out = x), then n_const
@@ -229,6 +238,12 @@ struct GemmArgs {
   bool accumulate;         // wgrad passes: add into c0/c1/db0/db1 instead of overwriting
   int act;                 // MOE_ACT_*: activation of the gate/up forward and down dgrad epilogues
   float act_alpha, act_limit;
+  // FP8 forward passes: a = E4M3 rows, w0 / w1 = the weight cache's E4M3 codes
+  // ([E][f][d] gate / up, [E][d][f] down), the float32 row and column scales
+  bool fp8;
+  const float* a_scale;    // [rows]
+  const float* b_scale0;   // [E][N] gate (or down) column scales
+  const float* b_scale1;   // [E][f] up column scales
 };
 int launch_gemm(const GemmArgs& a, hipStream_t s);
 

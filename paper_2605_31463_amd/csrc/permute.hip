@@ -146,6 +146,20 @@ __global__ __launch_bounds__(256) void permute_copy_kernel(PermArgs a) {
   const int nch = a.d / V;
   const XT* x = reinterpret_cast<const XT*>(a.x) + t * a.d;
   XT* xp = reinterpret_cast<XT*>(a.x_perm);
+  // FP8 forward: the token's E4M3 scale from a first pass over its row
+  float inv = 1.f, scale = 1.f;
+  if (a.xq) {
+    float m = 0.f;
+    for (int c = lane; c < nch; c += 64) {
+      float v[V];
+      Vec16<XT>::load(x + (int64_t)c * V, v);
+#pragma unroll
+      for (int q = 0; q < V; ++q) m = fmaxf(m, fabsf(v[q]));
+    }
+    m = wave_max(m);
+    inv = e4m3_inv(m);
+    scale = e4m3_scale(m);
+  }
   // rows at or past the FFN experts' end belong to zero-computation experts
   // (no activations): not written
   const int64_t r_end = a.offsets[a.E_rows];
@@ -170,6 +184,21 @@ __global__ __launch_bounds__(256) void permute_copy_kernel(PermArgs a) {
       for (int j = 0; j < CPL; ++j) {
         const int c = c0 + j * 64 + lane;
         if (c < nch) *reinterpret_cast<uint4*>(xp + rows[s] * a.d + (int64_t)c * V) = v[j];
+      }
+      if (a.xq) {
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+          const int c = c0 + j * 64 + lane;
+          if (c >= nch) continue;
+          float f8[V];
+          Vec16<XT>::load(reinterpret_cast<const XT*>(&v[j]), f8);
+          if constexpr (V == 8) {
+            const uint2 codes = make_uint2(e4m3x4(f8[0] * inv, f8[1] * inv, f8[2] * inv, f8[3] * inv),
+                                           e4m3x4(f8[4] * inv, f8[5] * inv, f8[6] * inv, f8[7] * inv));
+            *reinterpret_cast<uint2*>(a.xq + rows[s] * a.d + (int64_t)c * V) = codes;
+          }
+        }
+        if (lane == 0 && c0 == 0) a.sx[rows[s]] = scale;
       }
     }
   }

@@ -54,6 +54,16 @@ class MoELayer:
             g.update(d_threshold=e(s.E, dt=torch.float32))
         return g
 
+    def build_fp8_cache(self, params, stream=None):
+        """shape.fp8: quantise the expert weights into a cache (reused by every
+        forward until the weights change) and point params at it."""
+        if getattr(self, "fp8_cache", None) is None:
+            n = L.moe_fp8_cache_size(self.shape)
+            self.fp8_cache = torch.empty(max(n, 1), dtype=torch.uint8, device=self.device)
+        L.moe_fp8_cache_build(self.shape, params["w_gate"], params["w_up"], params["w_down"], self.fp8_cache, stream)
+        params["fp8_cache"] = self.fp8_cache
+        return params
+
     def forward(self, params, x, stream=None):
         L.moe_layer_fwd(self.shape, params, x, self.saved, self.y, self.ws_fwd, stream)
         return self.y

@@ -68,6 +68,8 @@ def test_workspace_sizes_scale_with_shape():
     (dict(router="sigmoid_threshold", n_copy=1), L.MOE_ERR_UNSUPPORTED),
     (dict(router="sigmoid_threshold", bias_mode="select"), L.MOE_ERR_UNSUPPORTED),
     (dict(router="sigmoid_threshold", E=16, n_groups=4, topk_groups=2), L.MOE_ERR_INVALID_ARG),
+    (dict(fp8=True, dtype="f32"), L.MOE_ERR_UNSUPPORTED),
+    (dict(fp8=True, dtype="bf16", d=192), L.MOE_ERR_UNSUPPORTED),
     (dict(act="clamped_glu", act_alpha=0.0), L.MOE_ERR_INVALID_ARG),
     (dict(act="clamped_glu", act_limit=float("inf")), L.MOE_ERR_INVALID_ARG),
 ])
@@ -116,14 +118,15 @@ def test_status_strings_and_kernel_names():
 
 def test_shape_struct_layout_matches_header():
     # int64 x5, int32 x3 (+pad), int64, int32 x2, float, int32 x3, float, int32 x3,
-    # float, int32, float x2 -> 120 bytes
-    assert ctypes.sizeof(L.moe_shape) == 120
+    # float, int32, float x2, int32 (+pad) -> 128 bytes
+    assert ctypes.sizeof(L.moe_shape) == 128
     assert L.moe_shape.f_shared.offset == 56
     assert L.moe_shape.aux_coef.offset == 88
     assert L.moe_shape.zc_aux_weight.offset == 104
     assert L.moe_shape.act_limit.offset == 116
+    assert L.moe_shape.fp8.offset == 120
     # pointer structs: one pointer per field, in the header's order
-    assert ctypes.sizeof(L.moe_params) == 15 * 8 and L.moe_params.gate_threshold.offset == 112
+    assert ctypes.sizeof(L.moe_params) == 16 * 8 and L.moe_params.fp8_cache.offset == 120
     assert ctypes.sizeof(L.moe_saved) == 15 * 8 and L.moe_saved.aux_loss.offset == 112
     assert ctypes.sizeof(L.moe_grads) == 13 * 8 and L.moe_grads.d_threshold.offset == 96
 
@@ -210,3 +213,21 @@ def test_threshold_router_on_the_host():
     st = L.LIB.moe_layer_bwd_wgrad(ctypes.byref(s), ctypes.byref(pr), fake, ctypes.byref(sv), fake,
                                    ctypes.byref(gr), 0, fake, 1 << 40, None)
     assert st == L.MOE_ERR_INVALID_ARG and "d_threshold" in L.last_error()
+
+
+def test_fp8_cache_on_the_host():
+    """The cache size scales with the experts; building needs shape.fp8 and a
+    large enough cache; the layer forward asks for the cache."""
+    s = L.make_shape(T=64, d=256, E=4, k=2, f=128, dtype="bf16", fp8=True)
+    n = L.moe_fp8_cache_size(s)
+    assert n >= 3 * 4 * 256 * 128 + 4 * (2 * 4 * 128 + 4 * 256) * 2
+    with pytest.raises(L.MoeError) as ei:
+        L.moe_fp8_cache_size(L.make_shape(T=64, d=256, E=4, k=2, f=128, dtype="bf16"))
+    assert ei.value.status == L.MOE_ERR_UNSUPPORTED
+    fake = ctypes.c_void_p(16)   # never dereferenced: validation fails first
+    st = L.LIB.moe_fp8_cache_build(ctypes.byref(s), fake, fake, fake, fake, n - 1, None)
+    assert st == L.MOE_ERR_WORKSPACE
+    pr = L.moe_params(w_r=fake, w_gate=fake, w_up=fake, w_down=fake)
+    sv = L.moe_saved(**{nm: fake for nm, _ in L.moe_saved._fields_})
+    st = L.LIB.moe_layer_fwd(ctypes.byref(s), ctypes.byref(pr), fake, ctypes.byref(sv), fake, fake, 1 << 40, None)
+    assert st == L.MOE_ERR_INVALID_ARG and "fp8_cache" in L.last_error()

@@ -1,0 +1,119 @@
+"""GPU parity of the FP8 (E4M3) forward of the routed experts against the fp64
+oracle's FP8 layer.
+
+  * the weight cache: every code bit-exact against the oracle's per-column
+    quantisation, every scale equal (the row quantisers of x and h share its
+    conversion and scale arithmetic);
+  * the layer (moe_layer_fwd / moe_layer_bwd with shape.fp8 = 1): gu, y, dx,
+    dW_r and the expert weight gradients against the oracle's FP8 layer (bar:
+    2e-2 normwise), and gu farther than that from the bf16 forward (so that the
+    comparison sees the quantisation), on both GEMM tile shapes (Qwen3 widths
+    with 32 experts: 32 rows per expert, 128-row tiles; with 16 experts: 512
+    rows, 256-row tiles), with expert biases, with the clamped GLU, and
+    DeepSeek-V3 widths with the (bf16) shared expert;
+  * the cache is reused across calls (two forwards, one build)."""
+import numpy as np
+import pytest
+
+from moe_inputs import layer_inputs, to_f64, variant
+from oracle import quantize_cols
+from tests.helpers import TOL, check_routing, dev, device_params, host, oracle_run, rel
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    "qwen3_small_tiles": variant("qwen3", T=256, E=32, k=4, fp8=True),
+    "qwen3_e16": variant("qwen3", T=1024, E=16, fp8=True),
+    "qwen3_e16_bias": variant("qwen3", T=1024, E=16, expert_bias=True, fp8=True),
+    "qwen3_e16_clamped": variant("qwen3", T=1024, E=16, act="clamped_glu", w_std=0.27, fp8=True),
+    "dsv3": variant("dsv3", T=384, d=512, f=256, f_shared=256, fp8=True),
+}
+
+
+def setup(cfg, inp):
+    import torch
+    from paper_2605_31463_amd import _lib as L
+    from paper_2605_31463_amd.layer import MoELayer
+    layer = MoELayer(L.shape_from_config(cfg))
+    p = device_params(inp, cfg)
+    layer.build_fp8_cache(p)
+    torch.cuda.synchronize()
+    return layer, p
+
+
+def test_weight_cache_codes_bit_exact():
+    import torch
+    from paper_2605_31463_amd import _lib as L
+    cfg = variant("qwen3", T=64, E=3, k=2, d=256, f=128, fp8=True)
+    inp = layer_inputs(cfg, seed=2)
+    # add exact zeros, a zero column and wide magnitudes to the weights
+    for n in ("w_gate", "w_up", "w_down"):
+        w = to_f64(inp[n], "bf16")
+        w[:, :, 0] = 0.0
+        w[:, 3, :] *= 1e3
+        inp[n] = (np.asarray(w, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    print("weight cache, E=3 d=256 f=128", flush=True)
+    layer, p = setup(cfg, inp)
+    E, d, f = cfg["E"], cfg["d"], cfg["f"]
+    raw = layer.fp8_cache.cpu().numpy()
+    off = 0
+
+    def region(nbytes):
+        nonlocal off
+        r = raw[off:off + nbytes]
+        off += (nbytes + 255) // 256 * 256
+        return r
+    qg, qu, qd = region(E * f * d), region(E * f * d), region(E * d * f)
+    for n_ in (f, f, d):
+        region(E * n_ * 4)                             # column maxima
+    sg, su, sd = (region(E * n * 4).view(np.float32) for n in (f, f, d))
+    for name, q, s, K, N in (("w_gate", qg, sg, d, f), ("w_up", qu, su, d, f), ("w_down", qd, sd, f, d)):
+        for e in range(E):
+            w = to_f64(inp[name][e], "bf16")
+            codes, scale, _ = quantize_cols(w)               # codes [K][N]
+            got = q[e * N * K:(e + 1) * N * K].reshape(N, K)  # transposed
+            assert np.array_equal(got, codes.T), (name, e, int((got != codes.T).sum()))
+            assert np.array_equal(s[e * N:(e + 1) * N].astype(np.float64), scale), (name, e)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_fp8_layer_parity(name):
+    import torch
+    cfg = CASES[name]
+    tol = TOL[cfg["dtype"]]
+    inp = layer_inputs(cfg, seed=0)
+    print("fp8 layer", name, flush=True)
+    layer, p = setup(cfg, inp)
+    x = dev(inp["x"], cfg["dtype"])
+    dy = dev(inp["dy"], cfg["dtype"])
+    layer.forward(p, x)
+    y = layer.forward(p, x)            # the cache serves repeated calls
+    grads = layer.alloc_grads()
+    dx = layer.backward(p, x, dy, grads)
+    torch.cuda.synchronize()
+    fwd, bwd = oracle_run(cfg, inp)
+    fwd0, _ = oracle_run(dict(cfg, fp8=False), inp)
+    amb, all_equal = check_routing(cfg, fwd, host(layer.saved["topk_idx"]))
+    assert all_equal
+    E, f = cfg["E"], cfg["f"]
+    n = int(host(layer.saved["expert_offsets"])[E])
+    gu = host(layer.saved["gu"][:n])
+    g_ref = np.concatenate([fwd["g"][e] for e in range(E) if e in fwd["g"]])
+    u_ref = np.concatenate([fwd["u"][e] for e in range(E) if e in fwd["u"]])
+    g_bf = np.concatenate([fwd0["g"][e] for e in range(E) if e in fwd0["g"]])
+    errs = {
+        "g": rel(gu[:, :f], g_ref), "u": rel(gu[:, f:], u_ref),
+        "y": rel(host(y), fwd["y"]), "dx": rel(host(dx), bwd["dx"]),
+        "dw_r": rel(host(grads["dw_r"]), bwd["dw_r"]),
+    }
+    for nm in ("dw_gate", "dw_up", "dw_down") + (("db_gate", "db_up", "db_down") if cfg["expert_bias"] else ()):
+        errs[nm] = rel(host(grads[nm]), np.stack([bwd["experts"][e][nm] for e in range(E)]))
+    if cfg["n_shared"]:
+        errs["dws_down"] = rel(host(grads["dws_down"]), bwd["shared"]["dw_down"])
+    dist_bf16 = rel(g_bf, g_ref)
+    print(name, "fp8 vs bf16 forward (oracle): g %.2e, y %.2e;" % (dist_bf16, rel(fwd0["y"], fwd["y"])),
+          {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+    assert dist_bf16 > 2 * errs["g"]          # the comparison resolves the quantisation
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, bad
