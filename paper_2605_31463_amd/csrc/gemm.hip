@@ -1286,33 +1286,6 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
     // transposed product: lane l has row 32i + l%32, register v = 4q + t
     // column 32j + 8q + 4(l/32) + t.
     const int mrow0 = tl.m0 + wm * C::TM;
-    if constexpr (FP8) {
-      // dequantise: row scale (activation row) times column scale (weight
-      // column); the column scales are loaded once per column block
-      float sr[MI];
-#pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        const int m = mrow0 + 32 * i + r32;
-        sr[i] = m < M ? a.a_scale[tl.row_base + m] : 0.f;
-      }
-#pragma unroll
-      for (int j = 0; j < NI; ++j) {
-        const bool up = MODE == G_FWD_GATEUP && j >= NI / 2;
-        const int c0 = MODE == G_FWD_GATEUP ? tl.n0 + wn * (C::TN / 2) + 32 * (up ? j - NI / 2 : j)
-                                            : tl.n0 + wn * C::TN + 32 * j;
-        const float* sc = (up ? a.b_scale1 : a.b_scale0) + (int64_t)g * N;
-        float cs[16];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int c = c0 + 8 * (v >> 2) + 4 * hh + (v & 3);
-          cs[v] = c < N ? sc[c] : 0.f;
-        }
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) acc[i][j][v] *= sr[i] * cs[v];
-      }
-    }
     if (MODE == G_FWD_GATEUP) {
       auto epi = [&](auto) {
         bf16_t* gu = reinterpret_cast<bf16_t*>(a.c0);
@@ -1324,22 +1297,30 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
         for (int j = 0; j < NI / 2; ++j) {
           const int jj0 = jbase + 32 * j;
           const int ncols = min(32, N - jj0);
-          float bgv[16], buv[16];
+          float bgv[16], buv[16], sgv[16], suv[16];
   #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int c = jj0 + 8 * (v >> 2) + 4 * hh + (v & 3);
             bgv[v] = (bgp && c < N) ? bf2f(bgp[(int64_t)g * f + c]) : 0.f;
             buv[v] = (bup && c < N) ? bf2f(bup[(int64_t)g * f + c]) : 0.f;
+            sgv[v] = 1.f;
+            suv[v] = 1.f;
+            if constexpr (FP8) {  // the weight columns' quantisation scales
+              sgv[v] = c < N ? a.b_scale0[(int64_t)g * f + c] : 0.f;
+              suv[v] = c < N ? a.b_scale1[(int64_t)g * f + c] : 0.f;
+            }
           }
   #pragma unroll
           for (int i = 0; i < MI; ++i) {
             const int m0 = mrow0 + 32 * i;
             if (m0 >= M || ncols <= 0) continue;
+            // FP8: the activation row's scale
+            const float sr = FP8 ? (m0 + r32 < M ? a.a_scale[tl.row_base + m0 + r32] : 0.f) : 1.f;
             float gv[16], uv[16], hv[16];
   #pragma unroll
             for (int v = 0; v < 16; ++v) {
-              gv[v] = acc[i][j][v] + bgv[v];
-              uv[v] = acc[i][j + NI / 2][v] + buv[v];
+              gv[v] = FP8 ? __builtin_fmaf(acc[i][j][v], sr * sgv[v], bgv[v]) : acc[i][j][v] + bgv[v];
+              uv[v] = FP8 ? __builtin_fmaf(acc[i][j + NI / 2][v], sr * suv[v], buv[v]) : acc[i][j + NI / 2][v] + buv[v];
               hv[v] = act_h_t<CL>(a, gv[v], uv[v]);
               gv[v] = act_store_g_t<CL>(a, gv[v]);
               uv[v] = act_store_u_t<CL>(a, uv[v]);
@@ -1423,19 +1404,22 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
       for (int j = 0; j < NI; ++j) {
         const int n0 = nbase + 32 * j;
         const int ncols = min(32, N - n0);
-        float bd[16];
+        float bd[16], sc[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int c = n0 + 8 * (v >> 2) + 4 * hh + (v & 3);
           bd[v] = (bdp && c < N) ? bf2f(bdp[(int64_t)g * d + c]) : 0.f;
+          sc[v] = 1.f;
+          if constexpr (FP8) sc[v] = c < N ? a.b_scale0[(int64_t)g * N + c] : 0.f;  // weight column scales
         }
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
           const int m0 = mrow0 + 32 * i;
           if (m0 >= M || ncols <= 0) continue;
+          const float sr = FP8 ? (m0 + r32 < M ? a.a_scale[tl.row_base + m0 + r32] : 0.f) : 1.f;
           float o[16];
 #pragma unroll
-          for (int v = 0; v < 16; ++v) o[v] = acc[i][j][v] + bd[v];
+          for (int v = 0; v < 16; ++v) o[v] = FP8 ? __builtin_fmaf(acc[i][j][v], sr * sc[v], bd[v]) : acc[i][j][v] + bd[v];
           if (MODE == G_DGRAD_DOWN) {
             // dSwiGLU with the saved gate/up values of this lane's row
             const int m = m0 + r32;
