@@ -40,7 +40,9 @@ Fields:
                          (the router covers E + their number)
   zc_aux_weight          their weight in the load-balancing loss
   theta_mean, theta_std  thresholds of the 'sigmoid_threshold' router
-  fp8                    the routed experts' forward GEMMs on E4M3 operands
+  fp8                    the routed experts' GEMMs on E4M3 operands: 0 none,
+                         1 (or True) the forward ones, 2 the forward and the
+                         data-gradient ones
   act, act_alpha, act_limit  routed experts' activation: 'swiglu' or
                          'clamped_glu' (the GPT-OSS release's variant; its
                          slope and clamp bound)
@@ -59,7 +61,7 @@ _BASE = dict(
     expert_bias=False, n_shared=0, f_shared=0,
     x_std=1.0, w_r_std=0.02, w_std=0.02, b_std=0.02, beta_std=0.1, dy_std=1.0,
     n_zero=0, n_copy=0, n_const=0, zc_aux_weight=1.0, zc_v_std=1.0, zc_wc_std=0.02,
-    act="swiglu", act_alpha=1.702, act_limit=7.0, theta_mean=1.8, theta_std=0.1, fp8=False,
+    act="swiglu", act_alpha=1.702, act_limit=7.0, theta_mean=1.8, theta_std=0.1, fp8=0,
 )
 
 

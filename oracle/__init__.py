@@ -36,5 +36,6 @@ from .moe_oracle import (  # noqa: F401
     e4m3_round,
     quantize_rows,
     quantize_cols,
+    fp8_expert_backward,
     fp8_expert_forward,
 )

@@ -458,14 +458,16 @@ def layer_forward(spec, x, w_r, beta, expert_fn, shared=None, aux_coef=0.0, aux_
                 h=hs, y=y, shared=sh, f=fwidth, aux=aux, zc=zf)
 
 
-def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bias=False, zc=None, act=None):
+def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bias=False, zc=None, act=None,
+                   fp8=False):
     """Backward of L = sum_t <dy_t, y_t> (+ the auxiliary loss) through the
     whole layer.
 
     Returns dx [T][d], dw_r [d][E_pool], per-expert dict of dW/db,
     shared-expert grads, omega [T][k], dl [T][k], with zc the
     zero-computation experts' dict (dv, dwc), and for the threshold router
-    dtheta [E].
+    dtheta [E].  fp8: the routed experts' data-gradient products on E4M3
+    operands (fp8_expert_backward).
     """
     x = np.asarray(x, np.float64)
     dy = np.asarray(dy, np.float64)
@@ -494,8 +496,9 @@ def layer_backward(spec, x, w_r, beta, expert_fn, fwd, dy, shared=None, with_bia
                 grads[e].update(db_gate=np.zeros(wg.shape[1]), db_up=np.zeros(wu.shape[1]),
                                 db_down=np.zeros(wd.shape[1]))
             continue
-        ge = expert_backward(fwd["x_perm"][r0:r1], fwd["g"][e], fwd["u"][e], fwd["h"][e],
-                             do[r0:r1], wg, wu, wd, with_bias=with_bias, act=act)
+        bwd_fn = fp8_expert_backward if fp8 else expert_backward
+        ge = bwd_fn(fwd["x_perm"][r0:r1], fwd["g"][e], fwd["u"][e], fwd["h"][e],
+                    do[r0:r1], wg, wu, wd, with_bias=with_bias, act=act)
         dx_perm[r0:r1] = ge.pop("dx")
         ge.pop("dg")
         ge.pop("du")
@@ -815,9 +818,17 @@ def zc_backward(dy, x, topk_idx, topk_w, E, zs, v, wc):
 # The activations are quantised from their stored bf16 values (FP8 runs bf16
 # layers): x is stored bf16 already, h is rounded to float32 and then to bf16
 # (nearest even) before its row is quantised.  The GEMMs multiply the
-# dequantised operands (code value times scale).  The backward uses the bf16
-# operands and weights as if the quantisation were the identity
-# (straight-through), with the activations gu and h of the FP8 forward.
+# dequantised operands (code value times scale).  With FP8 forward GEMMs only,
+# the backward uses the bf16 operands and weights as if the quantisation were
+# the identity (straight-through), with the activations gu and h of the FP8
+# forward.  With FP8 data-gradient GEMMs as well (fp8_expert_backward), the two
+# products that carry the gradient back to the input, dh = d_o W_down^T and
+# dx = [dg | du] [W_gate | W_up]^T, take E4M3 operands quantised in the same
+# way: the stored bf16 rows of d_o and of [dg | du] per row (one scale over a
+# row's gate and up halves together), W_down per row (an output column of dh)
+# and the concatenated rows of [W_gate | W_up] per row (an output column of dx,
+# again one scale over both halves).  The weight-gradient products stay on the
+# unquantised operands.
 
 _E4M3_MAX = 448.0
 
@@ -914,3 +925,30 @@ def fp8_expert_forward(xe, wg, wu, wd, bg=None, bu=None, bd=None, act=None):
     if bd is not None:
         o = o + bd
     return g, u, h, o
+
+
+def fp8_expert_backward(xe, g, u, h, do, wg, wu, wd, with_bias=False, act=None):
+    """expert_backward with its two data-gradient products on E4M3 operands:
+    dh from the row-quantised stored d_o and W_down, dx from the row-quantised
+    stored [dg | du] and [W_gate | W_up]; the weight gradients from the
+    unquantised d_o, dg, du (see the comment above e4m3_values)."""
+    _, _, doq = quantize_rows(round_bf16(do))
+    _, _, wdq = quantize_rows(wd)                        # [f][d]: a scale per output column j of dh
+    dh = doq @ wdq.T
+    _, hg, hu = glu(g, u, act)
+    dg = dh * hg
+    du = dh * hu
+    _, _, dguq = quantize_rows(round_bf16(np.concatenate([dg, du], axis=1)))
+    _, _, wguq = quantize_rows(np.concatenate([wg, wu], axis=1))   # [d][2f]: a scale per output column of dx
+    out = dict(
+        dw_down=h.T @ do,
+        dw_gate=xe.T @ dg,
+        dw_up=xe.T @ du,
+        dx=dguq @ wguq.T,
+        dg=dg, du=du,
+    )
+    if with_bias:
+        out["db_down"] = do.sum(axis=0)
+        out["db_gate"] = dg.sum(axis=0)
+        out["db_up"] = du.sum(axis=0)
+    return out

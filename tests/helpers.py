@@ -85,9 +85,9 @@ def oracle_run(cfg, inp, aux_coef=0.0, aux_f=None):
     act = act_of(cfg)
     theta = None if inp.get("gate_threshold") is None else inp["gate_threshold"].astype(np.float64)
     fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=aux_coef, aux_f=aux_f, zc=zc, act=act,
-                        theta=theta, fp8=cfg.get("fp8", False))
+                        theta=theta, fp8=bool(cfg.get("fp8", 0)))
     bwd = layer_backward(spec, x, w_r, beta, efn, fwd, to_f64(inp["dy"], dt), shared,
-                         with_bias=cfg["expert_bias"], zc=zc, act=act)
+                         with_bias=cfg["expert_bias"], zc=zc, act=act, fp8=cfg.get("fp8", 0) == 2)
     return fwd, bwd
 
 

@@ -1102,7 +1102,7 @@ def test_threshold_router_limits_reduce_to_fixed_k_routers():
 # FP8 (E4M3) forward of the expert GEMMs
 # ---------------------------------------------------------------------------
 
-from oracle import e4m3_round, e4m3_values, fp8_expert_forward, quantize_rows  # noqa: E402
+from oracle import e4m3_round, e4m3_values, expert_backward, fp8_expert_backward, fp8_expert_forward, quantize_rows  # noqa: E402
 
 
 def test_e4m3_values_and_rounding_match_torch():
@@ -1175,3 +1175,132 @@ def test_round_bf16_matches_torch():
     a = np.concatenate([rng.standard_normal(100000) * 10.0 ** rng.integers(-8, 8, 100000), [0.0, -0.0, 1.0]])
     want = torch.from_numpy(a).to(torch.float32).to(torch.bfloat16).double().numpy()
     assert np.array_equal(round_bf16(a), want)
+
+
+# ---------------------------------------------------------------------------
+# FP8 (E4M3) data-gradient products of the expert backward
+# ---------------------------------------------------------------------------
+
+def _fp8_bwd_case(seed, M=10, d=16, f=8):
+    rng = np.random.default_rng(seed)
+    xe = rng.standard_normal((M, d))
+    wg, wu = rng.standard_normal((d, f)) * 0.3, rng.standard_normal((d, f)) * 0.3
+    wd = rng.standard_normal((f, d)) * 0.3
+    g, u = xe @ wg, xe @ wu
+    h = g / (1 + np.exp(-g)) * u
+    do = rng.standard_normal((M, d))
+    return xe, g, u, h, do, wg, wu, wd
+
+
+def test_fp8_dgrad_exact_first_product_on_row_representable_operands():
+    """d_o rows and W_down rows that are E4M3 values times a power of two of
+    their own (rows 2^12 apart, so that no column scale could hold them), each
+    row reaching 448 times its power: the row quantisation of both operands is
+    exact, so dh and with it dg, du and the weight gradients equal the plain
+    backward's bit for bit (the stored-bf16 rounding of d_o is exact too)."""
+    xe, g, u, h, do, wg, wu, wd = _fp8_bwd_case(61)
+    rng = np.random.default_rng(62)
+    ev = e4m3_values()
+    fin = ev[np.isfinite(ev) & (np.abs(ev) <= 448)]
+    M, d = do.shape
+    f = wd.shape[0]
+    pw_do = 2.0 ** (12 * (np.arange(M) % 2) - 6)
+    do = rng.choice(fin, (M, d)) * pw_do[:, None]
+    do[:, 3] = 448 * pw_do
+    pw_wd = 2.0 ** (12 * (np.arange(f) % 2) - 9)
+    wd = rng.choice(fin, (f, d)) * pw_wd[:, None]
+    wd[:, 5] = -448 * pw_wd
+    ref = expert_backward(xe, g, u, h, do, wg, wu, wd)
+    got = fp8_expert_backward(xe, g, u, h, do, wg, wu, wd)
+    for n in ("dg", "du", "dw_gate", "dw_up", "dw_down"):
+        assert np.array_equal(got[n], ref[n]), n
+    assert not np.array_equal(got["dx"], ref["dx"])       # dx goes through the quantised [dg | du]
+
+
+def test_fp8_dgrad_row_scaling_equivariance():
+    """Scaling a row of d_o by 2^p scales the same row of dx by 2^p and leaves
+    every other row's bits alone (row-wise scales of d_o and of [dg | du]);
+    scaling row i of both W_gate and W_up by 2^p scales column i of dx by 2^p
+    and leaves the other columns alone (row-wise scales of [W_gate | W_up])."""
+    xe, g, u, h, do, wg, wu, wd = _fp8_bwd_case(63)
+    base = fp8_expert_backward(xe, g, u, h, do, wg, wu, wd)["dx"]
+    do2 = do.copy()
+    do2[4] *= 2.0 ** 7
+    got = fp8_expert_backward(xe, g, u, h, do2, wg, wu, wd)["dx"]
+    assert np.array_equal(got[4], base[4] * 2.0 ** 7)
+    keep = np.arange(do.shape[0]) != 4
+    assert np.array_equal(got[keep], base[keep])
+    wg2, wu2 = wg.copy(), wu.copy()
+    wg2[6] *= 2.0 ** -5
+    wu2[6] *= 2.0 ** -5
+    got = fp8_expert_backward(xe, g, u, h, do, wg2, wu2, wd)["dx"]
+    assert np.array_equal(got[:, 6], base[:, 6] * 2.0 ** -5)
+    keep = np.arange(wg.shape[0]) != 6
+    assert np.array_equal(got[:, keep], base[:, keep])
+    # a W_down row scaled by 2^p: dh column scales by 2^p; dx changes (through
+    # the quantised [dg | du]) but dW_down does not (unquantised operands)
+    wd2 = wd.copy()
+    wd2[2] *= 2.0 ** 3
+    a = fp8_expert_backward(xe, g, u, h, do, wg, wu, wd)
+    b = fp8_expert_backward(xe, g, u, h, do, wg, wu, wd2)
+    assert np.array_equal(b["dg"][:, 2], a["dg"][:, 2] * 8.0)
+    assert np.array_equal(np.delete(b["dg"], 2, axis=1), np.delete(a["dg"], 2, axis=1))
+
+
+def test_fp8_dgrad_one_scale_over_gate_and_up_halves():
+    """One scale per row over both halves: with W_up 2^-24 times W_gate (below
+    the smallest E4M3 step relative to the row's largest magnitude) the up
+    half quantises to zero and dx is the gate half's product alone; with
+    separate scales it would not be."""
+    xe, g, u, h, do, wg, wu, wd = _fp8_bwd_case(64)
+    tiny = fp8_expert_backward(xe, g, u, h, do, wg, wu * 2.0 ** -24, wd)
+    zero = fp8_expert_backward(xe, g, u, h, do, wg, wu * 0.0, wd)
+    # the [dg | du] quantisation is the same in both calls (du does not depend on W_up)
+    assert np.array_equal(tiny["dx"], zero["dx"])
+    sep = fp8_expert_backward(xe, g, u, h, do, wg * 0.0, wu * 2.0 ** -24, wd)["dx"]
+    assert np.abs(sep).max() > 0                              # alone, the up half is representable
+
+
+def test_fp8_dgrad_error_within_e4m3_bound():
+    """Against the plain backward, the FP8 products differ by quantisation
+    noise of E4M3's relative step (2^-3: at most 2^-4 per element) only."""
+    xe, g, u, h, do, wg, wu, wd = _fp8_bwd_case(65, M=64, d=128, f=96)
+    ref = expert_backward(xe, g, u, h, do, wg, wu, wd)
+    got = fp8_expert_backward(xe, g, u, h, do, wg, wu, wd)
+    for n in ("dg", "dx", "dw_gate"):
+        e = rel(got[n], ref[n])
+        assert 1e-3 < e < 2 * 2.0 ** -4, (n, e)
+    assert np.array_equal(got["dw_down"], ref["dw_down"])    # h^T d_o: unquantised operands
+
+
+def test_fp8_layer_backward_uses_fp8_dgrad():
+    """layer_backward(fp8=True) differs from the plain backward of the same
+    forward in dx and the expert weight gradients (through dh), by
+    quantisation noise, and the router gradient is untouched."""
+    spec = RouterSpec("softmax_topk", E=6, k=2)
+    c = make_case(spec, T=48, d=64, f=48, seed=66)
+    fwd = layer_forward(spec, c["x"], c["w_r"], None, efn(c), fp8=True)
+    b0 = layer_backward(spec, c["x"], c["w_r"], None, efn(c), fwd, c["dy"])
+    b1 = layer_backward(spec, c["x"], c["w_r"], None, efn(c), fwd, c["dy"], fp8=True)
+    assert 1e-3 < rel(b1["dx"], b0["dx"]) < 0.1
+    assert 1e-3 < rel(b1["experts"][0]["dw_gate"], b0["experts"][0]["dw_gate"]) < 0.1
+    assert np.array_equal(b1["experts"][0]["dw_down"], b0["experts"][0]["dw_down"])
+    assert np.array_equal(b1["dw_r"], b0["dw_r"])
+
+
+def test_fp8_dgrad_second_product_reads_e4m3_rows():
+    """With [W_gate | W_up] 0.875 times the identity (d = 2f: each row one
+    entry 448 * 2^-9, exactly representable with scale 2^-9), dx is 0.875
+    times the dequantised [dg | du]: every row of dx divided by its largest
+    magnitude / 448 lands on E4M3 values."""
+    f, d, M = 8, 16, 12
+    xe, g, u, h, do, _, _, wd = _fp8_bwd_case(67, M=M, d=d, f=f)
+    eye = np.eye(d) * 448 * 2.0 ** -9
+    wg, wu = eye[:, :f], eye[:, f:]
+    got = fp8_expert_backward(xe, g, u, h, do, wg, wu, wd)
+    ev = set(e4m3_values()[np.isfinite(e4m3_values())].tolist())
+    for r in range(M):
+        s = np.abs(got["dx"][r]).max() / 448.0
+        assert s > 0 and set((got["dx"][r] / s).tolist()) <= ev, r
+    ref = np.concatenate([got["dg"], got["du"]], axis=1) * 0.875
+    assert not np.array_equal(got["dx"], ref)               # quantised, not the plain [dg | du]
