@@ -26,7 +26,8 @@ sys.path.insert(0, ROOT)
 METRIC = "MoE layer fwd+bwd TFLOP/s and tokens/s on 1 MI355X; % of MFMA/HBM roofline"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
-FP8_KERNELS = ("gemm_gateup_fwd", "gemm_down_fwd")
+FP8_KERNELS = {1: ("gemm_gateup_fwd", "gemm_down_fwd"),
+               2: ("gemm_gateup_fwd", "gemm_down_fwd", "gemm_down_dgrad", "gemm_gateup_dgrad")}
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 GEMM_SOURCE = os.path.join(ROOT, "paper_2605_31463_amd", "csrc", "gemm.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
@@ -133,7 +134,8 @@ def cpu_baseline(cfg, seed, tokens, reps=1):
     for _ in range(reps):
         fwd = layer_forward(spec, x, w_r, beta, efn, shared, aux_coef=coef, zc=zc, theta=theta,
                             fp8=bool(cfg.get("fp8")))
-        layer_backward(spec, x, w_r, beta, efn, fwd, dy, shared, with_bias=scfg["expert_bias"], zc=zc)
+        layer_backward(spec, x, w_r, beta, efn, fwd, dy, shared, with_bias=scfg["expert_bias"], zc=zc,
+                       fp8=cfg.get("fp8") == 2)
     wall = time.perf_counter() - t0
     _, fb = layer_flops(scfg, rows=int(fwd["maps"]["offsets"][scfg["E"]]))
     blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
@@ -235,8 +237,9 @@ def main():
     ap.add_argument("--aux-coef", type=float, default=0.0,
                     help="add the global-level load-balancing loss of this coefficient (the paper "
                          "pretrains with 1e-3); 0: without it")
-    ap.add_argument("--fp8", action="store_true",
-                    help="the routed experts' forward GEMMs on FP8 (E4M3) operands; the weight cache is built "
+    ap.add_argument("--fp8", nargs="?", const="fwd", choices=("fwd", "all"), default=None,
+                    help="the routed experts' GEMMs on FP8 (E4M3) operands: the forward ones (fwd, the "
+                         "default) or the forward and data-gradient ones (all); the weight cache is built "
                          "once before the steps (as once per optimizer step) and its build time reported")
     ap.add_argument("--memory-kernels", action="store_true",
                     help="instead of the step benchmark: warm and cold (after a 1 GiB read scrub) times "
@@ -260,7 +263,7 @@ def main():
     if args.aux_coef:
         cfg = dict(cfg, aux_coef=args.aux_coef)
     if args.fp8:
-        cfg = dict(cfg, fp8=True)
+        cfg = dict(cfg, fp8=1 if args.fp8 == "fwd" else 2)
     dt = cfg["dtype"]
     torch.cuda.set_device(0)
     inp = layer_inputs(cfg, seed=args.seed)
@@ -374,8 +377,8 @@ def main():
     tflops = fb / (ms_per_step / 1e3) / 1e12
     bound, amount = work[dominant]
     dom_avg_s = dom_ms / max(dom_n, 1) / 1e3
-    fp8 = bool(cfg.get("fp8"))
-    mfma_peak = lambda name: PEAK_FP8_TFLOPS if fp8 and name in FP8_KERNELS else PEAK_BF16_TFLOPS  # noqa: E731
+    fp8 = int(cfg.get("fp8") or 0)
+    mfma_peak = lambda name: PEAK_FP8_TFLOPS if fp8 and name in FP8_KERNELS[fp8] else PEAK_BF16_TFLOPS  # noqa: E731
     if bound == "mfma":
         achieved = amount / dom_avg_s / 1e12
         peak, unit = mfma_peak(dominant), "TFLOP/s"
@@ -395,14 +398,15 @@ def main():
         "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "fp8 e4m3 (forward expert GEMMs) + bf16" if fp8 else dt,
+        "dtype": ("fp8 e4m3 (forward expert GEMMs) + bf16" if fp8 == 1 else
+                  "fp8 e4m3 (forward and data-gradient expert GEMMs) + bf16") if fp8 else dt,
         "data": "synthetic (seeded; shapes and distributions of the workload)",
         "config": dict({"workload": workload, "T": cfg["T"], "d": cfg["d"], "E": cfg["E"], "k": cfg["k"],
                         "f": cfg["f"], "router": cfg["router"], "aux_coef": cfg.get("aux_coef", 0.0)},
                        **({"n_zero": cfg["n_zero"], "n_copy": cfg["n_copy"], "n_const": cfg["n_const"],
                            "zc_aux_weight": cfg["zc_aux_weight"]} if zc else {}),
                        **({"ffn_rows": ffn_rows} if variable else {}),
-                       **({"fp8": True} if fp8 else {})),
+                       **({"fp8": "forward" if fp8 == 1 else "forward+dgrad"} if fp8 else {})),
         "tokens_per_s": round(cfg["T"] / (ms_per_step / 1e3), 1),
         "phases_median_of_last_10": {"fwd_ms": round(med(f_ms), 4), "bwd_ms": round(med(b_ms), 4),
                                      "step_ms": round(med(s_ms), 4),

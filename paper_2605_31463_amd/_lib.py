@@ -174,7 +174,7 @@ def make_shape(T, d, E, k, f, router="softmax_topk", n_groups=1, topk_groups=1, 
                      route_scale=route_scale, bias_mode=BIAS_MODES[bias_mode],
                      expert_bias=int(bool(expert_bias)), dtype=DTYPES[dtype], aux_coef=aux_coef,
                      n_zero=n_zero, n_copy=n_copy, n_const=n_const, zc_aux_weight=zc_aux_weight,
-                     act=ACTS[act], act_alpha=act_alpha, act_limit=act_limit, fp8=int(bool(fp8)))
+                     act=ACTS[act], act_alpha=act_alpha, act_limit=act_limit, fp8=int(fp8))
 
 
 def pool_size(shape):

@@ -110,7 +110,7 @@ int check_shape(const moe_shape* sh) {
     return moe_set_error(MOE_ERR_UNSUPPORTED, "zero-computation experts need a softmax router");
   if (s.router == MOE_ROUTER_SIGMOID_THRESHOLD && s.bias_mode != MOE_BIAS_NONE)
     return moe_set_error(MOE_ERR_UNSUPPORTED, "the threshold router takes no router bias");
-  if (s.fp8 != 0 && s.fp8 != 1) return moe_set_error(MOE_ERR_INVALID_ARG, "fp8 must be 0 or 1");
+  if (s.fp8 < 0 || s.fp8 > 2) return moe_set_error(MOE_ERR_INVALID_ARG, "fp8 must be 0, 1 or 2");
   if (s.fp8 && (s.dtype != MOE_BF16 || s.d % 128 || s.f % 128))
     return moe_set_error(MOE_ERR_UNSUPPORTED, "fp8 needs bf16 layers with d and f multiples of 128");
   if (s.act != MOE_ACT_SWIGLU && s.act != MOE_ACT_CLAMPED_GLU)
@@ -176,6 +176,7 @@ struct Plan {
   size_t d_o, dgu, dx_perm, dl, partial, w_rt, dgu_sh, dx_sh;
   size_t aux_dl, aux_dx, aux_off, aux_wpart;
   size_t zc_coef, zc_part, dth;
+  size_t doq, sdo, dguq, sdgu;
   size_t bwd_total;
   size_t saved_total;
 };
@@ -225,6 +226,12 @@ Plan plan(const moe_shape& s) {
   p.zc_coef = off; off += has_zc(s) ? align_up((size_t)R * 16) : 0;
   p.zc_part = off; off += s.n_const > 0 ? align_up((size_t)moe::route_dwr_tasks(R, s.n_const) * 3 * s.d * 4) : 0;
   p.dth = off; off += is_thr(s) ? align_up((size_t)R * 4) : 0;
+  // FP8 data-gradient GEMMs: E4M3 rows of d_o and dgu, and their scales
+  const bool q2 = s.fp8 == 2;
+  p.doq = off; off += q2 ? align_up((size_t)R * s.d) : 0;
+  p.sdo = off; off += q2 ? align_up((size_t)R * 4) : 0;
+  p.dguq = off; off += q2 ? align_up((size_t)R * 2 * s.f) : 0;
+  p.sdgu = off; off += q2 ? align_up((size_t)R * 4) : 0;
   p.bwd_total = off;
   size_t sv = 0;
   sv += (size_t)R * (4 + 4 + 4 + 4 + 4);  // topk_idx, topk_w, s_sel, row_of, token_of
@@ -274,9 +281,13 @@ GemmArgs gemm_base(const moe_shape& s, int mode, const int32_t* offsets) {
 
 // The shared expert (and the dense products of the auxiliary loss): SwiGLU.
 // FP8 weight cache regions: codes of gate, up [E][f][d] and down [E][d][f],
-// then the column maxima and scales of each (float32).
+// then the column maxima and scales of each (float32); with the data-gradient
+// GEMMs (fp8 = 2) also the row codes of [W_gate | W_up] [E][d][2f] and of
+// W_down [E][f][d] and their row scales.
 struct CachePlan {
-  size_t qg, qu, qd, ag, au, ad, sg, su, sd, total;
+  size_t qg, qu, qd, ag, au, ad, sg, su, sd;
+  size_t qgu_r, qd_r, sgu_r, sd_r;
+  size_t total;
 };
 CachePlan cache_plan(const moe_shape& s) {
   CachePlan c{};
@@ -291,6 +302,11 @@ CachePlan cache_plan(const moe_shape& s) {
   c.sg = off; off += align_up((size_t)s.E * s.f * 4);
   c.su = off; off += align_up((size_t)s.E * s.f * 4);
   c.sd = off; off += align_up((size_t)s.E * s.d * 4);
+  const bool q2 = s.fp8 == 2;
+  c.qgu_r = off; off += q2 ? align_up(2 * efd) : 0;
+  c.qd_r = off; off += q2 ? align_up(efd) : 0;
+  c.sgu_r = off; off += q2 ? align_up((size_t)s.E * s.d * 4) : 0;
+  c.sd_r = off; off += q2 ? align_up((size_t)s.E * s.f * 4) : 0;
   c.total = off;
   return c;
 }
@@ -379,7 +395,7 @@ int do_gemm_fwd_fp8(const moe_shape& s, const int32_t* offsets, const void* cach
   MOE_TRY(launch_gemm(g, st));
   uint8_t* hq = reinterpret_cast<uint8_t*>(wsp(ws, p.hq));
   float* sh = reinterpret_cast<float*>(wsp(ws, p.sh));
-  MOE_TRY(launch_quant_rows(h, offsets, (int)s.E, s.T * s.k, (int)s.f, hq, sh, st));
+  MOE_TRY(launch_quant_rows(h, nullptr, (int)s.f, 0, offsets, (int)s.E, s.T * s.k, hq, sh, st));
   g = gemm_base(s, G_FWD_DOWN, offsets);
   g.fp8 = true;
   g.a = hq;
@@ -388,6 +404,42 @@ int do_gemm_fwd_fp8(const moe_shape& s, const int32_t* offsets, const void* cach
   g.b_scale0 = reinterpret_cast<const float*>(cb + c.sd);
   g.bias0 = b_down;
   g.c0 = o;
+  return launch_gemm(g, st);
+}
+
+// FP8 data-gradient GEMMs of the routed experts: E4M3 rows of d_o through the
+// down dgrad (dSwiGLU in its epilogue, dgu stored bf16 for the weight
+// gradients), E4M3 rows of dgu through the gate/up dgrad, both against the
+// row-quantised weights of the cache.
+int do_gemm_dgrad_fp8(const moe_shape& s, const int32_t* offsets, const void* cache, const void* gu, const void* d_o,
+                      bool d_o_quantised, void* dgu, void* dx_perm, void* ws, hipStream_t st) {
+  const Plan p = plan(s);
+  const CachePlan c = cache_plan(s);
+  const char* cb = static_cast<const char*>(cache);
+  const int64_t R = s.T * s.k;
+  uint8_t* doq = reinterpret_cast<uint8_t*>(wsp(ws, p.doq));
+  float* sdo = reinterpret_cast<float*>(wsp(ws, p.sdo));
+  if (!d_o_quantised)  // (the combine backward writes them where it can)
+    MOE_TRY(launch_quant_rows(d_o, nullptr, (int)s.d, 0, offsets, (int)s.E, R, doq, sdo, st));
+  GemmArgs g = gemm_base(s, G_DGRAD_DOWN, offsets);
+  g.fp8 = true;
+  g.a = doq;
+  g.a_scale = sdo;
+  g.w0 = cb + c.qd_r;
+  g.b_scale0 = reinterpret_cast<const float*>(cb + c.sd_r);
+  g.aux = gu;
+  g.c0 = dgu;
+  MOE_TRY(launch_gemm(g, st));
+  uint8_t* dguq = reinterpret_cast<uint8_t*>(wsp(ws, p.dguq));
+  float* sdgu = reinterpret_cast<float*>(wsp(ws, p.sdgu));
+  MOE_TRY(launch_quant_rows(dgu, nullptr, 2 * (int)s.f, 0, offsets, (int)s.E, R, dguq, sdgu, st));
+  g = gemm_base(s, G_DGRAD_GATEUP, offsets);
+  g.fp8 = true;
+  g.a = dguq;
+  g.a_scale = sdgu;
+  g.w0 = cb + c.qgu_r;
+  g.b_scale0 = reinterpret_cast<const float*>(cb + c.sgu_r);
+  g.c0 = dx_perm;
   return launch_gemm(g, st);
 }
 
@@ -578,6 +630,7 @@ int check_layer_bwd(const moe_shape& s, const moe_params* prm, const void* x, co
   MOE_NEED(sv, "saved");
   MOE_NEED(prm->w_r, "params.w_r");
   MOE_NEED(sv->expert_offsets, "saved.expert_offsets");
+  if (s.fp8 == 2 && (phase & 1)) MOE_NEED(prm->fp8_cache, "params.fp8_cache");
   if (s.n_const > 0 && (phase & 1)) {
     MOE_NEED(prm->zc_v, "params.zc_v");
     MOE_NEED(prm->zc_wc, "params.zc_wc");
@@ -670,10 +723,19 @@ int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const void* x, co
   cb.topk_idx = sv->topk_idx;
   cb.zc = zc_args(s, prm, x, dy, wsp(ws, p.zc_coef));
   cb.dth = is_thr(s) ? reinterpret_cast<float*>(wsp(ws, p.dth)) : nullptr;
+  // FP8 data gradients: the E4M3 rows of d_o come with it (except with
+  // zero-computation experts, whose combine kernel does not write them)
+  const bool doq_fused = s.fp8 == 2 && !has_zc(s);
+  cb.doq = doq_fused ? reinterpret_cast<uint8_t*>(wsp(ws, p.doq)) : nullptr;
+  cb.sdo = doq_fused ? reinterpret_cast<float*>(wsp(ws, p.sdo)) : nullptr;
   MOE_TRY(launch_combine_bwd(cb, stream));
   // 2. expert dgrads
-  MOE_TRY(do_gemm_bwd(s, MOE_DGRAD, nullptr, sv->expert_offsets, sv->gu, nullptr, d_o, prm->w_gate, prm->w_up,
-                      prm->w_down, dgu, dx_perm, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, stream));
+  if (s.fp8 == 2)
+    MOE_TRY(do_gemm_dgrad_fp8(s, sv->expert_offsets, prm->fp8_cache, sv->gu, d_o, doq_fused, dgu, dx_perm, ws,
+                              stream));
+  else
+    MOE_TRY(do_gemm_bwd(s, MOE_DGRAD, nullptr, sv->expert_offsets, sv->gu, nullptr, d_o, prm->w_gate, prm->w_up,
+                        prm->w_down, dgu, dx_perm, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, stream));
   // 3. W_r^T for the router dx fused into the unpermute (zero rows up to the
   //    auxiliary loss's padded expert count)
   const bool aux = has_aux(s) && s.T > 0;
@@ -858,7 +920,10 @@ int moe_fp8_cache_build(const moe_shape* shape, const void* w_gate, const void* 
   const int E = (int)s.E, d = (int)s.d, f = (int)s.f;
   MOE_TRY(launch_weight_quant(w_gate, E, d, f, F(c.ag), F(c.sg), Q(c.qg), stream));
   MOE_TRY(launch_weight_quant(w_up, E, d, f, F(c.au), F(c.su), Q(c.qu), stream));
-  return launch_weight_quant(w_down, E, f, d, F(c.ad), F(c.sd), Q(c.qd), stream);
+  MOE_TRY(launch_weight_quant(w_down, E, f, d, F(c.ad), F(c.sd), Q(c.qd), stream));
+  if (s.fp8 != 2) return MOE_OK;
+  MOE_TRY(launch_quant_rows(w_gate, w_up, f, f, nullptr, E, (int64_t)E * d, Q(c.qgu_r), F(c.sgu_r), stream));
+  return launch_quant_rows(w_down, nullptr, d, 0, nullptr, E, (int64_t)E * f, Q(c.qd_r), F(c.sd_r), stream);
 }
 
 int moe_workspace_size(const moe_shape* shape, size_t* fwd_ws, size_t* saved_bytes, size_t* bwd_ws) {
@@ -942,6 +1007,8 @@ int moe_grouped_gemm_bwd(const moe_shape* shape, int32_t passes, const void* x_p
   if ((passes & MOE_ACCUMULATE) && !(passes & MOE_WGRAD))
     return moe_set_error(MOE_ERR_INVALID_ARG, "MOE_ACCUMULATE needs MOE_WGRAD");
   MOE_NEED(expert_offsets, "expert_offsets");
+  if ((passes & MOE_DGRAD) && s.fp8 == 2)
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "moe_grouped_gemm_bwd: FP8 data-gradient operands come from moe_layer_bwd");
   if (passes & MOE_DGRAD) {
     MOE_NEED(w_gate, "w_gate");
     MOE_NEED(w_up, "w_up");

@@ -94,7 +94,7 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(CombineBwdArgs a) {
   XT* d_o = reinterpret_cast<XT*>(a.d_o);
   const int64_t R = a.T * a.k;
   int64_t rows[KM];
-  float w[KM], om[KM];
+  float w[KM], om[KM], qi[KM];
   bool ok[KM];
 #pragma unroll
   for (int s = 0; s < KM; ++s) {
@@ -103,6 +103,27 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(CombineBwdArgs a) {
     om[s] = 0.f;
     ok[s] = s < k && (uint64_t)rows[s] < (uint64_t)R;
     if (!ok[s]) rows[s] = 0;
+  }
+  // FP8 data gradients: E4M3 rows of the stored d_o as well.  Row s is
+  // bf16(w_s dy_t); rounding is monotone and sign-symmetric, so its largest
+  // magnitude is bf16(|w_s| max|dy_t|), known before any value is written.
+  constexpr bool kQ = sizeof(XT) == 2;
+  const bool q8 = kQ && a.doq != nullptr;
+  if (q8) {
+    float m = 0.f;
+    for (int c = lane; c < nch; c += 64) {
+      float g[V];
+      Vec16<XT>::load(dy + t * a.d + (int64_t)c * V, g);
+#pragma unroll
+      for (int v = 0; v < V; ++v) m = fmaxf(m, fabsf(g[v]));
+    }
+    m = wave_max(m);
+#pragma unroll
+    for (int s = 0; s < KM; ++s) {
+      const float am = bf2f(f2bf(fabsf(w[s]) * m));
+      qi[s] = e4m3_inv(am);
+      if (lane == 0 && ok[s]) a.sdo[rows[s]] = e4m3_scale(am);
+    }
   }
   for (int c0 = 0; c0 < nch; c0 += 64 * CPL) {
 #pragma unroll
@@ -127,6 +148,15 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(CombineBwdArgs a) {
           out[v] = w[s] * g[v];
         }
         Vec16<XT>::store(d_o + rows[s] * a.d + (int64_t)c * V, out);
+        if constexpr (kQ) {
+          if (q8) {  // the codes of the stored (bf16) values
+            float b[8];
+#pragma unroll
+            for (int v = 0; v < 8; ++v) b[v] = bf2f(f2bf(out[v])) * qi[s];
+            *reinterpret_cast<uint2*>(a.doq + rows[s] * a.d + (int64_t)c * 8) =
+                make_uint2(e4m3x4(b[0], b[1], b[2], b[3]), e4m3x4(b[4], b[5], b[6], b[7]));
+          }
+        }
       }
     }
   }
@@ -680,6 +710,8 @@ int launch_combine_fwd(const CombineFwdArgs& a, hipStream_t s) {
 }
 
 int launch_combine_bwd(const CombineBwdArgs& a, hipStream_t s) {
+  if (a.doq && (a.zc.on || !a.bf16 || !a.sdo))
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "combine_bwd: E4M3 d_o rows need bf16 without zero-computation experts");
   if (a.T == 0) return MOE_OK;
   const int nb = (int)((a.T + 3) / 4);
   if (a.zc.on) {

@@ -1,14 +1,18 @@
-// FP8 (OCP E4M3) operands of the forward expert GEMMs.
+// FP8 (OCP E4M3) operands of the expert GEMMs.
 //
-//   quant_rows     E4M3 rows of h [R][f] with one scale per row (the row's
-//                  largest magnitude / 448), one wavefront per row, the rows
-//                  of the FFN experts only (below offsets[E]);
-//   weight quant   the weight cache: per expert, the largest magnitude of
-//                  every output column of W [K][N] (one thread per column,
-//                  rows read in order), then the codes of W^T [N][K] (64 x 64
-//                  tiles through LDS, so that both the bf16 reads and the code
-//                  writes are contiguous).  The GEMMs read both operands
-//                  K-contiguous.
+//   quant_rows     E4M3 rows with one scale per row (the row's largest
+//                  magnitude / 448), one wavefront per row.  A row is the
+//                  concatenation of a row of s0 (w0 values) and a row of s1
+//                  (w1 values, possibly none): activation rows of h, d_o or
+//                  [dg | du] (only the rows of the FFN experts, below
+//                  offsets[E]) and, for the data-gradient GEMMs, the weight
+//                  rows of W_down and of [W_gate | W_up] (one scale over both);
+//   weight quant   the forward's weight cache: per expert, the largest
+//                  magnitude of every output column of W [K][N] (one thread per
+//                  column, rows read in order), then the codes of W^T [N][K]
+//                  (64 x 64 tiles through LDS, so that both the bf16 reads and
+//                  the code writes are contiguous).  The GEMMs read both
+//                  operands K-contiguous.
 // A value v of a row (column) with largest magnitude amax is stored as the
 // E4M3 code nearest to clamp(v * (448 / amax)), the product in float32.
 #include "common.h"
@@ -18,30 +22,64 @@ namespace moe {
 
 namespace {
 
-__global__ __launch_bounds__(256) void quant_rows_kernel(const bf16_t* __restrict__ h, const int32_t* offsets, int E,
-                                                         int f, uint8_t* __restrict__ hq, float* __restrict__ sh) {
+struct QuantRowsArgs {
+  const bf16_t* s0;
+  const bf16_t* s1;
+  int w0, w1;
+  const int32_t* offsets;  // non-null: rows at or past offsets[E] are skipped
+  int E;
+  int64_t rows;
+  uint8_t* q;  // [rows][w0 + w1]
+  float* scale;  // [rows]
+};
+
+__global__ __launch_bounds__(256) void quant_rows_kernel(QuantRowsArgs a) {
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)__builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
-  if (r >= offsets[E]) return;
-  const bf16_t* row = h + r * f;
-  const int nch = f / 8;
-  float m = 0.f;
-  for (int c = lane; c < nch; c += 64) {
-    float v[8];
-    Vec16<bf16_t>::load(row + (int64_t)c * 8, v);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) m = fmaxf(m, fabsf(v[q]));
-  }
-  m = wave_max(m);
-  const float inv = e4m3_inv(m);
-  for (int c = lane; c < nch; c += 64) {
-    float v[8];
-    Vec16<bf16_t>::load(row + (int64_t)c * 8, v);
-    *reinterpret_cast<uint2*>(hq + r * f + (int64_t)c * 8) =
+  const int64_t r = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  if (r >= a.rows || (a.offsets && r >= a.offsets[a.E])) return;
+  const int n0 = a.w0 / 8, nch = (a.w0 + a.w1) / 8;
+  auto src = [&](int c) {
+    return c < n0 ? a.s0 + r * a.w0 + (int64_t)c * 8 : a.s1 + r * a.w1 + (int64_t)(c - n0) * 8;
+  };
+  auto put = [&](int c, const float* v, float inv) {
+    *reinterpret_cast<uint2*>(a.q + r * (a.w0 + a.w1) + (int64_t)c * 8) =
         make_uint2(e4m3x4(v[0] * inv, v[1] * inv, v[2] * inv, v[3] * inv),
                    e4m3x4(v[4] * inv, v[5] * inv, v[6] * inv, v[7] * inv));
+  };
+  float m = 0.f;
+  constexpr int HOLD = 4;  // rows of up to 64 * HOLD chunks stay in registers between the passes
+  if (nch <= 64 * HOLD) {
+    float v[HOLD][8];
+#pragma unroll
+    for (int j = 0; j < HOLD; ++j) {
+      const int c = lane + 64 * j;
+      if (c < nch) {
+        Vec16<bf16_t>::load(src(c), v[j]);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) m = fmaxf(m, fabsf(v[j][q]));
+      }
+    }
+    m = wave_max(m);
+    const float inv = e4m3_inv(m);
+#pragma unroll
+    for (int j = 0; j < HOLD; ++j)
+      if (lane + 64 * j < nch) put(lane + 64 * j, v[j], inv);
+  } else {
+    for (int c = lane; c < nch; c += 64) {
+      float v[8];
+      Vec16<bf16_t>::load(src(c), v);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) m = fmaxf(m, fabsf(v[q]));
+    }
+    m = wave_max(m);
+    const float inv = e4m3_inv(m);
+    for (int c = lane; c < nch; c += 64) {
+      float v[8];
+      Vec16<bf16_t>::load(src(c), v);
+      put(c, v, inv);
+    }
   }
-  if (lane == 0) sh[r] = e4m3_scale(m);
+  if (lane == 0) a.scale[r] = e4m3_scale(m);
 }
 
 // grid (ceil(N / 256), E): column maxima over the K rows of W[e]
@@ -80,13 +118,13 @@ __global__ __launch_bounds__(256) void quant_transpose_kernel(const bf16_t* __re
 
 }  // namespace
 
-int launch_quant_rows(const void* h, const int32_t* offsets, int E, int64_t R, int f, uint8_t* hq, float* sh,
-                      hipStream_t s) {
-  if (R == 0) return MOE_OK;
-  const int nb = (int)((R + 3) / 4);
-  return launch(K_QUANT_ROWS, s, "quant_rows", [&] {
-    quant_rows_kernel<<<nb, 256, 0, s>>>(reinterpret_cast<const bf16_t*>(h), offsets, E, f, hq, sh);
-  });
+int launch_quant_rows(const void* s0, const void* s1, int w0, int w1, const int32_t* offsets, int E, int64_t rows,
+                      uint8_t* q, float* scale, hipStream_t s) {
+  if (rows <= 0) return MOE_OK;
+  QuantRowsArgs a{reinterpret_cast<const bf16_t*>(s0), reinterpret_cast<const bf16_t*>(s1), w0, w1, offsets, E,
+                  rows, q, scale};
+  const int64_t nb = (rows + 3) / 4;
+  return launch(K_QUANT_ROWS, s, "quant_rows", [&] { quant_rows_kernel<<<(unsigned)nb, 256, 0, s>>>(a); });
 }
 
 int launch_weight_quant(const void* w, int E, int K, int N, float* amax, float* scale, uint8_t* q, hipStream_t s) {

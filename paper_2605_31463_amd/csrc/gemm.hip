@@ -966,7 +966,7 @@ __device__ __forceinline__ void tile_dims(const GemmArgs& a, const Tile& tl, int
 // column's quantisation scales.
 template <int MODE, class C, bool CL = false, bool FP8 = false>
 __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persistent(GemmArgs a) {
-  static_assert(!FP8 || MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN, "FP8 forward passes only");
+  static_assert(!FP8 || !is_wgrad<MODE>(), "FP8: the forward and data-gradient passes only");
   constexpr bool wgrad = is_wgrad<MODE>();
   constexpr bool a_mn = wgrad;
   constexpr bool b_mn = !FP8 && (MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN || wgrad);
@@ -1050,6 +1050,16 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
       kb.rsrc = make_rsrc(reinterpret_cast<const uint8_t*>(a.w0) + (int64_t)g * d * f, (int64_t)d * f);
       kb.init(wave, lane, tl.n0, f / 2);
       b_kstride = 2;
+    } else if (FP8 && MODE == G_DGRAD_DOWN) {
+      // cache rows: [E][f][d] row codes of the down weights
+      kb.rsrc = make_rsrc(reinterpret_cast<const uint8_t*>(a.w0) + (int64_t)g * f * d, (int64_t)f * d);
+      kb.init(wave, lane, tl.n0, d / 2);
+      b_kstride = 2;
+    } else if (FP8 && MODE == G_DGRAD_GATEUP) {
+      // cache rows: [E][d][2f] row codes of [W_gate | W_up]
+      kb.rsrc = make_rsrc(reinterpret_cast<const uint8_t*>(a.w0) + (int64_t)g * d * 2 * f, (int64_t)d * 2 * f);
+      kb.init(wave, lane, tl.n0, f);
+      b_kstride = 2;
     } else if (MODE == G_FWD_GATEUP) {
       const int32x4_t rg = make_rsrc(W0 + (int64_t)g * d * f, (int64_t)d * f * 2);
       const int32x4_t ru = make_rsrc(W1 + (int64_t)g * d * f, (int64_t)d * f * 2);
@@ -1122,11 +1132,11 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
     else ma.issue(As, wave, (uint32_t)(k0 * a_kstride));
     if (FP8 && MODE == G_FWD_GATEUP) {
       kgu.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
-    } else if (MODE == G_DGRAD_GATEUP) {
+    } else if (MODE == G_DGRAD_GATEUP && !FP8) {
       KOperand<BN, NW, BK> kk = kb;
       if (k0 >= f) kk.rsrc = b_up;
       kk.issue(Bs, wave, (uint32_t)((k0 >= f ? k0 - f : k0) * b_kstride));
-    } else if (MODE == G_DGRAD_DOWN || (FP8 && MODE == G_FWD_DOWN)) {
+    } else if (MODE == G_DGRAD_DOWN || MODE == G_DGRAD_GATEUP || (FP8 && MODE == G_FWD_DOWN)) {
       kb.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
     } else {
       mb.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
@@ -1353,6 +1363,8 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
           if (m0 >= M) continue;
           const int m = m0 + r32;
           const int64_t row = tl.row_base + (m < M ? m : M - 1);
+          // FP8: the d_o row's quantisation scale
+          const float sr = FP8 ? (m < M ? a.a_scale[row] : 0.f) : 1.f;
   #pragma unroll
           for (int jb = 0; jb < NI; jb += JB) {
             uint2 gr[JB][4], ur[JB][4];
@@ -1381,8 +1393,20 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
                                      __uint_as_float(gr[jj][q].y << 16), __uint_as_float(gr[jj][q].y & 0xffff0000u)};
                 const float uv[4] = {__uint_as_float(ur[jj][q].x << 16), __uint_as_float(ur[jj][q].x & 0xffff0000u),
                                      __uint_as_float(ur[jj][q].y << 16), __uint_as_float(ur[jj][q].y & 0xffff0000u)};
+                float sc[4] = {1.f, 1.f, 1.f, 1.f};
+                if constexpr (FP8) {  // the W_down rows' scales (dh columns c .. c + 3)
+                  const int c = n0 + 8 * q + 4 * hh;
+                  const float4 s4 = c < N ? *reinterpret_cast<const float4*>(a.b_scale0 + (int64_t)g * f + c)
+                                          : make_float4(0.f, 0.f, 0.f, 0.f);
+                  sc[0] = sr * s4.x;
+                  sc[1] = sr * s4.y;
+                  sc[2] = sr * s4.z;
+                  sc[3] = sr * s4.w;
+                }
   #pragma unroll
-                for (int t = 0; t < 4; ++t) act_grad_t<CL>(a, gv[t], uv[t], acc[i][j][4 * q + t], dg[4 * q + t], du[4 * q + t]);
+                for (int t = 0; t < 4; ++t)
+                  act_grad_t<CL>(a, gv[t], uv[t], FP8 ? acc[i][j][4 * q + t] * sc[t] : acc[i][j][4 * q + t],
+                                 dg[4 * q + t], du[4 * q + t]);
               }
               put_block(dg, [&](int r) -> bf16_t* {
                 return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + n0 : nullptr;
@@ -1398,7 +1422,6 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
     } else if (MODE == G_FWD_DOWN || MODE == G_DGRAD_GATEUP) {
       const int nbase = tl.n0 + wn * C::TN;
       const bf16_t* bdp = MODE == G_FWD_DOWN ? reinterpret_cast<const bf16_t*>(a.bias0) : nullptr;
-      const bf16_t* gup = reinterpret_cast<const bf16_t*>(a.aux);
       bf16_t* out = reinterpret_cast<bf16_t*>(a.c0);
 #pragma unroll
       for (int j = 0; j < NI; ++j) {
@@ -1420,37 +1443,9 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
           float o[16];
 #pragma unroll
           for (int v = 0; v < 16; ++v) o[v] = FP8 ? __builtin_fmaf(acc[i][j][v], sr * sc[v], bd[v]) : acc[i][j][v] + bd[v];
-          if (MODE == G_DGRAD_DOWN) {
-            // dSwiGLU with the saved gate/up values of this lane's row
-            const int m = m0 + r32;
-            float dg[16], du[16];
-            const int64_t row = tl.row_base + (m < M ? m : M - 1);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int c = n0 + 8 * q + 4 * hh;
-              uint2 gr = make_uint2(0, 0), ur = make_uint2(0, 0);
-              if (m < M && c < N) {
-                gr = *reinterpret_cast<const uint2*>(gup + row * 2 * f + c);
-                ur = *reinterpret_cast<const uint2*>(gup + row * 2 * f + f + c);
-              }
-              const float gv[4] = {__uint_as_float(gr.x << 16), __uint_as_float(gr.x & 0xffff0000u),
-                                   __uint_as_float(gr.y << 16), __uint_as_float(gr.y & 0xffff0000u)};
-              const float uv[4] = {__uint_as_float(ur.x << 16), __uint_as_float(ur.x & 0xffff0000u),
-                                   __uint_as_float(ur.y << 16), __uint_as_float(ur.y & 0xffff0000u)};
-#pragma unroll
-              for (int t = 0; t < 4; ++t) act_grad(a, gv[t], uv[t], o[4 * q + t], dg[4 * q + t], du[4 * q + t]);
-            }
-            put_block(dg, [&](int r) -> bf16_t* {
-              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + n0 : nullptr;
-            }, ncols);
-            put_block(du, [&](int r) -> bf16_t* {
-              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * 2 * f + f + n0 : nullptr;
-            }, ncols);
-          } else {
-            put_block(o, [&](int r) -> bf16_t* {
-              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * N + n0 : nullptr;
-            }, ncols);
-          }
+          put_block(o, [&](int r) -> bf16_t* {
+            return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * N + n0 : nullptr;
+          }, ncols);
         }
       }
     } else {
@@ -1695,8 +1690,8 @@ int launch_bf16_persistent(const GemmArgs& a, hipStream_t s) {
 
 template <int MODE>
 int launch_mode(const GemmArgs& a, hipStream_t s) {
-  if (a.fp8 && !(a.bf16 && MOE_GEMM_PERSISTENT && (MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN)))
-    return moe_set_error(MOE_ERR_UNSUPPORTED, "gemm: FP8 runs the bf16 forward passes only");
+  if (a.fp8 && !(a.bf16 && MOE_GEMM_PERSISTENT && !is_wgrad<MODE>()))
+    return moe_set_error(MOE_ERR_UNSUPPORTED, "gemm: FP8 runs the bf16 forward and data-gradient passes only");
   if (a.accumulate && !is_wgrad<MODE>())
     return moe_set_error(MOE_ERR_INVALID_ARG, "gemm: accumulate applies to the weight-gradient passes only");
   if (a.bf16 && a.accumulate && !MOE_GEMM_PERSISTENT)
@@ -1705,9 +1700,9 @@ int launch_mode(const GemmArgs& a, hipStream_t s) {
     const int G = a.offsets ? a.ngroups : 1;
     const int64_t rows_per_group = a.offsets ? a.max_rows / G : a.dense_rows;
     if constexpr (MOE_GEMM_PERSISTENT != 0) {
-      if constexpr (MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN) {
+      if constexpr (!is_wgrad<MODE>()) {
         if (a.fp8) {
-          if constexpr (MODE == G_FWD_GATEUP) {
+          if constexpr (MODE == G_FWD_GATEUP || MODE == G_DGRAD_DOWN) {
             if (a.act == MOE_ACT_CLAMPED_GLU) {
               if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, true, true>(a, s);
               return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big, true, true>(a, s);

@@ -49,9 +49,10 @@ struct PermArgs {
 };
 int launch_permute(const PermArgs& a, hipStream_t s);
 
-// FP8 forward: E4M3 rows of h [R][f] (rows below offsets[E]) and their scales.
-int launch_quant_rows(const void* h, const int32_t* offsets, int E, int64_t R, int f, uint8_t* hq, float* sh,
-                      hipStream_t s);
+// FP8: E4M3 rows of [s0 | s1] (bf16 [rows][w0] and [rows][w1], w1 may be 0;
+// with offsets, only the rows below offsets[E]) and their scales.
+int launch_quant_rows(const void* s0, const void* s1, int w0, int w1, const int32_t* offsets, int E, int64_t rows,
+                      uint8_t* q, float* scale, hipStream_t s);
 // FP8 weight cache of one expert weight W [E][K][N] (bf16): column maxima
 // amax [E][N], scales [E][N] = amax / 448, codes Q [E][N][K] (transposed).
 int launch_weight_quant(const void* w, int E, int K, int N, float* amax, float* scale, uint8_t* q, hipStream_t s);
@@ -104,6 +105,10 @@ struct CombineBwdArgs {
   const int32_t* topk_idx;  // read with zero-computation experts
   ZcArgs zc;
   float* dth;        // threshold router: per slot -s (c omega - sum w omega) / sum s, or null
+  // FP8 data gradients (bf16, without zero-computation experts): E4M3 rows of
+  // d_o [R][d] and their scales [R], or null
+  uint8_t* doq;
+  float* sdo;
 };
 int launch_combine_bwd(const CombineBwdArgs& a, hipStream_t s);
 

@@ -70,6 +70,8 @@ def test_workspace_sizes_scale_with_shape():
     (dict(router="sigmoid_threshold", E=16, n_groups=4, topk_groups=2), L.MOE_ERR_INVALID_ARG),
     (dict(fp8=True, dtype="f32"), L.MOE_ERR_UNSUPPORTED),
     (dict(fp8=True, dtype="bf16", d=192), L.MOE_ERR_UNSUPPORTED),
+    (dict(fp8=2, dtype="bf16", f=192), L.MOE_ERR_UNSUPPORTED),
+    (dict(fp8=3, dtype="bf16"), L.MOE_ERR_INVALID_ARG),
     (dict(act="clamped_glu", act_alpha=0.0), L.MOE_ERR_INVALID_ARG),
     (dict(act="clamped_glu", act_limit=float("inf")), L.MOE_ERR_INVALID_ARG),
 ])
@@ -231,3 +233,27 @@ def test_fp8_cache_on_the_host():
     sv = L.moe_saved(**{nm: fake for nm, _ in L.moe_saved._fields_})
     st = L.LIB.moe_layer_fwd(ctypes.byref(s), ctypes.byref(pr), fake, ctypes.byref(sv), fake, fake, 1 << 40, None)
     assert st == L.MOE_ERR_INVALID_ARG and "fp8_cache" in L.last_error()
+
+
+def test_fp8_dgrad_on_the_host():
+    """fp8 = 2 (data-gradient GEMMs too): the cache holds the row-quantised
+    weights as well (twice the codes), the layer backward asks for the cache,
+    and the standalone grouped backward refuses the FP8 data-gradient passes
+    (their operands are the layer's)."""
+    s1 = L.make_shape(T=64, d=256, E=4, k=2, f=128, dtype="bf16", fp8=1)
+    s2 = L.make_shape(T=64, d=256, E=4, k=2, f=128, dtype="bf16", fp8=2)
+    n1, n2 = L.moe_fp8_cache_size(s1), L.moe_fp8_cache_size(s2)
+    assert n2 >= n1 + 3 * 4 * 256 * 128 + 4 * (4 * 256 + 4 * 128)
+    fwd1, _, bwd1 = L.moe_workspace_size(s1)
+    fwd2, _, bwd2 = L.moe_workspace_size(s2)
+    R = 64 * 2
+    assert fwd2 == fwd1 and bwd2 >= bwd1 + R * (256 + 2 * 128) + 2 * R * 4
+    fake = ctypes.c_void_p(16)   # never dereferenced: validation fails first
+    pr = L.moe_params(w_r=fake, w_gate=fake, w_up=fake, w_down=fake)
+    sv = L.moe_saved(**{nm: fake for nm, _ in L.moe_saved._fields_})
+    st = L.LIB.moe_layer_bwd_dgrad(ctypes.byref(s2), ctypes.byref(pr), fake, ctypes.byref(sv), fake, fake,
+                                   fake, 1 << 40, None)
+    assert st == L.MOE_ERR_INVALID_ARG and "fp8_cache" in L.last_error()
+    st = L.LIB.moe_grouped_gemm_bwd(ctypes.byref(s2), L.MOE_DGRAD, fake, fake, fake, fake, fake, fake, fake, fake,
+                                    fake, fake, None, None, None, None, None, None, None)
+    assert st == L.MOE_ERR_UNSUPPORTED and "FP8" in L.last_error()

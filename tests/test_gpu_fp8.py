@@ -11,12 +11,18 @@ oracle's FP8 layer.
     with 32 experts: 32 rows per expert, 128-row tiles; with 16 experts: 512
     rows, 256-row tiles), with expert biases, with the clamped GLU, and
     DeepSeek-V3 widths with the (bf16) shared expert;
-  * the cache is reused across calls (two forwards, one build)."""
+  * the cache is reused across calls (two forwards, one build);
+  * MoE++ (zero-computation experts in the pool) at both levels;
+  * with shape.fp8 = 2 the data-gradient GEMMs also run on E4M3 operands: the
+    cache's row codes of W_down and [W_gate | W_up] bit-exact against the
+    oracle's row quantisation, and the same layer cases against the oracle's
+    FP8 backward, with dx farther than the bar from the backward of FP8
+    forward GEMMs only."""
 import numpy as np
 import pytest
 
 from moe_inputs import layer_inputs, to_f64, variant
-from oracle import quantize_cols
+from oracle import quantize_cols, quantize_rows
 from tests.helpers import TOL, check_routing, dev, device_params, host, oracle_run, rel
 
 pytestmark = pytest.mark.gpu
@@ -27,7 +33,12 @@ CASES = {
     "qwen3_e16_bias": variant("qwen3", T=1024, E=16, expert_bias=True, fp8=True),
     "qwen3_e16_clamped": variant("qwen3", T=1024, E=16, act="clamped_glu", w_std=0.27, fp8=True),
     "dsv3": variant("dsv3", T=384, d=512, f=256, f_shared=256, fp8=True),
+    # zero-computation experts in the pool: d_o rows quantised by their own pass
+    "moepp": variant("moepp", T=256, fp8=True),
 }
+
+
+LEVELS = [(n, 1) for n in CASES] + [(n, 2) for n in CASES]
 
 
 def setup(cfg, inp):
@@ -44,7 +55,7 @@ def setup(cfg, inp):
 def test_weight_cache_codes_bit_exact():
     import torch
     from paper_2605_31463_amd import _lib as L
-    cfg = variant("qwen3", T=64, E=3, k=2, d=256, f=128, fp8=True)
+    cfg = variant("qwen3", T=64, E=3, k=2, d=256, f=128, fp8=2)
     inp = layer_inputs(cfg, seed=2)
     # add exact zeros, a zero column and wide magnitudes to the weights
     for n in ("w_gate", "w_up", "w_down"):
@@ -74,16 +85,28 @@ def test_weight_cache_codes_bit_exact():
             got = q[e * N * K:(e + 1) * N * K].reshape(N, K)  # transposed
             assert np.array_equal(got, codes.T), (name, e, int((got != codes.T).sum()))
             assert np.array_equal(s[e * N:(e + 1) * N].astype(np.float64), scale), (name, e)
+    # the data-gradient GEMMs' row codes: [W_gate | W_up] [E][d][2f], W_down [E][f][d]
+    qgu, qd_r = region(E * d * 2 * f), region(E * f * d)
+    sgu, sd_r = region(E * d * 4).view(np.float32), region(E * f * 4).view(np.float32)
+    for e in range(E):
+        wgu = np.concatenate([to_f64(inp["w_gate"][e], "bf16"), to_f64(inp["w_up"][e], "bf16")], axis=1)
+        codes, scale, _ = quantize_rows(wgu)
+        assert np.array_equal(qgu[e * d * 2 * f:(e + 1) * d * 2 * f].reshape(d, 2 * f), codes), ("w_gu rows", e)
+        assert np.array_equal(sgu[e * d:(e + 1) * d].astype(np.float64), scale), ("w_gu scales", e)
+        codes, scale, _ = quantize_rows(to_f64(inp["w_down"][e], "bf16"))
+        assert np.array_equal(qd_r[e * f * d:(e + 1) * f * d].reshape(f, d), codes), ("w_down rows", e)
+        assert np.array_equal(sd_r[e * f:(e + 1) * f].astype(np.float64), scale), ("w_down scales", e)
+    assert off == len(raw)                            # every region of the cache checked
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("name", list(CASES))
-def test_fp8_layer_parity(name):
+@pytest.mark.parametrize("name,level", LEVELS)
+def test_fp8_layer_parity(name, level):
     import torch
-    cfg = CASES[name]
+    cfg = dict(CASES[name], fp8=level)
     tol = TOL[cfg["dtype"]]
     inp = layer_inputs(cfg, seed=0)
-    print("fp8 layer", name, flush=True)
+    print("fp8 layer", name, "level", level, flush=True)
     layer, p = setup(cfg, inp)
     x = dev(inp["x"], cfg["dtype"])
     dy = dev(inp["dy"], cfg["dtype"])
@@ -115,5 +138,10 @@ def test_fp8_layer_parity(name):
     print(name, "fp8 vs bf16 forward (oracle): g %.2e, y %.2e;" % (dist_bf16, rel(fwd0["y"], fwd["y"])),
           {k: "%.2e" % v for k, v in errs.items()}, flush=True)
     assert dist_bf16 > 2 * errs["g"]          # the comparison resolves the quantisation
+    if level == 2:
+        _, bwd1 = oracle_run(dict(cfg, fp8=1), inp)
+        dist_fwd_only = rel(bwd1["dx"], bwd["dx"])
+        print(name, "fp8 dgrad vs forward-only FP8 (oracle): dx %.2e" % dist_fwd_only, flush=True)
+        assert dist_fwd_only > 2 * errs["dx"]
     bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, bad
