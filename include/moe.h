@@ -165,8 +165,10 @@ typedef struct moe_shape {
   int32_t act;                 /* MOE_ACT_* of the routed experts */
   float act_alpha;             /* CLAMPED_GLU: slope inside the sigmoid (> 0) */
   float act_limit;             /* CLAMPED_GLU: clamp bound (> 0) */
-  int32_t fp8;                 /* 1: the routed experts' forward GEMMs take FP8
-                                  operands (see the FP8 section below); 0: bf16 */
+  int32_t fp8;                 /* routed experts' GEMMs on FP8 operands (see the
+                                  FP8 section below): 0 none (bf16), 1 the
+                                  forward ones, 2 the forward and the
+                                  data-gradient ones */
 } moe_shape;
 
 /* Parameters of the layer (device pointers; unused ones may be NULL). */
@@ -188,7 +190,7 @@ typedef struct moe_params {
   const float* zc_v;           /* [n_const][d] constant experts' vectors */
   const float* zc_wc;          /* [n_const][2][d] constant experts' mixing weights */
   const float* gate_threshold; /* [E] thresholds of MOE_ROUTER_SIGMOID_THRESHOLD */
-  const void* fp8_cache;       /* shape->fp8: the weight cache moe_fp8_cache_build wrote */
+  const void* fp8_cache;       /* shape->fp8 != 0: the weight cache moe_fp8_cache_build wrote */
 } moe_params;
 
 /* Tensors the forward writes and the backward reads (caller-allocated). */
@@ -262,7 +264,7 @@ int moe_permute(const moe_shape* shape, const void* x, const int32_t* topk_idx,
  * for every expert e over its rows expert_offsets[e] .. expert_offsets[e+1]-1,
  * scheduled on the device from expert_offsets (no host synchronisation).
  * b_* may be NULL when shape->expert_bias is 0.  out: gu, h, o.
- * (bf16 operands: a shape with fp8 = 1 is refused; moe_layer_fwd runs it.) */
+ * (bf16 operands: a shape with fp8 != 0 is refused; moe_layer_fwd runs it.) */
 int moe_grouped_gemm_fwd(const moe_shape* shape, const void* x_perm, const int32_t* expert_offsets,
                          const void* w_gate, const void* w_up, const void* w_down,
                          const void* b_gate, const void* b_up, const void* b_down,
@@ -279,7 +281,9 @@ int moe_grouped_gemm_fwd(const moe_shape* shape, const void* x_perm, const int32
  *             MOE_ACCUMULATE the gradients are added to dw_* / db_*.
  * Pointers of a pass that is not requested may be NULL.  Errors:
  * MOE_ERR_INVALID_ARG for a passes value outside these bits or
- * MOE_ACCUMULATE without MOE_WGRAD. */
+ * MOE_ACCUMULATE without MOE_WGRAD; MOE_ERR_UNSUPPORTED for MOE_DGRAD with
+ * shape->fp8 = 2 (moe_layer_bwd runs those passes).  With fp8 = 1 these are
+ * the bf16 passes. */
 int moe_grouped_gemm_bwd(const moe_shape* shape, int32_t passes,
                          const void* x_perm, const int32_t* expert_offsets,
                          const void* gu, const void* h, const void* d_o,
@@ -381,27 +385,39 @@ int moe_layer_bwd_wgrad(const moe_shape* shape, const moe_params* params, const 
                         const moe_saved* saved, const void* dy, const moe_grads* grads,
                         int32_t accumulate, void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* FP8 forward of the routed experts (the paper's FP8 training: fused
+/* FP8 GEMMs of the routed experts (the paper's FP8 training: fused
  * quantisation, quantised weights cached across micro-batches; it states no
- * scaling recipe, so this one is the library's).  With shape->fp8 = 1 (bf16
- * layers, d and f multiples of 128) moe_layer_fwd runs both expert GEMMs on
- * OCP FP8 E4M3 operands: the permutation also writes every routed row of x in
- * E4M3 with one scale per token, h is quantised per row after the gate/up
- * GEMM, and the weights come from the cache.  A value v of a row (column)
- * whose largest magnitude is amax is stored as the E4M3 value nearest to
- * clamp(v * (448 / amax), -448, 448) (float32 product, ties to even) with
- * scale amax / 448 (1 for an all-zero row); the GEMMs accumulate the code
- * products in float32 and multiply by the row and column scales.  gu, h and o
- * stay bf16; the backward is the bf16 backward of those activations and of the
- * bf16 weights (quantisation taken as the identity).  The shared expert stays
- * bf16.
+ * scaling recipe, so this one is the library's).  bf16 layers with d and f
+ * multiples of 128.  A value v of a row (column) whose largest magnitude is
+ * amax is stored as the OCP E4M3 value nearest to clamp(v * (448 / amax),
+ * -448, 448) (float32 product, ties to even) with scale amax / 448 (1 for an
+ * all-zero row); the GEMMs accumulate the code products in float32 and
+ * multiply by the row and column scales.  gu, h, o, d_o and dgu stay bf16; the
+ * shared expert and the weight-gradient GEMMs stay bf16.
  *
- * moe_fp8_cache_size: bytes of the cache for the shape.  moe_fp8_cache_build:
- * quantises w_gate, w_up [E][d][f] and w_down [E][f][d] (bf16) per output
- * column into the caller's cache (codes stored transposed, K-contiguous, with
- * the scales); call it again whenever the weights change, and reuse it for
- * every micro-batch in between.  Errors: MOE_ERR_UNSUPPORTED without
- * shape->fp8, MOE_ERR_WORKSPACE for a cache below the size. */
+ * shape->fp8 = 1: moe_layer_fwd runs both forward expert GEMMs on E4M3
+ * operands: the permutation also writes every routed row of x in E4M3 with
+ * one scale per token, h is quantised per row after the gate/up GEMM, and the
+ * weights (one scale per output column) come from the cache.  The backward is
+ * the bf16 backward of those activations and of the bf16 weights
+ * (quantisation taken as the identity).
+ * shape->fp8 = 2: in addition, the backward's two data-gradient GEMMs
+ * (dh = d_o W_down^T, dx_perm = [dg | du] [W_gate | W_up]^T) run on E4M3
+ * operands: the stored d_o rows (quantised by the combine backward, or by a
+ * pass of their own with zero-computation experts) and dgu rows (one scale
+ * over a row's gate and up halves), and the weights quantised per row (an
+ * output column of these products; one scale over a row of W_gate and W_up
+ * together) from the cache.
+ *
+ * moe_fp8_cache_size: bytes of the cache for the shape (fp8 = 2 about twice
+ * fp8 = 1).  moe_fp8_cache_build: quantises w_gate, w_up [E][d][f] and
+ * w_down [E][f][d] (bf16) per output column into the caller's cache (codes
+ * stored transposed, K-contiguous, with the scales) and, for fp8 = 2, per row
+ * as well; call it again whenever the weights change, and reuse it for every
+ * micro-batch in between.  The standalone moe_grouped_gemm_fwd / _bwd refuse
+ * FP8 passes (MOE_ERR_UNSUPPORTED): their operands are the layer's.  Errors:
+ * MOE_ERR_UNSUPPORTED without shape->fp8, MOE_ERR_WORKSPACE for a cache below
+ * the size. */
 int moe_fp8_cache_size(const moe_shape* shape, size_t* bytes);
 int moe_fp8_cache_build(const moe_shape* shape, const void* w_gate, const void* w_up, const void* w_down,
                         void* cache, size_t cache_bytes, hipStream_t stream);
