@@ -8,8 +8,8 @@
 //                  offsets[E]) and, for the data-gradient GEMMs, the weight
 //                  rows of W_down and of [W_gate | W_up] (one scale over both);
 //   weight quant   the forward's weight cache: per expert, the largest
-//                  magnitude of every output column of W [K][N] (one thread per
-//                  column, rows read in order), then the codes of W^T [N][K]
+//                  magnitude of every output column of W [K][N] (blocks of 256
+//                  rows, combined by an atomic max), then the codes of W^T [N][K]
 //                  (64 x 64 tiles through LDS, so that both the bf16 reads and
 //                  the code writes are contiguous).  The GEMMs read both
 //                  operands K-contiguous.
@@ -82,23 +82,58 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(QuantRowsArgs a) {
   if (lane == 0) a.scale[r] = e4m3_scale(m);
 }
 
-// grid (ceil(N / 256), E): column maxima over the K rows of W[e]
+// Column maxima of W[e] [K][N] (N a multiple of 4): grid (ceil(N / 256),
+// ceil(K / 256), E), each lane 4 adjacent columns over 64 rows, the block's
+// four wavefronts combined in LDS, the blocks of a column by an integer
+// atomic max on the float bits (the values are non-negative), into amax
+// cleared by amax_clear_kernel.
+__global__ __launch_bounds__(256) void amax_clear_kernel(float* amax, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) amax[i] = 0.f;
+}
+
 __global__ __launch_bounds__(256) void col_amax_kernel(const bf16_t* __restrict__ w, int K, int N,
-                                                       float* __restrict__ amax, float* __restrict__ scale) {
-  const int n = blockIdx.x * 256 + threadIdx.x;
-  const int e = blockIdx.y;
-  if (n >= N) return;
-  const bf16_t* p = w + (int64_t)e * K * N + n;
-  float m = 0.f;
-  for (int k = 0; k < K; ++k) m = fmaxf(m, fabsf(bf2f(p[(int64_t)k * N])));
-  amax[(int64_t)e * N + n] = m;
-  scale[(int64_t)e * N + n] = e4m3_scale(m);
+                                                       float* __restrict__ amax) {
+  __shared__ float4 part[4][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int n = blockIdx.x * 256 + lane * 4;
+  const int e = blockIdx.z;
+  const int k0 = blockIdx.y * 256 + wv * 64;
+  float4 m = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (n < N) {
+    const bf16_t* p = w + (int64_t)e * K * N + n;
+    const int k1 = min(K, k0 + 64);
+    for (int k = k0; k < k1; ++k) {
+      const uint2 u = *reinterpret_cast<const uint2*>(p + (int64_t)k * N);
+      m.x = fmaxf(m.x, fabsf(__uint_as_float(u.x << 16)));
+      m.y = fmaxf(m.y, fabsf(__uint_as_float(u.x & 0xffff0000u)));
+      m.z = fmaxf(m.z, fabsf(__uint_as_float(u.y << 16)));
+      m.w = fmaxf(m.w, fabsf(__uint_as_float(u.y & 0xffff0000u)));
+    }
+  }
+  part[wv][lane] = m;
+  __syncthreads();
+  if (wv == 0 && n < N) {
+#pragma unroll
+    for (int j = 1; j < 4; ++j) {
+      const float4 o = part[j][lane];
+      m.x = fmaxf(m.x, o.x);
+      m.y = fmaxf(m.y, o.y);
+      m.z = fmaxf(m.z, o.z);
+      m.w = fmaxf(m.w, o.w);
+    }
+    unsigned int* a = reinterpret_cast<unsigned int*>(amax + (int64_t)e * N + n);
+    atomicMax(a + 0, __float_as_uint(m.x));
+    atomicMax(a + 1, __float_as_uint(m.y));
+    atomicMax(a + 2, __float_as_uint(m.z));
+    atomicMax(a + 3, __float_as_uint(m.w));
+  }
 }
 
 // grid (K / 64, N / 64, E): Q[e][n][k] = code(W[e][k][n] * 448 / amax[e][n])
 __global__ __launch_bounds__(256) void quant_transpose_kernel(const bf16_t* __restrict__ w, int K, int N,
                                                               const float* __restrict__ amax,
-                                                              uint8_t* __restrict__ q) {
+                                                              uint8_t* __restrict__ q, float* __restrict__ scale) {
   __shared__ float tile[64][65];
   const int k0 = blockIdx.x * 64, n0 = blockIdx.y * 64, e = blockIdx.z;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 64 x 4
@@ -107,7 +142,9 @@ __global__ __launch_bounds__(256) void quant_transpose_kernel(const bf16_t* __re
   __syncthreads();
   // thread: one column n (row of Q) and 16 consecutive k
   const int n = threadIdx.x >> 2, kq = (threadIdx.x & 3) * 16;
-  const float inv = e4m3_inv(amax[(int64_t)e * N + n0 + n]);
+  const float am = amax[(int64_t)e * N + n0 + n];
+  const float inv = e4m3_inv(am);
+  if (k0 == 0 && (threadIdx.x & 3) == 0) scale[(int64_t)e * N + n0 + n] = e4m3_scale(am);
   uint32_t c[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j)
@@ -129,12 +166,16 @@ int launch_quant_rows(const void* s0, const void* s1, int w0, int w1, const int3
 
 int launch_weight_quant(const void* w, int E, int K, int N, float* amax, float* scale, uint8_t* q, hipStream_t s) {
   const bf16_t* wb = reinterpret_cast<const bf16_t*>(w);
-  const dim3 g1((N + 255) / 256, E);
-  int st = launch(K_WEIGHT_QUANT, s, "weight_quant", [&] { col_amax_kernel<<<g1, 256, 0, s>>>(wb, K, N, amax, scale); });
+  const int64_t na = (int64_t)E * N;
+  int st = launch(K_WEIGHT_QUANT, s, "weight_quant",
+                  [&] { amax_clear_kernel<<<(unsigned)((na + 255) / 256), 256, 0, s>>>(amax, na); });
+  if (st) return st;
+  const dim3 g1((N + 255) / 256, (K + 255) / 256, E);
+  st = launch(K_WEIGHT_QUANT, s, "weight_quant", [&] { col_amax_kernel<<<g1, 256, 0, s>>>(wb, K, N, amax); });
   if (st) return st;
   const dim3 g2(K / 64, N / 64, E);
   return launch(K_WEIGHT_QUANT, s, "weight_quant",
-                [&] { quant_transpose_kernel<<<g2, 256, 0, s>>>(wb, K, N, amax, q); });
+                [&] { quant_transpose_kernel<<<g2, 256, 0, s>>>(wb, K, N, amax, q, scale); });
 }
 
 }  // namespace moe
