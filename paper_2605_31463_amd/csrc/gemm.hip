@@ -958,12 +958,13 @@ __device__ __forceinline__ void tile_dims(const GemmArgs& a, const Tile& tl, int
 
 // CL: the clamped GLU activation (gate/up forward and down dgrad epilogues);
 // compiled as its own kernel so that the SwiGLU kernels carry none of its code.
-// FP8 (forward passes only): E4M3 operands, both K-contiguous (activation rows
-// and the weight cache's transposed weights), staged exactly like bf16 data of
-// half the K (a 16-byte chunk holds 16 codes); v_mfma_f32_32x32x64_f8f6f4 takes
-// two bf16-sized fragments per operand (the same k subset on both sides); the
-// epilogue first scales the float32 accumulators by the row's and the
-// column's quantisation scales.
+// FP8 (forward and data-gradient passes): E4M3 operands, both K-contiguous
+// (activation rows; the weight cache's transposed weights for the forward, its
+// row-quantised natural layouts for the data gradients), staged exactly like
+// bf16 data of half the K (a 16-byte chunk holds 16 codes);
+// v_mfma_f32_32x32x64_f8f6f4 takes two bf16-sized fragments per operand (the
+// same k subset on both sides); the epilogues multiply the float32
+// accumulators by the row's and the column's quantisation scales.
 template <int MODE, class C, bool CL = false, bool FP8 = false>
 __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persistent(GemmArgs a) {
   static_assert(!FP8 || !is_wgrad<MODE>(), "FP8: the forward and data-gradient passes only");

@@ -243,11 +243,13 @@ struct GemmArgs {
   bool accumulate;         // wgrad passes: add into c0/c1/db0/db1 instead of overwriting
   int act;                 // MOE_ACT_*: activation of the gate/up forward and down dgrad epilogues
   float act_alpha, act_limit;
-  // FP8 forward passes: a = E4M3 rows, w0 / w1 = the weight cache's E4M3 codes
-  // ([E][f][d] gate / up, [E][d][f] down), the float32 row and column scales
+  // FP8 forward and data-gradient passes: a = E4M3 rows, w0 / w1 = the weight
+  // cache's E4M3 codes (forward: [E][f][d] gate / up, [E][d][f] down; data
+  // gradients: [E][f][d] down rows, [E][d][2f] [gate | up] rows), the float32
+  // row and column scales
   bool fp8;
   const float* a_scale;    // [rows]
-  const float* b_scale0;   // [E][N] gate (or down) column scales
+  const float* b_scale0;   // [E][N] column scales (gate, down, or [gate | up] rows)
   const float* b_scale1;   // [E][f] up column scales
 };
 int launch_gemm(const GemmArgs& a, hipStream_t s);
