@@ -608,7 +608,8 @@ def aux_loss_backward(p, f, coef, eta=None, sig=None):
 # Evaluation of a layer too large to run whole
 # ----------------------------------------------------------------------------
 
-def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=None, act=None, theta=None):
+def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=None, act=None, theta=None,
+                           fp8=0):
     """Every per-token result of the layer for a batch of tokens: routing, y,
     omega, dl and dx (no weight gradients).
 
@@ -618,7 +619,10 @@ def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=No
     visited in ascending order, each once, with all of the batch's tokens
     that selected it.  dl_dense [T][E] holds dl at the selected experts and
     zero elsewhere: for a batch that contains every token routed to expert e,
-    column e of dW_r is x_batch^T dl_dense[:, e].
+    column e of dW_r is x_batch^T dl_dense[:, e].  fp8: 1 the experts' forward
+    products on E4M3 operands, 2 their data-gradient products too (the row
+    quantisation of x, h, d_o and [dg | du] is per token, the weights'
+    quantisation per column or row of the whole weight).
     """
     x = np.asarray(x, np.float64)
     dy = np.asarray(dy, np.float64)
@@ -640,11 +644,12 @@ def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=No
             continue                         # zero-computation experts (above), empty slots
         t, s = np.nonzero(idx == e)          # a token holds e in at most one slot
         wg, wu, wd, bg, bu, bd = expert_fn(int(e))
-        g, u, h, o = expert_forward(x[t], wg, wu, wd, bg, bu, bd, act=act)
+        g, u, h, o = (fp8_expert_forward if fp8 else expert_forward)(x[t], wg, wu, wd, bg, bu, bd, act=act)
         we = w[t, s][:, None]
         y[t] += we * o
         omega[t, s] = (dy[t] * o).sum(axis=1)
-        dx[t] += expert_backward(x[t], g, u, h, we * dy[t], wg, wu, wd, act=act)["dx"]
+        bwd_fn = fp8_expert_backward if fp8 == 2 else expert_backward
+        dx[t] += bwd_fn(x[t], g, u, h, we * dy[t], wg, wu, wd, act=act)["dx"]
     dl = router_backward(spec, rt, omega)
     dl_dense = _scatter_slots(dl, idx, E_pool)
     dx += dl_dense @ np.asarray(w_r, np.float64).T
@@ -655,7 +660,7 @@ def token_forward_backward(spec, x, dy, w_r, beta, expert_fn, shared=None, zc=No
     return dict(route=rt, y=y, dx=dx, omega=omega, dl=dl, dl_dense=dl_dense)
 
 
-def expert_weight_grads_at(xe, do, wg, wu, wd, bg=None, bu=None, cols=None, with_bias=False, act=None):
+def expert_weight_grads_at(xe, do, wg, wu, wd, bg=None, bu=None, cols=None, with_bias=False, act=None, fp8=0):
     """Weight gradients of one expert restricted to the intermediate indices
     `cols`: dW_gate[:, cols], dW_up[:, cols], dW_down[cols, :] (and db_gate,
     db_up at cols, db_down whole).
@@ -665,12 +670,19 @@ def expert_weight_grads_at(xe, do, wg, wu, wd, bg=None, bu=None, cols=None, with
     dh_j only row j of W_down), so the plain expert forward and backward on
     the sliced weights give exactly those slices of the full gradients.
     xe [M][d] are the expert's rows and do [M][d] their output gradients.
+    fp8 (1: forward products on E4M3 operands, 2: data-gradient products too)
+    keeps this: x and d_o are quantised per row over d, W_gate and W_up per
+    column, W_down per row (fp8 = 2), so g_j, u_j, h_j and dh_j still use only
+    column j (the quantisation of h and [dg | du] rows spans every column, but
+    feeds only o and dx, which are not returned).
     """
     cols = np.asarray(cols)
     wg_c, wu_c, wd_c = wg[:, cols], wu[:, cols], wd[cols, :]
-    g, u, h, _ = expert_forward(xe, wg_c, wu_c, wd_c,
-                                None if bg is None else bg[cols], None if bu is None else bu[cols], act=act)
-    out = expert_backward(xe, g, u, h, do, wg_c, wu_c, wd_c, with_bias=with_bias, act=act)
+    fwd_fn = fp8_expert_forward if fp8 else expert_forward
+    bwd_fn = fp8_expert_backward if fp8 == 2 else expert_backward
+    g, u, h, _ = fwd_fn(xe, wg_c, wu_c, wd_c,
+                        None if bg is None else bg[cols], None if bu is None else bu[cols], act=act)
+    out = bwd_fn(xe, g, u, h, do, wg_c, wu_c, wd_c, with_bias=with_bias, act=act)
     out.pop("dx")
     out.pop("dg")
     out.pop("du")

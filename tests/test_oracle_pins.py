@@ -1304,3 +1304,31 @@ def test_fp8_dgrad_second_product_reads_e4m3_rows():
         assert s > 0 and set((got["dx"][r] / s).tolist()) <= ev, r
     ref = np.concatenate([got["dg"], got["du"]], axis=1) * 0.875
     assert not np.array_equal(got["dx"], ref)               # quantised, not the plain [dg | du]
+
+
+@pytest.mark.parametrize("level", [1, 2])
+def test_fp8_token_subset_and_column_slices_equal_whole_layer(level):
+    """With FP8 products the per-token and per-column evaluations still give
+    the whole layer's values: the row quantisation is per token, the weights'
+    quantisation per column (forward) or per row (data gradients) of the whole
+    weight, and the slices of the weight gradients use column-local values."""
+    spec = RouterSpec("softmax_topk", E=6, k=2)
+    c = make_case(spec, T=40, d=32, f=24, seed=68)
+    fwd = layer_forward(spec, c["x"], c["w_r"], None, efn(c), fp8=True)
+    bwd = layer_backward(spec, c["x"], c["w_r"], None, efn(c), fwd, c["dy"], fp8=(level == 2))
+    sub = np.array([39, 3, 17, 0, 22, 5])
+    r = token_forward_backward(spec, c["x"][sub], c["dy"][sub], c["w_r"], None, efn(c), fp8=level)
+    for a, b in ((r["y"], fwd["y"][sub]), (r["dx"], bwd["dx"][sub]), (r["omega"], bwd["omega"][sub])):
+        assert rel(a, b) < 1e-12
+    cols = np.array([23, 0, 9, 10])
+    mp = fwd["maps"]
+    for e in range(spec.E):
+        r0, r1 = mp["offsets"][e], mp["offsets"][e + 1]
+        if r1 == r0:
+            continue
+        wg, wu, wd, bg, bu, _ = efn(c)(e)
+        part = expert_weight_grads_at(fwd["x_perm"][r0:r1], bwd["do"][r0:r1], wg, wu, wd, cols=cols, fp8=level)
+        full = bwd["experts"][e]
+        assert rel(part["dw_gate"], full["dw_gate"][:, cols]) < 1e-12
+        assert rel(part["dw_up"], full["dw_up"][:, cols]) < 1e-12
+        assert rel(part["dw_down"], full["dw_down"][cols, :]) < 1e-12
