@@ -840,7 +840,9 @@ def zc_backward(dy, x, topk_idx, topk_w, E, zs, v, wc):
 # row's gate and up halves together), W_down per row (an output column of dh)
 # and the concatenated rows of [W_gate | W_up] per row (an output column of dx,
 # again one scale over both halves).  The weight-gradient products stay on the
-# unquantised operands.
+# unquantised operands.  The gradient through the activation reads g and u as
+# the forward stored them (bf16, nearest even), so that the codes of [dg | du]
+# are decided on the values a bf16 layer holds, as the codes of h are.
 
 _E4M3_MAX = 448.0
 
@@ -942,12 +944,13 @@ def fp8_expert_forward(xe, wg, wu, wd, bg=None, bu=None, bd=None, act=None):
 def fp8_expert_backward(xe, g, u, h, do, wg, wu, wd, with_bias=False, act=None):
     """expert_backward with its two data-gradient products on E4M3 operands:
     dh from the row-quantised stored d_o and W_down, dx from the row-quantised
-    stored [dg | du] and [W_gate | W_up]; the weight gradients from the
-    unquantised d_o, dg, du (see the comment above e4m3_values)."""
+    stored [dg | du] and [W_gate | W_up]; the activation's derivatives at the
+    stored (bf16) g and u; the weight gradients from the unquantised d_o and
+    the resulting dg, du (see the comment above e4m3_values)."""
     _, _, doq = quantize_rows(round_bf16(do))
     _, _, wdq = quantize_rows(wd)                        # [f][d]: a scale per output column j of dh
     dh = doq @ wdq.T
-    _, hg, hu = glu(g, u, act)
+    _, hg, hu = glu(round_bf16(g), round_bf16(u), act)
     dg = dh * hg
     du = dh * hu
     _, _, dguq = quantize_rows(round_bf16(np.concatenate([dg, du], axis=1)))

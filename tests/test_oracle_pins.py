@@ -1182,11 +1182,12 @@ def test_round_bf16_matches_torch():
 # ---------------------------------------------------------------------------
 
 def _fp8_bwd_case(seed, M=10, d=16, f=8):
+    from oracle.moe_oracle import round_bf16
     rng = np.random.default_rng(seed)
     xe = rng.standard_normal((M, d))
     wg, wu = rng.standard_normal((d, f)) * 0.3, rng.standard_normal((d, f)) * 0.3
     wd = rng.standard_normal((f, d)) * 0.3
-    g, u = xe @ wg, xe @ wu
+    g, u = round_bf16(xe @ wg), round_bf16(xe @ wu)     # as a bf16 layer stores them
     h = g / (1 + np.exp(-g)) * u
     do = rng.standard_normal((M, d))
     return xe, g, u, h, do, wg, wu, wd
@@ -1332,3 +1333,21 @@ def test_fp8_token_subset_and_column_slices_equal_whole_layer(level):
         assert rel(part["dw_gate"], full["dw_gate"][:, cols]) < 1e-12
         assert rel(part["dw_up"], full["dw_up"][:, cols]) < 1e-12
         assert rel(part["dw_down"], full["dw_down"][cols, :]) < 1e-12
+
+
+
+def test_fp8_dgrad_reads_stored_activations():
+    """The FP8 backward takes the activation's derivatives at g and u as a
+    bf16 layer stores them: g and u off the bf16 grid give the same result as
+    their rounded values, and differ from the plain backward at the unrounded
+    ones."""
+    from oracle.moe_oracle import round_bf16
+    xe, g, u, h, do, wg, wu, wd = _fp8_bwd_case(69)
+    rng = np.random.default_rng(70)
+    g2 = g * (1 + rng.uniform(-2.0 ** -10, 2.0 ** -10, g.shape))   # within half a bf16 step
+    u2 = u * (1 + rng.uniform(-2.0 ** -10, 2.0 ** -10, u.shape))
+    assert np.array_equal(round_bf16(g2), g) and np.array_equal(round_bf16(u2), u)
+    a = fp8_expert_backward(xe, g2, u2, h, do, wg, wu, wd)
+    b = fp8_expert_backward(xe, g, u, h, do, wg, wu, wd)
+    for n in ("dg", "du", "dx", "dw_gate", "dw_up"):
+        assert np.array_equal(a[n], b[n]), n
