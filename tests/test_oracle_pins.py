@@ -1351,3 +1351,26 @@ def test_fp8_dgrad_reads_stored_activations():
     b = fp8_expert_backward(xe, g, u, h, do, wg, wu, wd)
     for n in ("dg", "du", "dx", "dw_gate", "dw_up"):
         assert np.array_equal(a[n], b[n]), n
+
+
+
+def test_round_bf16_keep_side():
+    """Plain nearest-even rounding away from the bounds; a value that would
+    round onto or across a bound stays on its side, at most one bf16 step from
+    where nearest rounding puts it (7 + 2^-8 rounds to 7 plainly, to the next
+    bf16 value 7 + 2^-5 here)."""
+    from oracle.moe_oracle import round_bf16, round_bf16_keep_side
+    rng = np.random.default_rng(71)
+    v = np.concatenate([rng.uniform(-9, 9, 200000), 7 + rng.uniform(-0.03, 0.03, 20000),
+                        -7 + rng.uniform(-0.03, 0.03, 20000), [7.0, -7.0, 7 + 2.0 ** -8, -7 - 2.0 ** -8]])
+    bounds = [(7.0, True), (-7.0, False)]
+    r = round_bf16_keep_side(v, bounds)
+    p = round_bf16(v)
+    assert np.array_equal(r > 7.0, v > 7.0) and np.array_equal(r < -7.0, v < -7.0)
+    assert np.array_equal(round_bf16(r), r)                      # on the bf16 grid
+    moved = r != p
+    assert moved.any() and np.all(np.abs(r - p)[moved] <= 2.0 ** -5 * (1 + 1e-12))
+    assert np.all(np.abs(v[moved]) > 6.9) and np.all(np.abs(v[moved]) < 7.1)
+    assert round_bf16_keep_side(np.array([7 + 2.0 ** -8]), bounds)[0] == 7 + 2.0 ** -5
+    assert round_bf16_keep_side(np.array([-7 - 2.0 ** -8]), bounds)[0] == -7 - 2.0 ** -5
+    assert round_bf16(np.array([7 + 2.0 ** -8]))[0] == 7.0
