@@ -145,3 +145,74 @@ def test_fp8_layer_parity(name, level):
         assert dist_fwd_only > 2 * errs["dx"]
     bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, bad
+
+
+def test_fp8_fullsize_qwen3_sampled():
+    """The Qwen3 workload at full size (T = 8192, 128 experts, the bench's
+    launch configuration) with fp8 = 2: routing and maps of every token
+    against the oracle; y and dx of sampled tokens against the oracle's
+    per-token FP8 evaluation; the expert weight gradients at sampled
+    intermediate columns of three experts (fewest rows, most rows, one at
+    random) against its per-column FP8 evaluation."""
+    import torch
+    from moe_inputs import config
+    from oracle import (expert_weight_grads_at, route, router_logits, sort_maps, spec_from_config,
+                        token_forward_backward)
+    from tests.helpers import check_maps_valid, expert_fn
+    cfg = dict(config("qwen3"), fp8=2)
+    T, E, k, f = cfg["T"], cfg["E"], cfg["k"], cfg["f"]
+    tol = TOL[cfg["dtype"]]
+    inp = layer_inputs(cfg, seed=0)
+    print("full-size qwen3 fp8 layer", flush=True)
+    layer, p = setup(cfg, inp)
+    x = dev(inp["x"], "bf16")
+    dy = dev(inp["dy"], "bf16")
+    y = layer.forward(p, x)
+    grads = layer.alloc_grads()
+    dx = layer.backward(p, x, dy, grads)
+    torch.cuda.synchronize()
+    print("oracle routing of every token", flush=True)
+    spec = spec_from_config(cfg)
+    x64, dy64 = to_f64(inp["x"], "bf16"), to_f64(inp["dy"], "bf16")
+    w_r = inp["w_r"].astype(np.float64)
+    beta = None if inp["router_bias"] is None else inp["router_bias"].astype(np.float64)
+    rt = route(spec, router_logits(x64, w_r), beta)
+    sv = {n: host(layer.saved[n]) for n in ("topk_idx", "expert_offsets", "row_of", "token_of")}
+    amb, all_equal = check_routing(cfg, {"route": rt}, sv["topk_idx"])
+    mp = sort_maps(rt["topk_idx"], E)
+    if all_equal:
+        for a, b in (("expert_offsets", "offsets"), ("row_of", "row_of"), ("token_of", "token_of")):
+            assert np.array_equal(sv[a], mp[b]), a
+    else:
+        check_maps_valid(sv["topk_idx"], sv["expert_offsets"], sv["row_of"], sv["token_of"], E)
+    differ = np.nonzero(np.any(sv["topk_idx"] != rt["topk_idx"], axis=1))[0]
+    rng = np.random.default_rng(7)
+    sample = np.sort(rng.choice(np.setdiff1d(np.arange(T), differ), 6, replace=False))
+    efn = expert_fn(inp, cfg)
+    print("oracle per-token FP8 results of", sample.size, "tokens", flush=True)
+    r = token_forward_backward(spec, x64[sample], dy64[sample], w_r, beta, efn, fp8=2)
+    st = torch.from_numpy(sample).cuda()
+    errs = {"y[sample]": rel(host(y[st]), r["y"]), "dx[sample]": rel(host(dx[st]), r["dx"])}
+    touched = set(np.unique(np.concatenate([sv["topk_idx"][differ].ravel(),
+                                            rt["topk_idx"][differ].ravel()])).tolist()) if differ.size else set()
+    counts = mp["counts"]
+    usable = [e for e in range(E) if counts[e] > 0 and e not in touched]
+    e_min = min(usable, key=lambda e: (counts[e], e))
+    e_max = max(usable, key=lambda e: (counts[e], -e))
+    e_rand = int(rng.choice([e for e in usable if e not in (e_min, e_max)]))
+    cols = np.unique(np.concatenate([[0, f - 1, f // 2], rng.choice(f, 13, replace=False)]))
+    ct = torch.from_numpy(cols).cuda()
+    for tag, e in (("e_min", e_min), ("e_max", e_max), ("e_rand", e_rand)):
+        rows = mp["token_of"][mp["offsets"][e]:mp["offsets"][e + 1]]
+        tt, ss = rows // k, rows % k
+        print("oracle FP8 weight gradients of expert", e, "rows", tt.size, flush=True)
+        wg, wu, wd, _, _, _ = efn(e)
+        do = rt["topk_w"][tt, ss][:, None] * dy64[tt]
+        g = expert_weight_grads_at(x64[tt], do, wg, wu, wd, cols=cols, fp8=2)
+        errs["dw_gate[%s]" % tag] = rel(host(grads["dw_gate"][e][:, ct]), g["dw_gate"])
+        errs["dw_up[%s]" % tag] = rel(host(grads["dw_up"][e][:, ct]), g["dw_up"])
+        errs["dw_down[%s]" % tag] = rel(host(grads["dw_down"][e][ct, :]), g["dw_down"])
+    print("qwen3 fp8 full size: ambiguous tokens", int(amb.sum()), "routed differently", differ.size,
+          {n: "%.2e" % v for n, v in errs.items()}, flush=True)
+    bad = {n: v for n, v in errs.items() if not v <= tol}
+    assert not bad, bad
