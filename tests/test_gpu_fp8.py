@@ -12,7 +12,8 @@ oracle's FP8 layer.
     rows, 256-row tiles), with expert biases, with the clamped GLU, and
     DeepSeek-V3 widths with the (bf16) shared expert;
   * the cache is reused across calls (two forwards, one build);
-  * MoE++ (zero-computation experts in the pool) at both levels;
+  * MoE++ (zero-computation experts in the pool) at both levels, and a
+    sparse batch (16 tokens over 32 experts: most experts without rows);
   * with shape.fp8 = 2 the data-gradient GEMMs also run on E4M3 operands: the
     cache's row codes of W_down and [W_gate | W_up] bit-exact against the
     oracle's row quantisation, and the same layer cases against the oracle's
@@ -29,6 +30,8 @@ pytestmark = pytest.mark.gpu
 
 CASES = {
     "qwen3_small_tiles": variant("qwen3", T=256, E=32, k=4, fp8=True),
+    # 32 slots over 32 experts: many experts without rows, one- and two-row experts
+    "qwen3_sparse": variant("qwen3", T=16, E=32, k=2, fp8=True),
     "qwen3_e16": variant("qwen3", T=1024, E=16, fp8=True),
     "qwen3_e16_bias": variant("qwen3", T=1024, E=16, expert_bias=True, fp8=True),
     "qwen3_e16_clamped": variant("qwen3", T=1024, E=16, act="clamped_glu", w_std=0.27, fp8=True),
