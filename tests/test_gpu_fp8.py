@@ -37,7 +37,7 @@ CASES = {
     "qwen3_e16_clamped": variant("qwen3", T=1024, E=16, act="clamped_glu", w_std=0.27, fp8=True),
     "dsv3": variant("dsv3", T=384, d=512, f=256, f_shared=256, fp8=True),
     # zero-computation experts in the pool: d_o rows quantised by their own pass
-    "moepp": variant("moepp", T=256, fp8=True),
+    "moepp": variant("moepp", T=256, E=32, d=512, f=256, fp8=True),
 }
 
 
