@@ -80,7 +80,9 @@ __global__ __launch_bounds__(256) void combine_fwd_kernel(CombineFwdArgs a) {
   }
 }
 
-template <class XT, int KT>
+// Q8: also the E4M3 rows of d_o (a kernel of its own, so that the bf16 path
+// keeps its register count and occupancy)
+template <class XT, int KT, bool Q8 = false>
 __global__ __launch_bounds__(256) void combine_bwd_kernel(CombineBwdArgs a) {
   constexpr int V = Vec16<XT>::N;
   constexpr int KM = KT > 0 ? KT : KMAX;
@@ -107,9 +109,8 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(CombineBwdArgs a) {
   // FP8 data gradients: E4M3 rows of the stored d_o as well.  Row s is
   // bf16(w_s dy_t); rounding is monotone and sign-symmetric, so its largest
   // magnitude is bf16(|w_s| max|dy_t|), known before any value is written.
-  constexpr bool kQ = sizeof(XT) == 2;
-  const bool q8 = kQ && a.doq != nullptr;
-  if (q8) {
+  static_assert(!Q8 || sizeof(XT) == 2, "E4M3 rows of bf16 layers only");
+  if constexpr (Q8) {
     float m = 0.f;
     for (int c = lane; c < nch; c += 64) {
       float g[V];
@@ -148,14 +149,12 @@ __global__ __launch_bounds__(256) void combine_bwd_kernel(CombineBwdArgs a) {
           out[v] = w[s] * g[v];
         }
         Vec16<XT>::store(d_o + rows[s] * a.d + (int64_t)c * V, out);
-        if constexpr (kQ) {
-          if (q8) {  // the codes of the stored (bf16) values
-            float b[8];
+        if constexpr (Q8) {  // the codes of the stored (bf16) values
+          float b[8];
 #pragma unroll
-            for (int v = 0; v < 8; ++v) b[v] = bf2f(f2bf(out[v])) * qi[s];
-            *reinterpret_cast<uint2*>(a.doq + rows[s] * a.d + (int64_t)c * 8) =
-                make_uint2(e4m3x4(b[0], b[1], b[2], b[3]), e4m3x4(b[4], b[5], b[6], b[7]));
-          }
+          for (int v = 0; v < 8; ++v) b[v] = bf2f(f2bf(out[v])) * qi[s];
+          *reinterpret_cast<uint2*>(a.doq + rows[s] * a.d + (int64_t)c * 8) =
+              make_uint2(e4m3x4(b[0], b[1], b[2], b[3]), e4m3x4(b[4], b[5], b[6], b[7]));
         }
       }
     }
@@ -717,6 +716,13 @@ int launch_combine_bwd(const CombineBwdArgs& a, hipStream_t s) {
   if (a.zc.on) {
     if (a.bf16) { MOE_BY_K("combine_bwd", K_COMBINE_BWD, combine_bwd_zc_kernel, bf16_t) }
     MOE_BY_K("combine_bwd", K_COMBINE_BWD, combine_bwd_zc_kernel, float)
+  }
+  if (a.doq) {
+    switch (a.k) {
+      case 8: return launch(K_COMBINE_BWD, s, "combine_bwd", [&] { combine_bwd_kernel<bf16_t, 8, true><<<nb, 256, 0, s>>>(a); });
+      case 4: return launch(K_COMBINE_BWD, s, "combine_bwd", [&] { combine_bwd_kernel<bf16_t, 4, true><<<nb, 256, 0, s>>>(a); });
+      default: return launch(K_COMBINE_BWD, s, "combine_bwd", [&] { combine_bwd_kernel<bf16_t, 0, true><<<nb, 256, 0, s>>>(a); });
+    }
   }
   if (a.bf16) { MOE_BY_K("combine_bwd", K_COMBINE_BWD, combine_bwd_kernel, bf16_t) }
   MOE_BY_K("combine_bwd", K_COMBINE_BWD, combine_bwd_kernel, float)
