@@ -1703,14 +1703,16 @@ int launch_mode(const GemmArgs& a, hipStream_t s) {
     if constexpr (MOE_GEMM_PERSISTENT != 0) {
       if constexpr (!is_wgrad<MODE>()) {
         if (a.fp8) {
+          // FP8: 2 x 4 wavefronts in every pass (the data-gradient passes ran
+          // 9% faster than with the bf16 kernels' 4 x 2, Qwen3 shape)
           if constexpr (MODE == G_FWD_GATEUP || MODE == G_DGRAD_DOWN) {
             if (a.act == MOE_ACT_CLAMPED_GLU) {
               if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, true, true>(a, s);
-              return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big, true, true>(a, s);
+              return launch_bf16_persistent<MODE, CfgWide, true, true>(a, s);
             }
           }
           if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, false, true>(a, s);
-          return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big, false, true>(a, s);
+          return launch_bf16_persistent<MODE, CfgWide, false, true>(a, s);
         }
       }
       if constexpr (MODE == G_FWD_GATEUP || MODE == G_DGRAD_DOWN) {
