@@ -225,3 +225,33 @@ def test_fp8_fullsize_qwen3_sampled():
           {n: "%.2e" % v for n, v in errs.items()}, flush=True)
     bad = {n: v for n, v in errs.items() if not v <= tol}
     assert not bad, bad
+
+
+
+def test_fp8_zero_rows_and_zero_gradients():
+    """Tokens whose x row is zero and whose dy row is zero: their rows quantise
+    with scale 1 to zero codes (no division by zero), the layer stays finite
+    and within the bar of the oracle at both levels."""
+    import torch
+    for level in (1, 2):
+        cfg = variant("qwen3", T=64, E=8, k=2, d=256, f=128, fp8=level)
+        inp = layer_inputs(cfg, seed=3)
+        inp["x"][[0, 5, 17]] = 0
+        inp["dy"][[0, 9, 33]] = 0
+        print("fp8 zero rows, level", level, flush=True)
+        layer, p = setup(cfg, inp)
+        x = dev(inp["x"], cfg["dtype"])
+        y = layer.forward(p, x)
+        grads = layer.alloc_grads()
+        dx = layer.backward(p, x, dev(inp["dy"], cfg["dtype"]), grads)
+        torch.cuda.synchronize()
+        fwd, bwd = oracle_run(cfg, inp)
+        check_routing(cfg, fwd, host(layer.saved["topk_idx"]))
+        hy, hdx = host(y), host(dx)
+        assert np.isfinite(hy).all() and np.isfinite(hdx).all()
+        for n in ("dw_gate", "dw_down"):
+            assert np.isfinite(host(grads[n])).all(), n
+        errs = {"y": rel(hy, fwd["y"]), "dx": rel(hdx, bwd["dx"]),
+                "dw_gate": rel(host(grads["dw_gate"]), np.stack([bwd["experts"][e]["dw_gate"] for e in range(8)]))}
+        print("level", level, {k: "%.2e" % v for k, v in errs.items()}, flush=True)
+        assert all(v <= TOL[cfg["dtype"]] for v in errs.values()), errs
