@@ -830,8 +830,8 @@ __device__ __forceinline__ Tile tile_at(const GemmArgs& a, int lin, const int* p
     return t;
   }
   const int mt = lin / nt;
-  t.n0 = (lin - mt * nt) * tile_cols<MODE, BN>();
   if (!a.offsets) {
+    t.n0 = (lin - mt * nt) * tile_cols<MODE, BN>();
     t.g = 0;
     t.row_base = 0;
     t.rows = (int)a.dense_rows;
@@ -846,7 +846,15 @@ __device__ __forceinline__ Tile tile_at(const GemmArgs& a, int lin, const int* p
   t.g = lo;
   t.row_base = a.offsets[lo];
   t.rows = a.offsets[lo + 1] - t.row_base;
-  t.m0 = (mt - pre[lo]) * BM;
+  // within the expert, bands of up to GM row tiles taken column by column
+  // (row tiles fastest): the neighbouring tiles that an XCD runs together
+  // share their weight column tiles as well as their row tiles
+  constexpr int GM = 8;
+  const int local = lin - pre[lo] * nt, mg = (t.rows + BM - 1) / BM;  // (pre[] has no entry past the last group)
+  const int q = local / (GM * nt), gm = min(GM, mg - q * GM);
+  const int r = local - q * GM * nt;
+  t.m0 = (q * GM + r % gm) * BM;
+  t.n0 = (r / gm) * tile_cols<MODE, BN>();
   return t;
 }
 
