@@ -414,7 +414,10 @@ int moe_layer_bwd_wgrad(const moe_shape* shape, const moe_params* params, const 
  * w_down [E][f][d] (bf16) per output column into the caller's cache (codes
  * stored transposed, K-contiguous, with the scales) and, for fp8 = 2, per row
  * as well; call it again whenever the weights change, and reuse it for every
- * micro-batch in between.  The standalone moe_grouped_gemm_fwd / _bwd refuse
+ * micro-batch in between.  The layer entry points read the cache as laid out
+ * for their own shape: it must have been built for the same shape (E, d, f
+ * and the fp8 level); a cache built for fp8 = 1 lacks the regions fp8 = 2
+ * reads.  The standalone moe_grouped_gemm_fwd / _bwd refuse
  * FP8 passes (MOE_ERR_UNSUPPORTED): their operands are the layer's.  Errors:
  * MOE_ERR_UNSUPPORTED without shape->fp8, MOE_ERR_WORKSPACE for a cache below
  * the size. */
