@@ -1461,13 +1461,14 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
       const int nbase = tl.n0 + wn * C::TN;
       bf16_t* c0 = reinterpret_cast<bf16_t*>(a.c0);
       bf16_t* c1 = reinterpret_cast<bf16_t*>(a.c1);
+      // row blocks outer: the adjacent 64-byte pieces of a row go out together
 #pragma unroll
-      for (int j = 0; j < NI; ++j) {
-        const int n0 = nbase + 32 * j;
-        const int ncols = min(32, N - n0);
+      for (int i = 0; i < MI; ++i) {
+        const int m0 = mrow0 + 32 * i;
 #pragma unroll
-        for (int i = 0; i < MI; ++i) {
-          const int m0 = mrow0 + 32 * i;
+        for (int j = 0; j < NI; ++j) {
+          const int n0 = nbase + 32 * j;
+          const int ncols = min(32, N - n0);
           if (m0 >= M || ncols <= 0) continue;
           float o[16];
 #pragma unroll
