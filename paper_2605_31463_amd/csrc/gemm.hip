@@ -830,12 +830,16 @@ __device__ __forceinline__ Tile tile_at(const GemmArgs& a, int lin, const int* p
     return t;
   }
   const int mt = lin / nt;
+  constexpr int GM = 8;  // bands of row tiles (see below)
   if (!a.offsets) {
-    t.n0 = (lin - mt * nt) * tile_cols<MODE, BN>();
     t.g = 0;
     t.row_base = 0;
     t.rows = (int)a.dense_rows;
-    t.m0 = mt * BM;
+    const int mg = (t.rows + BM - 1) / BM;
+    const int q = lin / (GM * nt), gm = min(GM, mg - q * GM);
+    const int r = lin - q * GM * nt;
+    t.m0 = (q * GM + r % gm) * BM;
+    t.n0 = (r / gm) * tile_cols<MODE, BN>();
     return t;
   }
   int lo = 0, hi = a.ngroups - 1;  // last g with pre[g] <= mt
@@ -846,10 +850,10 @@ __device__ __forceinline__ Tile tile_at(const GemmArgs& a, int lin, const int* p
   t.g = lo;
   t.row_base = a.offsets[lo];
   t.rows = a.offsets[lo + 1] - t.row_base;
-  // within the expert, bands of up to GM row tiles taken column by column
-  // (row tiles fastest): the neighbouring tiles that an XCD runs together
-  // share their weight column tiles as well as their row tiles
-  constexpr int GM = 8;
+  // within the expert (or the one dense group), bands of up to GM row tiles
+  // taken column by column (row tiles fastest): the neighbouring tiles that an
+  // XCD runs together share their weight column tiles as well as their row
+  // tiles
   const int local = lin - pre[lo] * nt, mg = (t.rows + BM - 1) / BM;  // (pre[] has no entry past the last group)
   const int q = local / (GM * nt), gm = min(GM, mg - q * GM);
   const int r = local - q * GM * nt;
