@@ -840,12 +840,12 @@ def zc_backward(dy, x, topk_idx, topk_w, E, zs, v, wc):
 # row's gate and up halves together), W_down per row (an output column of dh)
 # and the concatenated rows of [W_gate | W_up] per row (an output column of dx,
 # again one scale over both halves).  The weight-gradient products stay on the
-# unquantised operands.  The gradient through the activation reads g and u as
-# the forward stored them (bf16, nearest even; with the clamped GLU a value that
-# rounding would carry across a clamp bound keeps its own side, one bf16 step
-# back, so that the clamp masks stay those of the forward), so that the codes
-# of [dg | du] are decided on the values a bf16 layer holds, as the codes of h
-# are.
+# unquantised operands.  The smooth factors of the activation's derivative are
+# evaluated at g and u as a bf16 layer stores them (rounded to nearest even), so
+# that the codes of [dg | du] are decided on the values a bf16 layer holds, as
+# the codes of h are; the clamped GLU's clamp masks (which values pass a
+# gradient) are those of the forward's own values g and u: a clamp's derivative
+# belongs to the value it clamped, not to its stored rounding.
 
 _E4M3_MAX = 448.0
 
@@ -944,43 +944,31 @@ def fp8_expert_forward(xe, wg, wu, wd, bg=None, bu=None, bd=None, act=None):
     return g, u, h, o
 
 
-def round_bf16_keep_side(a, bounds):
-    """round_bf16(a), except where rounding would move a value across one of
-    the bounds: there the neighbouring bf16 value on the value's own side.
-    bounds: (b, upper) pairs; upper: the sides are v > b and v <= b, else
-    v < b and v >= b."""
-    a = np.asarray(a, np.float64)
-    r = round_bf16(a)
-    for b, upper in bounds:
-        side_a = a > b if upper else a < b
-        side_r = r > b if upper else r < b
-        bad = side_a != side_r
-        if not bad.any():
-            continue
-        bits = np.ascontiguousarray(r[bad], np.float32).view(np.uint32).astype(np.int64)
-        toward_up = a[bad] > r[bad]
-        # one bf16 step (2^16 in the float32 bit pattern) up or down in value
-        step = np.where(toward_up == (r[bad] >= 0), 0x10000, -0x10000)
-        r[bad] = (bits + step).astype(np.uint32).view(np.float32).astype(np.float64)
-    return r
-
-
 def fp8_expert_backward(xe, g, u, h, do, wg, wu, wd, with_bias=False, act=None):
     """expert_backward with its two data-gradient products on E4M3 operands:
     dh from the row-quantised stored d_o and W_down, dx from the row-quantised
-    stored [dg | du] and [W_gate | W_up]; the activation's derivatives at the
-    stored (bf16) g and u; the weight gradients from the unquantised d_o and
+    stored [dg | du] and [W_gate | W_up]; the activation's smooth derivative
+    factors at the stored (bf16) g and u, the clamp masks of the clamped GLU at
+    the forward's g and u; the weight gradients from the unquantised d_o and
     the resulting dg, du (see the comment above e4m3_values)."""
     _, _, doq = quantize_rows(round_bf16(do))
     _, _, wdq = quantize_rows(wd)                        # [f][d]: a scale per output column j of dh
     dh = doq @ wdq.T
+    gs, us = round_bf16(g), round_bf16(u)
     if act is None:
-        gs, us = round_bf16(g), round_bf16(u)
+        _, hg, hu = glu(gs, us)
     else:
-        lim = act[2]
-        gs = round_bf16_keep_side(g, [(lim, True)])
-        us = round_bf16_keep_side(u, [(lim, True), (-lim, False)])
-    _, hg, hu = glu(gs, us, act)
+        # the smooth factors at the stored values (gc, uc clipped as in the
+        # forward) ...
+        kind, alpha, lim = act
+        if kind != "clamped_glu":
+            raise ValueError("unknown activation " + str(kind))
+        gc = np.minimum(gs, lim)
+        uc = np.clip(us, -lim, lim)
+        sg = sigmoid(alpha * gc)
+        # ... and the masks of the forward's own g, u (bounds included)
+        hg = np.where(g <= lim, (uc + 1.0) * sg * (1.0 + alpha * gc * (1.0 - sg)), 0.0)
+        hu = np.where(np.abs(u) <= lim, gc * sg, 0.0)
     dg = dh * hg
     du = dh * hu
     _, _, dguq = quantize_rows(round_bf16(np.concatenate([dg, du], axis=1)))

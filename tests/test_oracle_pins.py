@@ -407,6 +407,29 @@ def test_margin_flags_near_ties():
     assert rt["margin"][0] < 1e-6 <= rt["margin"][1]
 
 
+def test_margins_of_the_sigmoid_routers_worked_by_hand():
+    """The selection margin of the grouped router (group gap at the kept /
+    dropped boundary, key gaps among the k+1 best candidates of the kept
+    groups) and of the threshold router (key gaps, distance of a candidate's
+    key from the threshold) on hand-worked one-token cases; each case is built
+    so that a margin taken at a wrong index or over the wrong set differs."""
+    g = json.load(open(os.path.join(GOLDEN, "route_margins.json")))
+    gg = g["sigmoid_grouped"]
+    spec = RouterSpec("sigmoid_grouped", E=gg["E"], k=gg["k"], n_groups=gg["n_groups"],
+                      topk_groups=gg["topk_groups"], route_scale=gg["route_scale"], bias_mode="select")
+    for c in gg["cases"]:
+        rt = route(spec, np.asarray([c["logits"]], np.float64), np.asarray(c["beta"], np.float64))
+        assert rt["topk_idx"][0].tolist() == c["topk_idx"]
+        np.testing.assert_allclose(rt["topk_w"][0], [n / m for n, m in c["topk_w_frac"]], rtol=0, atol=1e-15)
+        assert rt["margin"][0] == c["margin"], (rt["margin"][0], c["margin"])
+    gt = g["sigmoid_threshold"]
+    spec = RouterSpec("sigmoid_threshold", E=gt["E"], k=gt["k"])
+    for c in gt["cases"]:
+        rt = route(spec, np.asarray([c["logits"]], np.float64), theta=np.asarray(c["theta"], np.float64))
+        assert rt["topk_idx"][0].tolist() == c["topk_idx"]
+        assert rt["margin"][0] == c["margin"], (rt["margin"][0], c["margin"])
+
+
 def test_expert_backward_matches_finite_differences_on_its_own():
     rng = np.random.default_rng(11)
     x = rng.standard_normal((5, 4))
@@ -1354,23 +1377,63 @@ def test_fp8_dgrad_reads_stored_activations():
 
 
 
-def test_round_bf16_keep_side():
-    """Plain nearest-even rounding away from the bounds; a value that would
-    round onto or across a bound stays on its side, at most one bf16 step from
-    where nearest rounding puts it (7 + 2^-8 rounds to 7 plainly, to the next
-    bf16 value 7 + 2^-5 here)."""
-    from oracle.moe_oracle import round_bf16, round_bf16_keep_side
-    rng = np.random.default_rng(71)
-    v = np.concatenate([rng.uniform(-9, 9, 200000), 7 + rng.uniform(-0.03, 0.03, 20000),
-                        -7 + rng.uniform(-0.03, 0.03, 20000), [7.0, -7.0, 7 + 2.0 ** -8, -7 - 2.0 ** -8]])
-    bounds = [(7.0, True), (-7.0, False)]
-    r = round_bf16_keep_side(v, bounds)
-    p = round_bf16(v)
-    assert np.array_equal(r > 7.0, v > 7.0) and np.array_equal(r < -7.0, v < -7.0)
-    assert np.array_equal(round_bf16(r), r)                      # on the bf16 grid
-    moved = r != p
-    assert moved.any() and np.all(np.abs(r - p)[moved] <= 2.0 ** -5 * (1 + 1e-12))
-    assert np.all(np.abs(v[moved]) > 6.9) and np.all(np.abs(v[moved]) < 7.1)
-    assert round_bf16_keep_side(np.array([7 + 2.0 ** -8]), bounds)[0] == 7 + 2.0 ** -5
-    assert round_bf16_keep_side(np.array([-7 - 2.0 ** -8]), bounds)[0] == -7 - 2.0 ** -5
-    assert round_bf16(np.array([7 + 2.0 ** -8]))[0] == 7.0
+def _clamped_glu_torch(g, u, alpha, limit):
+    """The GPT-OSS release's clamped GLU written with torch primitives (an
+    independent formulation): gc = min(g, L), uc = clamp(u, -L, L),
+    h = gc sigmoid(alpha gc) (uc + 1)."""
+    gc = torch.clamp(g, max=limit)
+    uc = torch.clamp(u, min=-limit, max=limit)
+    return gc * torch.sigmoid(alpha * gc) * (uc + 1.0)
+
+
+def test_fp8_dgrad_clamped_glu_masks_of_the_forward_values():
+    """FP8 backward with the clamped GLU (alpha 1.702, L 7) on operands whose
+    row quantisation is exact, so dh = d_o W_down^T exactly: dg and du equal dh
+    times torch autograd's derivatives of the clamped GLU, the smooth factors
+    taken at the stored bf16 g, u and the clamp masks at the forward's own
+    g, u (torch's clamp passes the gradient inside its bounds, bounds
+    included).  Planted values just past a bound (7 + 2^-8, -7 - 2^-8: nearest
+    rounding puts them on the bound) pass no gradient, as the forward's clamp
+    cut them; autograd at the rounded value alone would pass it."""
+    from oracle.moe_oracle import round_bf16
+    alpha, L = 1.702, 7.0
+    act = ("clamped_glu", alpha, L)
+    rng = np.random.default_rng(72)
+    M, d, f = 12, 16, 8
+    ev = e4m3_values()
+    fin = ev[np.isfinite(ev) & (np.abs(ev) <= 448)]
+    do = rng.choice(fin, (M, d)) * 2.0 ** -6
+    do[:, 0] = 448 * 2.0 ** -6                               # each row's largest magnitude: exact scale
+    wd = rng.choice(fin, (f, d)) * 2.0 ** -9
+    wd[:, 1] = -448 * 2.0 ** -9
+    xe = rng.standard_normal((M, d))
+    wg, wu = rng.standard_normal((d, f)), rng.standard_normal((d, f))
+    g = rng.uniform(-9, 9, (M, f))
+    u = rng.uniform(-9, 9, (M, f))
+    g[0, :4] = [L + 2.0 ** -8, L, L - 2.0 ** -8, L + 2.0 ** -3]
+    u[1, :4] = [L + 2.0 ** -8, -L - 2.0 ** -8, L, -L]
+    assert round_bf16(np.array([L + 2.0 ** -8]))[0] == L     # rounding lands on the bound
+    h = _clamped_glu_torch(torch.from_numpy(g), torch.from_numpy(u), alpha, L).numpy()
+    got = fp8_expert_backward(xe, g, u, h, do, wg, wu, wd, act=act)
+    dh = do @ wd.T
+    # smooth factors: autograd at the stored values (a value inside a bound
+    # stays inside when rounded: the bounds are bf16 values)
+    gs = torch.tensor(round_bf16(g), requires_grad=True)
+    us = torch.tensor(round_bf16(u), requires_grad=True)
+    hs = _clamped_glu_torch(gs, us, alpha, L)
+    dgs, dus = torch.autograd.grad(hs, (gs, us), torch.from_numpy(dh))
+    # masks: autograd of the clamps at the forward's own values
+    g64 = torch.tensor(g, requires_grad=True)
+    u64 = torch.tensor(u, requires_grad=True)
+    mg, mu = torch.autograd.grad((torch.clamp(g64, max=L) + torch.clamp(u64, min=-L, max=L)).sum(), (g64, u64))
+    want_dg = dgs.numpy() * mg.numpy()
+    want_du = dus.numpy() * mu.numpy()
+    np.testing.assert_allclose(got["dg"], want_dg, rtol=1e-13, atol=1e-300)
+    np.testing.assert_allclose(got["du"], want_du, rtol=1e-13, atol=1e-300)
+    # the planted values: the forward's clamp cut them (no gradient) ...
+    assert got["dg"][0, 0] == 0.0 and got["dg"][0, 3] == 0.0
+    assert got["du"][1, 0] == 0.0 and got["du"][1, 1] == 0.0
+    # ... the bounds themselves pass it ...
+    assert got["dg"][0, 1] != 0.0 and got["du"][1, 2] != 0.0 and got["du"][1, 3] != 0.0
+    # ... and autograd at the stored (rounded) value alone would have passed it
+    assert dgs.numpy()[0, 0] != 0.0 and dus.numpy()[1, 0] != 0.0
