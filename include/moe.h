@@ -16,9 +16,11 @@
  *
  * Conventions shared by every entry point
  *   - Every tensor pointer is a DEVICE pointer owned by the caller; the
- *     library never allocates, frees or synchronises.  Every call only
- *     enqueues work on `stream` and returns; results are ready when the
- *     stream reaches that point.  Pointers must be 16-byte aligned.
+ *     compute entry points never allocate, free or synchronise.  Every call
+ *     only enqueues work on `stream` and returns; results are ready when the
+ *     stream reaches that point.  Pointers must be 16-byte aligned.  (The
+ *     kernel-timing facility at the end, for benchmarks, is the exception:
+ *     it creates HIP events on first use and moe_timing_read waits for them.)
  *   - Layouts are dense row-major.  T tokens, d hidden, E routed (FFN)
  *     experts, k experts per token, f expert width, R = T*k routed rows,
  *     E_pool = E + n_zero + n_copy + n_const experts the router chooses from
@@ -47,7 +49,9 @@
  *     FFN experts' rows) only list their tokens: x_perm, gu, h, o, d_o and
  *     dx_perm hold nothing there.
  *   - Results are bitwise reproducible run to run: no floating-point atomics.
- *   - Gradients overwrite their outputs (no accumulation).
+ *   - Gradients overwrite their outputs, unless accumulation is asked for
+ *     (MOE_ACCUMULATE in moe_grouped_gemm_bwd, accumulate = 1 in
+ *     moe_layer_bwd_wgrad): then they are added to the buffers' contents.
  *   - Return value: MOE_OK or a negative MOE_ERR_* code.  Argument checks run
  *     on the host before anything is enqueued; on error nothing is enqueued
  *     and moe_last_error() gives a message (thread-local).
@@ -55,7 +59,10 @@
  *     are written as zeros.
  *
  * Limits (MOE_ERR_UNSUPPORTED beyond them): 1 <= E <= E_pool <= 256,
- * 1 <= k <= 16, d and f multiples of 64, d <= 16384, renorm = 1.
+ * 1 <= k <= 16, d and f multiples of 64, d <= 16384, renorm = 1, and every
+ * operand the GEMMs and the router stage through 32-bit buffer descriptors
+ * below 4 GiB: R * max(d, 2f), T * max(d, 2 f_shared), d * 2f and, with the
+ * auxiliary loss, T * E_pool elements of the activation dtype.
  *
  * Zero-computation experts (MoE++; appendix B.3 of the paper lists it among
  * the new-feature tasks: zero, copy and constant experts in the pool, the
@@ -127,11 +134,12 @@ enum { MOE_F32 = 0, MOE_BF16 = 1 };
 /* Activation of the routed experts.  SWIGLU: h = silu(g) * u.  CLAMPED_GLU:
  * the GPT-OSS release's variant, gc = min(g, act_limit),
  * uc = clamp(u, -act_limit, act_limit), h = gc * sigmoid(act_alpha * gc) * (uc + 1)
- * (that release uses act_alpha = 1.702, act_limit = 7); in the backward the
- * clamps pass the gradient where the value lies inside them, bounds included.
- * With bf16 storage, a g or u value that rounding would carry across a clamp
- * bound is stored one bf16 step back on its own side, so that the backward's
- * clamp decisions (taken on the stored gu) are the forward's.
+ * (that release uses act_alpha = 1.702, act_limit = 7); in the backward a
+ * clamp passes the gradient where the forward's value lies inside it, bounds
+ * included.  The backward reads g and u from the saved gu, so with bf16
+ * storage a value that rounding would carry across a clamp bound is stored
+ * one bf16 step back on its own side: the clamp decisions taken on the
+ * stored values are then the forward's.
  * The shared expert always uses SwiGLU. */
 enum { MOE_ACT_SWIGLU = 0, MOE_ACT_CLAMPED_GLU = 1 };
 
@@ -191,6 +199,9 @@ typedef struct moe_params {
   const float* zc_wc;          /* [n_const][2][d] constant experts' mixing weights */
   const float* gate_threshold; /* [E] thresholds of MOE_ROUTER_SIGMOID_THRESHOLD */
   const void* fp8_cache;       /* shape->fp8 != 0: the weight cache moe_fp8_cache_build wrote */
+  size_t fp8_cache_bytes;      /* its size; the layer entry points refuse a cache smaller
+                                  than moe_fp8_cache_size gives for their shape
+                                  (MOE_ERR_WORKSPACE) */
 } moe_params;
 
 /* Tensors the forward writes and the backward reads (caller-allocated). */
@@ -230,11 +241,16 @@ typedef struct moe_grads {
   float* d_threshold;          /* [E], MOE_ROUTER_SIGMOID_THRESHOLD */
 } moe_grads;
 
-/* Workspace bytes.  fwd_ws: enough for moe_route, moe_permute and
- * moe_layer_fwd; bwd_ws: enough for moe_route_bwd, moe_grouped_gemm_bwd,
+/* Workspace bytes of the layer's scratch (section 3.2: the fused routing,
+ * token-scatter and SwiGLU kernels and the wgrad-delay split between them).
+ * fwd_ws: enough for moe_route, moe_permute and moe_layer_fwd (per-block
+ * expert histograms, the router's split weights and float64 logits, FP8 rows);
+ * bwd_ws: enough for moe_route_bwd, moe_grouped_gemm_bwd,
  * moe_shared_expert_bwd and moe_layer_bwd (which keeps d_o, dgu, dx_perm
- * and the router gradient scratch there); saved_bytes: total size of the
- * moe_saved tensors, for information.  Pure host arithmetic. */
+ * and the router gradient scratch there, for the wgrad half); saved_bytes:
+ * total size of the moe_saved tensors, for information.  Pure host
+ * arithmetic; MOE_ERR_INVALID_ARG / MOE_ERR_UNSUPPORTED for a shape outside
+ * the limits. */
 int moe_workspace_size(const moe_shape* shape, size_t* fwd_ws, size_t* saved_bytes, size_t* bwd_ws);
 
 /* Router forward (one fused kernel: logits x W_r (+ bias), selection,
@@ -292,18 +308,27 @@ int moe_grouped_gemm_bwd(const moe_shape* shape, int32_t passes,
                          void* dw_gate, void* dw_up, void* dw_down,
                          void* db_gate, void* db_up, void* db_down, hipStream_t stream);
 
-/* Weighted combine (gather, fixed slot order, float32 sum):
- *   y_t = sum_s topk_w[t][s] * o[row_of[t][s]]  (+ shared_o[t] if non-NULL). */
+/* Weighted combine, the reverse of the token scatter (section 3.2; the
+ * gating weights obey the routing-trace rules of appendix B.2.2): a gather
+ * in fixed slot order with a float32 sum,
+ *   y_t = sum_s topk_w[t][s] * o[row_of[t][s]]  (+ shared_o[t] if non-NULL).
+ * One pass over the rows of o.  Out: y [T][d].  MOE_ERR_UNSUPPORTED with
+ * zero-computation experts (the layer entry points run them). */
 int moe_combine_fwd(const moe_shape* shape, const void* o, const float* topk_w,
                     const int32_t* row_of, const void* shared_o, void* y, hipStream_t stream);
 
-/* Combine backward:
+/* Combine backward (the gradient of the weighted combine above; section
+ * 3.2's fused backward kernels):
  *   d_o[row_of[t][s]] = topk_w[t][s] * dy_t,
- *   d_topk_w[t][s]    = <dy_t, o[row_of[t][s]]>  (float32). */
+ *   d_topk_w[t][s]    = <dy_t, o[row_of[t][s]]>  (float32),
+ * one pass over dy and the rows of o.  Out: d_o [R][d], d_topk_w [T][k].
+ * MOE_ERR_UNSUPPORTED with zero-computation experts. */
 int moe_combine_bwd(const moe_shape* shape, const void* dy, const void* o, const float* topk_w,
                     const int32_t* row_of, void* d_o, float* d_topk_w, hipStream_t stream);
 
-/* Router backward.  dl on the selected experts only:
+/* Router backward (the gradient of the top-k routing kernel of appendix
+ * B.3 through the gating weights; weights as in the routing-trace rules of
+ * appendix B.2.2).  dl on the selected experts only:
  *   softmax families: dl_j = w_j (omega_j - sum_i w_i omega_i / route_scale)
  *   SIGMOID_GROUPED, SIGMOID_THRESHOLD:
  *                     dl_j = (route_scale omega_j - sum_i w_i omega_i) / sum_i s_i
@@ -318,8 +343,11 @@ int moe_route_bwd(const moe_shape* shape, const void* x, const float* w_r,
                   const float* d_topk_w, const int32_t* expert_offsets, const int32_t* token_of,
                   float* dw_r, float* dx_router, void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Unpermute-reduce: dx_t = sum_s dx_perm[row_of[t][s]] (slot order)
- *   + dx_router[t] (float32, may be NULL) + dx_shared[t] (may be NULL). */
+/* Unpermute-reduce, the backward of the token scatter (section 3.2): a
+ * gather of each token's k rows in fixed slot order with a float32 sum,
+ *   dx_t = sum_s dx_perm[row_of[t][s]]
+ *          + dx_router[t] (float32, may be NULL) + dx_shared[t] (may be NULL).
+ * Out: dx [T][d].  MOE_ERR_UNSUPPORTED with zero-computation experts. */
 int moe_unpermute_bwd(const moe_shape* shape, const void* dx_perm, const int32_t* row_of,
                       const float* dx_router, const void* dx_shared, void* dx, hipStream_t stream);
 

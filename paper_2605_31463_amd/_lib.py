@@ -67,7 +67,8 @@ _VP = ctypes.c_void_p
 class moe_params(ctypes.Structure):
     _fields_ = [(n, _VP) for n in ("w_r", "router_bias", "w_gate", "w_up", "w_down", "b_gate",
                                    "b_up", "b_down", "ws_gate", "ws_up", "ws_down", "aux_f",
-                                   "zc_v", "zc_wc", "gate_threshold", "fp8_cache")]
+                                   "zc_v", "zc_wc", "gate_threshold", "fp8_cache")] + \
+                [("fp8_cache_bytes", ctypes.c_size_t)]
 
 
 class moe_saved(ctypes.Structure):
@@ -277,7 +278,10 @@ def moe_shared_expert_bwd(shape, x, dy, gu_sh, h_sh, ws_gate, ws_up, ws_down, dx
 
 
 def _struct(cls, tensors):
-    return cls(**{n: P(t) for n, t in tensors.items() if n in dict(cls._fields_)})
+    """Pointer fields from tensors (or None); size fields from ints."""
+    f = dict(cls._fields_)
+    return cls(**{n: ((0 if t is None else int(t)) if f[n] is ctypes.c_size_t else P(t))
+                  for n, t in tensors.items() if n in f})
 
 
 def moe_layer_fwd(shape, params, x, saved, y, ws, stream=None):

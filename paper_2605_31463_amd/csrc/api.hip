@@ -79,7 +79,9 @@ const char* kernel_name(int id) {
       "wr_transpose", "route_dx", "gemm_down_dgrad", "gemm_gateup_dgrad", "gemm_down_wgrad",
       "gemm_gateup_wgrad", "unpermute", "rank", "wr_split", "route_select", "aux_stats", "aux_grad",
       "aux_dwr", "zc_param_partial", "zc_param_reduce", "threshold_grad", "aux_partial_rows", "quant_rows",
-      "weight_quant"};
+      "weight_quant", "gemm_shared_gateup_fwd", "gemm_shared_down_fwd", "gemm_shared_down_dgrad",
+      "gemm_shared_gateup_dgrad", "gemm_shared_down_wgrad", "gemm_shared_gateup_wgrad", "gemm_aux_dx",
+      "gemm_aux_dwr"};
   if (id < 0 || id >= K_NUM_KERNELS) return nullptr;
   return names[id];
 }
@@ -156,6 +158,22 @@ int check_shape(const moe_shape* sh) {
   if (s.d > 16384) return moe_set_error(MOE_ERR_UNSUPPORTED, "d above 16384");
   if (s.T * s.k >= (int64_t)1 << 31 || s.T * s.d >= (int64_t)1 << 40)
     return moe_set_error(MOE_ERR_UNSUPPORTED, "T too large");
+  {
+    // operands staged through 32-bit buffer descriptors (the GEMMs' per-expert
+    // activations and weights, the router's x, the dense passes) stay below 4 GiB
+    const int64_t eb = s.dtype == MOE_BF16 ? 2 : 4;
+    const int64_t R = s.T * s.k, lim = (int64_t)1 << 32;
+    const int64_t wmax = s.d > 2 * s.f ? s.d : 2 * s.f;
+    const int64_t shw = s.n_shared ? (s.d > 2 * s.f_shared ? s.d : 2 * s.f_shared) : 0;
+    const int64_t Ep = epool(s), Epad = (Ep + 63) / 64 * 64;
+    const int64_t big[4] = {R * wmax * eb, s.T * shw * eb, s.d * 2 * s.f * eb,
+                            s.aux_coef > 0.f ? s.T * (Epad > s.d ? Epad : s.d) * eb : 0};
+    for (int64_t b : big)
+      if (b >= lim)
+        return moe_set_error(MOE_ERR_UNSUPPORTED,
+                             "an operand of %lld bytes exceeds the 4 GiB reach of the kernels' buffer descriptors",
+                             (long long)b);
+  }
   if (s.router == MOE_ROUTER_SIGMOID_GROUPED && s.n_groups > 1) {
     const int64_t epl = (s.E + 63) / 64, gs = s.E / s.n_groups;
     const int64_t lpg = gs / epl;
@@ -312,7 +330,10 @@ CachePlan cache_plan(const moe_shape& s) {
 }
 
 GemmArgs gemm_dense(const moe_shape& s, int mode) {
+  static const int kid[6] = {K_GEMM_SH_GATEUP_FWD, K_GEMM_SH_DOWN_FWD, K_GEMM_SH_DOWN_DGRAD,
+                             K_GEMM_SH_GATEUP_DGRAD, K_GEMM_SH_DOWN_WGRAD, K_GEMM_SH_GATEUP_WGRAD};
   GemmArgs g = gemm_base(s, mode, nullptr);
+  g.kid = kid[mode];
   g.ngroups = 1;
   g.dense_rows = s.T;
   g.max_rows = s.T;
@@ -614,23 +635,36 @@ static_assert(sizeof(moe_shape) == 128 && offsetof(moe_shape, f_shared) == 56 &&
                   offsetof(moe_shape, aux_coef) == 88 && offsetof(moe_shape, zc_aux_weight) == 104 &&
                   offsetof(moe_shape, act_limit) == 116 && offsetof(moe_shape, fp8) == 120,
               "moe_shape layout");
-static_assert(sizeof(moe_params) == 16 * sizeof(void*) && sizeof(moe_saved) == 15 * sizeof(void*) &&
+static_assert(sizeof(moe_params) == 17 * sizeof(void*) && offsetof(moe_params, fp8_cache_bytes) == 128 &&
+                  sizeof(moe_saved) == 15 * sizeof(void*) &&
                   sizeof(moe_grads) == 13 * sizeof(void*),
               "pointer struct layouts");
 
 // ---------------------------------------------------------------------------
 // exported entry points
 // ---------------------------------------------------------------------------
+namespace {
+// The FP8 weight cache must hold the regions the shape's fp8 level reads.
+int check_fp8_cache(const moe_shape& s, const moe_params* prm) {
+  const size_t need = cache_plan(s).total;
+  if (prm->fp8_cache_bytes < need)
+    return moe_set_error(MOE_ERR_WORKSPACE, "params.fp8_cache_bytes %zu, the shape's cache needs %zu",
+                         prm->fp8_cache_bytes, need);
+  return MOE_OK;
+}
+
 // Argument checks of the layer backward; `phase` bit 1: input-gradient half,
 // bit 2: weight-gradient half.
-namespace {
 int check_layer_bwd(const moe_shape& s, const moe_params* prm, const void* x, const moe_saved* sv, const void* dy,
                     const void* dx, const moe_grads* gr, int phase) {
   MOE_NEED(prm, "params");
   MOE_NEED(sv, "saved");
   MOE_NEED(prm->w_r, "params.w_r");
   MOE_NEED(sv->expert_offsets, "saved.expert_offsets");
-  if (s.fp8 == 2 && (phase & 1)) MOE_NEED(prm->fp8_cache, "params.fp8_cache");
+  if (s.fp8 == 2 && (phase & 1)) {
+    MOE_NEED(prm->fp8_cache, "params.fp8_cache");
+    MOE_TRY(check_fp8_cache(s, prm));
+  }
   if (s.n_const > 0 && (phase & 1)) {
     MOE_NEED(prm->zc_v, "params.zc_v");
     MOE_NEED(prm->zc_wc, "params.zc_wc");
@@ -758,6 +792,7 @@ int layer_bwd_dgrad(const moe_shape& s, const moe_params* prm, const void* x, co
     g.a = aux_dl;
     g.w0 = w_rt;
     g.c0 = aux_dx;
+    g.kid = K_GEMM_AUX_DX;
     MOE_TRY(launch_gemm(g, stream));
   }
   // 4. shared expert input gradient
@@ -823,6 +858,7 @@ int layer_bwd_wgrad(const moe_shape& s, const moe_params* prm, const void* x, co
     g.a = x;
     g.b = wsp(ws, p.aux_dl);
     g.c0 = part;
+    g.kid = K_GEMM_AUX_DWR;
     MOE_TRY(launch_gemm(g, stream));
     MOE_TRY(launch_aux_dwr(part, G, (int)s.d, (int)epool(s), E_pad, s.dtype == MOE_BF16, gr->dw_r, stream));
   }
@@ -1240,7 +1276,10 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, 
     MOE_NEED(prm->zc_wc, "params.zc_wc");
   }
   if (is_thr(s)) MOE_NEED(prm->gate_threshold, "params.gate_threshold");
-  if (s.fp8) MOE_NEED(prm->fp8_cache, "params.fp8_cache");
+  if (s.fp8) {
+    MOE_NEED(prm->fp8_cache, "params.fp8_cache");
+    MOE_TRY(check_fp8_cache(s, prm));
+  }
   MOE_TRY(check_ws(ws, ws_bytes, plan(s).fwd_total));
   const void* bg = s.expert_bias ? prm->b_gate : nullptr;
   const void* bu = s.expert_bias ? prm->b_up : nullptr;

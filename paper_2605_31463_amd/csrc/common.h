@@ -41,6 +41,16 @@ enum KernelId {
   K_AUX_PARTIAL_ROWS,
   K_QUANT_ROWS,
   K_WEIGHT_QUANT,
+  // the shared expert's dense passes (same kernels as the routed passes)
+  K_GEMM_SH_GATEUP_FWD,
+  K_GEMM_SH_DOWN_FWD,
+  K_GEMM_SH_DOWN_DGRAD,
+  K_GEMM_SH_GATEUP_DGRAD,
+  K_GEMM_SH_DOWN_WGRAD,
+  K_GEMM_SH_GATEUP_WGRAD,
+  // the auxiliary loss's router products (dense dx, chunked dW_r)
+  K_GEMM_AUX_DX,
+  K_GEMM_AUX_DWR,
   K_NUM_KERNELS
 };
 

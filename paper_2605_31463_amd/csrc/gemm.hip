@@ -2,28 +2,35 @@
 // forward down, the down data-gradient with the fused SwiGLU backward, the
 // gate/up data-gradient, and both weight gradients (section 3.2: fused SwiGLU
 // forward and backward kernels; wgrad kept as a separate pass so that it can
-// be delayed).
+// be delayed).  The same kernels run the shared expert's dense passes.
 //
-// bf16 path (MFMA): one 256-thread workgroup computes a 128x128 output tile
-// with 4 wavefronts in a 2x2 arrangement (64x64 each, 4x4 blocks of
-// v_mfma_f32_16x16x32_bf16, float32 accumulators).  K advances 64 at a time
-// through two LDS stages filled by buffer_load ... lds (global -> LDS without
-// registers); the next stage's copy runs while the current one is
-// multiplied.  Operands contiguous along K are read with ds_read_b128,
-// operands contiguous along M or N (the weights in the forward, both
-// operands of the weight gradients) with the transposing ds_read_b64_tr_b16,
-// so no operand is ever transposed in registers.
+// bf16 path (MFMA): one persistent kernel, gemm_bf16_persistent, with one
+// workgroup per CU (two for the 128 x 128 tiles).  A workgroup of 8
+// wavefronts computes 256 x 256 output tiles (2 x 4 or 4 x 2 wavefronts, each
+// a 128 x 64 or 64 x 128 block of v_mfma_f32_32x32x16_bf16 32 x 32 products
+// with float32 accumulators); experts with fewer than 192 rows on average use
+// 128 x 128 tiles of 4 wavefronts.  K advances through 2 LDS stages of 64 k
+// (4 of 32 k in the weight gradients) filled by buffer_load ... lds (global ->
+// LDS without registers); the copies of the next stages are in flight while
+// the current one is multiplied, also across tile boundaries.  Operands
+// contiguous along K are read with ds_read_b128, operands contiguous along M
+// or N (the weights in the forward, both operands of the weight gradients)
+// with the transposing ds_read_b64_tr_b16, so no operand is ever transposed
+// in registers or in HBM.
 //
-// Scheduling happens on the device from expert_offsets: a block derives the
-// per-expert m-tile prefix in LDS and finds its (expert, m-tile, n-tile), so
-// variable per-expert row counts need no host synchronisation; blocks beyond
-// the real tile count exit.  Buffer descriptors bound each operand to its
+// Scheduling happens on the device from expert_offsets: every workgroup
+// counts the row tiles of each expert (a block scan), the tiles are numbered
+// expert by expert, each XCD owns a contiguous range of tile ids and its
+// workgroups take them round-robin, so variable per-expert row counts need
+// no host synchronisation.  Buffer descriptors bound each operand to its
 // expert's rows, so rows past an expert's end (and, for the weight gradients,
 // whose K is the expert's row count, k past the end) read as zero; outputs
-// past M or N are not stored.  Block ids are remapped so that each XCD works
-// on a contiguous range of tiles.
+// past M or N are not stored.  The epilogue is wavefront-local (each 32 x 32
+// block staged through a private LDS slot, written as 64-byte row pieces).
 //
-// fp32 path: a plain kernel, one thread per output (or output pair), for the
+// FP8: E4M3 instantiations of the forward and data-gradient passes
+// (v_mfma_f32_32x32x64_f8f6f4, quantisation scales folded into the
+// epilogues).  fp32 path: a plain kernel, one thread per output, for the
 // fp32 workload; same modes, same epilogues.
 #include <algorithm>
 #include <type_traits>
@@ -163,67 +170,6 @@ __host__ __device__ inline int n_tiles(int d, int f) {
 }
 template <int MODE>
 __host__ __device__ inline int wgrad_m(int d, int f) { return MODE == G_WGRAD_DOWN ? f : d; }
-
-template <int MODE, int BM, int BN>
-__device__ __forceinline__ Tile decode_tile(const GemmArgs& a, int* pre, int* sbuf) {
-  Tile t;
-  const int nt = n_tiles<MODE, BN>(a.d, a.f);
-  if (is_wgrad<MODE>() || !a.offsets) {
-    // exact grid: every block holds a tile
-    const int lin = xcd_remap(blockIdx.x, gridDim.x);
-    if (!is_wgrad<MODE>()) {
-      const int mt = lin / nt;
-      t.n0 = (lin - mt * nt) * tile_cols<MODE, BN>();
-      t.g = 0;
-      t.row_base = 0;
-      t.rows = (int)a.dense_rows;
-      t.m0 = mt * BM;
-      t.live = t.m0 < t.rows;
-      return t;
-    }
-    const int mt = (wgrad_m<MODE>(a.d, a.f) + BM - 1) / BM;
-    t.g = lin / (mt * nt);
-    const int rem = lin - t.g * mt * nt;
-    const int im = rem / nt;
-    t.m0 = im * BM;
-    t.n0 = (rem - im * nt) * BN;
-    if (a.offsets) {
-      t.row_base = a.offsets[t.g];
-      t.rows = a.offsets[t.g + 1] - t.row_base;
-    } else {
-      t.row_base = 0;
-      t.rows = (int)a.dense_rows;
-    }
-    t.live = t.g < (a.offsets ? a.ngroups : 1);
-    return t;
-  }
-  // variable rows per expert: the grid is an upper bound, so the live tiles
-  // are counted first and the XCD-contiguous remap runs over them alone
-  // (remapping the whole grid would leave the live tiles on a few XCDs).
-  const int G = a.ngroups;
-  int c = 0;
-  if ((int)threadIdx.x < G) c = (a.offsets[threadIdx.x + 1] - a.offsets[threadIdx.x] + BM - 1) / BM;
-  __shared__ int total;
-  const int ex = block_scan_256(c, sbuf, &total);
-  if ((int)threadIdx.x < G) pre[threadIdx.x] = ex;
-  __syncthreads();
-  const int live_tiles = total * nt;
-  t.live = (int)blockIdx.x < live_tiles;
-  if (!t.live) return t;
-  const int lin = xcd_remap(blockIdx.x, live_tiles);
-  const int mt = lin / nt;
-  t.n0 = (lin - mt * nt) * tile_cols<MODE, BN>();
-  int lo = 0, hi = G - 1;  // last g with pre[g] <= mt (empty experts share a prefix: take the last)
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (pre[mid] <= mt) lo = mid; else hi = mid - 1;
-  }
-  t.g = lo;
-  t.row_base = a.offsets[lo];
-  t.rows = a.offsets[lo + 1] - t.row_base;
-  t.m0 = (mt - pre[lo]) * BM;
-  return t;
-}
 
 // ---------------------------------------------------------------------------
 // bf16 operand staging.
@@ -380,402 +326,6 @@ __device__ __forceinline__ bf16x8 frag_mn(const bf16_t* tile, int cb, int ks, in
   const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4_t)(tile + mn_off<BK>(k, col)));
   const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4_t)(tile + mn_off<BK>(k + 4, col)));
   return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-}
-
-// ---------------------------------------------------------------------------
-// The bf16 MFMA kernel: BM x BN output tile, WM x WN wavefronts, each
-// BM/WM x BN/WN as blocks of v_mfma_f32_32x32x16_bf16, S-stage LDS pipeline.
-// ---------------------------------------------------------------------------
-template <int MODE, class C>
-__global__ __launch_bounds__(C::NT, 1) void gemm_bf16_kernel(GemmArgs a) {
-  constexpr bool wgrad = is_wgrad<MODE>();
-  constexpr bool a_mn = wgrad;                                               // A tile MN-contiguous
-  constexpr bool b_mn = MODE == G_FWD_GATEUP || MODE == G_FWD_DOWN || wgrad;  // B tile MN-contiguous
-  constexpr int BM = C::BM, BN = C::BN, MI = C::MI, NI = C::NI, S = C::S, NW = C::NW, BK = C::BK;
-  static_assert(MODE != G_FWD_GATEUP || NI % 2 == 0, "gate/up pairs need an even number of column blocks");
-  __shared__ __align__(16) bf16_t lds[S][C::STAGE_ELEMS];
-  __shared__ int pre[257];
-  __shared__ int sbuf[256];
-
-  const Tile tl = decode_tile<MODE, BM, BN>(a, pre, sbuf);
-  if (!tl.live) return;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave / C::WN, wn = wave % C::WN;
-  const int d = a.d, f = a.f;
-  const int g = tl.g;
-  const int l32 = lane & 31;
-
-  int K, M, N;
-  if (MODE == G_FWD_GATEUP) { K = d; M = tl.rows; N = f; }
-  else if (MODE == G_FWD_DOWN) { K = f; M = tl.rows; N = d; }
-  else if (MODE == G_DGRAD_DOWN) { K = d; M = tl.rows; N = f; }
-  else if (MODE == G_DGRAD_GATEUP) { K = 2 * f; M = tl.rows; N = d; }
-  else if (MODE == G_WGRAD_DOWN) { K = tl.rows; M = f; N = d; }
-  else { K = tl.rows; M = d; N = 2 * f; }
-
-  const bf16_t* A = reinterpret_cast<const bf16_t*>(a.a);
-  const bf16_t* Bact = reinterpret_cast<const bf16_t*>(a.b);
-  const bf16_t* W0 = reinterpret_cast<const bf16_t*>(a.w0);
-  const bf16_t* W1 = reinterpret_cast<const bf16_t*>(a.w1);
-
-  // ---- operand A (BM rows of the output)
-  KOperand<BM, NW, BK> ka;
-  MNOperand<BM / 64, NW, BK> ma;
-  int64_t a_kstride;  // soffset = k0 * a_kstride
-  if (!a_mn) {
-    const int lda = MODE == G_FWD_DOWN ? f : (MODE == G_DGRAD_GATEUP ? 2 * f : d);
-    ka.rsrc = make_rsrc(A + (int64_t)tl.row_base * lda, (int64_t)M * lda * 2);
-    ka.init(wave, lane, tl.m0, lda);
-    a_kstride = 2;
-  } else {
-    const int lda = MODE == G_WGRAD_DOWN ? f : d;  // h rows [f] or x_perm rows [d]
-    const int32x4_t r = make_rsrc(A + (int64_t)tl.row_base * lda, (int64_t)K * lda * 2);
-    int32x4_t src[BM / 64];
-    int col0[BM / 64];
-#pragma unroll
-    for (int s2 = 0; s2 < BM / 64; ++s2) {
-      src[s2] = r;
-      col0[s2] = tl.m0 + 64 * s2;
-    }
-    ma.init(wave, lane, src, col0, lda);
-    a_kstride = (int64_t)lda * 2;
-  }
-  // ---- operand B (BN columns of the output)
-  KOperand<BN, NW, BK> kb;
-  MNOperand<BN / 64, NW, BK> mb;
-  int64_t b_kstride;
-  int32x4_t b_up = make_rsrc(W0, 0);  // DGRAD_GATEUP: W_up rows for k >= f
-  if (MODE == G_FWD_GATEUP) {  // sub-tiles 0 .. BN/128-1: W_gate columns, then W_up columns
-    const int32x4_t rg = make_rsrc(W0 + (int64_t)g * d * f, (int64_t)d * f * 2);
-    const int32x4_t ru = make_rsrc(W1 + (int64_t)g * d * f, (int64_t)d * f * 2);
-    int32x4_t src[BN / 64];
-    int col0[BN / 64];
-#pragma unroll
-    for (int s2 = 0; s2 < BN / 64; ++s2) {
-      const bool up = s2 >= BN / 128;
-      src[s2] = up ? ru : rg;
-      col0[s2] = tl.n0 + 64 * (up ? s2 - BN / 128 : s2);
-    }
-    mb.init(wave, lane, src, col0, f);
-    b_kstride = (int64_t)f * 2;
-  } else if (MODE == G_FWD_DOWN) {
-    const int32x4_t r = make_rsrc(W0 + (int64_t)g * f * d, (int64_t)f * d * 2);
-    int32x4_t src[BN / 64];
-    int col0[BN / 64];
-#pragma unroll
-    for (int s2 = 0; s2 < BN / 64; ++s2) {
-      src[s2] = r;
-      col0[s2] = tl.n0 + 64 * s2;
-    }
-    mb.init(wave, lane, src, col0, d);
-    b_kstride = (int64_t)d * 2;
-  } else if (MODE == G_DGRAD_DOWN) {  // B[k=i][n=j] = W_down[g][j][i]: rows j of length d
-    kb.rsrc = make_rsrc(W0 + (int64_t)g * f * d, (int64_t)f * d * 2);
-    kb.init(wave, lane, tl.n0, d);
-    b_kstride = 2;
-  } else if (MODE == G_DGRAD_GATEUP) {  // B[k=j][n=i] = W_gate[g][i][j] (k < f), W_up[g][i][j-f]
-    kb.rsrc = make_rsrc(W0 + (int64_t)g * d * f, (int64_t)d * f * 2);
-    b_up = make_rsrc(W1 + (int64_t)g * d * f, (int64_t)d * f * 2);
-    kb.init(wave, lane, tl.n0, f);
-    b_kstride = 2;
-  } else {
-    const int ldb = MODE == G_WGRAD_DOWN ? d : 2 * f;  // d_o rows or dgu rows
-    const int32x4_t r = make_rsrc(Bact + (int64_t)tl.row_base * ldb, (int64_t)K * ldb * 2);
-    int32x4_t src[BN / 64];
-    int col0[BN / 64];
-#pragma unroll
-    for (int s2 = 0; s2 < BN / 64; ++s2) {
-      src[s2] = r;
-      col0[s2] = tl.n0 + 64 * s2;
-    }
-    mb.init(wave, lane, src, col0, ldb);
-    b_kstride = (int64_t)ldb * 2;
-  }
-  // DMA instructions per thread per stage
-  constexpr int NL = (BM + BN) * BK * 2 / 1024 / NW;
-
-  floatx16 acc[MI][NI];
-#pragma unroll
-  for (int i = 0; i < MI; ++i)
-#pragma unroll
-    for (int j = 0; j < NI; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-  // bias-gradient column sums (weight-gradient passes, first m-tile, wm == 0)
-  const bool colsum = wgrad && a.db0 && tl.m0 == 0 && wm == 0;
-  float bsum[NI];
-#pragma unroll
-  for (int j = 0; j < NI; ++j) bsum[j] = 0.f;
-
-  const uint32_t lds0 = lds_addr(&lds[0][0]);
-  auto issue_tile = [&](int k0, int buf) {
-    const uint32_t As = lds0 + buf * (C::STAGE_ELEMS * 2);
-    const uint32_t Bs = As + C::A_ELEMS * 2;
-    if (!a_mn) ka.issue(As, wave, (uint32_t)(k0 * a_kstride));
-    else ma.issue(As, wave, (uint32_t)(k0 * a_kstride));
-    if (MODE == G_DGRAD_GATEUP) {
-      KOperand<BN, NW, BK> kk = kb;
-      if (k0 >= f) kk.rsrc = b_up;
-      kk.issue(Bs, wave, (uint32_t)((k0 >= f ? k0 - f : k0) * b_kstride));
-    } else if (MODE == G_DGRAD_DOWN) {
-      kb.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
-    } else {
-      mb.issue(Bs, wave, (uint32_t)(k0 * b_kstride));
-    }
-  };
-  // tile-local 32-column block of this wave's fragment j (FWD_GATEUP: first
-  // half gate columns, second half the matching up columns)
-  auto bcol = [&](int j) {
-    if (MODE == G_FWD_GATEUP)
-      return (j < NI / 2) ? (wn * (NI / 2) + j) : (BN / 64 + wn * (NI / 2) + (j - NI / 2));
-    return wn * NI + j;
-  };
-
-  const int nk = (K + BK - 1) / BK;
-  const bool wave_rows = tl.m0 + wm * C::TM < M;
-#pragma unroll
-  for (int p = 0; p < S - 1; ++p)
-    if (p < nk) issue_tile(p * BK, p);
-  for (int kt = 0; kt < nk; ++kt) {
-    // stages issued after kt that may still be in flight
-    const int ahead = min(S - 2, nk - 1 - kt);
-    if (S >= 5 && ahead >= 3) wait_vmcnt<(S >= 5 ? 3 : 0) * NL>();
-    else if (S >= 4 && ahead >= 2) wait_vmcnt<(S >= 4 ? 2 : 0) * NL>();
-    else if (S >= 3 && ahead >= 1) wait_vmcnt<(S >= 3 ? 1 : 0) * NL>();
-    else wait_vmcnt<0>();
-    __syncthreads();
-    if (kt + S - 1 < nk) issue_tile((kt + S - 1) * BK, (kt + S - 1) % S);
-    const bf16_t* As = lds[kt % S];
-    const bf16_t* Bs = As + C::A_ELEMS;
-    // fragments double-buffered in registers: step ks+1 is read while the
-    // MFMAs of step ks run (the scheduling barriers keep that order)
-    bf16x8 af[2][MI], bfr[2][NI];
-    auto load_frags = [&](int ks, int slot) {
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-        af[slot][i] = a_mn ? frag_mn<BK>(As, wm * MI + i, ks, lane) : frag_k<BK>(As, wm * MI + i, ks, lane);
-#pragma unroll
-      for (int j = 0; j < NI; ++j)
-        bfr[slot][j] = b_mn ? frag_mn<BK>(Bs, bcol(j), ks, lane) : frag_k<BK>(Bs, bcol(j), ks, lane);
-    };
-    constexpr int KS = BK / 16;  // MFMA k-steps per stage
-    // a wavefront whose output rows all lie past the expert's last row
-    // (the ragged last tile of an expert) has nothing to multiply; its
-    // SIMD partner then has the matrix pipe to itself
-    if (!wave_rows) continue;
-    load_frags(0, 0);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int cur = ks & 1;
-      if (ks < KS - 1) load_frags(ks + 1, cur ^ 1);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[cur][j], af[cur][i], acc[i][j], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      if (colsum) {
-#pragma unroll
-        for (int j = 0; j < NI; ++j) {
-          const uint4 u = __builtin_bit_cast(uint4, bfr[cur][j]);
-          const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            bsum[j] += __uint_as_float(w4[q] << 16) + __uint_as_float(w4[q] & 0xffff0000u);
-        }
-      }
-    }
-  }
-
-  // ---- epilogue.  With the operands swapped in the MFMA, block (i, j) holds
-  // the transposed product: lane l has output row 32i + l%32 and, in register
-  // v = 4q + t, column 32j + 8q + 4(l/32) + t.  Each lane applies the fused
-  // epilogue math to its values, writes them (bf16, 4 columns = 8 bytes at a
-  // time) into its wavefront's LDS staging area, and the wavefront then
-  // writes whole rows to global memory with 16-byte stores.
-  __syncthreads();  // every wavefront is done with the LDS stages
-  constexpr int TN_OUT = MODE == G_FWD_GATEUP ? C::TN / 2 : C::TN;  // columns per output matrix
-  constexpr int CPR = TN_OUT / 8;                                    // 16-byte chunks per row
-  static_assert(C::NW * C::TM * TN_OUT * 2 * (MODE == G_FWD_GATEUP ? 2 : 1) <= C::LDS_BYTES, "staging fits");
-  const int lrow = lane & 31, hh = lane >> 5;
-  bf16_t* stg = &lds[0][0] + wave * (C::TM * TN_OUT * (MODE == G_FWD_GATEUP ? 2 : 1));
-  // staging layout [TM][TN_OUT], 16-byte chunk index XOR-swizzled by row & 7
-  auto st_off = [&](int r, int c) { return r * TN_OUT + ((((c >> 3) ^ (r & 7)) % CPR) << 3) + (c & 7); };
-  auto put4 = [&](bf16_t* base, int r, int c, float v0, float v1, float v2, float v3) {
-    const uint32_t lo = (uint32_t)f2bf(v0) | ((uint32_t)f2bf(v1) << 16);
-    const uint32_t hi = (uint32_t)f2bf(v2) | ((uint32_t)f2bf(v3) << 16);
-    *reinterpret_cast<uint2*>(base + st_off(r, c)) = make_uint2(lo, hi);
-  };
-  // write the staged [TM][TN_OUT] tile: row r -> dst_row(r) (or skip), column c -> dst_col(c)
-  auto flush = [&](const bf16_t* base, auto&& dst) {
-    __syncthreads();
-#pragma unroll 4
-    for (int idx = lane; idx < C::TM * CPR; idx += 64) {
-      const int r = idx / CPR, c = (idx % CPR) * 8;
-      const uint4 v = *reinterpret_cast<const uint4*>(base + st_off(r, c));
-      bf16_t* p = dst(r, c);
-      if (p) *reinterpret_cast<uint4*>(p) = v;
-    }
-  };
-  const int mrow0 = tl.m0 + wm * C::TM;  // first output row of this wavefront
-  if (MODE == G_FWD_GATEUP) {
-    bf16_t* gu = reinterpret_cast<bf16_t*>(a.c0);
-    bf16_t* h = reinterpret_cast<bf16_t*>(a.c1);
-    const bf16_t* bgp = reinterpret_cast<const bf16_t*>(a.bias0);
-    const bf16_t* bup = reinterpret_cast<const bf16_t*>(a.bias1);
-    bf16_t* sg = stg;                          // [TM][TN_OUT] gate, then up at + TM*TN_OUT
-    const int jbase = tl.n0 + wn * TN_OUT;     // first j of this wavefront
-#pragma unroll
-    for (int j = 0; j < NI / 2; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int c = 32 * j + 8 * q + 4 * hh;   // local column of values t = 0..3
-        float bgv[4] = {0.f, 0.f, 0.f, 0.f}, buv[4] = {0.f, 0.f, 0.f, 0.f};
-        if (bgp && jbase + c < N) {
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            bgv[t] = bf2f(bgp[(int64_t)g * f + jbase + c + t]);
-            buv[t] = bf2f(bup[(int64_t)g * f + jbase + c + t]);
-          }
-        }
-#pragma unroll
-        for (int i = 0; i < MI; ++i) {
-          const int r = 32 * i + lrow;
-          float gv[4], uv[4];
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            gv[t] = acc[i][j][4 * q + t] + bgv[t];
-            uv[t] = acc[i][j + NI / 2][4 * q + t] + buv[t];
-          }
-          put4(sg, r, c, act_store_g(a, gv[0]), act_store_g(a, gv[1]), act_store_g(a, gv[2]), act_store_g(a, gv[3]));
-          put4(sg + C::TM * TN_OUT, r, c, act_store_u(a, uv[0]), act_store_u(a, uv[1]), act_store_u(a, uv[2]),
-               act_store_u(a, uv[3]));
-          // h overwrites the accumulators of the gate block (already staged)
-#pragma unroll
-          for (int t = 0; t < 4; ++t) acc[i][j][4 * q + t] = act_h(a, gv[t], uv[t]);
-        }
-      }
-    auto dst_gu = [&](int half) {
-      return [&, half](int r, int c) -> bf16_t* {
-        const int m = mrow0 + r, jj = jbase + c;
-        if (m >= M || jj >= N) return nullptr;
-        return gu + (int64_t)(tl.row_base + m) * 2 * f + half * f + jj;
-      };
-    };
-    flush(sg, dst_gu(0));
-    flush(sg + C::TM * TN_OUT, dst_gu(1));
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < NI / 2; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-          put4(sg, 32 * i + lrow, 32 * j + 8 * q + 4 * hh, acc[i][j][4 * q], acc[i][j][4 * q + 1],
-               acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-    flush(sg, [&](int r, int c) -> bf16_t* {
-      const int m = mrow0 + r, jj = jbase + c;
-      if (m >= M || jj >= N) return nullptr;
-      return h + (int64_t)(tl.row_base + m) * f + jj;
-    });
-  } else if (MODE == G_FWD_DOWN || MODE == G_DGRAD_GATEUP || MODE == G_DGRAD_DOWN) {
-    const int nbase = tl.n0 + wn * C::TN;
-    const bf16_t* bdp = MODE == G_FWD_DOWN ? reinterpret_cast<const bf16_t*>(a.bias0) : nullptr;
-    const bf16_t* gu = reinterpret_cast<const bf16_t*>(a.aux);
-    bf16_t* out = reinterpret_cast<bf16_t*>(a.c0);
-    // DGRAD_DOWN writes dg then du (two staged passes); the others one
-    constexpr int PASSES = MODE == G_DGRAD_DOWN ? 2 : 1;
-#pragma unroll
-    for (int pass = 0; pass < PASSES; ++pass) {
-      if (pass) __syncthreads();
-#pragma unroll
-      for (int j = 0; j < NI; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int c = 32 * j + 8 * q + 4 * hh;
-          const bool cok = nbase + c < N;
-          float bd[4] = {0.f, 0.f, 0.f, 0.f};
-          if (bdp && cok) {
-#pragma unroll
-            for (int t = 0; t < 4; ++t) bd[t] = bf2f(bdp[(int64_t)g * d + nbase + c + t]);
-          }
-#pragma unroll
-          for (int i = 0; i < MI; ++i) {
-            const int r = 32 * i + lrow;
-            float o[4];
-#pragma unroll
-            for (int t = 0; t < 4; ++t) o[t] = acc[i][j][4 * q + t] + bd[t];
-            if (MODE == G_DGRAD_DOWN) {
-              const int m = mrow0 + r;
-              float gv[4] = {0.f, 0.f, 0.f, 0.f}, uv[4] = {0.f, 0.f, 0.f, 0.f};
-              if (m < M && cok) {
-                const int64_t row = tl.row_base + m;
-                const uint2 gr = *reinterpret_cast<const uint2*>(gu + row * 2 * f + nbase + c);
-                const uint2 ur = *reinterpret_cast<const uint2*>(gu + row * 2 * f + f + nbase + c);
-                gv[0] = __uint_as_float(gr.x << 16); gv[1] = __uint_as_float(gr.x & 0xffff0000u);
-                gv[2] = __uint_as_float(gr.y << 16); gv[3] = __uint_as_float(gr.y & 0xffff0000u);
-                uv[0] = __uint_as_float(ur.x << 16); uv[1] = __uint_as_float(ur.x & 0xffff0000u);
-                uv[2] = __uint_as_float(ur.y << 16); uv[3] = __uint_as_float(ur.y & 0xffff0000u);
-              }
-#pragma unroll
-              for (int t = 0; t < 4; ++t) {
-                float dg, du;
-                act_grad(a, gv[t], uv[t], o[t], dg, du);
-                o[t] = pass == 0 ? dg : du;
-              }
-            }
-            put4(stg, r, c, o[0], o[1], o[2], o[3]);
-          }
-        }
-      flush(stg, [&](int r, int c) -> bf16_t* {
-        const int m = mrow0 + r, n = nbase + c;
-        if (m >= M || n >= N) return nullptr;
-        if (MODE == G_DGRAD_DOWN) return out + (int64_t)(tl.row_base + m) * 2 * f + pass * f + n;
-        return out + (int64_t)(tl.row_base + m) * N + n;
-      });
-    }
-  } else {
-    // weight gradients of expert g: [M][N] at c0 (+ c1 for the up half)
-    const int nbase = tl.n0 + wn * C::TN;
-    bf16_t* c0 = reinterpret_cast<bf16_t*>(a.c0);
-    bf16_t* c1 = reinterpret_cast<bf16_t*>(a.c1);
-#pragma unroll
-    for (int j = 0; j < NI; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-          put4(stg, 32 * i + lrow, 32 * j + 8 * q + 4 * hh, acc[i][j][4 * q], acc[i][j][4 * q + 1],
-               acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-    flush(stg, [&](int r, int c) -> bf16_t* {
-      const int m = mrow0 + r, n = nbase + c;
-      if (m >= M || n >= N) return nullptr;
-      if (MODE == G_WGRAD_DOWN) return c0 + ((int64_t)g * f + m) * d + n;
-      if (n < f) return c0 + ((int64_t)g * d + m) * f + n;
-      return c1 + ((int64_t)g * d + m) * f + (n - f);
-    });
-    if (colsum) {
-#pragma unroll
-      for (int j = 0; j < NI; ++j) {
-        float v = bsum[j];
-        v += __shfl_xor(v, 32, 64);
-        const int col = tl.n0 + wn * C::TN + j * 32 + l32;
-        if (lane < 32 && col < N) {
-          if (MODE == G_WGRAD_DOWN) {
-            reinterpret_cast<bf16_t*>(a.db0)[(int64_t)g * d + col] = f2bf(v);
-          } else if (col < f) {
-            reinterpret_cast<bf16_t*>(a.db0)[(int64_t)g * f + col] = f2bf(v);
-          } else {
-            reinterpret_cast<bf16_t*>(a.db1)[(int64_t)g * f + col - f] = f2bf(v);
-          }
-        }
-      }
-    }
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1630,6 +1180,10 @@ const int kGemmKernelId[6] = {K_GEMM_GATEUP_FWD, K_GEMM_DOWN_FWD, K_GEMM_DOWN_DG
                               K_GEMM_GATEUP_DGRAD, K_GEMM_DOWN_WGRAD, K_GEMM_GATEUP_WGRAD};
 const char* kGemmName[6] = {"gemm_gateup_fwd", "gemm_down_fwd", "gemm_down_dgrad",
                             "gemm_gateup_dgrad", "gemm_down_wgrad", "gemm_gateup_wgrad"};
+// Timing id of a launch: the caller's (the shared expert's and the auxiliary
+// loss's dense passes have ids of their own), else the routed pass's.
+template <int MODE>
+int gemm_kernel_id(const GemmArgs& a) { return a.kid > 0 ? a.kid : kGemmKernelId[MODE]; }
 
 // Tile shapes per pass, chosen by timing the whole layer at the Qwen3 shape
 // (512 +- 33 rows per expert): 256 x 256 tiles, 8 wavefronts, 2 x 64-k or
@@ -1645,23 +1199,6 @@ template <> struct GemmShape<G_FWD_GATEUP> { using big = CfgWide; };
 template <> struct GemmShape<G_FWD_DOWN> { using big = CfgWide; };
 template <> struct GemmShape<G_DGRAD_DOWN> { using big = CfgTall; };
 template <> struct GemmShape<G_DGRAD_GATEUP> { using big = CfgTall; };
-
-template <int MODE, class C>
-int launch_bf16(const GemmArgs& a, hipStream_t s) {
-  const int G = a.offsets ? a.ngroups : 1;
-  const int nt = n_tiles<MODE, C::BN>(a.d, a.f);
-  int64_t nb;
-  if (is_wgrad<MODE>()) {
-    nb = (int64_t)G * ((wgrad_m<MODE>(a.d, a.f) + C::BM - 1) / C::BM) * nt;
-  } else {
-    const int64_t mt = a.offsets ? (a.max_rows + (int64_t)G * (C::BM - 1)) / C::BM
-                                 : (a.dense_rows + C::BM - 1) / C::BM;
-    nb = mt * nt;
-  }
-  if (nb <= 0) return MOE_OK;
-  return launch(kGemmKernelId[MODE], s, kGemmName[MODE],
-                [&] { gemm_bf16_kernel<MODE, C><<<(int)nb, C::NT, 0, s>>>(a); });
-}
 
 // Persistent launch: one workgroup per CU (a multiple of 8, so that every
 // XCD gets the same number), never more than the tiles' upper bound.
@@ -1694,52 +1231,41 @@ int launch_bf16_persistent(const GemmArgs& a, hipStream_t s) {
   constexpr int kLdsPerBlock = C::LDS_BYTES + C::NW * 2048 + (is_wgrad<MODE>() ? 3 : 2) * 1024 + 64;
   constexpr int kOcc = (160 * 1024) / kLdsPerBlock > 0 ? (160 * 1024) / kLdsPerBlock : 1;
   const int64_t grid = std::min<int64_t>((cu_count() * kOcc / 8) * 8, (nb + 7) / 8 * 8);
-  return launch(kGemmKernelId[MODE], s, kGemmName[MODE],
+  return launch(gemm_kernel_id<MODE>(a), s, kGemmName[MODE],
                 [&] { gemm_bf16_persistent<MODE, C, CL, FP8><<<(int)grid, C::NT, 0, s>>>(a); });
 }
 
-#ifndef MOE_GEMM_PERSISTENT
-#define MOE_GEMM_PERSISTENT 1
-#endif
-
 template <int MODE>
 int launch_mode(const GemmArgs& a, hipStream_t s) {
-  if (a.fp8 && !(a.bf16 && MOE_GEMM_PERSISTENT && !is_wgrad<MODE>()))
+  if (a.fp8 && !(a.bf16 && !is_wgrad<MODE>()))
     return moe_set_error(MOE_ERR_UNSUPPORTED, "gemm: FP8 runs the bf16 forward and data-gradient passes only");
   if (a.accumulate && !is_wgrad<MODE>())
     return moe_set_error(MOE_ERR_INVALID_ARG, "gemm: accumulate applies to the weight-gradient passes only");
-  if (a.bf16 && a.accumulate && !MOE_GEMM_PERSISTENT)
-    return moe_set_error(MOE_ERR_UNSUPPORTED, "gemm: accumulate needs the persistent bf16 kernels");
   if (a.bf16) {
     const int G = a.offsets ? a.ngroups : 1;
     const int64_t rows_per_group = a.offsets ? a.max_rows / G : a.dense_rows;
-    if constexpr (MOE_GEMM_PERSISTENT != 0) {
-      if constexpr (!is_wgrad<MODE>()) {
-        if (a.fp8) {
-          // FP8: 2 x 4 wavefronts in every pass (the data-gradient passes ran
-          // 9% faster than with the bf16 kernels' 4 x 2, Qwen3 shape)
-          if constexpr (MODE == G_FWD_GATEUP || MODE == G_DGRAD_DOWN) {
-            if (a.act == MOE_ACT_CLAMPED_GLU) {
-              if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, true, true>(a, s);
-              return launch_bf16_persistent<MODE, CfgWide, true, true>(a, s);
-            }
+    if constexpr (!is_wgrad<MODE>()) {
+      if (a.fp8) {
+        // FP8: 2 x 4 wavefronts in every pass (the data-gradient passes ran
+        // 9% faster than with the bf16 kernels' 4 x 2, Qwen3 shape)
+        if constexpr (MODE == G_FWD_GATEUP || MODE == G_DGRAD_DOWN) {
+          if (a.act == MOE_ACT_CLAMPED_GLU) {
+            if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, true, true>(a, s);
+            return launch_bf16_persistent<MODE, CfgWide, true, true>(a, s);
           }
-          if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, false, true>(a, s);
-          return launch_bf16_persistent<MODE, CfgWide, false, true>(a, s);
         }
+        if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, false, true>(a, s);
+        return launch_bf16_persistent<MODE, CfgWide, false, true>(a, s);
       }
-      if constexpr (MODE == G_FWD_GATEUP || MODE == G_DGRAD_DOWN) {
-        if (a.act == MOE_ACT_CLAMPED_GLU) {
-          if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, true>(a, s);
-          return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big, true>(a, s);
-        }
-      }
-      if (!is_wgrad<MODE>() && rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall>(a, s);
-      return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big>(a, s);
-    } else {
-      if (!is_wgrad<MODE>() && rows_per_group < 192) return launch_bf16<MODE, CfgSmall>(a, s);
-      return launch_bf16<MODE, typename GemmShape<MODE>::big>(a, s);
     }
+    if constexpr (MODE == G_FWD_GATEUP || MODE == G_DGRAD_DOWN) {
+      if (a.act == MOE_ACT_CLAMPED_GLU) {
+        if (rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall, true>(a, s);
+        return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big, true>(a, s);
+      }
+    }
+    if (!is_wgrad<MODE>() && rows_per_group < 192) return launch_bf16_persistent<MODE, CfgSmall>(a, s);
+    return launch_bf16_persistent<MODE, typename GemmShape<MODE>::big>(a, s);
   }
   constexpr bool wgrad = is_wgrad<MODE>();
   const int G = a.offsets ? a.ngroups : 1;
@@ -1755,7 +1281,7 @@ int launch_mode(const GemmArgs& a, hipStream_t s) {
     nb = mt * ((N + TS - 1) / TS);
   }
   if (nb <= 0) return MOE_OK;
-  return launch(kGemmKernelId[MODE], s, kGemmName[MODE],
+  return launch(gemm_kernel_id<MODE>(a), s, kGemmName[MODE],
                 [&] { gemm_f32_kernel<MODE><<<(int)nb, 256, 0, s>>>(a); });
 }
 

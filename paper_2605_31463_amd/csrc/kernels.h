@@ -251,6 +251,7 @@ struct GemmArgs {
   const float* a_scale;    // [rows]
   const float* b_scale0;   // [E][N] column scales (gate, down, or [gate | up] rows)
   const float* b_scale1;   // [E][f] up column scales
+  int kid;                 // timing id of the launch (0: the routed pass's own)
 };
 int launch_gemm(const GemmArgs& a, hipStream_t s);
 

@@ -62,6 +62,7 @@ class MoELayer:
             self.fp8_cache = torch.empty(max(n, 1), dtype=torch.uint8, device=self.device)
         L.moe_fp8_cache_build(self.shape, params["w_gate"], params["w_up"], params["w_down"], self.fp8_cache, stream)
         params["fp8_cache"] = self.fp8_cache
+        params["fp8_cache_bytes"] = self.fp8_cache.numel()
         return params
 
     def forward(self, params, x, stream=None):

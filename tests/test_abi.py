@@ -128,7 +128,8 @@ def test_shape_struct_layout_matches_header():
     assert L.moe_shape.act_limit.offset == 116
     assert L.moe_shape.fp8.offset == 120
     # pointer structs: one pointer per field, in the header's order
-    assert ctypes.sizeof(L.moe_params) == 16 * 8 and L.moe_params.fp8_cache.offset == 120
+    assert ctypes.sizeof(L.moe_params) == 17 * 8 and L.moe_params.fp8_cache.offset == 120
+    assert L.moe_params.fp8_cache_bytes.offset == 128
     assert ctypes.sizeof(L.moe_saved) == 15 * 8 and L.moe_saved.aux_loss.offset == 112
     assert ctypes.sizeof(L.moe_grads) == 13 * 8 and L.moe_grads.d_threshold.offset == 96
 
@@ -233,6 +234,10 @@ def test_fp8_cache_on_the_host():
     sv = L.moe_saved(**{nm: fake for nm, _ in L.moe_saved._fields_})
     st = L.LIB.moe_layer_fwd(ctypes.byref(s), ctypes.byref(pr), fake, ctypes.byref(sv), fake, fake, 1 << 40, None)
     assert st == L.MOE_ERR_INVALID_ARG and "fp8_cache" in L.last_error()
+    # a cache smaller than the shape's (say, built for another shape) is refused
+    pr = L.moe_params(w_r=fake, w_gate=fake, w_up=fake, w_down=fake, fp8_cache=fake, fp8_cache_bytes=n - 1)
+    st = L.LIB.moe_layer_fwd(ctypes.byref(s), ctypes.byref(pr), fake, ctypes.byref(sv), fake, fake, 1 << 40, None)
+    assert st == L.MOE_ERR_WORKSPACE and "fp8_cache_bytes" in L.last_error()
 
 
 def test_fp8_dgrad_on_the_host():
@@ -254,6 +259,31 @@ def test_fp8_dgrad_on_the_host():
     st = L.LIB.moe_layer_bwd_dgrad(ctypes.byref(s2), ctypes.byref(pr), fake, ctypes.byref(sv), fake, fake,
                                    fake, 1 << 40, None)
     assert st == L.MOE_ERR_INVALID_ARG and "fp8_cache" in L.last_error()
+    # a cache built at fp8 = 1 lacks the row codes fp8 = 2 reads: refused by size
+    pr = L.moe_params(w_r=fake, w_gate=fake, w_up=fake, w_down=fake, fp8_cache=fake, fp8_cache_bytes=n1)
+    st = L.LIB.moe_layer_bwd_dgrad(ctypes.byref(s2), ctypes.byref(pr), fake, ctypes.byref(sv), fake, fake,
+                                   fake, 1 << 40, None)
+    assert st == L.MOE_ERR_WORKSPACE and "fp8_cache_bytes" in L.last_error()
     st = L.LIB.moe_grouped_gemm_bwd(ctypes.byref(s2), L.MOE_DGRAD, fake, fake, fake, fake, fake, fake, fake, fake,
                                     fake, fake, None, None, None, None, None, None, None)
     assert st == L.MOE_ERR_UNSUPPORTED and "FP8" in L.last_error()
+
+
+def test_operands_beyond_the_descriptor_reach_are_refused():
+    """Operands staged through the kernels' 32-bit buffer descriptors must stay
+    below 4 GiB: a shape whose routed rows times the row width reach 2^32
+    bytes (one expert may hold every row), a shared expert whose dense gate/up
+    rows do, or an expert weight that does, is refused before anything runs."""
+    ok = L.make_shape(T=131072, d=8192, E=8, k=1, f=1024, dtype="bf16")          # R d 2 = 2 GiB
+    L.moe_workspace_size(ok)
+    for kw in (dict(T=262144, d=8192, E=8, k=1, f=1024),                          # R d 2 = 4 GiB
+               dict(T=65536, d=4096, E=8, k=8, f=1024),                           # R d 2 = 4 GiB
+               dict(T=16384, d=1024, E=8, k=8, f=8192),                           # R 2f 2 = 4 GiB
+               dict(T=64, d=16384, E=2, k=1, f=65536)):                           # d 2f 2 = 4 GiB
+        with pytest.raises(L.MoeError) as ei:
+            L.moe_workspace_size(L.make_shape(dtype="bf16", **kw))
+        assert ei.value.status == L.MOE_ERR_UNSUPPORTED and "4 GiB" in L.last_error(), kw
+    with pytest.raises(L.MoeError) as ei:
+        L.moe_workspace_size(L.make_shape(T=262144, d=4096, E=8, k=1, f=1024, dtype="bf16",
+                                          n_shared=1, f_shared=4096))             # T 2 fs 2 = 4 GiB
+    assert ei.value.status == L.MOE_ERR_UNSUPPORTED
