@@ -1,14 +1,16 @@
 """Throughput of one MoE layer forward + backward on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload qwen3] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload dsv3] [--no-cpu-baseline]
 
 A step is moe_layer_fwd + moe_layer_bwd over one batch of synthetic input
 already resident in HBM (routing, permutation, grouped SwiGLU expert GEMMs,
 combine, expert dgrad/wgrad, router gradient, unpermute).  Prints one JSON
-line: algorithmic TFLOP/s (value), tokens/s, the dominant kernel against its
-roofline (average launch time from HIP events recorded on the launch stream
-during the timed steps), and the fp64 CPU oracle timed on a bounded sample of
-the same workload on this host.
+line: algorithmic TFLOP/s (value, forward plus backward FLOPs over the step
+time), tokens/s, the dominant kernel against its roofline (average launch time
+from HIP events recorded on the launch stream during the timed steps), and the
+fp64 CPU oracle timed on a bounded sample of the same workload on this host.
+The default workload is the DeepSeek-V3-shaped layer, the largest of the
+workloads that fit one GPU.
 
 Only one GPU: the layer's one-GPU share is the workload; --gpus above 1 is
 refused.
@@ -38,9 +40,12 @@ def pool(cfg):
 
 
 def layer_flops(cfg, rows=None):
-    """Algorithmic FLOPs (2 per multiply-add): fwd = 2 T d E_pool + 6 R d f (+ 6 T d f_shared),
-    bwd = 2 fwd, with R = T k rows through the FFN experts (fewer when zero-computation
-    experts take some slots: then the routed FFN rows of the batch)."""
+    """Algorithmic FLOPs (2 per multiply-add) as (fwd, bwd):
+    fwd = 2 T d E_pool + 6 R d f (+ 6 T d f_shared), bwd = 2 fwd (every product of
+    the forward has a data-gradient and a weight-gradient product of the same
+    size), with R = T k rows through the FFN experts (fewer when zero-computation
+    experts take some slots: then the routed FFN rows of the batch).  A step
+    (forward and backward) is fwd + bwd = 3 fwd."""
     T, d, k, f = cfg["T"], cfg["d"], cfg["k"], cfg["f"]
     R = T * k if rows is None else rows
     fwd = 2 * T * d * pool(cfg) + 6 * R * d * f
@@ -59,7 +64,15 @@ def kernel_work(cfg, rows=None):
     eb = 2 if cfg["dtype"] == "bf16" else 4
     gu = 2.0 * R * d * 2 * f
     dn = 2.0 * R * f * d
-    return {
+    extra = {}
+    if cfg["n_shared"]:
+        # the shared expert's dense passes over all T tokens (kernel ids of their own)
+        fs = cfg["f_shared"]
+        sgu, sdn = 2.0 * T * d * 2 * fs, 2.0 * T * fs * d
+        extra.update({"gemm_shared_gateup_fwd": ("mfma", sgu), "gemm_shared_down_fwd": ("mfma", sdn),
+                      "gemm_shared_down_dgrad": ("mfma", sdn), "gemm_shared_gateup_dgrad": ("mfma", sgu),
+                      "gemm_shared_down_wgrad": ("mfma", sdn), "gemm_shared_gateup_wgrad": ("mfma", sgu)})
+    return dict(extra, **{
         "gemm_gateup_fwd": ("mfma", gu), "gemm_down_fwd": ("mfma", dn),
         "gemm_down_dgrad": ("mfma", dn), "gemm_gateup_dgrad": ("mfma", gu),
         "gemm_down_wgrad": ("mfma", dn), "gemm_gateup_wgrad": ("mfma", gu),
@@ -71,7 +84,7 @@ def kernel_work(cfg, rows=None):
         "combine_fwd": ("hbm", R * d * eb + T * d * eb + T * k * 8),
         "combine_bwd": ("hbm", T * d * eb + 2 * R * d * eb + T * k * 12),
         "unpermute": ("hbm", R * d * eb + T * d * eb + T * k * 12),
-    }
+    })
 
 
 def file_hash(path):
@@ -93,10 +106,20 @@ def traffic_for(kernel, workload):
     return None if ent is None else ent.get("bytes_per_launch")
 
 
-def cpu_baseline(cfg, seed, tokens, reps=1):
-    """The fp64 oracle, as it stands, on the first `tokens` tokens of the workload,
-    fwd+bwd repeated `reps` times on the same inputs (so that the timed CPU work is
-    long enough to measure)."""
+# Bounded CPU samples: the DeepSeek-V3-shaped layer whole (256 experts of
+# 352 MB of float64 weights and weight gradients each) is far beyond a few
+# minutes of the oracle, so its sample keeps d, f, k, the group-limited router
+# (8 groups, 4 kept) and the shared expert and cuts T and E together, so that
+# every expert still holds its ~256 rows as at full size.
+CPU_SAMPLES = {"dsv3": dict(T=1024, E=32)}
+
+
+def cpu_baseline(cfg, seed, tokens=0, reps=1):
+    """The fp64 oracle, as it stands, on a bounded sample of the workload: the
+    first `tokens` tokens (0: the workload's sample from CPU_SAMPLES, else all of
+    them), fwd+bwd repeated `reps` times on the same inputs (so that the timed
+    CPU work is long enough to measure).  Its value counts the sample's own
+    algorithmic FLOPs (forward + backward)."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -104,7 +127,9 @@ def cpu_baseline(cfg, seed, tokens, reps=1):
     from oracle import ZeroComputeSpec, layer_backward, layer_forward, spec_from_config
     from moe_inputs import to_f64
 
-    scfg = variant(cfg["name"].split("[")[0], T=tokens)
+    base = cfg["name"].split("[")[0]
+    over = dict(T=tokens) if tokens else dict(CPU_SAMPLES.get(base, dict(T=cfg["T"])))
+    scfg = variant(base, **over)
     inp = layer_inputs(scfg, seed=seed)
     dt = scfg["dtype"]
     spec = spec_from_config(scfg)
@@ -137,7 +162,7 @@ def cpu_baseline(cfg, seed, tokens, reps=1):
         layer_backward(spec, x, w_r, beta, efn, fwd, dy, shared, with_bias=scfg["expert_bias"], zc=zc,
                        fp8=cfg.get("fp8") == 2)
     wall = time.perf_counter() - t0
-    _, fb = layer_flops(scfg, rows=int(fwd["maps"]["offsets"][scfg["E"]]))
+    ff, fb = layer_flops(scfg, rows=int(fwd["maps"]["offsets"][scfg["E"]]))
     blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
     threads = max([p.get("num_threads", 1) for p in blas] or [1])
     cpu = "unknown"
@@ -146,12 +171,15 @@ def cpu_baseline(cfg, seed, tokens, reps=1):
             cpu = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), cpu)
     except OSError:
         pass
-    return {"value": round(reps * fb / wall / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
+    cut = ("%d of %d tokens" % (scfg["T"], cfg["T"]) if scfg["E"] == cfg["E"] else
+           "%d of %d tokens and %d of %d routed experts (~%d rows per expert, as at full size)"
+           % (scfg["T"], cfg["T"], scfg["E"], cfg["E"], scfg["T"] * scfg["k"] // scfg["E"]))
+    return {"value": round(reps * (ff + fb) / wall / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle", "cpu": cpu,
             "blas": ",".join(sorted({"%s %s" % (p.get("internal_api"), p.get("version")) for p in blas})),
-            "sample": "fp64 oracle fwd+bwd of %d of %d tokens (same shapes, seed %d), %d times, %.1f s wall"
-                      % (tokens, cfg["T"], seed, reps, wall),
-            "tokens_per_s": round(reps * tokens / wall, 1)}
+            "sample": "fp64 oracle fwd+bwd of %s (otherwise the workload's shapes, seed %d), %d times, "
+                      "%.1f s wall" % (cut, seed, reps, wall),
+            "tokens_per_s": round(reps * scfg["T"] / wall, 1)}
 
 
 def memory_kernels(cfg, L, layer, params, x, dy, reps=20, cold_reps=10, scrub_mib=1024):
@@ -228,11 +256,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="qwen3")
+    ap.add_argument("--workload", default="dsv3")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-tokens", type=int, default=0,
-                    help="tokens of the workload the CPU oracle runs (0: all of them)")
-    ap.add_argument("--cpu-reps", type=int, default=3, help="repetitions of the oracle's fwd+bwd")
+                    help="tokens of the workload the CPU oracle runs (0: the workload's bounded sample)")
+    ap.add_argument("--cpu-reps", type=int, default=0,
+                    help="repetitions of the oracle's fwd+bwd (0: 3, or 1 for the DeepSeek-V3 sample)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--aux-coef", type=float, default=0.0,
                     help="add the global-level load-balancing loss of this coefficient (the paper "
@@ -337,7 +366,8 @@ def main():
             step()
         torch.cuda.synchronize()
         ms, n = L.moe_timing_read()
-        per_kernel[name] = ms / max(n, 1)
+        if n:  # (a kernel the workload does not launch is left out)
+            per_kernel[name] = ms / n
     L.moe_timing_select(-1)
     dominant = max(per_kernel, key=lambda n: per_kernel[n])
 
@@ -373,8 +403,8 @@ def main():
     s_ms = [e[0].elapsed_time(e[2]) for e in evs][-10:]
     med = lambda v: sorted(v)[len(v) // 2]  # noqa: E731
 
-    _, fb = layer_flops(cfg, rows=ffn_rows)
-    tflops = fb / (ms_per_step / 1e3) / 1e12
+    ff, fb = layer_flops(cfg, rows=ffn_rows)
+    tflops = (ff + fb) / (ms_per_step / 1e3) / 1e12
     bound, amount = work[dominant]
     dom_avg_s = dom_ms / max(dom_n, 1) / 1e3
     fp8 = int(cfg.get("fp8") or 0)
@@ -410,8 +440,8 @@ def main():
         "tokens_per_s": round(cfg["T"] / (ms_per_step / 1e3), 1),
         "phases_median_of_last_10": {"fwd_ms": round(med(f_ms), 4), "bwd_ms": round(med(b_ms), 4),
                                      "step_ms": round(med(s_ms), 4),
-                                     "fwd_tflops": round(fb / 3 / (med(f_ms) / 1e3) / 1e12, 2),
-                                     "bwd_tflops": round(fb * 2 / 3 / (med(b_ms) / 1e3) / 1e12, 2)},
+                                     "fwd_tflops": round(ff / (med(f_ms) / 1e3) / 1e12, 2),
+                                     "bwd_tflops": round(fb / (med(b_ms) / 1e3) / 1e12, 2)},
         "wall_s_timed": round(wall, 4),
         "roofline": {"bound": bound, "kernel": dominant, "achieved": round(achieved, 2), "peak": peak,
                      "unit": unit, "frac": round(achieved / peak, 4),
@@ -422,7 +452,8 @@ def main():
     if fp8:
         out["fp8_cache_build_ms"] = round(cache_ms, 4)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, args.seed, args.cpu_tokens or cfg["T"], args.cpu_reps)
+        reps = args.cpu_reps or (1 if cfg["name"] in CPU_SAMPLES and not args.cpu_tokens else 3)
+        out["cpu_baseline"] = cpu_baseline(cfg, args.seed, args.cpu_tokens, reps)
     print(json.dumps(out), flush=True)
 
 
