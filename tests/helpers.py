@@ -42,6 +42,42 @@ def rel(gpu, ref):
     return float(np.linalg.norm(gpu - ref) / nr)
 
 
+ROW_FLOOR = 0.05
+
+
+def row_rel(gpu, ref, rows=None):
+    """Largest per-row normwise error: the maximum over rows r of
+    ||gpu_r - ref_r|| / max(||ref_r||, floor), floor = ROW_FLOOR times the RMS of
+    the reference's row norms (a row far below the typical size is measured
+    against 5% of that size).  rows: optional mask or indices of the rows to
+    compare.  One wrong row (a token of y or dx, a permuted row of o or dx_perm)
+    shows here at full weight, where the whole-tensor measure would dilute it
+    by the square root of the row count."""
+    g = np.asarray(gpu, np.float64)
+    r = np.asarray(ref, np.float64)
+    g = g.reshape(g.shape[0], -1)
+    r = r.reshape(r.shape[0], -1)
+    if rows is not None:
+        g, r = g[rows], r[rows]
+    if r.shape[0] == 0:
+        return 0.0
+    nr = np.linalg.norm(r, axis=1)
+    nd = np.linalg.norm(g - r, axis=1)
+    floor = ROW_FLOOR * float(np.sqrt(np.mean(nr ** 2)))
+    if floor == 0.0:
+        return float(nd.max())
+    return float((nd / np.maximum(nr, floor)).max())
+
+
+def group_rel(gpu, ref):
+    """Largest normwise error over the leading index (one expert's gradient per
+    index): max_e rel(gpu[e], ref[e]); an expert whose reference is zero (no
+    rows) counts the norm of the device value, which must then be 0."""
+    g = np.asarray(gpu, np.float64)
+    r = np.asarray(ref, np.float64)
+    return max((rel(g[e], r[e]) for e in range(r.shape[0])), default=0.0)
+
+
 def expert_fn(inp, cfg):
     dt = cfg["dtype"]
 
