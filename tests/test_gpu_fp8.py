@@ -156,23 +156,32 @@ def test_fp8_layer_parity(name, level):
     assert not bad, bad
 
 
-def test_fp8_fullsize_qwen3_sampled():
-    """The Qwen3 workload at full size (T = 8192, 128 experts, the bench's
-    launch configuration) with fp8 = 2: routing and maps of every token
-    against the oracle; y and dx of sampled tokens against the oracle's
-    per-token FP8 evaluation; the expert weight gradients at sampled
-    intermediate columns of three experts (fewest rows, most rows, one at
-    random) against its per-column FP8 evaluation."""
+# (workload, sampled tokens, experts whose weight gradients are sampled): the
+# oracle's E4M3 quantisation of one DeepSeek-V3 expert (five 7168 x 2048 weight
+# quantisations) takes ~18 s on the host, so that workload samples one token
+# (its 8 experts) and one expert's weight-gradient columns
+FP8_FULLSIZE = {"qwen3": (6, ("e_min", "e_max", "e_rand")), "dsv3": (1, ("e_min",))}
+
+
+@pytest.mark.parametrize("name", list(FP8_FULLSIZE))
+def test_fp8_fullsize_sampled(name):
+    """A workload at full size (the bench's launch configuration) with
+    fp8 = 2: routing and maps of every token against the oracle; y and dx of
+    sampled tokens (each row on its own too) against the oracle's per-token
+    FP8 evaluation (with the bf16 shared expert where there is one); the
+    expert weight gradients at sampled intermediate columns against its
+    per-column FP8 evaluation."""
     import torch
     from moe_inputs import config
     from oracle import (expert_weight_grads_at, route, router_logits, sort_maps, spec_from_config,
                         token_forward_backward)
-    from tests.helpers import check_maps_valid, expert_fn
-    cfg = dict(config("qwen3"), fp8=2)
+    from tests.helpers import check_maps_valid, expert_fn, row_rel, shared_of
+    n_tok, experts = FP8_FULLSIZE[name]
+    cfg = dict(config(name), fp8=2)
     T, E, k, f = cfg["T"], cfg["E"], cfg["k"], cfg["f"]
     tol = TOL[cfg["dtype"]]
     inp = layer_inputs(cfg, seed=0)
-    print("full-size qwen3 fp8 layer", flush=True)
+    print("full-size", name, "fp8 layer", flush=True)
     layer, p = setup(cfg, inp)
     x = dev(inp["x"], "bf16")
     dy = dev(inp["dy"], "bf16")
@@ -196,12 +205,14 @@ def test_fp8_fullsize_qwen3_sampled():
         check_maps_valid(sv["topk_idx"], sv["expert_offsets"], sv["row_of"], sv["token_of"], E)
     differ = np.nonzero(np.any(sv["topk_idx"] != rt["topk_idx"], axis=1))[0]
     rng = np.random.default_rng(7)
-    sample = np.sort(rng.choice(np.setdiff1d(np.arange(T), differ), 6, replace=False))
+    sample = np.sort(rng.choice(np.setdiff1d(np.arange(T), differ), n_tok, replace=False))
     efn = expert_fn(inp, cfg)
     print("oracle per-token FP8 results of", sample.size, "tokens", flush=True)
-    r = token_forward_backward(spec, x64[sample], dy64[sample], w_r, beta, efn, fp8=2)
+    r = token_forward_backward(spec, x64[sample], dy64[sample], w_r, beta, efn, shared_of(inp, cfg), fp8=2)
     st = torch.from_numpy(sample).cuda()
-    errs = {"y[sample]": rel(host(y[st]), r["y"]), "dx[sample]": rel(host(dx[st]), r["dx"])}
+    errs = {"y[sample]": rel(host(y[st]), r["y"]), "dx[sample]": rel(host(dx[st]), r["dx"]),
+            "y[sample, worst row]": row_rel(host(y[st]), r["y"]),
+            "dx[sample, worst row]": row_rel(host(dx[st]), r["dx"])}
     touched = set(np.unique(np.concatenate([sv["topk_idx"][differ].ravel(),
                                             rt["topk_idx"][differ].ravel()])).tolist()) if differ.size else set()
     counts = mp["counts"]
@@ -211,7 +222,8 @@ def test_fp8_fullsize_qwen3_sampled():
     e_rand = int(rng.choice([e for e in usable if e not in (e_min, e_max)]))
     cols = np.unique(np.concatenate([[0, f - 1, f // 2], rng.choice(f, 13, replace=False)]))
     ct = torch.from_numpy(cols).cuda()
-    for tag, e in (("e_min", e_min), ("e_max", e_max), ("e_rand", e_rand)):
+    picked = {"e_min": e_min, "e_max": e_max, "e_rand": e_rand}
+    for tag, e in ((t, picked[t]) for t in experts):
         rows = mp["token_of"][mp["offsets"][e]:mp["offsets"][e + 1]]
         tt, ss = rows // k, rows % k
         print("oracle FP8 weight gradients of expert", e, "rows", tt.size, flush=True)
@@ -221,7 +233,7 @@ def test_fp8_fullsize_qwen3_sampled():
         errs["dw_gate[%s]" % tag] = rel(host(grads["dw_gate"][e][:, ct]), g["dw_gate"])
         errs["dw_up[%s]" % tag] = rel(host(grads["dw_up"][e][:, ct]), g["dw_up"])
         errs["dw_down[%s]" % tag] = rel(host(grads["dw_down"][e][ct, :]), g["dw_down"])
-    print("qwen3 fp8 full size: ambiguous tokens", int(amb.sum()), "routed differently", differ.size,
+    print(name, "fp8 full size: ambiguous tokens", int(amb.sum()), "routed differently", differ.size,
           {n: "%.2e" % v for n, v in errs.items()}, flush=True)
     bad = {n: v for n, v in errs.items() if not v <= tol}
     assert not bad, bad
