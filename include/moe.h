@@ -273,6 +273,22 @@ int moe_permute(const moe_shape* shape, const void* x, const int32_t* topk_idx,
                 int32_t* expert_offsets, int32_t* row_of, int32_t* token_of, void* x_perm,
                 void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* moe_permute without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments and results as moe_permute (bitwise the
+ * same outputs); its scratch, the per-block expert histograms of
+ * ceil(T/256) * E_pool int32, lives in a fixed 4 MiB device array inside the
+ * library (each GPU holds its own copy until the process ends), so it
+ * allocates and frees nothing.  Shapes whose histograms exceed 4 MiB (for
+ * instance T above 1M tokens with 256 experts) get MOE_ERR_UNSUPPORTED.
+ * Every call on one GPU shares that array: calls that overlap on one GPU
+ * (on different streams without ordering between them) race; calls ordered
+ * on a stream are fine.  The first call on a device looks the array's
+ * address up (MOE_ERR_HIP if that fails). */
+int moe_permute_noalloc(const moe_shape* shape, const void* x, const int32_t* topk_idx,
+                        int32_t* expert_offsets, int32_t* row_of, int32_t* token_of, void* x_perm,
+                        hipStream_t stream);
+
 /* Grouped SwiGLU expert forward (section 3.2, fused SwiGLU forward):
  *   [g|u] = x_perm_e [W_gate,e | W_up,e] (+ b_gate,e | b_up,e),
  *   h = silu(g) * u  (or the shape's MOE_ACT_*; from the float32 accumulators),

@@ -103,6 +103,7 @@ def _load():
         "moe_workspace_size": [S, szp, szp, szp],
         "moe_route": [S, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, sz, _VP],
         "moe_permute": [S, _VP, _VP, _VP, _VP, _VP, _VP, _VP, sz, _VP],
+        "moe_permute_noalloc": [S, _VP, _VP, _VP, _VP, _VP, _VP, _VP],
         "moe_grouped_gemm_fwd": [S, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP],
         "moe_grouped_gemm_bwd": [S, i32] + [_VP] * 16 + [_VP],
         "moe_combine_fwd": [S, _VP, _VP, _VP, _VP, _VP, _VP],
@@ -223,6 +224,12 @@ def moe_permute(shape, x, topk_idx, expert_offsets, row_of, token_of, x_perm, ws
     return _check("moe_permute", LIB.moe_permute(ctypes.byref(shape), P(x), P(topk_idx),
                                                  P(expert_offsets), P(row_of), P(token_of),
                                                  P(x_perm), wp, wb, _stream(stream)))
+
+
+def moe_permute_noalloc(shape, x, topk_idx, expert_offsets, row_of, token_of, x_perm, stream=None):
+    return _check("moe_permute_noalloc", LIB.moe_permute_noalloc(ctypes.byref(shape), P(x), P(topk_idx),
+                                                                 P(expert_offsets), P(row_of), P(token_of),
+                                                                 P(x_perm), _stream(stream)))
 
 
 def moe_grouped_gemm_fwd(shape, x_perm, expert_offsets, w_gate, w_up, w_down, b_gate, b_up, b_down,

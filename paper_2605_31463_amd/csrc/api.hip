@@ -1005,6 +1005,37 @@ int moe_permute(const moe_shape* shape, const void* x, const int32_t* topk_idx, 
   return do_permute(s, x, topk_idx, expert_offsets, row_of, token_of, x_perm, ws, stream);
 }
 
+int moe_permute_noalloc(const moe_shape* shape, const void* x, const int32_t* topk_idx, int32_t* expert_offsets,
+                        int32_t* row_of, int32_t* token_of, void* x_perm, hipStream_t stream) {
+  MOE_TRY(check_shape(shape));
+  const moe_shape& s = *shape;
+  MOE_NEED(expert_offsets, "expert_offsets");
+  if (s.T > 0) {
+    MOE_NEED(x, "x");
+    MOE_NEED(topk_idx, "topk_idx");
+    MOE_NEED(row_of, "row_of");
+    MOE_NEED(token_of, "token_of");
+    MOE_NEED(x_perm, "x_perm");
+  }
+  int32_t* hist = nullptr;
+  MOE_TRY(permute_scratch((size_t)perm_blocks(s.T) * (size_t)epool(s) * sizeof(int32_t), &hist));
+  PermArgs a{};
+  a.x = x;
+  a.topk_idx = topk_idx;
+  a.T = s.T;
+  a.d = (int)s.d;
+  a.E = (int)epool(s);
+  a.E_rows = (int)s.E;
+  a.k = (int)s.k;
+  a.bf16 = s.dtype == MOE_BF16;
+  a.hist = hist;
+  a.offsets = expert_offsets;
+  a.row_of = row_of;
+  a.token_of = token_of;
+  a.x_perm = x_perm;
+  return launch_permute(a, stream);
+}
+
 int moe_grouped_gemm_fwd(const moe_shape* shape, const void* x_perm, const int32_t* expert_offsets,
                          const void* w_gate, const void* w_up, const void* w_down, const void* b_gate,
                          const void* b_up, const void* b_down, void* gu, void* h, void* o, hipStream_t stream) {

@@ -48,6 +48,12 @@ struct PermArgs {
   float* sx;         // [R] their row scales
 };
 int launch_permute(const PermArgs& a, hipStream_t s);
+// The allocation-free permutation's fixed scratch (per-block histograms):
+// its size, and the current device's address of it (MOE_ERR_UNSUPPORTED when
+// `need` bytes exceed it).
+constexpr size_t kPermScratchBytes = (size_t)4 << 20;
+constexpr int kMaxDevices = 64;
+int permute_scratch(size_t need, int32_t** out);
 
 // FP8: E4M3 rows of [s0 | s1] (bf16 [rows][w0] and [rows][w1], w1 may be 0;
 // with offsets, only the rows below offsets[E]) and their scales.

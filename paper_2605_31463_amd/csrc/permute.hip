@@ -15,10 +15,44 @@
 //            just list its tokens).
 // No atomics touch the row layout, so the permutation is the stable counting
 // sort by (expert, token) on every run.
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace moe {
+
+// Scratch of the allocation-free permutation entry point: the per-block
+// expert histograms [nblk][E_pool] int32 live in this fixed device array
+// instead of a caller's workspace.  Every GPU the library runs on holds its
+// own copy until the process ends; calls on one GPU share it (hist_kernel
+// writes every entry a call reads, so nothing carries over between calls).
+static __device__ __align__(256) int32_t scratch[kPermScratchBytes / sizeof(int32_t)];
+
+int permute_scratch(size_t need, int32_t** out) {
+  if (need > kPermScratchBytes)
+    return moe_set_error(MOE_ERR_UNSUPPORTED,
+                         "the allocation-free permutation needs %zu bytes of scratch, above its fixed %zu "
+                         "(per-block histograms: ceil(T/256) * E_pool * 4 bytes)",
+                         need, kPermScratchBytes);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return moe_set_error(MOE_ERR_HIP, "permute scratch: no usable current device (%d)", dev);
+  // the device address of this GPU's copy of the array, looked up once per
+  // device with that device current (the host-side name is not an address)
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return moe_set_error(MOE_ERR_HIP, "permute scratch: hipGetSymbolAddress: %s", hipGetErrorString(e));
+    addr[dev] = p;
+  }
+  *out = static_cast<int32_t*>(addr[dev]);
+  return MOE_OK;
+}
 
 namespace {
 
