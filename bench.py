@@ -81,9 +81,11 @@ def kernel_work(cfg, rows=None):
         # bytes: reads + writes of the HBM operands, once each
         "route_select": ("hbm", T * E * 8 + T * k * 8),
         "scatter": ("hbm", T * d * eb + R * d * eb + T * k * 4 * 3),
-        "combine_fwd": ("hbm", R * d * eb + T * d * eb + T * k * 8),
+        # (with a shared expert the combine also reads its output rows and the
+        # unpermute its input gradient rows)
+        "combine_fwd": ("hbm", R * d * eb + T * d * eb * (2 if cfg["n_shared"] else 1) + T * k * 8),
         "combine_bwd": ("hbm", T * d * eb + 2 * R * d * eb + T * k * 12),
-        "unpermute": ("hbm", R * d * eb + T * d * eb + T * k * 12),
+        "unpermute": ("hbm", R * d * eb + T * d * eb * (2 if cfg["n_shared"] else 1) + T * k * 12),
     })
 
 
@@ -93,16 +95,17 @@ def file_hash(path):
 
 
 def traffic_for(kernel, workload):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current GEMM source; else None."""
+    """HBM bytes per launch of a kernel on a workload from the committed
+    rocprofv3 counter summary (profiles/traffic.json), if it was taken on the
+    current GEMM source; else None."""
     try:
         with open(TRAFFIC_FILE) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
-    if t.get("gemm_source_sha256_16") != file_hash(GEMM_SOURCE) or t.get("workload") != workload:
+    if t.get("gemm_source_sha256_16") != file_hash(GEMM_SOURCE):
         return None
-    ent = t.get("kernels", {}).get(kernel)
+    ent = t.get("workloads", {}).get(workload, {}).get("kernels", {}).get(kernel)
     return None if ent is None else ent.get("bytes_per_launch")
 
 
@@ -261,7 +264,7 @@ def main():
     ap.add_argument("--cpu-tokens", type=int, default=0,
                     help="tokens of the workload the CPU oracle runs (0: the workload's bounded sample)")
     ap.add_argument("--cpu-reps", type=int, default=0,
-                    help="repetitions of the oracle's fwd+bwd (0: 3, or 1 for the DeepSeek-V3 sample)")
+                    help="repetitions of the oracle's fwd+bwd (0: 3)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--aux-coef", type=float, default=0.0,
                     help="add the global-level load-balancing loss of this coefficient (the paper "
@@ -452,7 +455,7 @@ def main():
     if fp8:
         out["fp8_cache_build_ms"] = round(cache_ms, 4)
     if not args.no_cpu_baseline:
-        reps = args.cpu_reps or (1 if cfg["name"] in CPU_SAMPLES and not args.cpu_tokens else 3)
+        reps = args.cpu_reps or 3
         out["cpu_baseline"] = cpu_baseline(cfg, args.seed, args.cpu_tokens, reps)
     print(json.dumps(out), flush=True)
 
