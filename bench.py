@@ -89,6 +89,58 @@ def kernel_work(cfg, rows=None):
     })
 
 
+def gemm_hbm_floor(cfg, counts, rows=None):
+    """Smallest HBM traffic (bytes) of each expert GEMM pass: every operand read
+    once, every output written once.  The weights of an expert are read only if
+    it holds rows; every expert's weight gradient is written (zero for an expert
+    without rows).  counts: rows per routed expert.  FP8 passes read one-byte
+    codes of the weights and of the activation operand."""
+    T, d, E, k, f = cfg["T"], cfg["d"], cfg["E"], cfg["k"], cfg["f"]
+    R = T * k if rows is None else rows
+    eb = 2 if cfg["dtype"] == "bf16" else 4
+    act = sum(1 for c in counts if c > 0)
+    fp8 = int(cfg.get("fp8") or 0)
+    q = lambda name: 1 if fp8 and name in FP8_KERNELS[fp8] else eb  # noqa: E731
+    out = {
+        "gemm_gateup_fwd": act * 2 * d * f * q("gemm_gateup_fwd") + R * d * q("gemm_gateup_fwd") + R * 3 * f * eb,
+        "gemm_down_fwd": act * f * d * q("gemm_down_fwd") + R * f * q("gemm_down_fwd") + R * d * eb,
+        "gemm_down_dgrad": act * f * d * q("gemm_down_dgrad") + R * d * q("gemm_down_dgrad") + R * 4 * f * eb,
+        "gemm_gateup_dgrad": act * 2 * d * f * q("gemm_gateup_dgrad") + R * 2 * f * q("gemm_gateup_dgrad")
+        + R * d * eb,
+        "gemm_down_wgrad": E * f * d * eb + R * (f + d) * eb,
+        "gemm_gateup_wgrad": E * 2 * d * f * eb + R * (d + 2 * f) * eb,
+    }
+    if cfg["n_shared"]:
+        fs = cfg["f_shared"]
+        out.update({
+            "gemm_shared_gateup_fwd": 2 * d * fs * eb + T * (d + 3 * fs) * eb,
+            "gemm_shared_down_fwd": fs * d * eb + T * (fs + d) * eb,
+            "gemm_shared_down_dgrad": fs * d * eb + T * (d + 4 * fs) * eb,
+            "gemm_shared_gateup_dgrad": 2 * d * fs * eb + T * (2 * fs + d) * eb,
+            "gemm_shared_down_wgrad": fs * d * eb + T * (fs + d) * eb,
+            "gemm_shared_gateup_wgrad": 2 * d * fs * eb + T * (d + 2 * fs) * eb,
+        })
+    return out
+
+
+def gemm_roof(flops, floor_bytes, secs, mfma_peak_tflops, hbm_peak_gbs=PEAK_HBM_GBS):
+    """Two-sided roofline of one GEMM launch of `secs` seconds: the binding side
+    is the one whose peak takes longer for the launch's work (flops at the MFMA
+    peak, or its smallest HBM traffic at the HBM peak).  Returns the binding
+    side's achieved rate, peak and fraction, the other side's, and mfma_ceiling,
+    the largest MFMA fraction the HBM floor leaves: t_mfma / max(t_mfma, t_hbm)."""
+    t_c = flops / (mfma_peak_tflops * 1e12)
+    t_m = floor_bytes / (hbm_peak_gbs * 1e9)
+    mf = {"achieved": flops / secs / 1e12, "peak": mfma_peak_tflops, "unit": "TFLOP/s"}
+    mf["frac"] = mf["achieved"] / mf["peak"]
+    hb = {"achieved": floor_bytes / secs / 1e9, "peak": hbm_peak_gbs, "unit": "GB/s", "bytes": floor_bytes}
+    hb["frac"] = hb["achieved"] / hb["peak"]
+    r = dict(mf if t_c >= t_m else hb, bound="mfma" if t_c >= t_m else "hbm")
+    r["other_side"] = dict(hb, bound="hbm") if t_c >= t_m else dict(mf, bound="mfma")
+    r["mfma_ceiling"] = min(1.0, t_c / max(t_c, t_m))
+    return r
+
+
 def file_hash(path):
     with open(path, "rb") as fh:
         return hashlib.sha256(fh.read()).hexdigest()[:16]
@@ -408,25 +460,38 @@ def main():
 
     ff, fb = layer_flops(cfg, rows=ffn_rows)
     tflops = (ff + fb) / (ms_per_step / 1e3) / 1e12
-    bound, amount = work[dominant]
     dom_avg_s = dom_ms / max(dom_n, 1) / 1e3
     fp8 = int(cfg.get("fp8") or 0)
     mfma_peak = lambda name: PEAK_FP8_TFLOPS if fp8 and name in FP8_KERNELS[fp8] else PEAK_BF16_TFLOPS  # noqa: E731
-    if bound == "mfma":
-        achieved = amount / dom_avg_s / 1e12
-        peak, unit = mfma_peak(dominant), "TFLOP/s"
-    else:
-        achieved = amount / dom_avg_s / 1e9
-        peak, unit = PEAK_HBM_GBS, "GB/s"
+    # expert GEMMs: two-sided roofline, the larger of the MFMA time of their
+    # flops and the HBM time of their smallest traffic (the binding side is
+    # the kernel's bound; the other side is reported beside it)
+    counts = (layer.saved["expert_offsets"][1:cfg["E"] + 1] - layer.saved["expert_offsets"][:cfg["E"]]).tolist()
+    floor_b = gemm_hbm_floor(cfg, counts, rows=ffn_rows)
+
+    def roof(name, secs):
+        b, amt = work[name]
+        if b != "mfma" or name not in floor_b:
+            rate = amt / secs / (1e12 if b == "mfma" else 1e9)
+            peak = mfma_peak(name) if b == "mfma" else PEAK_HBM_GBS
+            return {"bound": b, "achieved": rate, "peak": peak, "unit": "TFLOP/s" if b == "mfma" else "GB/s",
+                    "frac": rate / peak}
+        return gemm_roof(amt, floor_b[name], secs, mfma_peak(name))
+
+    rdom = roof(dominant, dom_avg_s)
+    bound, achieved, peak, unit = rdom["bound"], rdom["achieved"], rdom["peak"], rdom["unit"]
     workload = "%s moe layer T=%d d=%d E=%d k=%d f=%d" % (cfg["name"], cfg["T"], cfg["d"], cfg["E"],
                                                          cfg["k"], cfg["f"])
     kernels = {}
     for name, ms in per_kernel.items():
-        b, amt = work[name]
-        rate = amt / (ms / 1e3) / (1e12 if b == "mfma" else 1e9)
-        kernels[name] = {"avg_us": round(ms * 1e3, 2), "bound": b,
-                         "achieved": round(rate, 1), "unit": "TFLOP/s" if b == "mfma" else "GB/s",
-                         "frac": round(rate / (mfma_peak(name) if b == "mfma" else PEAK_HBM_GBS), 4)}
+        r = roof(name, ms / 1e3)
+        kernels[name] = {"avg_us": round(ms * 1e3, 2), "bound": r["bound"], "achieved": round(r["achieved"], 1),
+                         "unit": r["unit"], "frac": round(r["frac"], 4)}
+        if "other_side" in r:
+            o = r["other_side"]
+            kernels[name]["other_side"] = {"bound": o["bound"], "achieved": round(o["achieved"], 1),
+                                           "unit": o["unit"], "frac": round(o["frac"], 4)}
+            kernels[name]["mfma_ceiling"] = round(r["mfma_ceiling"], 4)
     out = {
         "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
@@ -446,10 +511,14 @@ def main():
                                      "fwd_tflops": round(ff / (med(f_ms) / 1e3) / 1e12, 2),
                                      "bwd_tflops": round(fb / (med(b_ms) / 1e3) / 1e12, 2)},
         "wall_s_timed": round(wall, 4),
-        "roofline": {"bound": bound, "kernel": dominant, "achieved": round(achieved, 2), "peak": peak,
-                     "unit": unit, "frac": round(achieved / peak, 4),
-                     "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": dom_n,
-                     "traffic": traffic_for(dominant, workload)},
+        "roofline": dict({"bound": bound, "kernel": dominant, "achieved": round(achieved, 2), "peak": peak,
+                          "unit": unit, "frac": round(achieved / peak, 4),
+                          "avg_launch_us": round(dom_avg_s * 1e6, 2), "launches": dom_n,
+                          "traffic": traffic_for(dominant, workload)},
+                         **({"hbm_floor_bytes": floor_b[dominant],
+                             "other_side": {k2: (round(v2, 4) if isinstance(v2, float) else v2)
+                                            for k2, v2 in rdom["other_side"].items() if k2 != "bytes"},
+                             "mfma_ceiling": round(rdom["mfma_ceiling"], 4)} if "other_side" in rdom else {})),
         "kernels": kernels,
     }
     if fp8:
