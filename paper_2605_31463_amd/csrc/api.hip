@@ -188,7 +188,7 @@ inline size_t act_bytes(const moe_shape& s) { return s.dtype == MOE_BF16 ? 2 : 4
 
 struct Plan {
   // forward
-  size_t hist, wsplit, lg, aux_part, xq, sx, hq, sh;
+  size_t hist, sync, wsplit, lg, aux_part, xq, sx, hq, sh;
   size_t fwd_total;
   // backward
   size_t d_o, dgu, dx_perm, dl, partial, w_rt, dgu_sh, dx_sh;
@@ -215,6 +215,8 @@ Plan plan(const moe_shape& s) {
   const int64_t Ep = epool(s);
   p.hist = off;
   off += align_up((size_t)moe::perm_blocks(s.T) * Ep * 4);
+  p.sync = off;
+  off += align_up(4);
   p.wsplit = off;
   off += s.dtype == MOE_BF16 ? align_up((size_t)3 * Ep * s.d * 2) : 0;
   p.lg = off;
@@ -343,10 +345,18 @@ GemmArgs gemm_dense(const moe_shape& s, int mode) {
   return g;
 }
 
+// maps (may be null): the forward layer's expert_offsets; the selection then
+// also builds the permutation's block bases and offsets when it can, and
+// *maps_built says whether it did
 int do_route(const moe_shape& s, const void* x, const float* w_r, const float* bias, int32_t* topk_idx,
              float* topk_w, float* s_sel, int32_t* counts, void* ws, hipStream_t st, float* probs = nullptr,
-             const float* threshold = nullptr) {
+             const float* threshold = nullptr, int32_t* maps_offsets = nullptr, bool* maps_built = nullptr) {
   RouteArgs a{};
+  if (maps_offsets) {
+    a.hist = reinterpret_cast<int32_t*>(wsp(ws, plan(s).hist));
+    a.sync = reinterpret_cast<int32_t*>(wsp(ws, plan(s).sync));
+    a.offsets = maps_offsets;
+  }
   a.probs = probs;
   a.threshold = threshold;
   a.wsplit = s.dtype == MOE_BF16 ? wsp(ws, plan(s).wsplit) : nullptr;
@@ -368,12 +378,14 @@ int do_route(const moe_shape& s, const void* x, const float* w_r, const float* b
   a.topk_w = topk_w;
   a.s_sel = s_sel;
   a.counts = counts;
-  return launch_route(a, st);
+  return launch_route(a, st, maps_built);
 }
 
 int do_permute(const moe_shape& s, const void* x, const int32_t* topk_idx, int32_t* offsets, int32_t* row_of,
-               int32_t* token_of, void* x_perm, void* ws, hipStream_t st, bool fp8_rows = false) {
+               int32_t* token_of, void* x_perm, void* ws, hipStream_t st, bool fp8_rows = false,
+               bool maps_ready = false) {
   PermArgs a{};
+  a.maps_ready = maps_ready;
   a.x = x;
   a.topk_idx = topk_idx;
   a.T = s.T;
@@ -1315,10 +1327,11 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, 
   const void* bg = s.expert_bias ? prm->b_gate : nullptr;
   const void* bu = s.expert_bias ? prm->b_up : nullptr;
   const void* bd = s.expert_bias ? prm->b_down : nullptr;
+  bool maps = false;
   MOE_TRY(do_route(s, x, prm->w_r, prm->router_bias, sv->topk_idx, sv->topk_w, sv->s_sel, nullptr, ws, stream,
-                   has_aux(s) ? sv->router_probs : nullptr, prm->gate_threshold));
+                   has_aux(s) ? sv->router_probs : nullptr, prm->gate_threshold, sv->expert_offsets, &maps));
   MOE_TRY(do_permute(s, x, sv->topk_idx, sv->expert_offsets, sv->row_of, sv->token_of, sv->x_perm, ws, stream,
-                     s.fp8 != 0));
+                     s.fp8 != 0, maps));
   if (has_aux(s)) {
     AuxArgs aa = aux_args(s, prm, sv);
     aa.part = reinterpret_cast<double*>(wsp(ws, plan(s).aux_part));

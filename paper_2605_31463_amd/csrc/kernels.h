@@ -25,13 +25,21 @@ struct RouteArgs {
   float* probs;      // [T][E] softmax over all experts (auxiliary loss), or null;
                      // the threshold router writes its sigmoid scores there
   const float* threshold;  // [E] thresholds of the threshold router
+  // the permutation's maps inputs, built by the selection when these are set
+  // and the path supports it (launch_route reports whether it did): per-block
+  // expert counts turned into each block's base inside its expert
+  // [perm_blocks(T)][E], expert_offsets [E+1], and one arrival counter
+  int32_t* hist;
+  int32_t* offsets;
+  int32_t* sync;
 };
-int launch_route(const RouteArgs& a, hipStream_t s);
+// maps_built (may be null): set to whether hist / offsets were produced
+int launch_route(const RouteArgs& a, hipStream_t s, bool* maps_built = nullptr);
 int zero_i32(int32_t* p, int64_t n, hipStream_t s);
 
 // Permutation: histogram per block of PERM_TB tokens, scan, scatter.
 constexpr int PERM_TB = 256;
-inline int64_t perm_blocks(int64_t T) { return (T + PERM_TB - 1) / PERM_TB; }
+__host__ __device__ inline int64_t perm_blocks(int64_t T) { return (T + PERM_TB - 1) / PERM_TB; }
 struct PermArgs {
   const void* x;
   const int32_t* topk_idx;
@@ -46,6 +54,7 @@ struct PermArgs {
   void* x_perm;      // [R][d]
   uint8_t* xq;       // [R][d] E4M3 rows of the FFN experts (FP8 forward), or null
   float* sx;         // [R] their row scales
+  bool maps_ready;   // hist holds the block bases and offsets is written (by the route)
 };
 int launch_permute(const PermArgs& a, hipStream_t s);
 // The allocation-free permutation's fixed scratch (per-block histograms):

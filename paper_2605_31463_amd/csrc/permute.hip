@@ -243,6 +243,15 @@ __global__ __launch_bounds__(256) void permute_copy_kernel(PermArgs a) {
 int launch_permute(const PermArgs& a, hipStream_t s) {
   const int64_t nblk = perm_blocks(a.T);
   int st;
+  if (a.maps_ready) {  // block bases and offsets from the route's selection
+    if (nblk == 0) return MOE_OK;
+    st = launch(K_RANK, s, "rank", [&] { rank_kernel<<<nblk, 256, 0, s>>>(a); });
+    if (st) return st;
+    const int ncopy = (int)((a.T + 3) / 4);
+    if (a.bf16)
+      return launch(K_SCATTER, s, "scatter", [&] { permute_copy_kernel<bf16_t><<<ncopy, 256, 0, s>>>(a); });
+    return launch(K_SCATTER, s, "scatter", [&] { permute_copy_kernel<float><<<ncopy, 256, 0, s>>>(a); });
+  }
   if (nblk > 0) {
     st = launch(K_HIST, s, "hist", [&] { hist_kernel<<<nblk, 256, 0, s>>>(a.topk_idx, a.T, a.k, a.E, a.hist); });
     if (st) return st;

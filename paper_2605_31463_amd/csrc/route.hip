@@ -345,7 +345,18 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-__global__ void wr_split_kernel(const float* __restrict__ w, bf16_t* __restrict__ ws, int d, int E) {
+// The launch also clears what the selection then accumulates into: the
+// expert counts (nz0), the permutation's per-block counts (nz1) and the
+// selection's arrival counter (nz2); pointers may be null.
+__global__ void wr_split_kernel(const float* __restrict__ w, bf16_t* __restrict__ ws, int d, int E,
+                                int32_t* z0, int nz0, int32_t* z1, int64_t nz1, int32_t* z2, int nz2) {
+  {
+    const int64_t nth = (int64_t)gridDim.x * gridDim.y * blockDim.x;
+    const int64_t g = ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * blockDim.x + threadIdx.x;
+    for (int64_t i = g; i < nz0; i += nth) z0[i] = 0;
+    for (int64_t i = g; i < nz1; i += nth) z1[i] = 0;
+    for (int64_t i = g; i < nz2; i += nth) z2[i] = 0;
+  }
   __shared__ float tile[32][33];
   const int e0 = blockIdx.x * 32, i0 = blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
@@ -658,10 +669,20 @@ __device__ void select_tokens16(const RouteArgs& a, const double* lg, int ld, in
 // Selection over the float64 logits in the workspace, 16 tokens per
 // workgroup: KPL > 0, one DPP row per token (KPL = E / 16 experts per lane);
 // KPL = 0, one wavefront per token.
+//
+// With a.hist set, the selection also builds the permutation's maps inputs
+// (section 3.2's token scatter needs, per expert, the rows before each block
+// and the expert offsets): every block adds its counts into the count of its
+// PERM_TB-token block (cleared by the preceding W_r split launch), and the
+// last block to finish (arrival counter, device-scope fences on both sides)
+// turns the block counts into bases inside each expert and writes
+// expert_offsets.  Nothing waits: the last arrival does the work.
 template <int KPL>
 __global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a) {
   constexpr int TPB = 16;
+  static_assert(PERM_TB % TPB == 0, "selection blocks tile the permutation's blocks");
   __shared__ int hist[256];
+  __shared__ int last;
   for (int e = threadIdx.x; e < 256; e += 256) hist[e] = 0;
   __syncthreads();
   const int64_t t0 = (int64_t)blockIdx.x * TPB;
@@ -671,17 +692,59 @@ __global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a) {
   else
     select_tokens(a, a.lg + t0 * a.E, a.E, t0, ntok, hist);
   __syncthreads();
+  const int E = a.E;
   if (a.counts) {
-    for (int e = threadIdx.x; e < a.E; e += 256)
+    for (int e = threadIdx.x; e < E; e += 256)
       if (hist[e]) atomicAdd(&a.counts[e], hist[e]);
   }
+  if (!a.hist) return;
+  // the block counts and the arrival counter are device-scope atomics, all
+  // performed where every XCD sees them; a block counts its arrival only once
+  // its count additions have returned, and the last block reads the counts
+  // with device-scope atomic loads
+  int32_t* bh = a.hist + (t0 / PERM_TB) * E;
+  for (int e = threadIdx.x; e < E; e += 256)
+    if (hist[e]) (void)__hip_atomic_fetch_add(&bh[e], hist[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  wait_vmcnt<0>();
+  __syncthreads();
+  if (threadIdx.x == 0)
+    last = __hip_atomic_fetch_add(a.sync, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (int)gridDim.x - 1;
+  __syncthreads();
+  if (!last) return;
+  // the last block: bases inside each expert, then the expert offsets
+  const int64_t nblk = perm_blocks(a.T);
+  int tot = 0;
+  if ((int)threadIdx.x < E) {
+    const int e = threadIdx.x;
+    for (int64_t b0 = 0; b0 < nblk; b0 += 16) {
+      int v[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        v[q] = b0 + q < nblk ? __hip_atomic_load(&a.hist[(b0 + q) * E + e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                             : 0;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        if (b0 + q < nblk) a.hist[(b0 + q) * E + e] = tot;
+        tot += v[q];
+      }
+    }
+  }
+  __shared__ int sbuf[256];
+  __shared__ int total;
+  const int ex = block_scan_256(tot, sbuf, &total);
+  if ((int)threadIdx.x < E) a.offsets[threadIdx.x] = ex;
+  if (threadIdx.x == 0) a.offsets[E] = total;
 }
 
 int launch_route_gemm(const RouteArgs& a, hipStream_t s) {
   {
     dim3 grid((a.E + 31) / 32, (a.d + 31) / 32);
     bf16_t* wsp = reinterpret_cast<bf16_t*>(a.wsplit);
-    const int st = launch(K_WR_SPLIT, s, "wr_split", [&] { wr_split_kernel<<<grid, 256, 0, s>>>(a.w_r, wsp, a.d, a.E); });
+    const int64_t nh = a.hist ? perm_blocks(a.T) * a.E : 0;
+    const int st = launch(K_WR_SPLIT, s, "wr_split", [&] {
+      wr_split_kernel<<<grid, 256, 0, s>>>(a.w_r, wsp, a.d, a.E, a.counts, a.counts ? a.E : 0, a.hist, nh, a.sync,
+                                           a.hist ? 1 : 0);
+    });
     if (st) return st;
   }
   // a router weight that fits in L2 is re-read per 64-token tile; a larger
@@ -855,7 +918,9 @@ int launch_route_mfma(const RouteArgs& a, hipStream_t s) {
   {
     dim3 grid((a.E + 31) / 32, (a.d + 31) / 32);
     bf16_t* wsp = reinterpret_cast<bf16_t*>(a.wsplit);
-    const int st = launch(K_WR_SPLIT, s, "wr_split", [&] { wr_split_kernel<<<grid, 256, 0, s>>>(a.w_r, wsp, a.d, a.E); });
+    const int st = launch(K_WR_SPLIT, s, "wr_split", [&] {
+      wr_split_kernel<<<grid, 256, 0, s>>>(a.w_r, wsp, a.d, a.E, a.counts, a.counts ? a.E : 0, nullptr, 0, nullptr, 0);
+    });
     if (st) return st;
   }
 #define MOE_RM(NTW_, SPLIT_, TBM_)                                                                           \
@@ -898,15 +963,30 @@ int zero_i32(int32_t* p, int64_t n, hipStream_t s) {
   return launch(K_COUNT_ZERO, s, "zero", [&] { zero_i32_kernel<<<nb, 256, 0, s>>>(p, n); });
 }
 
-int launch_route(const RouteArgs& a, hipStream_t s) {
-  if (a.counts) {
+int launch_route(const RouteArgs& a, hipStream_t s, bool* maps_built) {
+  if (maps_built) *maps_built = false;
+  const bool gemm_path = a.T > 0 && a.bf16 && a.wsplit && a.lg && a.E % 32 == 0;
+  const bool mfma_path = a.T > 0 && a.bf16 && a.wsplit && a.E % 16 == 0;
+  // (the W_r split launch of the MFMA paths clears the counts itself)
+  if (a.counts && !gemm_path && !mfma_path) {
     int st = zero_i32(a.counts, a.E, s);
     if (st) return st;
   }
   if (a.T == 0) return MOE_OK;
-  if (a.bf16 && a.wsplit && a.lg && a.E % 32 == 0) return launch_route_gemm(a, s);
-  if (a.bf16 && a.wsplit && a.E % 16 == 0) return launch_route_mfma(a, s);
-  return a.bf16 ? launch_route_t<bf16_t>(a, s) : launch_route_t<float>(a, s);
+  if (gemm_path) {
+    // the selection builds the permutation's block bases and offsets when
+    // the last block's serial pass over the blocks stays short
+    RouteArgs b = a;
+    const bool maps = a.hist && a.offsets && a.sync && a.E <= 256 && perm_blocks(a.T) <= 512;
+    if (!maps) b.hist = nullptr;
+    const int st = launch_route_gemm(b, s);
+    if (st == MOE_OK && maps_built) *maps_built = maps;
+    return st;
+  }
+  RouteArgs b = a;
+  b.hist = nullptr;
+  if (mfma_path) return launch_route_mfma(b, s);
+  return a.bf16 ? launch_route_t<bf16_t>(b, s) : launch_route_t<float>(b, s);
 }
 
 }  // namespace moe
