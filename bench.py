@@ -165,7 +165,7 @@ def traffic_for(kernel, workload):
 # 352 MB of float64 weights and weight gradients each) is far beyond a few
 # minutes of the oracle, so its sample keeps d, f, k, the group-limited router
 # (8 groups, 4 kept) and the shared expert and cuts T and E together, so that
-# every expert still holds its ~256 rows as at full size.
+# the experts still hold ~256 rows each on average, as at full size.
 CPU_SAMPLES = {"dsv3": dict(T=1024, E=32)}
 
 
@@ -227,7 +227,7 @@ def cpu_baseline(cfg, seed, tokens=0, reps=1):
     except OSError:
         pass
     cut = ("%d of %d tokens" % (scfg["T"], cfg["T"]) if scfg["E"] == cfg["E"] else
-           "%d of %d tokens and %d of %d routed experts (~%d rows per expert, as at full size)"
+           "%d of %d tokens and %d of %d routed experts (~%d rows per expert on average, as at full size)"
            % (scfg["T"], cfg["T"], scfg["E"], cfg["E"], scfg["T"] * scfg["k"] // scfg["E"]))
     return {"value": round(reps * (ff + fb) / wall / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle", "cpu": cpu,
