@@ -29,6 +29,10 @@ CASES = {
     # >= 384 rows per expert: the 256 x 256 tiles of the row-tiled GEMMs
     "qwen3_e16": variant("qwen3", T=1024, E=16),
     "gptoss_big": variant("gptoss", T=3072),
+    # bf16 with E a multiple of 32: the layer's selection builds the maps
+    # (block counts, last-arrival scan); T ends mid selection block and mid
+    # 256-token block
+    "dsv3_odd": variant("dsv3", T=1001, d=512, f=256, f_shared=256),
 }
 
 _CACHE = {}
