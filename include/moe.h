@@ -244,7 +244,8 @@ typedef struct moe_grads {
 /* Workspace bytes of the layer's scratch (section 3.2: the fused routing,
  * token-scatter and SwiGLU kernels and the wgrad-delay split between them).
  * fwd_ws: enough for moe_route, moe_permute and moe_layer_fwd (per-block
- * expert histograms, the router's split weights and float64 logits, FP8 rows);
+ * expert histograms, an arrival counter, the router's split weights and
+ * float64 logits, FP8 rows);
  * bwd_ws: enough for moe_route_bwd, moe_grouped_gemm_bwd,
  * moe_shared_expert_bwd and moe_layer_bwd (which keeps d_o, dgu, dx_perm
  * and the router gradient scratch there, for the wgrad half); saved_bytes:
@@ -253,8 +254,12 @@ typedef struct moe_grads {
  * the limits. */
 int moe_workspace_size(const moe_shape* shape, size_t* fwd_ws, size_t* saved_bytes, size_t* bwd_ws);
 
-/* Router forward (one fused kernel: logits x W_r (+ bias), selection,
- * weights, per-block expert histogram; then the counts).
+/* Router forward: logits x W_r (+ bias), selection, weights, expert counts.
+ * bf16 layers split W_r into three bf16 parts (a launch that also clears the
+ * counts) and, with E_pool a multiple of 32, compute the logits as a tiled
+ * MFMA product into the float64 logits of the workspace, then select in a
+ * second kernel; other bf16 pools run one fused logits-and-selection kernel,
+ * fp32 layers one kernel.
  * Logits are accumulated with float32 partial sums of 16 products folded
  * into a float64 total, and selection compares float64 keys.
  * out: topk_idx, topk_w [T][k]; s_sel [T][k] (SIGMOID_GROUPED, else may be
@@ -386,7 +391,11 @@ int moe_shared_expert_bwd(const moe_shape* shape, const void* x, const void* dy,
 
 /* Whole layer forward: route, permute, grouped SwiGLU experts, shared expert,
  * combine.  Fills every pointer of *saved (s_sel only for the sigmoid routers,
- * the *_sh tensors only with a shared expert) and y.  ws: fwd_ws bytes. */
+ * the *_sh tensors only with a shared expert) and y.  ws: fwd_ws bytes.
+ * (On the two-kernel bf16 route path the selection also builds the
+ * permutation's block counts and expert offsets, so the permutation runs
+ * only its ranking and copy; the results are those of moe_route followed by
+ * moe_permute, bitwise.) */
 int moe_layer_fwd(const moe_shape* shape, const moe_params* params, const void* x,
                   const moe_saved* saved, void* y, void* ws, size_t ws_bytes, hipStream_t stream);
 
