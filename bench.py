@@ -78,13 +78,16 @@ def kernel_work(cfg, rows=None):
         "gemm_down_wgrad": ("mfma", dn), "gemm_gateup_wgrad": ("mfma", gu),
         # router logits: bf16 x times the three bf16 parts of W_r
         "route": ("mfma", 2.0 * T * d * E * 3),
-        # bytes: reads + writes of the HBM operands, once each
+        # bytes: reads + writes of the HBM operands, once each (FP8: the
+        # permutation also writes the E4M3 rows of x_perm and their scales,
+        # the combine backward at level 2 those of d_o)
         "route_select": ("hbm", T * E * 8 + T * k * 8),
-        "scatter": ("hbm", T * d * eb + R * d * eb + T * k * 4 * 3),
+        "scatter": ("hbm", T * d * eb + R * d * eb + T * k * 4 * 3 + (R * (d + 4) if cfg.get("fp8") else 0)),
         # (with a shared expert the combine also reads its output rows and the
         # unpermute its input gradient rows)
         "combine_fwd": ("hbm", R * d * eb + T * d * eb * (2 if cfg["n_shared"] else 1) + T * k * 8),
-        "combine_bwd": ("hbm", T * d * eb + 2 * R * d * eb + T * k * 12),
+        "combine_bwd": ("hbm", T * d * eb + 2 * R * d * eb + T * k * 12
+                        + (R * (d + 4) if int(cfg.get("fp8") or 0) == 2 else 0)),
         "unpermute": ("hbm", R * d * eb + T * d * eb * (2 if cfg["n_shared"] else 1) + T * k * 12),
     })
 

@@ -51,3 +51,13 @@ def test_two_sided_roofline(flops, bytes_, secs, bound):
     assert r["mfma_ceiling"] == pytest.approx(min(1.0, t_c / max(t_c, t_m)))
     mf = r if bound == "mfma" else r["other_side"]
     assert mf["achieved"] == pytest.approx(flops / secs / 1e12)
+
+
+def test_fp8_gather_kernels_count_their_code_rows():
+    base = config("qwen3")
+    T, d, k = base["T"], base["d"], base["k"]
+    R = T * k
+    w0, w1, w2 = (bench.kernel_work(dict(base, fp8=lv)) for lv in (0, 1, 2))
+    assert w1["scatter"][1] - w0["scatter"][1] == R * (d + 4)
+    assert w1["combine_bwd"][1] == w0["combine_bwd"][1]
+    assert w2["combine_bwd"][1] - w0["combine_bwd"][1] == R * (d + 4)
