@@ -244,8 +244,8 @@ typedef struct moe_grads {
 /* Workspace bytes of the layer's scratch (section 3.2: the fused routing,
  * token-scatter and SwiGLU kernels and the wgrad-delay split between them).
  * fwd_ws: enough for moe_route, moe_permute and moe_layer_fwd (per-block
- * expert histograms, an arrival counter, the router's split weights and
- * float64 logits, FP8 rows);
+ * expert histograms, per-16-token expert counts, an arrival counter, the
+ * router's split weights and float64 logits, FP8 rows);
  * bwd_ws: enough for moe_route_bwd, moe_grouped_gemm_bwd,
  * moe_shared_expert_bwd and moe_layer_bwd (which keeps d_o, dgu, dx_perm
  * and the router gradient scratch there, for the wgrad half); saved_bytes:
@@ -393,8 +393,9 @@ int moe_shared_expert_bwd(const moe_shape* shape, const void* x, const void* dy,
  * combine.  Fills every pointer of *saved (s_sel only for the sigmoid routers,
  * the *_sh tensors only with a shared expert) and y.  ws: fwd_ws bytes.
  * (On the two-kernel bf16 route path the selection also builds the
- * permutation's block counts and expert offsets, so the permutation runs
- * only its ranking and copy; the results are those of moe_route followed by
+ * permutation's block counts, expert offsets and each slot's rank inside its
+ * 16-token block, so the permutation runs only its copy, which finishes
+ * row_of and token_of; the results are those of moe_route followed by
  * moe_permute, bitwise.) */
 int moe_layer_fwd(const moe_shape* shape, const moe_params* params, const void* x,
                   const moe_saved* saved, void* y, void* ws, size_t ws_bytes, hipStream_t stream);

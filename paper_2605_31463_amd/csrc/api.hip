@@ -188,7 +188,7 @@ inline size_t act_bytes(const moe_shape& s) { return s.dtype == MOE_BF16 ? 2 : 4
 
 struct Plan {
   // forward
-  size_t hist, sync, wsplit, lg, aux_part, xq, sx, hq, sh;
+  size_t hist, sync, cnt16, wsplit, lg, aux_part, xq, sx, hq, sh;
   size_t fwd_total;
   // backward
   size_t d_o, dgu, dx_perm, dl, partial, w_rt, dgu_sh, dx_sh;
@@ -217,6 +217,8 @@ Plan plan(const moe_shape& s) {
   off += align_up((size_t)moe::perm_blocks(s.T) * Ep * 4);
   p.sync = off;
   off += align_up(4);
+  p.cnt16 = off;
+  off += align_up((size_t)((s.T + 15) / 16) * Ep * 4);
   p.wsplit = off;
   off += s.dtype == MOE_BF16 ? align_up((size_t)3 * Ep * s.d * 2) : 0;
   p.lg = off;
@@ -350,12 +352,15 @@ GemmArgs gemm_dense(const moe_shape& s, int mode) {
 // *maps_built says whether it did
 int do_route(const moe_shape& s, const void* x, const float* w_r, const float* bias, int32_t* topk_idx,
              float* topk_w, float* s_sel, int32_t* counts, void* ws, hipStream_t st, float* probs = nullptr,
-             const float* threshold = nullptr, int32_t* maps_offsets = nullptr, bool* maps_built = nullptr) {
+             const float* threshold = nullptr, int32_t* maps_offsets = nullptr, int32_t* maps_row_of = nullptr,
+             bool* maps_built = nullptr) {
   RouteArgs a{};
   if (maps_offsets) {
     a.hist = reinterpret_cast<int32_t*>(wsp(ws, plan(s).hist));
     a.sync = reinterpret_cast<int32_t*>(wsp(ws, plan(s).sync));
+    a.cnt16 = reinterpret_cast<int32_t*>(wsp(ws, plan(s).cnt16));
     a.offsets = maps_offsets;
+    a.row_of = maps_row_of;
   }
   a.probs = probs;
   a.threshold = threshold;
@@ -386,6 +391,7 @@ int do_permute(const moe_shape& s, const void* x, const int32_t* topk_idx, int32
                bool maps_ready = false) {
   PermArgs a{};
   a.maps_ready = maps_ready;
+  a.cnt16 = reinterpret_cast<const int32_t*>(wsp(ws, plan(s).cnt16));
   a.x = x;
   a.topk_idx = topk_idx;
   a.T = s.T;
@@ -1329,7 +1335,8 @@ int moe_layer_fwd(const moe_shape* shape, const moe_params* prm, const void* x, 
   const void* bd = s.expert_bias ? prm->b_down : nullptr;
   bool maps = false;
   MOE_TRY(do_route(s, x, prm->w_r, prm->router_bias, sv->topk_idx, sv->topk_w, sv->s_sel, nullptr, ws, stream,
-                   has_aux(s) ? sv->router_probs : nullptr, prm->gate_threshold, sv->expert_offsets, &maps));
+                   has_aux(s) ? sv->router_probs : nullptr, prm->gate_threshold, sv->expert_offsets, sv->row_of,
+                   &maps));
   MOE_TRY(do_permute(s, x, sv->topk_idx, sv->expert_offsets, sv->row_of, sv->token_of, sv->x_perm, ws, stream,
                      s.fp8 != 0, maps));
   if (has_aux(s)) {

@@ -32,6 +32,11 @@ struct RouteArgs {
   int32_t* hist;
   int32_t* offsets;
   int32_t* sync;
+  // and, for the permutation's copy to finish the maps: each 16-token
+  // selection block's expert counts [ceil(T/16)][E] and, in row_of, each
+  // slot's rank among the block's earlier tokens of its expert (-1: no expert)
+  int32_t* cnt16;
+  int32_t* row_of;
 };
 // maps_built (may be null): set to whether hist / offsets were produced
 int launch_route(const RouteArgs& a, hipStream_t s, bool* maps_built = nullptr);
@@ -54,7 +59,10 @@ struct PermArgs {
   void* x_perm;      // [R][d]
   uint8_t* xq;       // [R][d] E4M3 rows of the FFN experts (FP8 forward), or null
   float* sx;         // [R] their row scales
-  bool maps_ready;   // hist holds the block bases and offsets is written (by the route)
+  bool maps_ready;   // the route built the maps' inputs: hist holds the block bases,
+                     // offsets is written, row_of holds ranks inside 16-token blocks
+                     // whose counts are in cnt16; the copy finishes row_of, token_of
+  const int32_t* cnt16;
 };
 int launch_permute(const PermArgs& a, hipStream_t s);
 // The allocation-free permutation's fixed scratch (per-block histograms):

@@ -197,19 +197,56 @@ __global__ __launch_bounds__(256) void permute_copy_kernel(PermArgs a) {
   // rows at or past the FFN experts' end belong to zero-computation experts
   // (no activations): not written
   const int64_t r_end = a.offsets[a.E_rows];
-  int64_t rows[16];
-#pragma unroll
-  for (int s = 0; s < 16; ++s) {
-    rows[s] = s < k ? a.row_of[t * k + s] : -1;
-    if (rows[s] >= r_end) rows[s] = -1;
-  }
-  for (int c0 = 0; c0 < nch; c0 += 64 * CPL) {
-    uint4 v[CPL];
+  // the first chunks' loads are issued before the row look-up, so their
+  // latency overlaps its dependent loads
+  uint4 v[CPL];
+  auto load_chunks = [&](int c0) {
 #pragma unroll
     for (int j = 0; j < CPL; ++j) {
       const int c = c0 + j * 64 + lane;
       if (c < nch) v[j] = *reinterpret_cast<const uint4*>(x + (int64_t)c * V);
     }
+  };
+  load_chunks(0);
+  int64_t rows[16];
+  if (a.maps_ready) {
+    // the slot's row: its expert's offset, the base of its 256-token block,
+    // the counts of the block's earlier 16-token selection blocks and its
+    // rank inside its own (lane s holds slot s)
+    int myrow = -1;
+    if (lane < k) {
+      const int e = a.topk_idx[t * k + lane];
+      if ((unsigned)e < (unsigned)a.E) {
+        const int64_t b = t / PERM_TB;
+        const int q = (int)((t % PERM_TB) >> 4);
+        const int32_t* c16 = a.cnt16 + (b * (PERM_TB / 16)) * a.E + e;
+        // all loads issued at once: rows past q repeat row q (it exists) and
+        // are not counted
+        int cv[PERM_TB / 16 - 1];
+#pragma unroll
+        for (int u = 0; u < PERM_TB / 16 - 1; ++u) cv[u] = c16[(int64_t)min(u, q) * a.E];
+        int pre = 0;
+#pragma unroll
+        for (int u = 0; u < PERM_TB / 16 - 1; ++u) pre += u < q ? cv[u] : 0;
+        myrow = a.offsets[e] + a.hist[b * a.E + e] + pre + a.row_of[t * k + lane];
+        a.row_of[t * k + lane] = myrow;
+        a.token_of[myrow] = (int32_t)(t * k + lane);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+      rows[s] = s < k ? __builtin_amdgcn_readlane(myrow, s) : -1;
+      if (rows[s] >= r_end) rows[s] = -1;
+    }
+  } else {
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+      rows[s] = s < k ? a.row_of[t * k + s] : -1;
+      if (rows[s] >= r_end) rows[s] = -1;
+    }
+  }
+  for (int c0 = 0; c0 < nch; c0 += 64 * CPL) {
+    if (c0) load_chunks(c0);
 #pragma unroll
     for (int s = 0; s < 16; ++s) {
       if (s >= k) break;
@@ -243,10 +280,8 @@ __global__ __launch_bounds__(256) void permute_copy_kernel(PermArgs a) {
 int launch_permute(const PermArgs& a, hipStream_t s) {
   const int64_t nblk = perm_blocks(a.T);
   int st;
-  if (a.maps_ready) {  // block bases and offsets from the route's selection
+  if (a.maps_ready) {  // the route's selection built the maps' inputs; the copy finishes them
     if (nblk == 0) return MOE_OK;
-    st = launch(K_RANK, s, "rank", [&] { rank_kernel<<<nblk, 256, 0, s>>>(a); });
-    if (st) return st;
     const int ncopy = (int)((a.T + 3) / 4);
     if (a.bf16)
       return launch(K_SCATTER, s, "scatter", [&] { permute_copy_kernel<bf16_t><<<ncopy, 256, 0, s>>>(a); });

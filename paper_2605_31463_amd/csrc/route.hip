@@ -65,7 +65,10 @@ __device__ __forceinline__ double wave_max_d(double v, int width) {
 // Top-k selection and gating weights for `ntok` tokens whose float64 logits
 // sit in LDS (lg[token][ld]); one wavefront per token, four wavefronts per
 // block.  Adds each selected expert to the block histogram `hist`.
-__device__ void select_tokens(const RouteArgs& a, const double* lg, int ld, int64_t t0, int ntok, int* hist) {
+// sel (may be null): [16][16] LDS, the expert of (token tl, slot s) at
+// 16 tl + s (-1: none)
+__device__ void select_tokens(const RouteArgs& a, const double* lg, int ld, int64_t t0, int ntok, int* hist,
+                              int* sel = nullptr) {
   const int tid = threadIdx.x;
   const int E = a.E;
   const int EPAD = ld;
@@ -231,6 +234,7 @@ __device__ void select_tokens(const RouteArgs& a, const double* lg, int ld, int6
       a.topk_w[t * k + lane] = (float)w;
       if (sigm && a.s_sel) a.s_sel[t * k + lane] = (float)sc;
       atomicAdd(&hist[my_idx], 1);
+      if (sel && tl < 16) sel[tl * 16 + lane] = my_idx;
     } else if (holds) {
       a.topk_idx[t * k + lane] = -1;
       a.topk_w[t * k + lane] = 0.f;
@@ -553,7 +557,8 @@ __device__ __forceinline__ void dpp_top2_step(double& m1, double& m2) {
 // KPL = E / 16 experts per lane (contiguous); E <= 256.  Needs, with a group
 // limit, groups of a whole power-of-two number of lanes.
 template <int KPL>
-__device__ void select_tokens16(const RouteArgs& a, const double* lg, int ld, int64_t t0, int ntok, int* hist) {
+__device__ void select_tokens16(const RouteArgs& a, const double* lg, int ld, int64_t t0, int ntok, int* hist,
+                                int* sel = nullptr) {
   const int tid = threadIdx.x;
   const int E = a.E;
   const int lane = tid & 63, sub = lane & 15;
@@ -663,6 +668,7 @@ __device__ void select_tokens16(const RouteArgs& a, const double* lg, int ld, in
     a.topk_w[t * k + sub] = (float)w;
     if (sigm && a.s_sel) a.s_sel[t * k + sub] = (float)sc;
     atomicAdd(&hist[my_idx], 1);
+    if (sel) sel[tl * 16 + sub] = my_idx;
   }
 }
 
@@ -682,15 +688,18 @@ __global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a) {
   constexpr int TPB = 16;
   static_assert(PERM_TB % TPB == 0, "selection blocks tile the permutation's blocks");
   __shared__ int hist[256];
+  __shared__ int sel[TPB * 16];
   __shared__ int last;
   for (int e = threadIdx.x; e < 256; e += 256) hist[e] = 0;
+  for (int i = threadIdx.x; i < TPB * 16; i += 256) sel[i] = -1;
   __syncthreads();
   const int64_t t0 = (int64_t)blockIdx.x * TPB;
   const int ntok = (int)min((int64_t)TPB, a.T - t0);
+  int* sl = a.hist ? sel : nullptr;
   if constexpr (KPL > 0)
-    select_tokens16<KPL>(a, a.lg + t0 * a.E, a.E, t0, ntok, hist);
+    select_tokens16<KPL>(a, a.lg + t0 * a.E, a.E, t0, ntok, hist, sl);
   else
-    select_tokens(a, a.lg + t0 * a.E, a.E, t0, ntok, hist);
+    select_tokens(a, a.lg + t0 * a.E, a.E, t0, ntok, hist, sl);
   __syncthreads();
   const int E = a.E;
   if (a.counts) {
@@ -698,6 +707,23 @@ __global__ __launch_bounds__(256) void route_select_kernel(RouteArgs a) {
       if (hist[e]) atomicAdd(&a.counts[e], hist[e]);
   }
   if (!a.hist) return;
+  // this block's counts, and each slot's rank among the block's earlier
+  // tokens of its expert (a token never repeats an expert)
+  for (int e = threadIdx.x; e < E; e += 256) a.cnt16[(int64_t)blockIdx.x * E + e] = hist[e];
+  {
+    const int tl = threadIdx.x >> 4, s = threadIdx.x & 15;
+    if (tl < ntok && s < a.k) {
+      const int e = sel[tl * 16 + s];
+      int r = -1;
+      if (e >= 0) {
+        r = 0;
+        for (int u = 0; u < tl; ++u)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) r += sel[u * 16 + v] == e;
+      }
+      a.row_of[(t0 + tl) * a.k + s] = r;
+    }
+  }
   // the block counts and the arrival counter are device-scope atomics, all
   // performed where every XCD sees them; a block counts its arrival only once
   // its count additions have returned, and the last block reads the counts
@@ -977,7 +1003,8 @@ int launch_route(const RouteArgs& a, hipStream_t s, bool* maps_built) {
     // the selection builds the permutation's block bases and offsets when
     // the last block's serial pass over the blocks stays short
     RouteArgs b = a;
-    const bool maps = a.hist && a.offsets && a.sync && a.E <= 256 && perm_blocks(a.T) <= 512;
+    const bool maps = a.hist && a.offsets && a.sync && a.cnt16 && a.row_of && a.E <= 256 && a.k <= 16 &&
+                      perm_blocks(a.T) <= 512;
     if (!maps) b.hist = nullptr;
     const int st = launch_route_gemm(b, s);
     if (st == MOE_OK && maps_built) *maps_built = maps;
