@@ -999,6 +999,29 @@ __global__ __launch_bounds__(C::NT, C::NW == 4 ? 2 : 1) void gemm_bf16_persisten
       const int nbase = tl.n0 + wn * C::TN;
       const bf16_t* bdp = MODE == G_FWD_DOWN ? reinterpret_cast<const bf16_t*>(a.bias0) : nullptr;
       bf16_t* out = reinterpret_cast<bf16_t*>(a.c0);
+      if (MODE == G_FWD_DOWN && !FP8 && !bdp) {
+        // nothing to load per column block: row blocks outer, so that the two
+        // 64-byte pieces of a row's 128-byte line leave one after the other
+        // (down forward, Qwen3 shape 286 -> 267 us, DeepSeek-V3 2365 -> 2352;
+        // the gate/up dgrad's 4 x 2 wavefront tiles were 1-3% slower with it)
+#pragma unroll
+        for (int i = 0; i < MI; ++i) {
+          const int m0 = mrow0 + 32 * i;
+          if (m0 >= M) continue;
+#pragma unroll
+          for (int j = 0; j < NI; ++j) {
+            const int n0 = nbase + 32 * j;
+            const int ncols = min(32, N - n0);
+            if (ncols <= 0) continue;
+            float o[16];
+#pragma unroll
+            for (int v = 0; v < 16; ++v) o[v] = acc[i][j][v];
+            put_block(o, [&](int r) -> bf16_t* {
+              return m0 + r < M ? out + (int64_t)(tl.row_base + m0 + r) * N + n0 : nullptr;
+            }, ncols);
+          }
+        }
+      } else
 #pragma unroll
       for (int j = 0; j < NI; ++j) {
         const int n0 = nbase + 32 * j;
