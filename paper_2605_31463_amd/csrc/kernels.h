@@ -209,6 +209,7 @@ struct UnpermuteArgs {
   int d, k;
   bool bf16;
   ZcArgs zc;                // zero-computation slots: no dx_perm row, dx from coef
+  int ns;                   // column slices (set by the launcher)
 };
 int launch_unpermute(const UnpermuteArgs& a, hipStream_t s);
 
