@@ -33,6 +33,11 @@ CASES = {
     # (block counts, last-arrival scan); T ends mid selection block and mid
     # 256-token block
     "dsv3_odd": variant("dsv3", T=1001, d=512, f=256, f_shared=256),
+    # the selection builds the maps while the last arrival's pass stays within
+    # 512 blocks of 256 tokens: exactly 512 here; one block more and the layer
+    # falls back to the permutation's own histogram, scan and rank
+    "long_maps": variant("tiny", T=131072, E=32, k=2, d=64, f=64, dtype="bf16"),
+    "long": variant("tiny", T=133120, E=32, k=2, d=64, f=64, dtype="bf16"),
 }
 
 _CACHE = {}
