@@ -38,6 +38,10 @@ CASES = {
     # falls back to the permutation's own histogram, scan and rank
     "long_maps": variant("tiny", T=131072, E=32, k=2, d=64, f=64, dtype="bf16"),
     "long": variant("tiny", T=133120, E=32, k=2, d=64, f=64, dtype="bf16"),
+    # the selection's maps at the extremes of k: 16 slots per token (every
+    # lane of a token's 16-lane row holds one) and a single slot
+    "k16": variant("tiny", T=777, E=32, k=16, d=64, f=64, dtype="bf16"),
+    "k1": variant("tiny", T=999, E=64, k=1, d=128, f=64, dtype="bf16"),
 }
 
 _CACHE = {}
