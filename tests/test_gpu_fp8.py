@@ -38,6 +38,8 @@ CASES = {
     "dsv3": variant("dsv3", T=384, d=512, f=256, f_shared=256, fp8=True),
     # zero-computation experts in the pool: d_o rows quantised by their own pass
     "moepp": variant("moepp", T=256, E=32, d=512, f=256, fp8=True),
+    # the threshold router: 1 to k filled slots per token, rows quantised as usual
+    "dynmoe": variant("dynmoe", T=256, E=32, d=512, f=256, fp8=True),
 }
 
 
